@@ -1,0 +1,125 @@
+"""Seeded synthetic inputs for the DeepPCR workloads.
+
+This module only draws random numbers and shapes them; it holds none of the
+method's arithmetic (no layer evaluation, no Jacobians, no solves).  Both the
+GPU path's tests/bench and the CPU oracle receive the arrays produced here.
+
+Distributions follow the workload definitions.  N(m, v) is read as mean m and
+VARIANCE v (N(0, 1/w) only makes sense as a variance), so W has standard
+deviation 1/sqrt(w) and the bias sqrt(0.1).  Every array is drawn in float64
+from ``numpy.random.default_rng(seed)`` (PCG64) in a fixed order and then
+rounded to float32, so every consumer sees bit-identical float32 inputs.
+"""
+from __future__ import annotations
+
+import hashlib
+from dataclasses import dataclass, field
+
+import numpy as np
+
+TANH_MLP = 0       # Z_l = tanh(W_l Z_{l-1} + b_l)
+TANH_RESIDUAL = 1  # Z_l = Z_{l-1} + alpha * tanh(W_l Z_{l-1} + b_l)
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One named workload: shapes, layer kind and Newton settings."""
+
+    name: str
+    kind: str            # "pcr" (standalone solve) or "mlp"
+    B: int
+    L: int
+    w: int
+    layer: int = TANH_MLP
+    alpha: float = 1.0
+    tol: float = 1e-5
+    max_iter: int = 20
+    transpose: int = 1   # standalone solve: backward-pass (transposed) form
+    passes: tuple = field(default=("fwd",))
+    seed: int = 0
+
+
+# The five workloads the build is measured on (tanh MLPs / residual nets with
+# random weights, and a standalone block-bidiagonal solve).
+WORKLOADS = {
+    "tiny_fwd": Workload("tiny_fwd", "mlp", B=1, L=16, w=4, passes=("fwd",)),
+    "pcr_solve": Workload("pcr_solve", "pcr", B=64, L=1024, w=16, transpose=1,
+                          passes=("pcr",)),
+    "mlp_fwd": Workload("mlp_fwd", "mlp", B=256, L=256, w=32, passes=("fwd",)),
+    "mlp_bwd": Workload("mlp_bwd", "mlp", B=64, L=1024, w=64, passes=("bwd",)),
+    "resnet_fwd_bwd": Workload("resnet_fwd_bwd", "mlp", B=16, L=1024, w=128,
+                               layer=TANH_RESIDUAL, alpha=0.1,
+                               passes=("fwd", "bwd")),
+}
+
+
+def _f32(a: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def mlp_inputs(B: int, L: int, w: int, seed: int = 0) -> dict:
+    """Random MLP parameters, input and output cotangent.
+
+    Draw order: W, bias, z0, G.
+      W[L, w, w]  ~ N(0, 1/w)   (row-major, W[l] acts on column vectors)
+      bias[L, w]  ~ N(0, 0.1)
+      z0[B, w]    ~ N(0, 1)
+      G[B, w]     ~ N(0, 1)     (dLoss/dZ_{L-1} for Loss = sum_b <G_b, Z_{b,L-1}>)
+    """
+    rng = np.random.default_rng(seed)
+    W = rng.standard_normal((L, w, w)) / np.sqrt(w)
+    bias = rng.standard_normal((L, w)) * np.sqrt(0.1)
+    z0 = rng.standard_normal((B, w))
+    G = rng.standard_normal((B, w))
+    return {"W": _f32(W), "bias": _f32(bias), "z0": _f32(z0), "G": _f32(G)}
+
+
+def haar_orthogonal(rng: np.random.Generator, shape_prefix: tuple, w: int) -> np.ndarray:
+    """Haar-distributed orthogonal w x w matrices: QR of a Gaussian, with the
+    signs of R's diagonal folded into Q."""
+    g = rng.standard_normal(shape_prefix + (w, w))
+    q, rr = np.linalg.qr(g)
+    sgn = np.sign(np.diagonal(rr, axis1=-2, axis2=-1))
+    sgn[sgn == 0] = 1.0
+    return q * sgn[..., None, :]
+
+
+def pcr_inputs(B: int, L: int, w: int, seed: int = 0) -> dict:
+    """Standalone block-bidiagonal system.
+
+    Draw order: the Gaussian for QR, then u, then r.
+      J[b, l] = 0.9 * Q[b, l] @ diag(u[b, l]),  Q Haar orthogonal, u ~ U(0, 1)
+      r[B, L, w] ~ N(0, 1)
+    """
+    rng = np.random.default_rng(seed)
+    q = haar_orthogonal(rng, (B, L), w)
+    u = rng.uniform(0.0, 1.0, size=(B, L, w))
+    r = rng.standard_normal((B, L, w))
+    J = 0.9 * q * u[..., None, :]
+    return {"J": _f32(J), "r": _f32(r)}
+
+
+def random_system(B: int, L: int, w: int, seed: int, scale: float = 1.0) -> dict:
+    """Generic random system for shape sweeps: J ~ N(0, scale^2 / w), r ~ N(0, 1)."""
+    rng = np.random.default_rng(seed)
+    J = rng.standard_normal((B, L, w, w)) * (scale / np.sqrt(w))
+    r = rng.standard_normal((B, L, w))
+    return {"J": _f32(J), "r": _f32(r)}
+
+
+def workload_inputs(wl: Workload) -> dict:
+    if wl.kind == "pcr":
+        return pcr_inputs(wl.B, wl.L, wl.w, wl.seed)
+    return mlp_inputs(wl.B, wl.L, wl.w, wl.seed)
+
+
+def digest(arrays: dict) -> str:
+    """sha256 over the named float32 arrays, in sorted-name order."""
+    h = hashlib.sha256()
+    for k in sorted(arrays):
+        a = np.ascontiguousarray(arrays[k])
+        h.update(k.encode())
+        h.update(str(a.dtype).encode())
+        h.update(str(a.shape).encode())
+        h.update(a.tobytes())
+    return h.hexdigest()
