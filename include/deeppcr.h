@@ -1,0 +1,169 @@
+/*
+ * deeppcr.h -- C ABI of the DeepPCR hot path for AMD Instinct MI355X (gfx950).
+ *
+ * DeepPCR (Danieli et al., "DeepPCR: Parallelizing Sequential Operations in
+ * Neural Networks", NeurIPS 2023) writes an L-step recurrence
+ * z_l = f_l(z_{l-1}) as one system F(z) = 0 (Sec. 2, Eq. 1), solves it with
+ * Newton's method (Eq. 2) whose linear systems are block bidiagonal (Eq. 3),
+ * and solves those with Parallel Cyclic Reduction in ceil(log2 L) levels
+ * (Sec. 3, Alg. 1).  The backward pass is the transposed block-bidiagonal
+ * system, solved by one PCR pass without Newton (App. A.2, Eq. 12).
+ *
+ * Conventions for every entry point
+ *   - Indices are 0-based.  Layer l = 0..L-1 maps Z[:, l-1] to Z[:, l] with
+ *     Z[:, -1] := z0 (an input).  J_l = dZ[:, l] / dZ[:, l-1].
+ *   - Every array pointer is a DEVICE pointer to contiguous, row-major float32
+ *     memory owned by the caller.  The library never allocates device memory;
+ *     all scratch lives in the caller's `workspace` (size from
+ *     deeppcr_workspace_bytes), which must not overlap any other argument.
+ *     One workspace must not be used by two calls that run concurrently.
+ *   - All GPU work is enqueued on `stream` (a hipStream_t passed as void*;
+ *     NULL is the default stream).  pcr_solve_block_bidiag and
+ *     deeppcr_mlp_backward return without waiting for the GPU;
+ *     deeppcr_mlp_forward waits once per Newton iteration to read its
+ *     convergence measure.
+ *   - Host out-parameters are plain host pointers.
+ *   - Arguments are validated before any HIP call: an invalid argument returns
+ *     DEEPPCR_EINVAL (or DEEPPCR_EWORKSPACE for a short workspace) and
+ *     launches nothing.  A HIP runtime error returns DEEPPCR_EHIP; its text is
+ *     available from deeppcr_last_error().
+ *   - Arithmetic is float32 with float32 accumulation (no reduced-precision
+ *     matrix instructions).  Results are deterministic run to run.
+ */
+#ifndef DEEPPCR_H
+#define DEEPPCR_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    DEEPPCR_OK = 0,
+    DEEPPCR_EINVAL = 1,      /* bad pointer, size, flag or overlap            */
+    DEEPPCR_ENOCONV = 2,     /* Newton hit max_iter before the tolerance      */
+    DEEPPCR_ENONFINITE = 3,  /* a NaN/Inf appeared in the Newton iterate      */
+    DEEPPCR_EHIP = 4,        /* HIP runtime error                             */
+    DEEPPCR_EWORKSPACE = 5   /* workspace_bytes below deeppcr_workspace_bytes */
+};
+
+/* Layer kinds.  TANH_MLP is the MLP layer of App. A.1 (Eq. 7) written on
+ * post-activation states; TANH_RESIDUAL is a residual block with a skip of
+ * length one (App. A.3). */
+enum {
+    DEEPPCR_TANH_MLP = 0,      /* Z_l = tanh(W_l Z_{l-1} + b_l)                 */
+    DEEPPCR_TANH_RESIDUAL = 1  /* Z_l = Z_{l-1} + alpha*tanh(W_l Z_{l-1} + b_l) */
+};
+
+enum { DEEPPCR_OP_PCR = 0, DEEPPCR_OP_FWD = 1, DEEPPCR_OP_BWD = 2 };
+
+/* Largest supported state width w. */
+#define DEEPPCR_MAX_WIDTH 128
+
+/* Bytes of device workspace that operation `op` (DEEPPCR_OP_*) needs for a
+ * batch of B systems of L rows of width w: two ping-pong copies of the
+ * operators A_l ([B, L, w, w] each; the extra memory the paper attributes to
+ * the stored A_l, Sec. 3.1) plus vectors and a small reduction area.
+ * Returns 0 for invalid sizes. */
+size_t deeppcr_workspace_bytes(int op, int B, int L, int w);
+
+/* Static text for a DEEPPCR_* status code. */
+const char* deeppcr_status_string(int status);
+
+/* Text of the last DEEPPCR_EHIP error raised on the calling thread. */
+const char* deeppcr_last_error(void);
+
+/*
+ * Standalone block-bidiagonal solve by Parallel Cyclic Reduction
+ * (Sec. 3, Alg. 1 and Eqs. 4-6; the transposed form is the system of
+ * App. A.2, Eq. 12).  B independent systems:
+ *   transpose = 0:  x[b,l] = J[b,l] x[b,l-1] + r[b,l],        l = 0..L-1, x[b,-1] = 0
+ *   transpose = 1:  x[b,l] = J[b,l+1]^T x[b,l+1] + r[b,l],    l = L-1..0, x[b,L]  = 0
+ * i.e. M x = r (or M^T x = r) with M = identity blocks on the diagonal and
+ * -J[b,l] in block (l, l-1).  J[b,0] is never read.
+ *   J  [B, L, w, w]  input, read only
+ *   r  [B, L, w]     input
+ *   x  [B, L, w]     output; may alias r, must not overlap J
+ * 1 <= w <= DEEPPCR_MAX_WIDTH, B >= 1, L >= 1, transpose in {0, 1};
+ * workspace_bytes >= deeppcr_workspace_bytes(DEEPPCR_OP_PCR, B, L, w).
+ */
+int pcr_solve_block_bidiag(const float* J, const float* r, float* x,
+                           int B, int L, int w, int transpose,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Forward pass of a depth-L network by Newton + PCR (Sec. 2, Eqs. 1-3).
+ * Each Newton iteration evaluates every layer and its Jacobian at the current
+ * iterate in parallel (App. A.1, Eq. 8), forms the residual
+ * r_l = f_l(Z_{l-1}) - Z_l, solves the block-bidiagonal system for the
+ * update by PCR and applies it.
+ *   W     [L, w, w]  weights (row-major, W[l] acts on column vectors)
+ *   bias  [L, w]
+ *   z0    [B, w]     network input (the fixed state before layer 0)
+ *   Z     [B, L, w]  output: Z[:, l] = output of layer l
+ *   layer DEEPPCR_TANH_MLP or DEEPPCR_TANH_RESIDUAL; alpha is the residual
+ *         branch scale (ignored for TANH_MLP)
+ *   Z_init NULL: every row starts at the first layer's output f_0(z0)
+ *         (App. F.2); else [B, L, w] warm start (App. F.2).  May alias Z.
+ *   tol   stop once max|dZ| < tol * max(1, max|Z|) after an update; tol = 0
+ *         runs exactly max_iter iterations (fixed-count Newton, App. F.1)
+ *   max_iter >= 1: at most this many PCR solves
+ *   iters_out       (host, may be NULL) number of PCR solves performed
+ *   last_update_out (host, may be NULL) max|dZ| of the last iteration
+ * Returns DEEPPCR_ENOCONV if tol > 0 and max_iter iterations did not reach it
+ * (Z then holds the last iterate), DEEPPCR_ENONFINITE if the iterate became
+ * NaN/Inf (Z holds that iterate).
+ */
+int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, float* Z,
+                        int B, int L, int w, int layer, float alpha,
+                        float tol, int max_iter, const float* Z_init,
+                        void* workspace, size_t workspace_bytes,
+                        int* iters_out, float* last_update_out, void* stream);
+
+/*
+ * Backward pass by one transposed PCR solve (App. A.2, Eqs. 10-12) for
+ * Loss = sum_b <G[b], Z[b, L-1]>.  The layer Jacobians are evaluated at the
+ * stored layer inputs Z[:, l-1] (Eq. 11).  With
+ * d_l = 1 - tanh(W_l Z_{l-1} + b_l)^2 and c = 1 (TANH_MLP) or alpha
+ * (TANH_RESIDUAL), the parameter gradients of Eq. 10 read
+ *   dW[l] = c * sum_b (d_l * Lambda[b,l]) Z[b,l-1]^T,  db[l] = c * sum_b d_l * Lambda[b,l].
+ *   W, bias, z0  as for deeppcr_mlp_forward;  Z [B, L, w] forward states
+ *   G      [B, w]     dLoss/dZ[:, L-1]
+ *   Lambda [B, L, w]  output: dLoss/dZ[:, l]
+ *   dz0    [B, w]     output: dLoss/dz0
+ *   dW     [L, w, w]  output (overwritten; summed over the batch)
+ *   db     [L, w]     output (overwritten; summed over the batch)
+ * workspace_bytes >= deeppcr_workspace_bytes(DEEPPCR_OP_BWD, B, L, w).
+ */
+int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, const float* Z,
+                         const float* G, float* Lambda, float* dz0, float* dW, float* db,
+                         int B, int L, int w, int layer, float alpha,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Instrumentation (not part of the numerical path).  While enabled, the
+ * library brackets every kernel launch with HIP events on the launch's own
+ * stream and records, per kernel class, the launch count, the summed device
+ * time and the algorithmic bytes and flops of each launch.  Enabling adds a
+ * few microseconds per launch.  Not thread-safe.
+ */
+enum {
+    DEEPPCR_KCLASS_PCR_LEVEL = 0,  /* one PCR level (Alg. 1 inner parfor)      */
+    DEEPPCR_KCLASS_LAYER = 1,      /* layers + Jacobian blocks + residual      */
+    DEEPPCR_KCLASS_UPDATE = 2,     /* Newton update and convergence reduction  */
+    DEEPPCR_KCLASS_WGRAD = 3,      /* parameter gradients                      */
+    DEEPPCR_KCLASS_OTHER = 4,      /* initial guess, copies, dz0               */
+    DEEPPCR_KCLASS_COUNT = 5
+};
+int deeppcr_profile_enable(int on);
+void deeppcr_profile_reset(void);
+/* Waits for the recorded events, then reports class `kclass`. */
+int deeppcr_profile_read(int kclass, long long* launches, double* total_ms,
+                         double* alg_bytes, double* alg_flops);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DEEPPCR_H */

@@ -259,12 +259,13 @@ def seq_backward(layer: int, alpha: float, W, bias, z0, Z, G):
     W, bias, z0, Z, G = _f64(W), _f64(bias), _f64(z0), _f64(Z), _f64(G)
     B, L, w = Z.shape
     Zprev = layer_inputs(Z, z0)
-    J = all_jacobians(layer, alpha, W, bias, Zprev)
     lam = np.empty((B, L, w))
     lam[:, L - 1] = G
     for l in range(L - 2, -1, -1):
-        lam[:, l] = np.einsum("bji,bj->bi", J[:, l + 1], lam[:, l + 1])
-    dz0 = np.einsum("bji,bj->bi", J[:, 0], lam[:, 0])
+        J_next = step_jacobian(layer, alpha, W[l + 1], bias[l + 1], Zprev[:, l + 1])
+        lam[:, l] = np.einsum("bji,bj->bi", J_next, lam[:, l + 1])
+    J_0 = step_jacobian(layer, alpha, W[0], bias[0], Zprev[:, 0])
+    dz0 = np.einsum("bji,bj->bi", J_0, lam[:, 0])
     c = 1.0 if layer == TANH_MLP else alpha
     dW = np.empty((L, w, w))
     db = np.empty((L, w))

@@ -1,0 +1,411 @@
+// Host side of the DeepPCR C ABI: argument validation (before any HIP call),
+// workspace carving, the PCR level loop and the Newton driver.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <vector>
+
+#include "../../include/deeppcr.h"
+#include "internal.h"
+
+using namespace deeppcr;
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+int hip_fail(hipError_t e, const char* where) {
+    std::snprintf(g_last_error, sizeof g_last_error, "%s: %s (%d)", where, hipGetErrorString(e),
+                  (int)e);
+    return DEEPPCR_EHIP;
+}
+
+#define DEEPPCR_HIP(call)                                  \
+    do {                                                   \
+        hipError_t e_ = (call);                            \
+        if (e_ != hipSuccess) return hip_fail(e_, #call);  \
+    } while (0)
+
+// ------------------------------------------------------------ instrumentation
+struct ProfRec {
+    int kclass;
+    hipEvent_t e0, e1;
+    double bytes, flops;
+};
+
+struct Prof {
+    bool on = false;
+    std::vector<ProfRec> pending;
+    std::vector<hipEvent_t> pool;
+    long long launches[DEEPPCR_KCLASS_COUNT] = {};
+    double ms[DEEPPCR_KCLASS_COUNT] = {};
+    double bytes[DEEPPCR_KCLASS_COUNT] = {};
+    double flops[DEEPPCR_KCLASS_COUNT] = {};
+};
+Prof g_prof;
+
+hipEvent_t take_event() {
+    if (!g_prof.pool.empty()) {
+        hipEvent_t e = g_prof.pool.back();
+        g_prof.pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Runs `launch` (which enqueues one kernel on `st` and returns its
+// hipGetLastError), bracketed by events when instrumentation is on.
+template <class F>
+hipError_t timed(int kclass, double bytes, double flops, hipStream_t st, F&& launch) {
+    if (!g_prof.on) return launch();
+    hipEvent_t e0 = take_event(), e1 = take_event();
+    if (!e0 || !e1) return launch();
+    hipError_t e = hipEventRecord(e0, st);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(e1, st);
+    if (e != hipSuccess) return e;
+    g_prof.pending.push_back({kclass, e0, e1, bytes, flops});
+    return hipSuccess;
+}
+
+// ------------------------------------------------------------------ sizes
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+    size_t A[2], r[2], dscale, red, total;
+};
+
+bool sizes_ok(int B, int L, int w) {
+    return B >= 1 && L >= 1 && w >= 1 && w <= DEEPPCR_MAX_WIDTH &&
+           (double)B * L * w * w * 4.0 * 2.0 < 9.0e18;
+}
+
+Layout layout(int op, int B, int L, int w) {
+    const size_t nA = (size_t)B * L * w * w * sizeof(float);
+    const size_t nr = (size_t)B * L * w * sizeof(float);
+    Layout lo{};
+    size_t off = 0;
+    lo.A[0] = off; off += align_up(nA);
+    lo.A[1] = off; off += align_up(nA);
+    lo.r[0] = off; off += align_up(nr);
+    lo.r[1] = off; off += align_up(nr);
+    lo.dscale = off;
+    if (op == DEEPPCR_OP_BWD) off += align_up(nr);
+    lo.red = off; off += kAlign;
+    lo.total = off;
+    return lo;
+}
+
+int num_levels(int L) {
+    int k = 0;
+    for (long long s = 1; s < L; s *= 2) ++k;
+    return k;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + nb && b0 < a0 + na;
+}
+
+// Algorithmic work of one PCR level at stride s over B systems: (L-s) mat-vecs
+// and (L-2s)+ block products per system; bytes = A_l reads for l >= s, A writes
+// for l >= 2s, one read and one write of every r row.
+void level_work(int B, int L, int w, int s, double* bytes, double* flops) {
+    const double nr = (double)(L - s), na = (double)(L - 2 * s > 0 ? L - 2 * s : 0);
+    const double w2 = (double)w * w;
+    *bytes = 4.0 * B * (nr * w2 + na * w2 + 2.0 * L * w);
+    *flops = (double)B * (nr * 2.0 * w2 + na * 2.0 * w2 * w);
+}
+
+// Runs all PCR levels.  Level 0 reads (A0, r0); level k writes operators to
+// ws A buffer (k + a_first) % 2 and vectors to ws r buffer (k + r_first) % 2,
+// except the last level, which writes the solution to `x`.
+hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int B, int L, int w,
+                     float* wsA[2], float* wsr[2], int a_first, int r_first, hipStream_t st) {
+    const int K = num_levels(L);
+    if (K == 0) {
+        const double bytes = 8.0 * B * L * w;
+        return timed(DEEPPCR_KCLASS_OTHER, bytes, 0.0, st,
+                     [&] { return launch_copy_rows(r0, x, B, L, w, st); });
+    }
+    BlockSrc Ain = A0;
+    VecSrc rin = r0;
+    int s = 1;
+    for (int k = 0; k < K; ++k, s *= 2) {
+        const bool last = (k == K - 1);
+        float* Aout = wsA[(k + a_first) & 1];
+        VecDst rout = last ? x
+                           : VecDst{wsr[(k + r_first) & 1], (long long)L * w, (long long)w};
+        double bytes, flops;
+        level_work(B, L, w, s, &bytes, &flops);
+        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+            return launch_pcr_level(Ain, rin, Aout, rout, B, L, w, s, st);
+        });
+        if (e != hipSuccess) return e;
+        Ain = BlockSrc{Aout, (long long)L * w * w, (long long)w * w, 0};
+        rin = VecSrc{rout.base, rout.bstride, rout.rstride};
+    }
+    return hipSuccess;
+}
+
+struct Ws {
+    float* A[2];
+    float* r[2];
+    float* dscale;
+    unsigned* red;
+};
+
+Ws carve(void* workspace, const Layout& lo) {
+    char* p = (char*)workspace;
+    Ws ws;
+    ws.A[0] = (float*)(p + lo.A[0]);
+    ws.A[1] = (float*)(p + lo.A[1]);
+    ws.r[0] = (float*)(p + lo.r[0]);
+    ws.r[1] = (float*)(p + lo.r[1]);
+    ws.dscale = (float*)(p + lo.dscale);
+    ws.red = (unsigned*)(p + lo.red);
+    return ws;
+}
+
+// Pinned host word pair for the per-iteration convergence read-back.
+unsigned* host_words() {
+    thread_local unsigned* words = nullptr;
+    if (!words) {
+        void* p = nullptr;
+        if (hipHostMalloc(&p, 64, hipHostMallocDefault) != hipSuccess) return nullptr;
+        words = (unsigned*)p;
+    }
+    return words;
+}
+
+float bits_to_float(unsigned u) {
+    float f;
+    std::memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t deeppcr_workspace_bytes(int op, int B, int L, int w) {
+    if (op < DEEPPCR_OP_PCR || op > DEEPPCR_OP_BWD || !sizes_ok(B, L, w)) return 0;
+    return layout(op, B, L, w).total;
+}
+
+const char* deeppcr_status_string(int status) {
+    switch (status) {
+        case DEEPPCR_OK: return "ok";
+        case DEEPPCR_EINVAL: return "invalid argument";
+        case DEEPPCR_ENOCONV: return "Newton did not reach the tolerance within max_iter";
+        case DEEPPCR_ENONFINITE: return "non-finite value in the Newton iterate";
+        case DEEPPCR_EHIP: return "HIP runtime error";
+        case DEEPPCR_EWORKSPACE: return "workspace too small";
+        default: return "unknown status";
+    }
+}
+
+const char* deeppcr_last_error(void) { return g_last_error; }
+
+int pcr_solve_block_bidiag(const float* J, const float* r, float* x, int B, int L, int w,
+                           int transpose, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+    if (!J || !r || !x || !workspace || !sizes_ok(B, L, w) || (transpose != 0 && transpose != 1))
+        return DEEPPCR_EINVAL;
+    const Layout lo = layout(DEEPPCR_OP_PCR, B, L, w);
+    if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
+    const size_t nJ = (size_t)B * L * w * w * 4, nv = (size_t)B * L * w * 4;
+    if (overlaps(x, nv, J, nJ) || overlaps(workspace, lo.total, J, nJ) ||
+        overlaps(workspace, lo.total, r, nv) || overlaps(workspace, lo.total, x, nv))
+        return DEEPPCR_EINVAL;
+    if ((x != r) && overlaps(x, nv, r, nv)) return DEEPPCR_EINVAL;
+
+    hipStream_t st = (hipStream_t)stream;
+    Ws ws = carve(workspace, lo);
+    const long long bw2 = (long long)L * w * w, w2 = (long long)w * w;
+    BlockSrc A0;
+    VecSrc r0;
+    VecDst xd;
+    if (!transpose) {
+        A0 = BlockSrc{J, bw2, w2, 0};
+        r0 = VecSrc{r, (long long)L * w, w};
+        xd = VecDst{x, (long long)L * w, w};
+    } else {
+        // Transposed system in reversed row order: row m = L-1-l has operator
+        // J_{L-m}^T and right-hand side r_{L-1-m}.
+        A0 = BlockSrc{J + (long long)L * w2, bw2, -w2, 1};
+        r0 = VecSrc{r + (long long)(L - 1) * w, (long long)L * w, -(long long)w};
+        xd = VecDst{x + (long long)(L - 1) * w, (long long)L * w, -(long long)w};
+    }
+    hipError_t e = pcr_sweep(A0, r0, xd, B, L, w, ws.A, ws.r, 0, 0, st);
+    if (e != hipSuccess) return hip_fail(e, "pcr_solve_block_bidiag");
+    return DEEPPCR_OK;
+}
+
+int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
+                        int L, int w, int layer, float alpha, float tol, int max_iter,
+                        const float* Z_init, void* workspace, size_t workspace_bytes,
+                        int* iters_out, float* last_update_out, void* stream) {
+    if (!W || !bias || !z0 || !Z || !workspace || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
+    if (layer != DEEPPCR_TANH_MLP && layer != DEEPPCR_TANH_RESIDUAL) return DEEPPCR_EINVAL;
+    if (!(tol >= 0.f) || !std::isfinite(tol) || max_iter < 1 || !std::isfinite(alpha))
+        return DEEPPCR_EINVAL;
+    const Layout lo = layout(DEEPPCR_OP_FWD, B, L, w);
+    if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
+    const size_t nv = (size_t)B * L * w * 4;
+    if (overlaps(workspace, lo.total, Z, nv) || overlaps(workspace, lo.total, W, (size_t)L * w * w * 4) ||
+        overlaps(workspace, lo.total, z0, (size_t)B * w * 4) ||
+        overlaps(workspace, lo.total, bias, (size_t)L * w * 4) ||
+        overlaps(workspace, lo.total, Z_init, Z_init ? nv : 0))
+        return DEEPPCR_EINVAL;
+    if (Z_init && Z_init != Z && overlaps(Z_init, nv, Z, nv)) return DEEPPCR_EINVAL;
+
+    hipStream_t st = (hipStream_t)stream;
+    Ws ws = carve(workspace, lo);
+    unsigned* hw = host_words();
+    if (!hw) return hip_fail(hipErrorOutOfMemory, "hipHostMalloc");
+    if (iters_out) *iters_out = 0;
+    if (last_update_out) *last_update_out = 0.f;
+
+    const double w2 = (double)w * w;
+    const double eval_bytes = 4.0 * B * L * (w2 + 2.0 * w);
+    const double eval_flops = (double)B * L * (2.0 * w2 + w2);
+    if (Z_init) {
+        if (Z_init != Z) DEEPPCR_HIP(hipMemcpyAsync(Z, Z_init, nv, hipMemcpyDeviceToDevice, st));
+    } else {
+        hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * B * L * w, 2.0 * B * w * w, st, [&] {
+            return launch_initial_guess(W, bias, z0, Z, B, L, w, layer, alpha, st);
+        });
+        if (e != hipSuccess) return hip_fail(e, "initial_guess");
+    }
+    const long long n = (long long)B * L * w;
+    const VecDst xd{ws.r[(num_levels(L) + 1) & 1], (long long)L * w, (long long)w};
+    for (int k = 1; k <= max_iter; ++k) {
+        // Layers, Jacobian blocks (forward order) and residuals at the iterate.
+        hipError_t e = timed(DEEPPCR_KCLASS_LAYER, eval_bytes, eval_flops, st, [&] {
+            return launch_forward_eval(W, bias, z0, Z, ws.A[1], ws.r[1], ws.red, B, L, w, layer,
+                                       alpha, st);
+        });
+        if (e != hipSuccess) return hip_fail(e, "forward_eval");
+        // PCR solve of Eq. 3 for the update; level 0 reads ws A[1], r[1].
+        e = pcr_sweep(BlockSrc{ws.A[1], (long long)L * w * w, (long long)w * w, 0},
+                      VecSrc{ws.r[1], (long long)L * w, (long long)w}, xd, B, L, w, ws.A, ws.r,
+                      0, 0, st);
+        if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+        e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
+                  [&] { return launch_update_reduce(Z, xd.base, n, ws.red, st); });
+        if (e != hipSuccess) return hip_fail(e, "update_reduce");
+        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * sizeof(unsigned), hipMemcpyDeviceToHost, st));
+        DEEPPCR_HIP(hipStreamSynchronize(st));
+        const unsigned mx = hw[0], mz = hw[1];
+        if (iters_out) *iters_out = k;
+        if (last_update_out) *last_update_out = bits_to_float(mx);
+        if (mx >= 0x7f800000u || mz >= 0x7f800000u) return DEEPPCR_ENONFINITE;
+        const float m = bits_to_float(mx), zmax = bits_to_float(mz);
+        if (tol > 0.f && m < tol * (zmax > 1.f ? zmax : 1.f)) return DEEPPCR_OK;
+    }
+    return tol > 0.f ? DEEPPCR_ENOCONV : DEEPPCR_OK;
+}
+
+int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, const float* Z,
+                         const float* G, float* Lambda, float* dz0, float* dW, float* db, int B,
+                         int L, int w, int layer, float alpha, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+    if (!W || !bias || !z0 || !Z || !G || !Lambda || !dz0 || !dW || !db || !workspace ||
+        !sizes_ok(B, L, w))
+        return DEEPPCR_EINVAL;
+    if (layer != DEEPPCR_TANH_MLP && layer != DEEPPCR_TANH_RESIDUAL) return DEEPPCR_EINVAL;
+    if (!std::isfinite(alpha)) return DEEPPCR_EINVAL;
+    const Layout lo = layout(DEEPPCR_OP_BWD, B, L, w);
+    if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
+    const size_t nv = (size_t)B * L * w * 4, nW = (size_t)L * w * w * 4;
+    const void* ins[] = {W, bias, z0, Z, G};
+    const size_t nins[] = {nW, (size_t)L * w * 4, (size_t)B * w * 4, nv, (size_t)B * w * 4};
+    void* outs[] = {Lambda, dz0, dW, db};
+    const size_t nouts[] = {nv, (size_t)B * w * 4, nW, (size_t)L * w * 4};
+    for (int i = 0; i < 4; ++i) {
+        if (overlaps(workspace, lo.total, outs[i], nouts[i])) return DEEPPCR_EINVAL;
+        for (int j = 0; j < 5; ++j)
+            if (overlaps(outs[i], nouts[i], ins[j], nins[j])) return DEEPPCR_EINVAL;
+        for (int j = i + 1; j < 4; ++j)
+            if (overlaps(outs[i], nouts[i], outs[j], nouts[j])) return DEEPPCR_EINVAL;
+    }
+    for (int j = 0; j < 5; ++j)
+        if (overlaps(workspace, lo.total, ins[j], nins[j])) return DEEPPCR_EINVAL;
+
+    hipStream_t st = (hipStream_t)stream;
+    Ws ws = carve(workspace, lo);
+    const double w2 = (double)w * w;
+    hipError_t e = timed(DEEPPCR_KCLASS_LAYER, 4.0 * B * L * (w2 + 3.0 * w),
+                         (double)B * L * 3.0 * w2, st, [&] {
+        return launch_backward_assemble(W, bias, z0, Z, G, ws.A[1], ws.r[1], ws.dscale, B, L, w,
+                                        layer, alpha, st);
+    });
+    if (e != hipSuccess) return hip_fail(e, "backward_assemble");
+    const VecDst lam{Lambda + (long long)(L - 1) * w, (long long)L * w, -(long long)w};
+    e = pcr_sweep(BlockSrc{ws.A[1], (long long)L * w * w, (long long)w * w, 0},
+                  VecSrc{ws.r[1], (long long)L * w, (long long)w}, lam, B, L, w, ws.A, ws.r, 0, 0,
+                  st);
+    if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+    e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * (w2 + 3.0 * B * w), 2.0 * B * w2, st, [&] {
+        return launch_dz0(W, ws.dscale, Lambda, dz0, B, L, w, layer, st);
+    });
+    if (e != hipSuccess) return hip_fail(e, "dz0");
+    e = timed(DEEPPCR_KCLASS_WGRAD, 4.0 * (3.0 * B * L * w + L * (w2 + w)), 2.0 * B * L * w2, st,
+              [&] { return launch_wgrad(z0, Z, ws.dscale, Lambda, dW, db, B, L, w, st); });
+    if (e != hipSuccess) return hip_fail(e, "wgrad");
+    return DEEPPCR_OK;
+}
+
+int deeppcr_profile_enable(int on) {
+    g_prof.on = on != 0;
+    return DEEPPCR_OK;
+}
+
+void deeppcr_profile_reset(void) {
+    for (auto& p : g_prof.pending) {
+        (void)hipEventSynchronize(p.e1);
+        g_prof.pool.push_back(p.e0);
+        g_prof.pool.push_back(p.e1);
+    }
+    g_prof.pending.clear();
+    for (int c = 0; c < DEEPPCR_KCLASS_COUNT; ++c) {
+        g_prof.launches[c] = 0;
+        g_prof.ms[c] = g_prof.bytes[c] = g_prof.flops[c] = 0.0;
+    }
+}
+
+int deeppcr_profile_read(int kclass, long long* launches, double* total_ms, double* alg_bytes,
+                         double* alg_flops) {
+    if (kclass < 0 || kclass >= DEEPPCR_KCLASS_COUNT) return DEEPPCR_EINVAL;
+    for (auto& p : g_prof.pending) {
+        hipError_t e = hipEventSynchronize(p.e1);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, p.e0, p.e1);
+        if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+        g_prof.launches[p.kclass] += 1;
+        g_prof.ms[p.kclass] += ms;
+        g_prof.bytes[p.kclass] += p.bytes;
+        g_prof.flops[p.kclass] += p.flops;
+        g_prof.pool.push_back(p.e0);
+        g_prof.pool.push_back(p.e1);
+    }
+    g_prof.pending.clear();
+    if (launches) *launches = g_prof.launches[kclass];
+    if (total_ms) *total_ms = g_prof.ms[kclass];
+    if (alg_bytes) *alg_bytes = g_prof.bytes[kclass];
+    if (alg_flops) *alg_flops = g_prof.flops[kclass];
+    return DEEPPCR_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,88 @@
+// Internal interface between the host driver (api.hip) and the kernel files.
+// Not installed; the public interface is include/deeppcr.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace deeppcr {
+
+constexpr int kMaxWidth = 128;
+
+// A batch of w x w blocks addressed as base + b*bstride + m*rstride (floats).
+// Row strides may be negative (the transposed system is stored reversed).
+// trans = 1: element (i, k) of block m is stored at [k*w + i].
+struct BlockSrc {
+    const float* base;
+    long long bstride;
+    long long rstride;
+    int trans;
+};
+
+// A batch of length-w vectors, addressed like BlockSrc.
+struct VecSrc {
+    const float* base;
+    long long bstride;
+    long long rstride;
+};
+
+struct VecDst {
+    float* base;
+    long long bstride;
+    long long rstride;
+};
+
+// ---------------------------------------------------------------- PCR level
+// One level (stride s) of Parallel Cyclic Reduction over B systems of L rows:
+//   rows l <  s : rout[l] = rin[l]                     (already final)
+//   rows l >= s : rout[l] = rin[l] + Ain[l] rin[l-s]
+//   rows l >= 2s: Aout[l] = Ain[l] Ain[l-s]
+// Aout is contiguous [B, L, w, w] in internal row order.
+hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
+                            const VecDst& rout, int B, int L, int w, int s,
+                            hipStream_t stream);
+
+// ------------------------------------------------------------ layer kernels
+// Forward Newton step: for every (b, l) evaluate the layer at Zprev = Z[b,l-1]
+// (z0[b] for l = 0), write r[b,l] = f_l(Zprev) - Z[b,l] and, for l >= 1,
+// the Jacobian block J_l into A ([B, L, w, w], forward row order).  Block 0
+// of the grid also clears the two reduction words `red`.
+hipError_t launch_forward_eval(const float* W, const float* bias, const float* z0,
+                               const float* Z, float* A, float* r, unsigned* red,
+                               int B, int L, int w, int layer, float alpha,
+                               hipStream_t stream);
+
+// Z[b, l] = f_0(z0[b]) for every l.
+hipError_t launch_initial_guess(const float* W, const float* bias, const float* z0,
+                                float* Z, int B, int L, int w, int layer, float alpha,
+                                hipStream_t stream);
+
+// Z += x over n floats; red[0] = max bits of |x|, red[1] = max bits of |Z|
+// (atomic max on the IEEE bit patterns of non-negative floats; NaN > Inf).
+hipError_t launch_update_reduce(float* Z, const float* x, long long n, unsigned* red,
+                                hipStream_t stream);
+
+// Backward: Jacobian blocks of the transposed system in reversed row order,
+// blocks[m = L-l] = J_l^T for l >= 1, right-hand side rrev[m] = G if m == 0
+// else 0, and dscale[b, l] = c * (1 - tanh(a_l)^2) in natural order.
+hipError_t launch_backward_assemble(const float* W, const float* bias, const float* z0,
+                                    const float* Z, const float* G, float* A, float* rrev,
+                                    float* dscale, int B, int L, int w, int layer,
+                                    float alpha, hipStream_t stream);
+
+// dz0[b] = J_0^T Lambda[b, 0].
+hipError_t launch_dz0(const float* W, const float* dscale, const float* Lambda, float* dz0,
+                      int B, int L, int w, int layer, hipStream_t stream);
+
+// dW[l] = sum_b (dscale*Lambda)[b,l] Zprev[b,l]^T, db[l] = sum_b (dscale*Lambda)[b,l].
+hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
+                        const float* Lambda, float* dW, float* db, int B, int L, int w,
+                        hipStream_t stream);
+
+// dst[b, l] = src[b, l] for every (b, l) (used when L = 1).
+hipError_t launch_copy_rows(const VecSrc& src, const VecDst& dst, int B, int L, int w,
+                            hipStream_t stream);
+
+}  // namespace deeppcr

@@ -1,0 +1,312 @@
+// Layer evaluation, Jacobian assembly, Newton update and gradient kernels of
+// the DeepPCR hot path.
+//
+// Layers (App. A.1, Eqs. 7-9, post-activation form; App. A.3 with a skip of
+// length one):
+//   TANH_MLP      : f_l(z) = tanh(W_l z + b_l),          J_l = diag(1 - t^2) W_l
+//   TANH_RESIDUAL : f_l(z) = z + alpha tanh(W_l z + b_l), J_l = I + alpha diag(1 - t^2) W_l
+// with t = tanh(W_l z + b_l).
+#include "internal.h"
+
+namespace deeppcr {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+__device__ inline float wave_sum(float v) {
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+__device__ inline unsigned wave_umax(unsigned v) {
+    for (int off = 32; off > 0; off >>= 1) v = max(v, (unsigned)__shfl_xor((int)v, off, 64));
+    return v;
+}
+
+// a_i = sum_j W[i][j] z[j] + b[i] for all rows i < w; one wave per row,
+// lanes stride over j.  z lives in LDS.  Results go to out[i] in LDS.
+__device__ inline void preactivations(const float* __restrict__ Wl, const float* __restrict__ bl,
+                                      const float* z, float* out, int w) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int i = wave; i < w; i += kWaves) {
+        float acc = 0.f;
+        for (int j = lane; j < w; j += 64) acc = fmaf(Wl[(long long)i * w + j], z[j], acc);
+        acc = wave_sum(acc);
+        if (lane == 0) out[i] = acc + bl[i];
+    }
+}
+
+// ---------------------------------------------------------------- forward
+__global__ __launch_bounds__(kThreads) void forward_eval_kernel(
+    const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ Z, float* __restrict__ A, float* __restrict__ r,
+    unsigned* __restrict__ red, int L, int w, int layer, float alpha) {
+    const long long row = blockIdx.x;
+    const int l = (int)(row % L);
+    const int b = (int)(row / L);
+    const int t = threadIdx.x;
+    if (row == 0 && t < 2) red[t] = 0u;
+
+    __shared__ float zp[kMaxWidth];
+    __shared__ float a[kMaxWidth];
+    __shared__ float dsc[kMaxWidth];
+    const float* zprev = (l == 0) ? z0 + (long long)b * w : Z + (row - 1) * w;
+    for (int i = t; i < w; i += kThreads) zp[i] = zprev[i];
+    __syncthreads();
+    const float* Wl = W + (long long)l * w * w;
+    preactivations(Wl, bias + (long long)l * w, zp, a, w);
+    __syncthreads();
+    for (int i = t; i < w; i += kThreads) {
+        const float th = tanhf(a[i]);
+        const float d = 1.f - th * th;
+        const float f = (layer == 0) ? th : fmaf(alpha, th, zp[i]);
+        r[row * w + i] = f - Z[row * w + i];
+        dsc[i] = (layer == 0) ? d : alpha * d;
+    }
+    __syncthreads();
+    if (l == 0) return;
+    float* Ab = A + row * w * w;
+    for (int idx = t; idx < w * w; idx += kThreads) {
+        const int i = idx / w, j = idx - (idx / w) * w;
+        float v = dsc[i] * Wl[idx];
+        if (layer != 0 && i == j) v += 1.f;
+        Ab[idx] = v;
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void initial_guess_kernel(
+    const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
+    float* __restrict__ Z, int L, int w, int layer, float alpha, int rows_per_block) {
+    const int chunks = (L + rows_per_block - 1) / rows_per_block;
+    const int b = blockIdx.x / chunks;
+    const int l0 = (blockIdx.x % chunks) * rows_per_block;
+    const int t = threadIdx.x;
+    __shared__ float zp[kMaxWidth];
+    __shared__ float a[kMaxWidth];
+    __shared__ float f0[kMaxWidth];
+    for (int i = t; i < w; i += kThreads) zp[i] = z0[(long long)b * w + i];
+    __syncthreads();
+    preactivations(W, bias, zp, a, w);
+    __syncthreads();
+    for (int i = t; i < w; i += kThreads) {
+        const float th = tanhf(a[i]);
+        f0[i] = (layer == 0) ? th : fmaf(alpha, th, zp[i]);
+    }
+    __syncthreads();
+    const int l1 = min(L, l0 + rows_per_block);
+    for (long long idx = t; idx < (long long)(l1 - l0) * w; idx += kThreads) {
+        const int i = (int)(idx % w);
+        Z[((long long)b * L + l0) * w + idx] = f0[i];
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void update_reduce_kernel(
+    float* __restrict__ Z, const float* __restrict__ x, long long n, unsigned* __restrict__ red) {
+    unsigned mx = 0u, mz = 0u;
+    for (long long i = (long long)blockIdx.x * kThreads + threadIdx.x; i < n;
+         i += (long long)gridDim.x * kThreads) {
+        const float dx = x[i];
+        const float z = Z[i] + dx;
+        Z[i] = z;
+        mx = max(mx, __float_as_uint(fabsf(dx)));
+        mz = max(mz, __float_as_uint(fabsf(z)));
+    }
+    mx = wave_umax(mx);
+    mz = wave_umax(mz);
+    __shared__ unsigned sx[kWaves], sz[kWaves];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) {
+        sx[wave] = mx;
+        sz[wave] = mz;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned a = sx[0], c = sz[0];
+        for (int i = 1; i < kWaves; ++i) {
+            a = max(a, sx[i]);
+            c = max(c, sz[i]);
+        }
+        atomicMax(red + 0, a);
+        atomicMax(red + 1, c);
+    }
+}
+
+// --------------------------------------------------------------- backward
+__global__ __launch_bounds__(kThreads) void backward_assemble_kernel(
+    const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ Z, const float* __restrict__ G, float* __restrict__ A,
+    float* __restrict__ rrev, float* __restrict__ dscale, int L, int w, int layer, float alpha) {
+    const long long row = blockIdx.x;  // natural (b, l)
+    const int l = (int)(row % L);
+    const int b = (int)(row / L);
+    const int t = threadIdx.x;
+    __shared__ float zp[kMaxWidth];
+    __shared__ float a[kMaxWidth];
+    __shared__ float dsc[kMaxWidth];
+    const float* zprev = (l == 0) ? z0 + (long long)b * w : Z + (row - 1) * w;
+    for (int i = t; i < w; i += kThreads) zp[i] = zprev[i];
+    __syncthreads();
+    const float* Wl = W + (long long)l * w * w;
+    preactivations(Wl, bias + (long long)l * w, zp, a, w);
+    __syncthreads();
+    const int m = L - 1 - l;  // reversed row of this layer's adjoint
+    for (int i = t; i < w; i += kThreads) {
+        const float th = tanhf(a[i]);
+        const float d = 1.f - th * th;
+        const float c = (layer == 0) ? d : alpha * d;
+        dsc[i] = c;
+        dscale[row * w + i] = c;
+        rrev[((long long)b * L + m) * w + i] = (m == 0) ? G[(long long)b * w + i] : 0.f;
+    }
+    __syncthreads();
+    if (l == 0) return;
+    // Reversed row L - l holds J_l^T: element (i, k) = J_l[k][i] = dsc[k] W_l[k][i] (+ delta).
+    float* Ab = A + ((long long)b * L + (L - l)) * w * w;
+    for (int idx = t; idx < w * w; idx += kThreads) {
+        const int i = idx / w, k = idx - (idx / w) * w;
+        float v = dsc[k] * Wl[(long long)k * w + i];
+        if (layer != 0 && i == k) v += 1.f;
+        Ab[idx] = v;
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void dz0_kernel(
+    const float* __restrict__ W, const float* __restrict__ dscale, const float* __restrict__ Lambda,
+    float* __restrict__ dz0, int L, int w, int layer) {
+    const int b = blockIdx.x;
+    const int t = threadIdx.x;
+    __shared__ float g[kMaxWidth];
+    const float* lam = Lambda + (long long)b * L * w;  // row l = 0
+    const float* dsc = dscale + (long long)b * L * w;
+    for (int k = t; k < w; k += kThreads) g[k] = dsc[k] * lam[k];
+    __syncthreads();
+    for (int i = t; i < w; i += kThreads) {
+        float acc = 0.f;
+        for (int k = 0; k < w; ++k) acc = fmaf(W[(long long)k * w + i], g[k], acc);
+        dz0[(long long)b * w + i] = (layer != 0) ? lam[i] + acc : acc;
+    }
+}
+
+constexpr int kWgradBC = 32;  // batch rows staged per LDS chunk
+
+__global__ __launch_bounds__(kThreads) void wgrad_kernel(
+    const float* __restrict__ z0, const float* __restrict__ Z, const float* __restrict__ dscale,
+    const float* __restrict__ Lambda, float* __restrict__ dW, float* __restrict__ db, int B, int L,
+    int w) {
+    const int l = blockIdx.x;
+    const int t = threadIdx.x;
+    __shared__ float g[kWgradBC][kMaxWidth];
+    __shared__ float zp[kWgradBC][kMaxWidth];
+    constexpr int kAcc = kMaxWidth * kMaxWidth / kThreads;
+    float acc[kAcc];
+#pragma unroll
+    for (int q = 0; q < kAcc; ++q) acc[q] = 0.f;
+    float dbacc = 0.f;
+    const int nout = w * w;
+    for (int b0 = 0; b0 < B; b0 += kWgradBC) {
+        const int nb = min(kWgradBC, B - b0);
+        for (int idx = t; idx < nb * w; idx += kThreads) {
+            const int bb = idx / w, i = idx - (idx / w) * w;
+            const long long rowi = ((long long)(b0 + bb) * L + l) * w + i;
+            g[bb][i] = dscale[rowi] * Lambda[rowi];
+            zp[bb][i] = (l == 0) ? z0[(long long)(b0 + bb) * w + i] : Z[rowi - w];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < kAcc; ++q) {
+            const int idx = t + q * kThreads;
+            if (idx < nout) {
+                const int i = idx / w, j = idx - (idx / w) * w;
+                float a = acc[q];
+                for (int bb = 0; bb < nb; ++bb) a = fmaf(g[bb][i], zp[bb][j], a);
+                acc[q] = a;
+            }
+        }
+        if (t < w) {
+            for (int bb = 0; bb < nb; ++bb) dbacc += g[bb][t];
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int q = 0; q < kAcc; ++q) {
+        const int idx = t + q * kThreads;
+        if (idx < nout) dW[(long long)l * nout + idx] = acc[q];
+    }
+    if (t < w) db[(long long)l * w + t] = dbacc;
+}
+
+__global__ __launch_bounds__(kThreads) void copy_rows_kernel(VecSrc src, VecDst dst, int L, int w) {
+    const long long row = blockIdx.x;
+    const int l = (int)(row % L);
+    const int b = (int)(row / L);
+    const float* s = src.base + b * src.bstride + (long long)l * src.rstride;
+    float* d = dst.base + b * dst.bstride + (long long)l * dst.rstride;
+    for (int i = threadIdx.x; i < w; i += kThreads) d[i] = s[i];
+}
+
+}  // namespace
+
+hipError_t launch_forward_eval(const float* W, const float* bias, const float* z0,
+                               const float* Z, float* A, float* r, unsigned* red,
+                               int B, int L, int w, int layer, float alpha,
+                               hipStream_t stream) {
+    hipLaunchKernelGGL(forward_eval_kernel, dim3((unsigned)((long long)B * L)), dim3(kThreads), 0,
+                       stream, W, bias, z0, Z, A, r, red, L, w, layer, alpha);
+    return hipGetLastError();
+}
+
+hipError_t launch_initial_guess(const float* W, const float* bias, const float* z0, float* Z,
+                                int B, int L, int w, int layer, float alpha,
+                                hipStream_t stream) {
+    const int rows_per_block = 64;
+    const int chunks = (L + rows_per_block - 1) / rows_per_block;
+    hipLaunchKernelGGL(initial_guess_kernel, dim3((unsigned)((long long)B * chunks)),
+                       dim3(kThreads), 0, stream, W, bias, z0, Z, L, w, layer, alpha,
+                       rows_per_block);
+    return hipGetLastError();
+}
+
+hipError_t launch_update_reduce(float* Z, const float* x, long long n, unsigned* red,
+                                hipStream_t stream) {
+    long long blocks = (n + kThreads * 8 - 1) / (kThreads * 8);
+    if (blocks > 4096) blocks = 4096;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(update_reduce_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, Z,
+                       x, n, red);
+    return hipGetLastError();
+}
+
+hipError_t launch_backward_assemble(const float* W, const float* bias, const float* z0,
+                                    const float* Z, const float* G, float* A, float* rrev,
+                                    float* dscale, int B, int L, int w, int layer,
+                                    float alpha, hipStream_t stream) {
+    hipLaunchKernelGGL(backward_assemble_kernel, dim3((unsigned)((long long)B * L)),
+                       dim3(kThreads), 0, stream, W, bias, z0, Z, G, A, rrev, dscale, L, w,
+                       layer, alpha);
+    return hipGetLastError();
+}
+
+hipError_t launch_dz0(const float* W, const float* dscale, const float* Lambda, float* dz0,
+                      int B, int L, int w, int layer, hipStream_t stream) {
+    hipLaunchKernelGGL(dz0_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, W, dscale,
+                       Lambda, dz0, L, w, layer);
+    return hipGetLastError();
+}
+
+hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
+                        const float* Lambda, float* dW, float* db, int B, int L, int w,
+                        hipStream_t stream) {
+    hipLaunchKernelGGL(wgrad_kernel, dim3((unsigned)L), dim3(kThreads), 0, stream, z0, Z, dscale,
+                       Lambda, dW, db, B, L, w);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy_rows(const VecSrc& src, const VecDst& dst, int B, int L, int w,
+                            hipStream_t stream) {
+    hipLaunchKernelGGL(copy_rows_kernel, dim3((unsigned)((long long)B * L)), dim3(kThreads), 0,
+                       stream, src, dst, L, w);
+    return hipGetLastError();
+}
+
+}  // namespace deeppcr

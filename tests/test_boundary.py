@@ -1,0 +1,140 @@
+"""The C ABI loads, exports every function include/deeppcr.h declares, and
+rejects invalid arguments before any HIP call (so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2309_16318_amd import deeppcr
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "deeppcr.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) - {"defined"})
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("pcr_solve_block_bidiag", "deeppcr_mlp_forward", "deeppcr_mlp_backward",
+              "deeppcr_workspace_bytes"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = deeppcr.lib()
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+        assert n in deeppcr.SIGNATURES, n
+
+
+def test_workspace_sizes():
+    f = deeppcr.workspace_bytes
+    B, L, w = 3, 7, 5
+    nA = B * L * w * w * 4
+    nr = B * L * w * 4
+    up = lambda x: (x + 255) // 256 * 256
+    assert f(deeppcr.OP_PCR, B, L, w) == 2 * up(nA) + 2 * up(nr) + 256
+    assert f(deeppcr.OP_FWD, B, L, w) == 2 * up(nA) + 2 * up(nr) + 256
+    assert f(deeppcr.OP_BWD, B, L, w) == 2 * up(nA) + 3 * up(nr) + 256
+    for bad in ((0, 1, 1), (1, 0, 1), (1, 1, 0), (1, 1, 129), (-1, 4, 4)):
+        assert f(deeppcr.OP_PCR, *bad) == 0
+    assert f(7, 1, 1, 1) == 0
+
+
+def test_status_strings():
+    for s in range(6):
+        assert deeppcr.status_string(s)
+    assert deeppcr.status_string(99) == "unknown status"
+
+
+# Fake, non-overlapping "device" addresses: validation must reject before use.
+P = [ctypes.c_void_p(0x10000000 * (i + 1)) for i in range(12)]
+BIG = 1 << 40
+
+
+def _pcr(J=P[0], r=P[1], x=P[2], B=2, L=8, w=4, tr=0, ws=P[3], nws=BIG):
+    return deeppcr.lib().pcr_solve_block_bidiag(J, r, x, B, L, w, tr, ws, nws, None)
+
+
+def test_pcr_solve_rejects_invalid_arguments():
+    E = deeppcr.EINVAL
+    assert _pcr(J=None) == E
+    assert _pcr(r=None) == E
+    assert _pcr(x=None) == E
+    assert _pcr(ws=None) == E
+    assert _pcr(B=0) == E
+    assert _pcr(L=0) == E
+    assert _pcr(w=0) == E
+    assert _pcr(w=129) == E
+    assert _pcr(tr=2) == E
+    # x overlapping J, workspace overlapping r
+    assert _pcr(x=ctypes.c_void_p(P[0].value + 64)) == E
+    assert _pcr(ws=ctypes.c_void_p(P[1].value - 16)) == E
+    # x partially overlapping r (exact aliasing is allowed)
+    assert _pcr(x=ctypes.c_void_p(P[1].value + 4)) == E
+    assert _pcr(nws=deeppcr.workspace_bytes(deeppcr.OP_PCR, 2, 8, 4) - 1) == deeppcr.EWORKSPACE
+
+
+def _fwd(W=P[0], b=P[1], z0=P[2], Z=P[3], B=2, L=8, w=4, layer=0, alpha=1.0, tol=1e-5,
+         max_iter=20, Zi=None, ws=P[5], nws=BIG):
+    it = ctypes.c_int(-1)
+    lu = ctypes.c_float(-1)
+    return deeppcr.lib().deeppcr_mlp_forward(W, b, z0, Z, B, L, w, layer, alpha, tol, max_iter,
+                                             Zi, ws, nws, ctypes.byref(it), ctypes.byref(lu),
+                                             None)
+
+
+def test_forward_rejects_invalid_arguments():
+    E = deeppcr.EINVAL
+    assert _fwd(W=None) == E
+    assert _fwd(Z=None) == E
+    assert _fwd(layer=2) == E
+    assert _fwd(max_iter=0) == E
+    assert _fwd(tol=-1.0) == E
+    assert _fwd(tol=float("nan")) == E
+    assert _fwd(tol=float("inf")) == E
+    assert _fwd(alpha=float("nan")) == E
+    assert _fwd(w=200) == E
+    assert _fwd(Zi=ctypes.c_void_p(P[3].value + 4)) == E     # partial overlap with Z
+    assert _fwd(ws=ctypes.c_void_p(P[3].value)) == E          # workspace over Z
+    assert _fwd(nws=100) == deeppcr.EWORKSPACE
+
+
+def _bwd(ptrs=None, B=2, L=8, w=4, layer=0, alpha=1.0, ws=P[10], nws=BIG):
+    p = list(P[:9]) if ptrs is None else ptrs
+    return deeppcr.lib().deeppcr_mlp_backward(*p, B, L, w, layer, alpha, ws, nws, None)
+
+
+def test_backward_rejects_invalid_arguments():
+    E = deeppcr.EINVAL
+    for i in range(9):
+        p = list(P[:9])
+        p[i] = None
+        assert _bwd(p) == E
+    p = list(P[:9])
+    p[5] = P[3]  # Lambda over Z
+    assert _bwd(p) == E
+    p = list(P[:9])
+    p[7] = ctypes.c_void_p(P[8].value - 16)  # dW runs into db
+    assert _bwd(p) == E
+    assert _bwd(layer=-1) == E
+    assert _bwd(w=0) == E
+    assert _bwd(alpha=float("inf")) == E
+    assert _bwd(nws=1) == deeppcr.EWORKSPACE
+
+
+def test_profile_read_rejects_bad_class():
+    st = deeppcr.lib().deeppcr_profile_read(99, None, None, None, None)
+    assert st == deeppcr.EINVAL
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(deeppcr, "_lib", None)
+    monkeypatch.setattr(deeppcr, "LIB_PATH", str(tmp_path / "nope.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        deeppcr.lib()
