@@ -1,0 +1,205 @@
+"""Throughput of the DeepPCR hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step = one pass of the whole path over one batch of synthetic input that
+is already resident in HBM.  The default workload is the deep residual net
+(L = 1024 blocks, width 128, batch 16): Newton + PCR forward pass, then the
+transposed-PCR backward pass with parameter gradients.  Prints one JSON line:
+layer-steps/s = B*L / (seconds per step), the roofline position of the PCR
+level kernel (timed with HIP events on its own stream by the library's
+instrumentation), and the CPU oracle timed on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
+PEAK_FP32_TFLOPS = 157.3     # MI355X dense fp32 (matrix and vector), TFLOP/s
+RIDGE = PEAK_FP32_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="resnet_fwd_bwd")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=10.0)
+    return p.parse_args()
+
+
+def make_step(wl, dev):
+    """Returns (step(), info) for the workload with inputs resident on `dev`."""
+    import torch
+
+    from paper_2309_16318_amd import deeppcr, synth
+
+    d = synth.workload_inputs(wl)
+    t = {k: torch.from_numpy(v).to(dev) for k, v in d.items()}
+    B, L, w = wl.B, wl.L, wl.w
+    info = {"iters": None}
+    if wl.kind == "pcr":
+        ws = torch.empty(deeppcr.workspace_bytes(deeppcr.OP_PCR, B, L, w), dtype=torch.uint8,
+                         device=dev)
+        x = torch.empty_like(t["r"])
+
+        def step():
+            deeppcr.pcr_solve_block_bidiag(t["J"], t["r"], x, transpose=wl.transpose,
+                                           workspace=ws)
+        return step, info
+
+    op_ws = {}
+    Z = torch.empty((B, L, w), dtype=torch.float32, device=dev)
+    if "fwd" in wl.passes:
+        op_ws["fwd"] = torch.empty(deeppcr.workspace_bytes(deeppcr.OP_FWD, B, L, w),
+                                   dtype=torch.uint8, device=dev)
+    if "bwd" in wl.passes:
+        op_ws["bwd"] = torch.empty(deeppcr.workspace_bytes(deeppcr.OP_BWD, B, L, w),
+                                   dtype=torch.uint8, device=dev)
+        outs = dict(Lambda=torch.empty((B, L, w), dtype=torch.float32, device=dev),
+                    dz0=torch.empty((B, w), dtype=torch.float32, device=dev),
+                    dW=torch.empty((L, w, w), dtype=torch.float32, device=dev),
+                    db=torch.empty((L, w), dtype=torch.float32, device=dev))
+        if "fwd" not in wl.passes:
+            # backward alone: forward states from one Newton + PCR pass, outside the timing
+            res = deeppcr.deeppcr_mlp_forward(t["W"], t["bias"], t["z0"], Z, layer=wl.layer,
+                                              alpha=wl.alpha, tol=wl.tol, max_iter=wl.max_iter)
+            if res.status != deeppcr.OK:
+                raise RuntimeError(f"forward status {res.status}")
+
+    def step():
+        if "fwd" in wl.passes:
+            res = deeppcr.deeppcr_mlp_forward(t["W"], t["bias"], t["z0"], Z, layer=wl.layer,
+                                              alpha=wl.alpha, tol=wl.tol, max_iter=wl.max_iter,
+                                              workspace=op_ws["fwd"])
+            if res.status != deeppcr.OK:
+                raise RuntimeError(f"forward status {res.status}")
+            info["iters"] = res.iters
+        if "bwd" in wl.passes:
+            deeppcr.deeppcr_mlp_backward(t["W"], t["bias"], t["z0"], Z, t["G"], layer=wl.layer,
+                                         alpha=wl.alpha, workspace=op_ws["bwd"], **outs)
+    return step, info
+
+
+def cpu_baseline(wl, budget_s):
+    """The oracle (numpy float64, sequential substitution) on the same
+    workload, repeated until about `budget_s` seconds of CPU work."""
+    import oracle
+    from paper_2309_16318_amd import synth
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    d = synth.workload_inputs(wl)
+    B, L = wl.B, wl.L
+    Zs = None
+    if wl.kind == "mlp" and "fwd" not in wl.passes:
+        Zs = oracle.seq_forward(wl.layer, wl.alpha, d["W"], d["bias"], d["z0"])
+
+    def once():
+        if wl.kind == "pcr":
+            oracle.seq_solve(d["J"], d["r"], bool(wl.transpose))
+            return
+        Z = Zs
+        if "fwd" in wl.passes:
+            Z = oracle.seq_forward(wl.layer, wl.alpha, d["W"], d["bias"], d["z0"])
+        if "bwd" in wl.passes:
+            oracle.seq_backward(wl.layer, wl.alpha, d["W"], d["bias"], d["z0"], Z, d["G"])
+
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        once()
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    parts = "+".join(("seq_solve",) if wl.kind == "pcr" else
+                     tuple(p for p, on in (("seq_forward", "fwd" in wl.passes),
+                                           ("seq_backward", "bwd" in wl.passes)) if on))
+    return {"value": B * L * reps / el, "unit": "layer-steps/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"full workload ({parts}, numpy float64) x {reps} repetitions, "
+                      f"{el:.1f} s wall"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2309_16318_amd import deeppcr, synth
+
+    wl = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    deeppcr.lib()
+    step, info = make_step(wl, dev)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    deeppcr.profile_reset()
+    deeppcr.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    deeppcr.profile_enable(False)
+    prof = {deeppcr.KCLASS_NAMES[c]: deeppcr.profile_read(c) for c in range(5)}
+
+    ms_step = el * 1e3 / args.steps
+    value = wl.B * wl.L / (el / args.steps)
+    lvl = prof["pcr_level"]
+    intensity = lvl["flops"] / max(lvl["bytes"], 1.0)
+    if intensity >= RIDGE * 0.75 or wl.w >= 64:
+        achieved = lvl["flops"] / (lvl["ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4)}
+    else:
+        achieved = lvl["bytes"] / (lvl["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["traffic"] = None
+    roof["kernel"] = "pcr_level"
+    roof["avg_launch_us"] = round(lvl["ms"] * 1e3 / max(lvl["launches"], 1), 3)
+    roof["launches"] = lvl["launches"]
+
+    cfg = {"workload": wl.name, "B": wl.B, "L": wl.L, "w": wl.w,
+           "layer": ("tanh_mlp" if wl.layer == 0 else "tanh_residual") if wl.kind == "mlp"
+           else None, "alpha": wl.alpha if wl.kind == "mlp" else None,
+           "passes": list(wl.passes), "newton_iters": info["iters"],
+           "newton_tol": wl.tol if "fwd" in wl.passes else None,
+           "parallelism": "single-gpu"}
+    out = {
+        "metric": "layer-steps/sec (B*L/s) for Newton+PCR forward and PCR backward",
+        "value": round(value, 1), "unit": "layer-steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": cfg, "roofline": roof,
+        "kernel_ms_per_step": {k: round(v["ms"] / args.steps, 4) for k, v in prof.items()},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
