@@ -35,6 +35,17 @@ struct VecDst {
 };
 
 // ---------------------------------------------------------------- PCR level
+// Work decomposition of one level with stride s: the rows l >= s form s
+// chains (l mod s); each chain is cut into segments of at most n rows;
+// segs_per_class segments per chain, total = B * s * segs_per_class items.
+struct LevelPlan {
+    int s;
+    int n;
+    int segs_per_class;
+    long long total;
+};
+LevelPlan plan_level(int B, int L, int s, long long target_items, int n_max);
+
 // One level (stride s) of Parallel Cyclic Reduction over B systems of L rows:
 //   rows l <  s : rout[l] = rin[l]                     (already final)
 //   rows l >= s : rout[l] = rin[l] + Ain[l] rin[l-s]
