@@ -352,7 +352,8 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
     });
     if (e != hipSuccess) return hip_fail(e, "backward_assemble");
     const VecDst lam{Lambda + (long long)(L - 1) * w, (long long)L * w, -(long long)w};
-    e = pcr_sweep(BlockSrc{ws.A[1], (long long)L * w * w, (long long)w * w, 0},
+    e = pcr_sweep(BlockSrc{ws.A[1], (long long)L * w * w, (long long)w * w,
+                           backward_blocks_transposed(w) ? 1 : 0},
                   VecSrc{ws.r[1], (long long)L * w, (long long)w}, lam, B, L, w, ws.A, ws.r, 0, 0,
                   st);
     if (e != hipSuccess) return hip_fail(e, "pcr_sweep");

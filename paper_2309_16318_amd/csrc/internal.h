@@ -76,8 +76,11 @@ hipError_t launch_update_reduce(float* Z, const float* x, long long n, unsigned*
                                 hipStream_t stream);
 
 // Backward: Jacobian blocks of the transposed system in reversed row order,
-// blocks[m = L-l] = J_l^T for l >= 1, right-hand side rrev[m] = G if m == 0
-// else 0, and dscale[b, l] = c * (1 - tanh(a_l)^2) in natural order.
+// blocks[m = L-l] = J_l^T for l >= 1 (stored as J_l itself, i.e. to be read
+// transposed, when backward_blocks_transposed(w)), right-hand side
+// rrev[m] = G if m == 0 else 0, and dscale[b, l] = c * (1 - tanh(a_l)^2) in
+// natural order.
+bool backward_blocks_transposed(int w);
 hipError_t launch_backward_assemble(const float* W, const float* bias, const float* z0,
                                     const float* Z, const float* G, float* A, float* rrev,
                                     float* dscale, int B, int L, int w, int layer,

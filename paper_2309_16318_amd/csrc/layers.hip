@@ -245,16 +245,112 @@ __global__ __launch_bounds__(kThreads) void copy_rows_kernel(VecSrc src, VecDst 
     for (int i = threadIdx.x; i < w; i += kThreads) d[i] = s[i];
 }
 
+// ---------------------------------------------------------------------------
+// Vectorized layer + Jacobian evaluation for w in {16, 32, 64, 128}.
+// Every thread owns float4 chunks of W_l (row i, columns 4c..4c+3); the W/4
+// threads of a row form a contiguous lane group, so the pre-activation
+// a_i = W_l[i,:] z + b_i is reduced by lane shuffles inside the group and
+// every lane of the group then holds a_i.  The Jacobian rows are written with
+// float4 stores.  Mode FWD writes J_l at row l and the residual; mode BWD
+// writes J_l (not transposed) at reversed row L - l, c * d_l and the
+// reversed right-hand side (G at reversed row 0).
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <int W>
+struct EvalShape {
+    static constexpr int ROWS_PER_WG = (W * W >= 1024) ? 1 : 1024 / (W * W);  // (b, l) rows
+    static constexpr int NCH = W * W / 4;                                      // chunks per block
+    static constexpr int TPB = NCH < 256 ? NCH : 256;                          // threads per block
+    static constexpr int CPT = NCH / TPB;                                      // chunks per thread
+    static constexpr int GROUP = W / 4;                                        // lanes per row
+};
+
+template <int W, bool BWD>
+__global__ __launch_bounds__(256) void layer_eval_vec(
+    const float* __restrict__ W_, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ Z, const float* __restrict__ G, float* __restrict__ A,
+    float* __restrict__ r, float* __restrict__ dscale, unsigned* __restrict__ red, int B, int L,
+    int layer, float alpha) {
+    using S = EvalShape<W>;
+    const int t = threadIdx.x;
+    const long long row = (long long)blockIdx.x * S::ROWS_PER_WG + t / S::TPB;  // b*L + l
+    if (!BWD && blockIdx.x == 0 && t < 2) red[t] = 0u;
+    if (row >= (long long)B * L) return;
+    const int l = (int)(row % L);
+    const int b = (int)(row / L);
+    const int tt = t % S::TPB;
+    const float* zprev = (l == 0) ? z0 + (long long)b * W : Z + (row - 1) * W;
+    const float* Wl = W_ + (long long)l * W * W;
+    const int m_rev = L - l;  // reversed row of J_l (backward)
+    float* Ab = BWD ? A + ((long long)b * L + m_rev) * W * W : A + row * W * W;
+#pragma unroll
+    for (int p = 0; p < S::CPT; ++p) {
+        const int f = tt + S::TPB * p;
+        const int i = f / S::GROUP;
+        const int c4 = 4 * (f % S::GROUP);
+        const v4f w4 = *reinterpret_cast<const v4f*>(Wl + i * W + c4);
+        const v4f z4 = *reinterpret_cast<const v4f*>(zprev + c4);
+        float part = w4[0] * z4[0];
+        part = fmaf(w4[1], z4[1], part);
+        part = fmaf(w4[2], z4[2], part);
+        part = fmaf(w4[3], z4[3], part);
+#pragma unroll
+        for (int off = 1; off < S::GROUP; off <<= 1) part += __shfl_xor(part, off, 64);
+        const float a = part + bias[(long long)l * W + i];
+        const float th = tanhf(a);
+        const float d = 1.f - th * th;
+        const float dsc = (layer == 0) ? d : alpha * d;
+        const bool lead = (f % S::GROUP) == 0;
+        if (!BWD) {
+            if (lead) {
+                const float zi = zprev[i];
+                const float fv = (layer == 0) ? th : fmaf(alpha, th, zi);
+                r[row * W + i] = fv - Z[row * W + i];
+            }
+        } else if (lead) {
+            dscale[row * W + i] = dsc;
+            const int mr = L - 1 - l;
+            r[((long long)b * L + mr) * W + i] = (mr == 0) ? G[(long long)b * W + i] : 0.f;
+        }
+        if (l >= 1) {
+            v4f j4 = w4 * dsc;
+            if (layer != 0 && i >= c4 && i < c4 + 4) j4[i - c4] += 1.f;
+            *reinterpret_cast<v4f*>(Ab + i * W + c4) = j4;
+        }
+    }
+}
+
 }  // namespace
+
+template <int W, bool BWD>
+hipError_t launch_eval_vec(const float* W_, const float* bias, const float* z0, const float* Z,
+                           const float* G, float* A, float* r, float* dscale, unsigned* red, int B,
+                           int L, int layer, float alpha, hipStream_t stream) {
+    using S = EvalShape<W>;
+    const long long rows = (long long)B * L;
+    const long long grid = (rows + S::ROWS_PER_WG - 1) / S::ROWS_PER_WG;
+    hipLaunchKernelGGL((layer_eval_vec<W, BWD>), dim3((unsigned)grid), dim3(256), 0, stream, W_,
+                       bias, z0, Z, G, A, r, dscale, red, B, L, layer, alpha);
+    return hipGetLastError();
+}
 
 hipError_t launch_forward_eval(const float* W, const float* bias, const float* z0,
                                const float* Z, float* A, float* r, unsigned* red,
                                int B, int L, int w, int layer, float alpha,
                                hipStream_t stream) {
+    switch (w) {
+        case 16: return launch_eval_vec<16, false>(W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, layer, alpha, stream);
+        case 32: return launch_eval_vec<32, false>(W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, layer, alpha, stream);
+        case 64: return launch_eval_vec<64, false>(W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, layer, alpha, stream);
+        case 128: return launch_eval_vec<128, false>(W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, layer, alpha, stream);
+        default: break;
+    }
     hipLaunchKernelGGL(forward_eval_kernel, dim3((unsigned)((long long)B * L)), dim3(kThreads), 0,
                        stream, W, bias, z0, Z, A, r, red, L, w, layer, alpha);
     return hipGetLastError();
 }
+
+bool backward_blocks_transposed(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
 
 hipError_t launch_initial_guess(const float* W, const float* bias, const float* z0, float* Z,
                                 int B, int L, int w, int layer, float alpha,
@@ -281,6 +377,13 @@ hipError_t launch_backward_assemble(const float* W, const float* bias, const flo
                                     const float* Z, const float* G, float* A, float* rrev,
                                     float* dscale, int B, int L, int w, int layer,
                                     float alpha, hipStream_t stream) {
+    switch (w) {
+        case 16: return launch_eval_vec<16, true>(W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, layer, alpha, stream);
+        case 32: return launch_eval_vec<32, true>(W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, layer, alpha, stream);
+        case 64: return launch_eval_vec<64, true>(W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, layer, alpha, stream);
+        case 128: return launch_eval_vec<128, true>(W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, layer, alpha, stream);
+        default: break;
+    }
     hipLaunchKernelGGL(backward_assemble_kernel, dim3((unsigned)((long long)B * L)),
                        dim3(kThreads), 0, stream, W, bias, z0, Z, G, A, rrev, dscale, L, w,
                        layer, alpha);

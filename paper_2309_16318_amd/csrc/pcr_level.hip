@@ -213,7 +213,9 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
     const float* ab = Ain.base + sg.b * Ain.bstride;
     float* Ob = Aout + (long long)sg.b * L * W * W;
 
-    float aR[S::NV], pT[S::NV], rp[S::NV];
+    // Software pipeline: the next row's block is requested before this row's
+    // results are stored, so waiting for it never waits for those stores.
+    float aR[S::NV], pT[S::NV], rp[S::NV], rn[S::NV];
     int l = sg.c + s * sg.m0;
     {
         const int lp = l - s;
@@ -225,13 +227,24 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
             lds_transpose<W>(lds, aR, i, g, pT);
         }
     }
-    for (int m = sg.m0; m <= sg.m1; ++m, l += s) {
-        load_R<W>(ab + (long long)l * Ain.rstride, Ain.trans, i, g, aR);
+    load_R<W>(ab + (long long)l * Ain.rstride, Ain.trans, i, g, aR);
+    float ri;
+    {
         const float* rrow = rb + (long long)l * rin.rstride;
-        const float ri = rrow[i];
-        float rn[S::NV];
+        ri = rrow[i];
 #pragma unroll
         for (int v = 0; v < S::NV; ++v) rn[v] = rrow[S::col(v, g)];
+    }
+    for (int m = sg.m0; m <= sg.m1; ++m, l += s) {
+        const bool more = m < sg.m1;
+        float aN[S::NV], rnN[S::NV], riN = 0.f;
+        if (more) {
+            load_R<W>(ab + (long long)(l + s) * Ain.rstride, Ain.trans, i, g, aN);
+            const float* rrow = rb + (long long)(l + s) * rin.rstride;
+            riN = rrow[i];
+#pragma unroll
+            for (int v = 0; v < S::NV; ++v) rnN[v] = rrow[S::col(v, g)];
+        }
         // r_l + A_l r_{l-s}
         float part = 0.f;
 #pragma unroll
@@ -260,20 +273,32 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
                 }
             }
         }
-        if (m < sg.m1) lds_transpose<W>(lds, aR, i, g, pT);
+        if (more) {
+            lds_transpose<W>(lds, aR, i, g, pT);
 #pragma unroll
-        for (int v = 0; v < S::NV; ++v) rp[v] = rn[v];
+            for (int v = 0; v < S::NV; ++v) {
+                aR[v] = aN[v];
+                rp[v] = rn[v];
+                rn[v] = rnN[v];
+            }
+            ri = riN;
+        }
     }
 }
 
 // ---- 4-wave workgroup per segment, w = 64 or 128 --------------------------
 template <int W>
 struct TileShape {
+    static constexpr int NT = (W == 128) ? 512 : 256;  // threads per workgroup
+    static constexpr int NWV = NT / 64;                 // waves
     static constexpr int PITCH = W + 4;
-    static constexpr int NL = W * W / 4 / 256;    // float4 loads per thread per block
-    static constexpr int TW = W / 64;             // 32x32 tiles per wave along each axis... (1 or 2)
-    static constexpr int RPT = 256 / W;           // threads per row in the mat-vec (4 or 2)
-    static constexpr int KPT = W / RPT;           // columns per thread in the mat-vec
+    static constexpr int NL = W * W / 4 / NT;           // float4 loads per thread per block
+    static constexpr int T = W / 32;                    // 32x32 tiles per side
+    static constexpr int WPR = NWV / T;                 // waves per tile row
+    static constexpr int TW_C = T / WPR;                // column tiles per wave (one row tile)
+    static constexpr int NQ = W / 8;                    // k-steps of 8 (4 per lane half)
+    static constexpr int NST = 4 * TW_C;                // float4 stores per lane per product
+    static_assert(NL <= NQ && NST <= NQ, "prefetch/stores are spread over the k-steps");
 };
 
 template <int W>
@@ -281,15 +306,15 @@ __device__ inline void load_block_regs(const float* blk, v4f* pre) {
     using S = TileShape<W>;
 #pragma unroll
     for (int p = 0; p < S::NL; ++p)
-        pre[p] = *reinterpret_cast<const v4f*>(blk + 4 * (threadIdx.x + 256 * p));
+        pre[p] = *reinterpret_cast<const v4f*>(blk + 4 * (threadIdx.x + S::NT * p));
 }
 
 template <int W>
-__device__ inline void regs_to_lds(const v4f* pre, float* buf, int trans) {
+__device__ inline void regs_to_lds(const v4f* pre, float* buf, bool trans) {
     using S = TileShape<W>;
 #pragma unroll
     for (int p = 0; p < S::NL; ++p) {
-        const int f = 4 * (threadIdx.x + 256 * p);
+        const int f = 4 * (threadIdx.x + S::NT * p);
         const int row = f / W, col = f % W;
         if (!trans) {
             *reinterpret_cast<v4f*>(buf + row * S::PITCH + col) = pre[p];
@@ -300,8 +325,75 @@ __device__ inline void regs_to_lds(const v4f* pre, float* buf, int trans) {
     }
 }
 
-template <int W>
-__global__ __launch_bounds__(256) void pcr_level_tile(
+// One row of a tile segment.  The wave owns row tile tr and column tiles
+// tc0 + bb of the product and, through the same A operands, the matching
+// rows of the mat-vec A_l r_{l-s}.  Interleaved with the MFMAs of k-step q:
+// the LDS operands of step q+1 and float4 number q of the previous row's
+// product (acc_old, when STORE); the prefetch of the next block is issued
+// at step 0.  The memory traffic of a row thus overlaps its matrix work.  PROD and
+// STORE are compile-time so that the unrolled k-loop is one basic block.
+template <int W, bool PROD, bool STORE>
+__device__ __forceinline__ void tile_row(const float* cur, const float* prv, const float* rprv,
+                                         const float* next_blk, v4f (&pre)[TileShape<W>::NL],
+                                         v16f (&acc)[TileShape<W>::TW_C],
+                                         const v16f (&acc_old)[TileShape<W>::TW_C], float* old_dst,
+                                         int tr, int tc0, int i, int h, float& part) {
+    using S = TileShape<W>;
+#pragma unroll
+    for (int bb = 0; bb < S::TW_C; ++bb) acc[bb] = v16f{};
+    part = 0.f;
+    v4f av[2], rv[2];
+    float pv[2][S::TW_C][4];
+#pragma unroll
+    for (int q = 0; q <= S::NQ; ++q) {
+        if (q < S::NQ) {
+            const int k = 8 * q + 4 * h;
+            av[q & 1] = *reinterpret_cast<const v4f*>(cur + (tr * 32 + i) * S::PITCH + k);
+            rv[q & 1] = *reinterpret_cast<const v4f*>(rprv + k);
+            if (PROD) {
+#pragma unroll
+                for (int bb = 0; bb < S::TW_C; ++bb)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        pv[q & 1][bb][e] = prv[(k + e) * S::PITCH + (tc0 + bb) * 32 + i];
+            }
+        }
+        if (q == 0) {
+#pragma unroll
+            for (int p = 0; p < S::NL; ++p)
+                pre[p] = *reinterpret_cast<const v4f*>(next_blk + 4 * (threadIdx.x + S::NT * p));
+        }
+        if (STORE && q < S::NST) {
+            const int bb = q / 4, qq = q % 4;
+            const v16f& x = acc_old[bb];
+            v4f y = {x[4 * qq], x[4 * qq + 1], x[4 * qq + 2], x[4 * qq + 3]};
+            *reinterpret_cast<v4f*>(old_dst + (tc0 + bb) * 32 + 8 * qq) = y;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (q > 0) {
+            const int qb = (q - 1) & 1;
+            if (PROD) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int bb = 0; bb < S::TW_C; ++bb)
+                        acc[bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[qb][bb][e], av[qb][e],
+                                                                       acc[bb], 0, 0, 0);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) part = fmaf(av[qb][e], rv[qb][e], part);
+        }
+    }
+    part += __shfl_xor(part, 32, 64);
+}
+
+// Chain walk with a double-buffered LDS block pair per workgroup: at the u-th
+// row of the segment cur = bufs[u&1] holds A_l and prv = bufs[(u+1)&1] holds
+// A_{l-s}; after the row, the prefetched A_{l+s} replaces prv.  Products are
+// kept in one of two accumulator sets and stored during the next row.
+template <int W, bool TRANS>
+__global__ __launch_bounds__(TileShape<W>::NT)
+__attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile(
     BlockSrc Ain, VecSrc rin, float* __restrict__ Aout, VecDst rout, int L, LevelPlan plan) {
     using S = TileShape<W>;
     __shared__ float bufs[2][W * S::PITCH];
@@ -319,92 +411,78 @@ __global__ __launch_bounds__(256) void pcr_level_tile(
     float* Ob = Aout + (long long)sg.b * L * W * W;
     const int lane = t & 63, wv = t >> 6;
     const int i = lane & 31, h = lane >> 5;
-    // output tiles of this wave: rows (TW*(wv>>1) + a)*32, cols (TW*(wv&1) + bb)*32
-    const int tr0 = S::TW * (wv >> 1), tc0 = S::TW * (wv & 1);
+    const int tr = wv / S::WPR, tc0 = (wv % S::WPR) * S::TW_C;
+    const bool writes_r = (wv % S::WPR) == 0 && h == 0;
+    const int orow_off = (tr * 32 + i) * W + 4 * h;  // this lane's place in a product block
 
-    v4f pre[S::NL];
-    float rl_pre = 0.f;
     int l = sg.c + s * sg.m0;
     {
         const int lp = l - s;
+        v4f pre[S::NL];
         if (t < W) rpv[1][t] = rb[(long long)lp * rin.rstride + t];
         if (sg.m0 >= 2) {
             load_block_regs<W>(ab + (long long)lp * Ain.rstride, pre);
-            regs_to_lds<W>(pre, bufs[1], Ain.trans);
+            regs_to_lds<W>(pre, bufs[1], TRANS);
         }
+        load_block_regs<W>(ab + (long long)l * Ain.rstride, pre);
+        regs_to_lds<W>(pre, bufs[0], TRANS);
+        if (t < W) rpv[0][t] = rb[(long long)l * rin.rstride + t];
     }
-    load_block_regs<W>(ab + (long long)l * Ain.rstride, pre);
-    if (t < W) rl_pre = rb[(long long)l * rin.rstride + t];
 
-    for (int m = sg.m0, u = 0; m <= sg.m1; ++m, ++u, l += s) {
-        float* cur = bufs[u & 1];
-        const float* prv = bufs[(u + 1) & 1];
-        const float* rprev = rpv[(u + 1) & 1];
-        regs_to_lds<W>(pre, cur, Ain.trans);
-        if (t < W) rpv[u & 1][t] = rl_pre;
+    v16f accA[S::TW_C], accB[S::TW_C];
+    float* pending = nullptr;  // destination of the product held in the "old" set
+    int m = sg.m0, u = 0;
+    auto row = [&](v16f (&an)[S::TW_C], v16f (&ao)[S::TW_C]) -> bool {
+        const float* cur = bufs[u & 1];
+        float* prv = bufs[(u + 1) & 1];
+        const float* rcur = rpv[u & 1];
+        float* rprv = rpv[(u + 1) & 1];
+        const bool more = m < sg.m1;
+        const bool prod = m >= 2;
         __syncthreads();
-        if (m < sg.m1) {
-            load_block_regs<W>(ab + (long long)(l + s) * Ain.rstride, pre);
-            if (t < W) rl_pre = rb[(long long)(l + s) * rin.rstride + t];
+        float rl_next = 0.f;
+        if (more && t < W) rl_next = rb[(long long)(l + s) * rin.rstride + t];
+        v4f pre[S::NL];
+        float part;
+        // without a next row the prefetch rereads the current block (unused)
+        const float* nb = ab + (long long)(more ? l + s : l) * Ain.rstride;
+        if (prod && pending)
+            tile_row<W, true, true>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part);
+        else if (prod)
+            tile_row<W, true, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part);
+        else
+            tile_row<W, false, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part);
+        if (writes_r) ob[(long long)l * rout.rstride + tr * 32 + i] = rcur[tr * 32 + i] + part;
+        pending = prod ? Ob + (long long)l * W * W + orow_off : nullptr;
+        __syncthreads();  // every wave is done with prv and rprv
+        if (more) {
+            regs_to_lds<W>(pre, prv, TRANS);
+            if (t < W) rprv[t] = rl_next;
         }
-        // r_l + A_l r_{l-s}: RPT threads per row, KPT columns each.
-        {
-            const int row = t / S::RPT, k0 = (t % S::RPT) * S::KPT;
-            float part = 0.f;
+        ++m;
+        ++u;
+        l += s;
+        return more;
+    };
+    bool last_in_A = true;
+    for (;;) {
+        if (!row(accA, accB)) { last_in_A = true; break; }
+        if (!row(accB, accA)) { last_in_A = false; break; }
+    }
+    if (pending) {
+        auto flush = [&](const v16f (&acc)[S::TW_C]) {
 #pragma unroll
-            for (int k = 0; k < S::KPT; k += 4) {
-                const v4f a = *reinterpret_cast<const v4f*>(cur + row * S::PITCH + k0 + k);
-                part = fmaf(a[0], rprev[k0 + k], part);
-                part = fmaf(a[1], rprev[k0 + k + 1], part);
-                part = fmaf(a[2], rprev[k0 + k + 2], part);
-                part = fmaf(a[3], rprev[k0 + k + 3], part);
+            for (int q = 0; q < S::NST; ++q) {
+                const int bb = q / 4, qq = q % 4;
+                v4f y = {acc[bb][4 * qq], acc[bb][4 * qq + 1], acc[bb][4 * qq + 2],
+                         acc[bb][4 * qq + 3]};
+                *reinterpret_cast<v4f*>(pending + (tc0 + bb) * 32 + 8 * qq) = y;
             }
-#pragma unroll
-            for (int off = 1; off < S::RPT; off <<= 1) part += __shfl_xor(part, off, 64);
-            if (t % S::RPT == 0) ob[(long long)l * rout.rstride + row] = rpv[u & 1][row] + part;
-        }
-        // A_l A_{l-s} on MFMA: D = (A P)^T tiles.
-        if (m >= 2) {
-            v16f acc[S::TW][S::TW];
-#pragma unroll
-            for (int a = 0; a < S::TW; ++a)
-#pragma unroll
-                for (int bb = 0; bb < S::TW; ++bb) acc[a][bb] = v16f{};
-#pragma unroll 2
-            for (int q = 0; q < W / 8; ++q) {
-                const int k = 8 * q + 4 * h;
-                v4f av[S::TW];
-                float pv[S::TW][4];
-#pragma unroll
-                for (int a = 0; a < S::TW; ++a)
-                    av[a] = *reinterpret_cast<const v4f*>(cur + ((tr0 + a) * 32 + i) * S::PITCH + k);
-#pragma unroll
-                for (int bb = 0; bb < S::TW; ++bb)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) pv[bb][e] = prv[(k + e) * S::PITCH + (tc0 + bb) * 32 + i];
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-#pragma unroll
-                    for (int a = 0; a < S::TW; ++a)
-#pragma unroll
-                        for (int bb = 0; bb < S::TW; ++bb)
-                            acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[bb][e], av[a][e],
-                                                                              acc[a][bb], 0, 0, 0);
-            }
-            float* cb = Ob + (long long)l * W * W;
-#pragma unroll
-            for (int a = 0; a < S::TW; ++a)
-#pragma unroll
-                for (int bb = 0; bb < S::TW; ++bb)
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const v16f& x = acc[a][bb];
-                        v4f y = {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
-                        *reinterpret_cast<v4f*>(cb + ((tr0 + a) * 32 + i) * W + (tc0 + bb) * 32 +
-                                                8 * q + 4 * h) = y;
-                    }
-        }
-        __syncthreads();
+        };
+        if (last_in_A)
+            flush(accA);
+        else
+            flush(accB);
     }
 }
 
@@ -441,12 +519,22 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
     }
     if (w == 64 || w == 128) {
         const LevelPlan p = plan_level(B, L, s, w == 64 ? 4096 : 1024, 64);
-        if (w == 64)
-            hipLaunchKernelGGL(pcr_level_tile<64>, dim3((unsigned)p.total), dim3(256), 0, stream,
-                               Ain, rin, Aout, rout, L, p);
-        else
-            hipLaunchKernelGGL(pcr_level_tile<128>, dim3((unsigned)p.total), dim3(256), 0, stream,
-                               Ain, rin, Aout, rout, L, p);
+        const dim3 grid((unsigned)p.total), block(w == 64 ? 256 : 512);
+        if (w == 64) {
+            if (Ain.trans)
+                hipLaunchKernelGGL((pcr_level_tile<64, true>), grid, block, 0, stream, Ain, rin,
+                                   Aout, rout, L, p);
+            else
+                hipLaunchKernelGGL((pcr_level_tile<64, false>), grid, block, 0, stream, Ain, rin,
+                                   Aout, rout, L, p);
+        } else {
+            if (Ain.trans)
+                hipLaunchKernelGGL((pcr_level_tile<128, true>), grid, block, 0, stream, Ain, rin,
+                                   Aout, rout, L, p);
+            else
+                hipLaunchKernelGGL((pcr_level_tile<128, false>), grid, block, 0, stream, Ain, rin,
+                                   Aout, rout, L, p);
+        }
         return hipGetLastError();
     }
     const long long rows = (long long)B * L;
