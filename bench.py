@@ -137,6 +137,23 @@ def cpu_baseline(wl, budget_s):
                       f"{el:.1f} s wall"}
 
 
+def measured_traffic(workload):
+    """HBM bytes per PCR-level launch from the committed rocprofv3 counter
+    summary of this workload (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy
+    of known size), or None if there is none or the kernel source changed
+    since the counters were taken."""
+    from paper_2309_16318_amd import pmc_traffic
+
+    fn = os.path.join(ROOT, "profiles", f"pcr_level_hbm_traffic_{workload}.json")
+    if not os.path.exists(fn):
+        return None
+    with open(fn) as f:
+        t = json.load(f)
+    if t.get("kernel_source_sha256") != pmc_traffic.kernel_source_sha256():
+        return None
+    return round(t["traffic_bytes_per_launch"])
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -177,7 +194,8 @@ def main():
         achieved = lvl["bytes"] / (lvl["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(wl.name)
+    roof["alg_bytes_per_launch"] = round(lvl["bytes"] / max(lvl["launches"], 1))
     roof["kernel"] = "pcr_level"
     roof["avg_launch_us"] = round(lvl["ms"] * 1e3 / max(lvl["launches"], 1), 3)
     roof["launches"] = lvl["launches"]
