@@ -99,7 +99,7 @@ Layout layout(int op, int B, int L, int w) {
     lo.r[1] = off; off += align_up(nr);
     lo.dscale = off;
     if (op == DEEPPCR_OP_BWD) off += align_up(nr);
-    lo.red = off; off += kAlign;
+    lo.red = off; off += align_up(2 * kRedShards * sizeof(unsigned));
     lo.total = off;
     return lo;
 }
@@ -176,21 +176,85 @@ Ws carve(void* workspace, const Layout& lo) {
     return ws;
 }
 
-// Pinned host word pair for the per-iteration convergence read-back.
+// Pinned host copy of the reduction slots for the per-iteration read-back.
 unsigned* host_words() {
     thread_local unsigned* words = nullptr;
     if (!words) {
         void* p = nullptr;
-        if (hipHostMalloc(&p, 64, hipHostMallocDefault) != hipSuccess) return nullptr;
+        if (hipHostMalloc(&p, 2 * kRedShards * sizeof(unsigned), hipHostMallocDefault) !=
+            hipSuccess)
+            return nullptr;
         words = (unsigned*)p;
     }
     return words;
+}
+
+// Max over the slots of the two reductions.
+void reduce_slots(const unsigned* hw, unsigned* mx, unsigned* mz) {
+    unsigned a = 0u, b = 0u;
+    for (int k = 0; k < kRedShards; ++k) {
+        a = hw[k] > a ? hw[k] : a;
+        b = hw[kRedShards + k] > b ? hw[kRedShards + k] : b;
+    }
+    *mx = a;
+    *mz = b;
 }
 
 float bits_to_float(unsigned u) {
     float f;
     std::memcpy(&f, &u, sizeof f);
     return f;
+}
+
+// One Newton linear solve and update with the layer evaluation fused into the
+// first PCR level and the update + reduction fused into the last level
+// (w = 16, 32).  For L <= 2 the solution is written to `x` and applied by the
+// separate update kernel.
+hipError_t newton_solve_fused(const NewtonArgs& na, int B, int L, int w, const Ws& ws,
+                              const VecDst& x, hipStream_t st) {
+    const int K = num_levels(L);
+    const double w2 = (double)w * w;
+    const long long ld = (long long)L * w;
+    {
+        // level 1 with the layers: W once, Z read twice, products and r written
+        const double na2 = (double)(L - 2 > 0 ? L - 2 : 0);
+        const double bytes = 4.0 * ((double)L * w2 + B * (na2 * w2 + 3.0 * L * w));
+        const double flops = (double)B * (L * 3.0 * w2 + (L - 1) * 2.0 * w2 + na2 * 2.0 * w2 * w);
+        const VecDst out = (K <= 1) ? x : VecDst{ws.r[0], ld, (long long)w};
+        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+            return launch_first_level_fwd(na, ws.A[0], out, B, L, w, st);
+        });
+        if (e != hipSuccess) return e;
+    }
+    if (K <= 1) {
+        const long long n = (long long)B * L * w;
+        return timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
+                     [&] { return launch_update_reduce(na.Z, x.base, n, na.red, st); });
+    }
+    BlockSrc Ain{ws.A[0], (long long)L * w * w, (long long)w * w, 0};
+    VecSrc rin{ws.r[0], ld, (long long)w};
+    int s = 2;
+    for (int k = 1; k < K; ++k, s *= 2) {
+        double bytes, flops;
+        level_work(B, L, w, s, &bytes, &flops);
+        hipError_t e;
+        if (k == K - 1) {
+            bytes += 8.0 * B * L * w;  // the iterate is read and written
+            e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+                return launch_last_level_update(Ain, rin, na, B, L, w, s, st);
+            });
+        } else {
+            float* Aout = ws.A[k & 1];
+            const VecDst rout{ws.r[k & 1], ld, (long long)w};
+            e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+                return launch_pcr_level(Ain, rin, Aout, rout, B, L, w, s, st);
+            });
+            Ain = BlockSrc{Aout, (long long)L * w * w, (long long)w * w, 0};
+            rin = VecSrc{rout.base, rout.bstride, rout.rstride};
+        }
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace
@@ -289,7 +353,24 @@ int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, floa
     }
     const long long n = (long long)B * L * w;
     const VecDst xd{ws.r[(num_levels(L) + 1) & 1], (long long)L * w, (long long)w};
+    const bool fused = fused_newton_levels(w);
+    const NewtonArgs na{W, bias, z0, Z, ws.red, layer, alpha};
     for (int k = 1; k <= max_iter; ++k) {
+        if (fused) {
+            hipError_t e = newton_solve_fused(na, B, L, w, ws, xd, st);
+            if (e != hipSuccess) return hip_fail(e, "newton_solve_fused");
+            DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
+                                   hipMemcpyDeviceToHost, st));
+            DEEPPCR_HIP(hipStreamSynchronize(st));
+            unsigned mx, mz;
+            reduce_slots(hw, &mx, &mz);
+            if (iters_out) *iters_out = k;
+            if (last_update_out) *last_update_out = bits_to_float(mx);
+            if (mx >= 0x7f800000u || mz >= 0x7f800000u) return DEEPPCR_ENONFINITE;
+            const float m = bits_to_float(mx), zmax = bits_to_float(mz);
+            if (tol > 0.f && m < tol * (zmax > 1.f ? zmax : 1.f)) return DEEPPCR_OK;
+            continue;
+        }
         // Layers, Jacobian blocks (forward order) and residuals at the iterate.
         hipError_t e = timed(DEEPPCR_KCLASS_LAYER, eval_bytes, eval_flops, st, [&] {
             return launch_forward_eval(W, bias, z0, Z, ws.A[1], ws.r[1], ws.red, B, L, w, layer,
@@ -304,9 +385,11 @@ int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, floa
         e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
                   [&] { return launch_update_reduce(Z, xd.base, n, ws.red, st); });
         if (e != hipSuccess) return hip_fail(e, "update_reduce");
-        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * sizeof(unsigned), hipMemcpyDeviceToHost, st));
+        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
+                                   hipMemcpyDeviceToHost, st));
         DEEPPCR_HIP(hipStreamSynchronize(st));
-        const unsigned mx = hw[0], mz = hw[1];
+        unsigned mx, mz;
+        reduce_slots(hw, &mx, &mz);
         if (iters_out) *iters_out = k;
         if (last_update_out) *last_update_out = bits_to_float(mx);
         if (mx >= 0x7f800000u || mz >= 0x7f800000u) return DEEPPCR_ENONFINITE;

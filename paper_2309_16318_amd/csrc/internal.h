@@ -11,6 +11,11 @@ namespace deeppcr {
 
 constexpr int kMaxWidth = 128;
 
+// The Newton convergence maxima are reduced into kRedShards slots each
+// (slot = workgroup index mod kRedShards) to keep atomic contention low; the
+// host takes the max over the slots after its one read-back per iteration.
+constexpr int kRedShards = 256;
+
 // A batch of w x w blocks addressed as base + b*bstride + m*rstride (floats).
 // Row strides may be negative (the transposed system is stored reversed).
 // trans = 1: element (i, k) of block m is stored at [k*w + i].
@@ -46,6 +51,36 @@ struct LevelPlan {
 };
 LevelPlan plan_level(int B, int L, int s, long long target_items, int n_max);
 
+// Inputs of the layer evaluation fused into the first PCR level of a Newton
+// iteration, and of the Newton update fused into the last level.
+struct NewtonArgs {
+    const float* W;      // [L, w, w]
+    const float* bias;   // [L, w]
+    const float* z0;     // [B, w]
+    float* Z;            // [B, L, w] current iterate (read by the first level,
+                         // updated by the last level)
+    unsigned* red;       // kRedShards words of max|dZ| bits, then kRedShards of max|Z|
+    int layer;
+    float alpha;
+};
+
+// Whether the fused first/last level kernels exist for width w.
+bool fused_newton_levels(int w);
+
+// First level (s = 1) of the Newton linear solve with the layers, Jacobian
+// blocks and residuals evaluated on the fly (never stored):
+//   r_l = f_l(Z_{l-1}) - Z_l, J_l = df_l at Z_{l-1};
+//   rout[l] = r_l + J_l r_{l-1} (rout[0] = r_0), Aout[l] = J_l J_{l-1} (l >= 2).
+// Also clears the 2 * kRedShards reduction words.
+hipError_t launch_first_level_fwd(const NewtonArgs& na, float* Aout, const VecDst& rout, int B,
+                                  int L, int w, hipStream_t stream);
+
+// Last level of the Newton linear solve (stride s, reading the previous
+// level's blocks and vectors) fused with the update: Z[l] += x_l for every
+// row, and atomic max of |x| and |Z| into na.red.
+hipError_t launch_last_level_update(const BlockSrc& Ain, const VecSrc& rin, const NewtonArgs& na,
+                                    int B, int L, int w, int s, hipStream_t stream);
+
 // One level (stride s) of Parallel Cyclic Reduction over B systems of L rows:
 //   rows l <  s : rout[l] = rin[l]                     (already final)
 //   rows l >= s : rout[l] = rin[l] + Ain[l] rin[l-s]
@@ -58,8 +93,8 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
 // ------------------------------------------------------------ layer kernels
 // Forward Newton step: for every (b, l) evaluate the layer at Zprev = Z[b,l-1]
 // (z0[b] for l = 0), write r[b,l] = f_l(Zprev) - Z[b,l] and, for l >= 1,
-// the Jacobian block J_l into A ([B, L, w, w], forward row order).  Block 0
-// of the grid also clears the two reduction words `red`.
+// the Jacobian block J_l into A ([B, L, w, w], forward row order).  The grid
+// also clears the 2 * kRedShards reduction words `red`.
 hipError_t launch_forward_eval(const float* W, const float* bias, const float* z0,
                                const float* Z, float* A, float* r, unsigned* red,
                                int B, int L, int w, int layer, float alpha,
@@ -70,8 +105,9 @@ hipError_t launch_initial_guess(const float* W, const float* bias, const float* 
                                 float* Z, int B, int L, int w, int layer, float alpha,
                                 hipStream_t stream);
 
-// Z += x over n floats; red[0] = max bits of |x|, red[1] = max bits of |Z|
-// (atomic max on the IEEE bit patterns of non-negative floats; NaN > Inf).
+// Z += x over n floats; red[slot] = max bits of |x|, red[kRedShards + slot]
+// = max bits of |Z| (atomic max on the IEEE bit patterns of non-negative
+// floats, which orders NaN above Inf).
 hipError_t launch_update_reduce(float* Z, const float* x, long long n, unsigned* red,
                                 hipStream_t stream);
 

@@ -46,7 +46,8 @@ __global__ __launch_bounds__(kThreads) void forward_eval_kernel(
     const int l = (int)(row % L);
     const int b = (int)(row / L);
     const int t = threadIdx.x;
-    if (row == 0 && t < 2) red[t] = 0u;
+    if (row == 0)
+        for (int k = t; k < 2 * kRedShards; k += kThreads) red[k] = 0u;
 
     __shared__ float zp[kMaxWidth];
     __shared__ float a[kMaxWidth];
@@ -127,8 +128,9 @@ __global__ __launch_bounds__(kThreads) void update_reduce_kernel(
             a = max(a, sx[i]);
             c = max(c, sz[i]);
         }
-        atomicMax(red + 0, a);
-        atomicMax(red + 1, c);
+        const int slot = blockIdx.x % kRedShards;
+        atomicMax(red + slot, a);
+        atomicMax(red + kRedShards + slot, c);
     }
 }
 
@@ -274,7 +276,8 @@ __global__ __launch_bounds__(256) void layer_eval_vec(
     using S = EvalShape<W>;
     const int t = threadIdx.x;
     const long long row = (long long)blockIdx.x * S::ROWS_PER_WG + t / S::TPB;  // b*L + l
-    if (!BWD && blockIdx.x == 0 && t < 2) red[t] = 0u;
+    if (!BWD && blockIdx.x == 0)
+        for (int k = t; k < 2 * kRedShards; k += 256) red[k] = 0u;
     if (row >= (long long)B * L) return;
     const int l = (int)(row % L);
     const int b = (int)(row / L);

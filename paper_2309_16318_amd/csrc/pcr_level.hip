@@ -159,10 +159,10 @@ struct WaveShape {
     __device__ static int col(int v, int g) { return 4 * NG * (v / 4) + 4 * g + (v % 4); }
 };
 
-template <int W>
-__device__ inline void load_R(const float* blk, int trans, int i, int g, float* out) {
+template <int W, bool TRANS>
+__device__ inline void load_R(const float* blk, int i, int g, float* out) {
     using S = WaveShape<W>;
-    if (!trans) {
+    if constexpr (!TRANS) {
 #pragma unroll
         for (int q = 0; q < S::NV / 4; ++q) {
             const v4f x = *reinterpret_cast<const v4f*>(blk + i * W + S::col(4 * q, g));
@@ -191,97 +191,251 @@ __device__ inline void lds_transpose(float* lds, const float* aR, int i, int g, 
     for (int v = 0; v < S::NV; ++v) pT[v] = lds[S::col(v, g) * S::PITCH + i];
 }
 
+// Per-wave LDS: the transpose buffer, a two-row ring of right-hand-side rows
+// (the current row's r and the previous row's r, both of the previous level),
+// and, for the fused first level, a two-row ring of iterate rows Z.
 template <int W>
-__global__ __launch_bounds__(256) void pcr_level_wave(
-    BlockSrc Ain, VecSrc rin, float* __restrict__ Aout, VecDst rout, int L, LevelPlan plan) {
+struct WaveLds {
+    float tr[W * WaveShape<W>::PITCH];
+    float r[2][W];
+    float z[2][W];
+};
+
+enum { SRC_MEM = 0, SRC_LAYER = 1 };
+
+// Layer l evaluated at zprev (a row in LDS) for lane (i, g):
+//   a_i = W_l[i, :] zprev + b_i, t = tanh a_i, d = 1 - t^2,
+//   J_l row i = c d_i W_l[i, :] (+ e_i for the residual layer), c = 1 or alpha,
+//   r_i = f_i - zcur_i with f_i = t (tanh MLP) or zprev_i + alpha t (residual).
+// w_in holds W_l[i, col(v)] (layer R) and is turned into J_l[i, col(v)].
+template <int W>
+__device__ inline float eval_layer_row(const NewtonArgs& na, int l, const float* zprev,
+                                       float zcur_i, int i, int g, float* w_in) {
     using S = WaveShape<W>;
-    __shared__ float lds_all[4][W * S::PITCH];
+    float part = 0.f;
+#pragma unroll
+    for (int q = 0; q < S::NV / 4; ++q) {
+        const v4f z4 = *reinterpret_cast<const v4f*>(zprev + S::col(4 * q, g));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) part = fmaf(w_in[4 * q + e], z4[e], part);
+    }
+#pragma unroll
+    for (int off = W; off < 64; off <<= 1) part += __shfl_xor(part, off, 64);
+    const float a = part + na.bias[(long long)l * W + i];
+    const float th = tanhf(a);
+    const float d = 1.f - th * th;
+    const bool resid = na.layer != 0;
+    const float dsc = resid ? na.alpha * d : d;
+    const float f = resid ? fmaf(na.alpha, th, zprev[i]) : th;
+#pragma unroll
+    for (int v = 0; v < S::NV; ++v) {
+        float j = dsc * w_in[v];
+        if (resid && S::col(v, g) == i) j += 1.f;
+        w_in[v] = j;
+    }
+    return f - zcur_i;
+}
+
+template <int W>
+__device__ inline void wave_umax2(unsigned& a, unsigned& b) {
+    for (int off = 32; off > 0; off >>= 1) {
+        a = max(a, (unsigned)__shfl_xor((int)a, off, 64));
+        b = max(b, (unsigned)__shfl_xor((int)b, off, 64));
+    }
+}
+
+// The chain walk of one wave.  SRC_MEM reads the previous level's blocks and
+// vectors (Ain, rin); SRC_LAYER (first level, s = 1) evaluates them from the
+// layers at the iterate.  UPD (last level) adds the solution rows to the
+// iterate and reduces max|dZ|, max|Z| instead of storing them.
+template <int W, bool TRANS, int SRC, bool UPD>
+__global__ __launch_bounds__(256) void pcr_level_wave(
+    BlockSrc Ain, VecSrc rin, float* __restrict__ Aout, VecDst rout, int L, LevelPlan plan,
+    NewtonArgs na) {
+    using S = WaveShape<W>;
+    __shared__ WaveLds<W> lds_all[4];
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
     const long long item = (long long)blockIdx.x * 4 + wv;
+    if (SRC == SRC_LAYER && blockIdx.x == 0)
+        for (int k = threadIdx.x; k < 2 * kRedShards; k += 256) na.red[k] = 0u;
     if (item >= plan.total) return;
     const Seg sg = decode_segment(item, plan, L);
     const int s = plan.s;
-    const float* rb = rin.base + sg.b * rin.bstride;
-    float* ob = rout.base + sg.b * rout.bstride;
-    if (sg.j == 0 && lane < W) ob[sg.c * rout.rstride + lane] = rb[sg.c * rin.rstride + lane];
-    if (sg.m0 > sg.count) return;
-
-    float* lds = lds_all[wv];
+    WaveLds<W>& lds = lds_all[wv];
     const int i = lane % W;
     const int g = lane / W;
-    const float* ab = Ain.base + sg.b * Ain.bstride;
-    float* Ob = Aout + (long long)sg.b * L * W * W;
+    const float* rb = rin.base + sg.b * rin.bstride;
+    float* ob = rout.base + sg.b * rout.bstride;
+    const float* zb = na.Z + (long long)sg.b * L * W;      // SRC_LAYER / UPD
+    float* zw = na.Z + (long long)sg.b * L * W;
+    const float* z0b = na.z0 + (long long)sg.b * W;
+    unsigned mx = 0u, mz = 0u;  // UPD reductions
 
-    // Software pipeline: the next row's block is requested before this row's
-    // results are stored, so waiting for it never waits for those stores.
-    float aR[S::NV], pT[S::NV], rp[S::NV], rn[S::NV];
-    int l = sg.c + s * sg.m0;
-    {
-        const int lp = l - s;
-        const float* rrow = rb + (long long)lp * rin.rstride;
-#pragma unroll
-        for (int v = 0; v < S::NV; ++v) rp[v] = rrow[S::col(v, g)];
-        if (sg.m0 >= 2) {
-            load_R<W>(ab + (long long)lp * Ain.rstride, Ain.trans, i, g, aR);
-            lds_transpose<W>(lds, aR, i, g, pT);
+    // Writes solution / next-level row l (lanes with g == 0 hold element i).
+    auto emit = [&](int l, float x) {
+        if (g != 0) return;
+        if constexpr (UPD) {
+            const long long o = (long long)l * W + i;
+            const float z = zw[o] + x;
+            zw[o] = z;
+            mx = max(mx, __float_as_uint(fabsf(x)));
+            mz = max(mz, __float_as_uint(fabsf(z)));
+        } else {
+            ob[(long long)l * rout.rstride + i] = x;
+        }
+    };
+    // row c (< s) is final: copied, or for the fused first level evaluated.
+    if (sg.j == 0) {
+        if constexpr (SRC == SRC_LAYER) {
+            // r_0 = f_0(z0) - Z_0
+            if (lane < W) lds.z[0][lane] = z0b[lane];
+            wave_sync();
+            float w_in[S::NV];
+            load_R<W, false>(na.W, i, g, w_in);
+            const float r0 = eval_layer_row<W>(na, 0, lds.z[0], zb[i], i, g, w_in);
+            emit(0, r0);
+        } else {
+            emit(sg.c, rb[sg.c * rin.rstride + i]);
         }
     }
-    load_R<W>(ab + (long long)l * Ain.rstride, Ain.trans, i, g, aR);
-    float ri;
-    {
-        const float* rrow = rb + (long long)l * rin.rstride;
-        ri = rrow[i];
-#pragma unroll
-        for (int v = 0; v < S::NV; ++v) rn[v] = rrow[S::col(v, g)];
-    }
-    for (int m = sg.m0; m <= sg.m1; ++m, l += s) {
-        const bool more = m < sg.m1;
-        float aN[S::NV], rnN[S::NV], riN = 0.f;
-        if (more) {
-            load_R<W>(ab + (long long)(l + s) * Ain.rstride, Ain.trans, i, g, aN);
-            const float* rrow = rb + (long long)(l + s) * rin.rstride;
-            riN = rrow[i];
-#pragma unroll
-            for (int v = 0; v < S::NV; ++v) rnN[v] = rrow[S::col(v, g)];
+    // With DEEP the next block (row l+s) is already in registers (aF) when
+    // row l starts and the block of row l+2s is requested: two blocks in
+    // flight per wave.
+    constexpr bool DEEP = (W == 32) && (SRC == SRC_MEM);
+    float aR[S::NV], pT[S::NV], aF[DEEP ? S::NV : 1];
+    if (sg.m0 <= sg.count) {
+        int l = sg.c + s * sg.m0;
+        if constexpr (SRC == SRC_LAYER) {
+            // rows l-1 and l of the iterate, and r_{l-1} / J_{l-1} from row l-1's layer
+            wave_sync();
+            if (lane < W) {
+                lds.z[0][lane] = zb[(long long)l * W + lane];              // Z_l
+                lds.z[1][lane] = zb[(long long)(l - 1) * W + lane];        // Z_{l-1}
+                lds.r[0][lane] = (l >= 2) ? zb[(long long)(l - 2) * W + lane] : z0b[lane];
+            }
+            wave_sync();
+            // evaluate layer l-1 at Z_{l-2} (parked in lds.r[0] for the moment)
+            float w_in[S::NV];
+            load_R<W, false>(na.W + (long long)(l - 1) * W * W, i, g, w_in);
+            const float rp = eval_layer_row<W>(na, l - 1, lds.r[0], lds.z[1][i], i, g, w_in);
+            if (sg.m0 >= 2) lds_transpose<W>(lds.tr, w_in, i, g, pT);
+            wave_sync();
+            if (g == 0) lds.r[1][i] = rp;  // r_{l-1}
+            wave_sync();
+            load_R<W, false>(na.W + (long long)l * W * W, i, g, aR);
+        } else {
+            if (lane < W) {
+                lds.r[1][lane] = rb[(long long)(l - s) * rin.rstride + lane];
+                lds.r[0][lane] = rb[(long long)l * rin.rstride + lane];
+            }
+            if (sg.m0 >= 2) {
+                load_R<W, TRANS>(Ain.base + sg.b * Ain.bstride + (long long)(l - s) * Ain.rstride, i, g, aR);
+                lds_transpose<W>(lds.tr, aR, i, g, pT);
+            }
+            load_R<W, TRANS>(Ain.base + sg.b * Ain.bstride + (long long)l * Ain.rstride, i, g, aR);
+            if (DEEP && sg.m0 < sg.m1)
+                load_R<W, TRANS>(Ain.base + sg.b * Ain.bstride + (long long)(l + s) * Ain.rstride,
+                                 i, g, aF);
+            wave_sync();
         }
-        // r_l + A_l r_{l-s}
-        float part = 0.f;
-#pragma unroll
-        for (int v = 0; v < S::NV; ++v) part = fmaf(aR[v], rp[v], part);
-#pragma unroll
-        for (int off = W; off < 64; off <<= 1) part += __shfl_xor(part, off, 64);
-        if (g == 0) ob[(long long)l * rout.rstride + i] = ri + part;
-        // A_l A_{l-s}
-        if (m >= 2) {
-            float* cb = Ob + (long long)l * W * W + i * W;
-            if constexpr (W == 16) {
-                v4f acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(pT[v], aR[v], acc, 0, 0, 0);
-                *reinterpret_cast<v4f*>(cb + S::col(0, g)) = acc;
+        const float* ab = Ain.base + sg.b * Ain.bstride;
+        float* Ob = Aout + (long long)sg.b * L * W * W;
+        for (int m = sg.m0, u = 0; m <= sg.m1; ++m, ++u, l += s) {
+            const bool more = m < sg.m1;
+            float* rcur = lds.r[u & 1];
+            float* rprev = lds.r[(u + 1) & 1];
+            float aN[S::NV];
+            float rnext = 0.f;
+            float ri;
+            if constexpr (SRC == SRC_LAYER) {
+                // this row's layer: A_l = J_l from W_l at Z_{l-1}, r_l
+                const float* zcur = lds.z[u & 1];
+                const float* zprv = lds.z[(u + 1) & 1];
+                if (more) {
+                    load_R<W, false>(na.W + (long long)(l + 1) * W * W, i, g, aN);
+                    if (lane < W) rnext = zb[(long long)(l + 1) * W + lane];  // Z_{l+1}
+                }
+                ri = eval_layer_row<W>(na, l, zprv, zcur[i], i, g, aR);
             } else {
-                v16f acc = {};
+                if constexpr (DEEP) {
+                    if (m + 1 < sg.m1) load_R<W, TRANS>(ab + (long long)(l + 2 * s) * Ain.rstride, i, g, aN);
+                } else {
+                    if (more) load_R<W, TRANS>(ab + (long long)(l + s) * Ain.rstride, i, g, aN);
+                }
+                if (more && lane < W) rnext = rb[(long long)(l + s) * rin.rstride + lane];
+                ri = rcur[i];
+            }
+            // r_l + A_l r_{l-s}
+            float part = 0.f;
 #pragma unroll
-                for (int v = 0; v < 16; ++v)
-                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(pT[v], aR[v], acc, 0, 0, 0);
+            for (int q = 0; q < S::NV / 4; ++q) {
+                const v4f rp = *reinterpret_cast<const v4f*>(rprev + S::col(4 * q, g));
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    v4f x = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
-                    *reinterpret_cast<v4f*>(cb + S::col(4 * q, g)) = x;
+                for (int e = 0; e < 4; ++e) part = fmaf(aR[4 * q + e], rp[e], part);
+            }
+#pragma unroll
+            for (int off = W; off < 64; off <<= 1) part += __shfl_xor(part, off, 64);
+            emit(l, ri + part);
+            // A_l A_{l-s}
+            if (m >= 2) {
+                if constexpr (W == 16) {
+                    float* cb = Ob + (long long)l * W * W + i * W;
+                    v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(pT[v], aR[v], acc, 0, 0, 0);
+                    *reinterpret_cast<v4f*>(cb + S::col(0, g)) = acc;
+                } else {
+                    v16f acc = {};
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(pT[v], aR[v], acc, 0, 0, 0);
+                    // Each lane holds 32-byte pieces of 16 rows; stage the block in LDS
+                    // so the global stores are contiguous 1 KiB per instruction.
+                    wave_sync();
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        v4f x = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+                        *reinterpret_cast<v4f*>(lds.tr + i * S::PITCH + S::col(4 * q, g)) = x;
+                    }
+                    wave_sync();
+                    float* blk = Ob + (long long)l * W * W;
+#pragma unroll
+                    for (int p = 0; p < 4; ++p) {
+                        const int e = 4 * (lane + 64 * p);
+                        *reinterpret_cast<v4f*>(blk + e) =
+                            *reinterpret_cast<const v4f*>(lds.tr + (e / W) * S::PITCH + e % W);
+                    }
+                }
+            }
+            if (more) {
+                lds_transpose<W>(lds.tr, aR, i, g, pT);  // begins with a wave sync
+                if constexpr (SRC == SRC_LAYER) {
+                    if (g == 0) rcur[i] = ri;                        // r_l replaces r_{l-1}...
+                    if (lane < W) lds.z[(u + 1) & 1][lane] = rnext;  // Z_{l+1} replaces Z_{l-1}
+                } else {
+                    if (lane < W) rprev[lane] = rnext;  // the ring slot of r_{l-s}
+                }
+                wave_sync();
+#pragma unroll
+                for (int v = 0; v < S::NV; ++v) {
+                    if constexpr (DEEP) {
+                        aR[v] = aF[v];
+                        aF[v] = aN[v];
+                    } else {
+                        aR[v] = aN[v];
+                    }
                 }
             }
         }
-        if (more) {
-            lds_transpose<W>(lds, aR, i, g, pT);
-#pragma unroll
-            for (int v = 0; v < S::NV; ++v) {
-                aR[v] = aN[v];
-                rp[v] = rn[v];
-                rn[v] = rnN[v];
-            }
-            ri = riN;
+    }
+    if constexpr (UPD) {
+        wave_umax2<W>(mx, mz);
+        if (lane == 0) {
+            const int slot = blockIdx.x % kRedShards;
+            atomicMax(na.red + slot, mx);
+            atomicMax(na.red + kRedShards + slot, mz);
         }
     }
 }
@@ -508,13 +662,23 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
                             hipStream_t stream) {
     if (w == 16 || w == 32) {
         const LevelPlan p = plan_level(B, L, s, 8192, 64);
-        const unsigned grid = (unsigned)((p.total + 3) / 4);
-        if (w == 16)
-            hipLaunchKernelGGL(pcr_level_wave<16>, dim3(grid), dim3(256), 0, stream, Ain, rin,
-                               Aout, rout, L, p);
-        else
-            hipLaunchKernelGGL(pcr_level_wave<32>, dim3(grid), dim3(256), 0, stream, Ain, rin,
-                               Aout, rout, L, p);
+        const dim3 g3((unsigned)((p.total + 3) / 4)), block(256);
+        const NewtonArgs na{};
+        if (w == 16) {
+            if (Ain.trans)
+                hipLaunchKernelGGL((pcr_level_wave<16, true, SRC_MEM, false>), g3, block, 0,
+                                   stream, Ain, rin, Aout, rout, L, p, na);
+            else
+                hipLaunchKernelGGL((pcr_level_wave<16, false, SRC_MEM, false>), g3, block, 0,
+                                   stream, Ain, rin, Aout, rout, L, p, na);
+        } else {
+            if (Ain.trans)
+                hipLaunchKernelGGL((pcr_level_wave<32, true, SRC_MEM, false>), g3, block, 0,
+                                   stream, Ain, rin, Aout, rout, L, p, na);
+            else
+                hipLaunchKernelGGL((pcr_level_wave<32, false, SRC_MEM, false>), g3, block, 0,
+                                   stream, Ain, rin, Aout, rout, L, p, na);
+        }
         return hipGetLastError();
     }
     if (w == 64 || w == 128) {
@@ -540,6 +704,42 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
     const long long rows = (long long)B * L;
     hipLaunchKernelGGL(pcr_level_generic, dim3((unsigned)rows), dim3(kThreads), 0, stream,
                        Ain, rin, Aout, rout, L, w, s);
+    return hipGetLastError();
+}
+
+bool fused_newton_levels(int w) { return w == 16 || w == 32; }
+
+hipError_t launch_first_level_fwd(const NewtonArgs& na, float* Aout, const VecDst& rout, int B,
+                                  int L, int w, hipStream_t stream) {
+    const LevelPlan p = plan_level(B, L, 1, 8192, 64);
+    const dim3 g3((unsigned)((p.total + 3) / 4)), block(256);
+    const BlockSrc noA{nullptr, 0, 0, 0};
+    const VecSrc nor{nullptr, 0, 0};
+    if (w == 16)
+        hipLaunchKernelGGL((pcr_level_wave<16, false, SRC_LAYER, false>), g3, block, 0, stream,
+                           noA, nor, Aout, rout, L, p, na);
+    else if (w == 32)
+        hipLaunchKernelGGL((pcr_level_wave<32, false, SRC_LAYER, false>), g3, block, 0, stream,
+                           noA, nor, Aout, rout, L, p, na);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_last_level_update(const BlockSrc& Ain, const VecSrc& rin, const NewtonArgs& na,
+                                    int B, int L, int w, int s, hipStream_t stream) {
+    const LevelPlan p = plan_level(B, L, s, 8192, 64);
+    const dim3 g3((unsigned)((p.total + 3) / 4)), block(256);
+    const VecDst noout{nullptr, 0, 0};
+    if (Ain.trans) return hipErrorInvalidValue;
+    if (w == 16)
+        hipLaunchKernelGGL((pcr_level_wave<16, false, SRC_MEM, true>), g3, block, 0, stream, Ain,
+                           rin, nullptr, noout, L, p, na);
+    else if (w == 32)
+        hipLaunchKernelGGL((pcr_level_wave<32, false, SRC_MEM, true>), g3, block, 0, stream, Ain,
+                           rin, nullptr, noout, L, p, na);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

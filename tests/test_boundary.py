@@ -38,9 +38,10 @@ def test_workspace_sizes():
     nA = B * L * w * w * 4
     nr = B * L * w * 4
     up = lambda x: (x + 255) // 256 * 256
-    assert f(deeppcr.OP_PCR, B, L, w) == 2 * up(nA) + 2 * up(nr) + 256
-    assert f(deeppcr.OP_FWD, B, L, w) == 2 * up(nA) + 2 * up(nr) + 256
-    assert f(deeppcr.OP_BWD, B, L, w) == 2 * up(nA) + 3 * up(nr) + 256
+    red = 2 * 256 * 4  # two sets of 256 reduction slots
+    assert f(deeppcr.OP_PCR, B, L, w) == 2 * up(nA) + 2 * up(nr) + red
+    assert f(deeppcr.OP_FWD, B, L, w) == 2 * up(nA) + 2 * up(nr) + red
+    assert f(deeppcr.OP_BWD, B, L, w) == 2 * up(nA) + 3 * up(nr) + red
     for bad in ((0, 1, 1), (1, 0, 1), (1, 1, 0), (1, 1, 129), (-1, 4, 4)):
         assert f(deeppcr.OP_PCR, *bad) == 0
     assert f(7, 1, 1, 1) == 0

@@ -150,7 +150,9 @@ def test_forward_residual_workload(dev):
 
 
 @pytest.mark.parametrize("w,L,B", [(1, 5, 2), (3, 40, 3), (16, 100, 2), (17, 33, 2),
-                                   (32, 64, 2), (64, 20, 2), (128, 9, 2)])
+                                   (32, 64, 2), (64, 20, 2), (128, 9, 2),
+                                   (16, 1, 3), (16, 2, 3), (16, 3, 2), (32, 1, 2), (32, 2, 5),
+                                   (32, 3, 2), (32, 5, 3), (16, 257, 4), (32, 130, 3)])
 @pytest.mark.parametrize("layer,alpha", [(0, 1.0), (1, 0.1)])
 def test_forward_shapes(dev, w, L, B, layer, alpha):
     _say(f"forward shapes w={w} L={L} B={B} layer={layer}")
@@ -163,11 +165,12 @@ def test_forward_shapes(dev, w, L, B, layer, alpha):
     assert ok and abs(res.iters - k_ref) <= 1
 
 
-def test_forward_fixed_count_and_prefix_exactness(dev):
+@pytest.mark.parametrize("w", [8, 16, 32, 64])
+def test_forward_fixed_count_and_prefix_exactness(dev, w):
     """tol = 0 runs exactly max_iter iterations; after k iterations from a
     zero start the first k rows equal the sequential pass (Eq. 3 is block
     lower-triangular)."""
-    L, w, B = 12, 8, 3
+    L, B = 12, 3
     d = synth.mlp_inputs(B, L, w, seed=41)
     ref = oracle.seq_forward(0, 1.0, d["W"], d["bias"], d["z0"])
     for k in (1, 3, 6):
