@@ -340,6 +340,22 @@ int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, floa
     if (iters_out) *iters_out = 0;
     if (last_update_out) *last_update_out = 0.f;
 
+    if (tiny_eligible(B, L, w)) {
+        // one launch for the whole solve; reads W, bias, z0 (and Z_init), writes Z
+        const double io = 4.0 * ((double)L * w * (w + 1) + B * w + 2.0 * B * L * w);
+        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, io, 0.0, st, [&] {
+            return launch_newton_tiny(W, bias, z0, Z, Z_init, B, L, w, layer, alpha, tol, max_iter,
+                                      ws.red, st);
+        });
+        if (e != hipSuccess) return hip_fail(e, "newton_tiny");
+        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 3 * sizeof(unsigned), hipMemcpyDeviceToHost, st));
+        DEEPPCR_HIP(hipStreamSynchronize(st));
+        if (iters_out) *iters_out = (int)hw[1];
+        if (last_update_out) *last_update_out = bits_to_float(hw[2]);
+        if (hw[0] == 3u) return DEEPPCR_ENONFINITE;
+        if (hw[0] == 2u) return DEEPPCR_ENOCONV;
+        return DEEPPCR_OK;
+    }
     const double w2 = (double)w * w;
     const double eval_bytes = 4.0 * B * L * (w2 + 2.0 * w);
     const double eval_flops = (double)B * L * (2.0 * w2 + w2);

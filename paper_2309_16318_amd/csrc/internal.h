@@ -135,4 +135,15 @@ hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
 hipError_t launch_copy_rows(const VecSrc& src, const VecDst& dst, int B, int L, int w,
                             hipStream_t stream);
 
+// ------------------------------------------------------------- tiny path
+// Whole Newton + PCR forward solve in one workgroup with everything in LDS,
+// for batches that fit in 64 KiB.  result[0] = status (0 ok, 2 no
+// convergence, 3 non-finite), result[1] = iterations, result[2] = bits of the
+// last max|dZ|.  Z_init may be null or alias Z.
+bool tiny_eligible(int B, int L, int w);
+size_t tiny_lds_bytes(int B, int L, int w);
+hipError_t launch_newton_tiny(const float* W, const float* bias, const float* z0, float* Z,
+                              const float* Z_init, int B, int L, int w, int layer, float alpha,
+                              float tol, int max_iter, unsigned* result, hipStream_t stream);
+
 }  // namespace deeppcr

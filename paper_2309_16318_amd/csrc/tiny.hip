@@ -1,0 +1,192 @@
+// Newton + PCR forward pass for small problems in a single workgroup
+// (Sec. 2, Eqs. 1-3; Sec. 3, Alg. 1): the iterate, the Jacobian blocks and
+// the right-hand sides live in LDS, every Newton iteration (layer and
+// Jacobian evaluation, all PCR levels, update, convergence test) runs inside
+// one launch, and the host reads back one status record.  Used when the whole
+// batch fits in 64 KiB of LDS, where a multi-kernel solve would be dominated
+// by launch and synchronisation latency.
+#include "internal.h"
+
+namespace deeppcr {
+namespace {
+
+constexpr int kThreads = 256;
+
+struct TinyLds {
+    float* Z;      // [B, L, w]
+    float* A[2];   // [B, L, w, w] ping-pong
+    float* r[2];   // [B, L, w] ping-pong
+    float* dsc;    // [B, L, w]
+    unsigned* red; // [2 * kThreads / 64]
+};
+
+__device__ inline unsigned wave_umax(unsigned v) {
+    for (int off = 32; off > 0; off >>= 1) v = max(v, (unsigned)__shfl_xor((int)v, off, 64));
+    return v;
+}
+
+// f_l and its Jacobian at the current iterate: r = f_l(Z_{l-1}) - Z_l into r,
+// J_l into A (rows l >= 1).
+__device__ void tiny_eval(const float* __restrict__ W, const float* __restrict__ bias,
+                          const float* __restrict__ z0, const TinyLds& s, float* A, float* r,
+                          int B, int L, int w, int layer, float alpha) {
+    const int n = B * L * w;
+    for (int idx = threadIdx.x; idx < n; idx += kThreads) {
+        const int i = idx % w;
+        const int bl = idx / w;
+        const int l = bl % L, b = bl / L;
+        const float* zp = (l == 0) ? z0 + b * w : s.Z + (bl - 1) * w;
+        const float* Wr = W + ((long long)l * w + i) * w;
+        float a = 0.f;
+        for (int j = 0; j < w; ++j) a = fmaf(Wr[j], zp[j], a);
+        a += bias[l * w + i];
+        const float th = tanhf(a);
+        const float d = 1.f - th * th;
+        const float f = (layer == 0) ? th : fmaf(alpha, th, zp[i]);
+        r[idx] = f - s.Z[idx];
+        s.dsc[idx] = (layer == 0) ? d : alpha * d;
+    }
+    __syncthreads();
+    const int na = B * L * w * w;
+    for (int idx = threadIdx.x; idx < na; idx += kThreads) {
+        const int j = idx % w;
+        const int i = (idx / w) % w;
+        const int bl = idx / (w * w);
+        const int l = bl % L;
+        float v = s.dsc[bl * w + i] * W[((long long)l * w + i) * w + j];
+        if (layer != 0 && i == j) v += 1.f;
+        A[idx] = v;
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(kThreads) void newton_tiny_kernel(
+    const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
+    float* __restrict__ Zout, const float* __restrict__ Z_init, int B, int L, int w, int layer,
+    float alpha, float tol, int max_iter, unsigned* __restrict__ result) {
+    extern __shared__ float smem[];
+    const int nz = B * L * w, na = nz * w;
+    TinyLds s;
+    s.Z = smem;
+    s.A[0] = s.Z + nz;
+    s.A[1] = s.A[0] + na;
+    s.r[0] = s.A[1] + na;
+    s.r[1] = s.r[0] + nz;
+    s.dsc = s.r[1] + nz;
+    s.red = reinterpret_cast<unsigned*>(s.dsc + nz);
+    const int t = threadIdx.x;
+
+    // initial guess: Z_init, or f_0(z0) in every row (App. F.2)
+    for (int idx = t; idx < nz; idx += kThreads) {
+        if (Z_init) {
+            s.Z[idx] = Z_init[idx];
+        } else {
+            const int i = idx % w, b = idx / (L * w);
+            const float* zp = z0 + b * w;
+            float a = 0.f;
+            for (int j = 0; j < w; ++j) a = fmaf(W[i * w + j], zp[j], a);
+            const float th = tanhf(a + bias[i]);
+            s.Z[idx] = (layer == 0) ? th : fmaf(alpha, th, zp[i]);
+        }
+    }
+    __syncthreads();
+
+    unsigned status = 2u;  // no convergence unless tol == 0
+    unsigned mx = 0u, iters = 0u;
+    for (int k = 1; k <= max_iter; ++k) {
+        tiny_eval(W, bias, z0, s, s.A[0], s.r[0], B, L, w, layer, alpha);
+        // PCR levels (Alg. 1): read level k-1 buffers, write level k buffers
+        int cur = 0;
+        for (int st = 1; st < L; st *= 2) {
+            const float* Ai = s.A[cur];
+            const float* ri = s.r[cur];
+            float* Ao = s.A[cur ^ 1];
+            float* ro = s.r[cur ^ 1];
+            for (int idx = t; idx < nz; idx += kThreads) {
+                const int i = idx % w, bl = idx / w, l = bl % L;
+                float v = ri[idx];
+                if (l >= st) {
+                    const float* Ar = Ai + ((long long)bl * w + i) * w;
+                    const float* rp = ri + (bl - st) * w;
+                    float acc = 0.f;
+                    for (int j = 0; j < w; ++j) acc = fmaf(Ar[j], rp[j], acc);
+                    v += acc;
+                }
+                ro[idx] = v;
+            }
+            for (int idx = t; idx < na; idx += kThreads) {
+                const int j = idx % w, i = (idx / w) % w, bl = idx / (w * w), l = bl % L;
+                if (l < 2 * st) continue;
+                const float* Ar = Ai + ((long long)bl * w + i) * w;
+                const float* Pb = Ai + (long long)(bl - st) * w * w;
+                float acc = 0.f;
+                for (int q = 0; q < w; ++q) acc = fmaf(Ar[q], Pb[q * w + j], acc);
+                Ao[idx] = acc;
+            }
+            __syncthreads();
+            cur ^= 1;
+        }
+        // update and convergence measures
+        const float* x = s.r[cur];
+        unsigned lmx = 0u, lmz = 0u;
+        for (int idx = t; idx < nz; idx += kThreads) {
+            const float z = s.Z[idx] + x[idx];
+            s.Z[idx] = z;
+            lmx = max(lmx, __float_as_uint(fabsf(x[idx])));
+            lmz = max(lmz, __float_as_uint(fabsf(z)));
+        }
+        lmx = wave_umax(lmx);
+        lmz = wave_umax(lmz);
+        if ((t & 63) == 0) {
+            s.red[2 * (t >> 6)] = lmx;
+            s.red[2 * (t >> 6) + 1] = lmz;
+        }
+        __syncthreads();
+        unsigned gmx = 0u, gmz = 0u;
+        for (int q = 0; q < kThreads / 64; ++q) {
+            gmx = max(gmx, s.red[2 * q]);
+            gmz = max(gmz, s.red[2 * q + 1]);
+        }
+        __syncthreads();
+        mx = gmx;
+        iters = (unsigned)k;
+        if (gmx >= 0x7f800000u || gmz >= 0x7f800000u) {
+            status = 3u;
+            break;
+        }
+        const float m = __uint_as_float(gmx), zmax = __uint_as_float(gmz);
+        if (tol > 0.f && m < tol * fmaxf(1.f, zmax)) {
+            status = 0u;
+            break;
+        }
+    }
+    if (tol == 0.f && status == 2u) status = 0u;
+    for (int idx = t; idx < nz; idx += kThreads) Zout[idx] = s.Z[idx];
+    if (t == 0) {
+        result[0] = status;
+        result[1] = iters;
+        result[2] = mx;
+    }
+}
+
+}  // namespace
+
+size_t tiny_lds_bytes(int B, int L, int w) {
+    const size_t nz = (size_t)B * L * w, na = nz * w;
+    return (3 * nz + 2 * na + nz) * sizeof(float) + 2 * (kThreads / 64) * sizeof(unsigned);
+}
+
+bool tiny_eligible(int B, int L, int w) {
+    return (double)B * L * w * (w + 4.0) * 4.0 <= 60000.0 && tiny_lds_bytes(B, L, w) <= 65536;
+}
+
+hipError_t launch_newton_tiny(const float* W, const float* bias, const float* z0, float* Z,
+                              const float* Z_init, int B, int L, int w, int layer, float alpha,
+                              float tol, int max_iter, unsigned* result, hipStream_t stream) {
+    const size_t lds = tiny_lds_bytes(B, L, w);
+    hipLaunchKernelGGL(newton_tiny_kernel, dim3(1), dim3(kThreads), lds, stream, W, bias, z0, Z,
+                       Z_init, B, L, w, layer, alpha, tol, max_iter, result);
+    return hipGetLastError();
+}
+
+}  // namespace deeppcr

@@ -152,7 +152,8 @@ def test_forward_residual_workload(dev):
 @pytest.mark.parametrize("w,L,B", [(1, 5, 2), (3, 40, 3), (16, 100, 2), (17, 33, 2),
                                    (32, 64, 2), (64, 20, 2), (128, 9, 2),
                                    (16, 1, 3), (16, 2, 3), (16, 3, 2), (32, 1, 2), (32, 2, 5),
-                                   (32, 3, 2), (32, 5, 3), (16, 257, 4), (32, 130, 3)])
+                                   (32, 3, 2), (32, 5, 3), (16, 257, 4), (32, 130, 3),
+                                   (4, 600, 2), (2, 3000, 1)])
 @pytest.mark.parametrize("layer,alpha", [(0, 1.0), (1, 0.1)])
 def test_forward_shapes(dev, w, L, B, layer, alpha):
     _say(f"forward shapes w={w} L={L} B={B} layer={layer}")
