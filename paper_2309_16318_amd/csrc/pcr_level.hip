@@ -486,13 +486,39 @@ __device__ inline void regs_to_lds(const v4f* pre, float* buf, bool trans) {
 // product (acc_old, when STORE); the prefetch of the next block is issued
 // at step 0.  The memory traffic of a row thus overlaps its matrix work.  PROD and
 // STORE are compile-time so that the unrolled k-loop is one basic block.
+// A 32x32 product tile in the MFMA output layout (lane (i, h) holds row i at
+// columns 8q + 4h .. +3) is written to the wave's LDS staging area with its
+// 16-byte chunks XOR-swizzled by row, and read back so that lane t holds row
+// 8p + t/8, columns 4(t%8) .. +3: each global store then covers 8 whole
+// 128-byte rows of the tile instead of 32-byte pieces of 32 rows.
+__device__ inline void stage_tile(float* stg, const v16f& acc, int i, int h, v4f (&cst)[4]) {
+    wave_sync();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        v4f x = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+        *reinterpret_cast<v4f*>(stg + i * 32 + 4 * ((2 * q + h) ^ (i & 7))) = x;
+    }
+    wave_sync();
+    const int t = threadIdx.x & 63;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const int r = 8 * p + t / 8;
+        cst[p] = *reinterpret_cast<const v4f*>(stg + r * 32 + 4 * ((t % 8) ^ (r & 7)));
+    }
+}
+
 template <int W, bool PROD, bool STORE>
 __device__ __forceinline__ void tile_row(const float* cur, const float* prv, const float* rprv,
                                          const float* next_blk, v4f (&pre)[TileShape<W>::NL],
                                          v16f (&acc)[TileShape<W>::TW_C],
                                          const v16f (&acc_old)[TileShape<W>::TW_C], float* old_dst,
-                                         int tr, int tc0, int i, int h, float& part) {
+                                         int tr, int tc0, int i, int h, float& part, float* stg) {
     using S = TileShape<W>;
+    // w = 64: the previous row's product goes out through the staging area
+    // (old_dst is then the tile's first element in the product block).
+    constexpr bool STAGED = (W == 64);
+    v4f cst[4];
+    if constexpr (STORE && STAGED) stage_tile(stg, acc_old[0], i, h, cst);
 #pragma unroll
     for (int bb = 0; bb < S::TW_C; ++bb) acc[bb] = v16f{};
     part = 0.f;
@@ -518,10 +544,15 @@ __device__ __forceinline__ void tile_row(const float* cur, const float* prv, con
                 pre[p] = *reinterpret_cast<const v4f*>(next_blk + 4 * (threadIdx.x + S::NT * p));
         }
         if (STORE && q < S::NST) {
-            const int bb = q / 4, qq = q % 4;
-            const v16f& x = acc_old[bb];
-            v4f y = {x[4 * qq], x[4 * qq + 1], x[4 * qq + 2], x[4 * qq + 3]};
-            *reinterpret_cast<v4f*>(old_dst + (tc0 + bb) * 32 + 8 * qq) = y;
+            if constexpr (STAGED) {
+                const int t = threadIdx.x & 63;
+                *reinterpret_cast<v4f*>(old_dst + (8 * q + t / 8) * W + 4 * (t % 8)) = cst[q];
+            } else {
+                const int bb = q / 4, qq = q % 4;
+                const v16f& x = acc_old[bb];
+                v4f y = {x[4 * qq], x[4 * qq + 1], x[4 * qq + 2], x[4 * qq + 3]};
+                *reinterpret_cast<v4f*>(old_dst + (tc0 + bb) * 32 + 8 * qq) = y;
+            }
         }
         __builtin_amdgcn_sched_barrier(0);
         if (q > 0) {
@@ -552,6 +583,8 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
     using S = TileShape<W>;
     __shared__ float bufs[2][W * S::PITCH];
     __shared__ float rpv[2][W];
+    constexpr bool STAGED = (W == 64);
+    __shared__ float stg_all[STAGED ? S::NWV : 1][STAGED ? 32 * 32 : 1];
     const int t = threadIdx.x;
     const long long item = blockIdx.x;
     const Seg sg = decode_segment(item, plan, L);
@@ -560,6 +593,7 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
     float* ob = rout.base + sg.b * rout.bstride;
     if (sg.j == 0 && t < W) ob[sg.c * rout.rstride + t] = rb[sg.c * rin.rstride + t];
     if (sg.m0 > sg.count) return;  // uniform over the workgroup
+    float* stg = stg_all[STAGED ? (t >> 6) : 0];
 
     const float* ab = Ain.base + sg.b * Ain.bstride;
     float* Ob = Aout + (long long)sg.b * L * W * W;
@@ -567,7 +601,8 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
     const int i = lane & 31, h = lane >> 5;
     const int tr = wv / S::WPR, tc0 = (wv % S::WPR) * S::TW_C;
     const bool writes_r = (wv % S::WPR) == 0 && h == 0;
-    const int orow_off = (tr * 32 + i) * W + 4 * h;  // this lane's place in a product block
+    // this lane's place in a product block (staged: the wave's tile origin)
+    const int orow_off = STAGED ? tr * 32 * W + tc0 * 32 : (tr * 32 + i) * W + 4 * h;
 
     int l = sg.c + s * sg.m0;
     {
@@ -601,11 +636,11 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
         // without a next row the prefetch rereads the current block (unused)
         const float* nb = ab + (long long)(more ? l + s : l) * Ain.rstride;
         if (prod && pending)
-            tile_row<W, true, true>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part);
+            tile_row<W, true, true>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part, stg);
         else if (prod)
-            tile_row<W, true, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part);
+            tile_row<W, true, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part, stg);
         else
-            tile_row<W, false, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part);
+            tile_row<W, false, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part, stg);
         if (writes_r) ob[(long long)l * rout.rstride + tr * 32 + i] = rcur[tr * 32 + i] + part;
         pending = prod ? Ob + (long long)l * W * W + orow_off : nullptr;
         __syncthreads();  // every wave is done with prv and rprv
@@ -625,12 +660,21 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
     }
     if (pending) {
         auto flush = [&](const v16f (&acc)[S::TW_C]) {
+            if constexpr (STAGED) {
+                v4f cst[4];
+                stage_tile(stg, acc[0], i, h, cst);
+                const int tl = t & 63;
 #pragma unroll
-            for (int q = 0; q < S::NST; ++q) {
-                const int bb = q / 4, qq = q % 4;
-                v4f y = {acc[bb][4 * qq], acc[bb][4 * qq + 1], acc[bb][4 * qq + 2],
-                         acc[bb][4 * qq + 3]};
-                *reinterpret_cast<v4f*>(pending + (tc0 + bb) * 32 + 8 * qq) = y;
+                for (int q = 0; q < 4; ++q)
+                    *reinterpret_cast<v4f*>(pending + (8 * q + tl / 8) * W + 4 * (tl % 8)) = cst[q];
+            } else {
+#pragma unroll
+                for (int q = 0; q < S::NST; ++q) {
+                    const int bb = q / 4, qq = q % 4;
+                    v4f y = {acc[bb][4 * qq], acc[bb][4 * qq + 1], acc[bb][4 * qq + 2],
+                             acc[bb][4 * qq + 3]};
+                    *reinterpret_cast<v4f*>(pending + (tc0 + bb) * 32 + 8 * qq) = y;
+                }
             }
         };
         if (last_in_A)
