@@ -48,12 +48,19 @@ enum {
     DEEPPCR_EWORKSPACE = 5   /* workspace_bytes below deeppcr_workspace_bytes */
 };
 
-/* Layer kinds.  TANH_MLP is the MLP layer of App. A.1 (Eq. 7) written on
- * post-activation states; TANH_RESIDUAL is a residual block with a skip of
- * length one (App. A.3). */
+/* Layer kinds: code = 2 * activation + residual.  The plain kinds are the
+ * MLP layer of App. A.1 (Eq. 7) written on post-activation states; the
+ * residual kinds are residual blocks with a skip of length one (App. A.3).
+ * The activations are those of the paper's MLP experiments (Sec. 4.1,
+ * App. C): tanh, logistic sigmoid and ReLU (whose derivative is taken as 0
+ * at 0). */
 enum {
-    DEEPPCR_TANH_MLP = 0,      /* Z_l = tanh(W_l Z_{l-1} + b_l)                 */
-    DEEPPCR_TANH_RESIDUAL = 1  /* Z_l = Z_{l-1} + alpha*tanh(W_l Z_{l-1} + b_l) */
+    DEEPPCR_TANH_MLP = 0,         /* Z_l = tanh(W_l Z_{l-1} + b_l)                    */
+    DEEPPCR_TANH_RESIDUAL = 1,    /* Z_l = Z_{l-1} + alpha*tanh(W_l Z_{l-1} + b_l)    */
+    DEEPPCR_SIGMOID_MLP = 2,      /* Z_l = sigmoid(W_l Z_{l-1} + b_l)                 */
+    DEEPPCR_SIGMOID_RESIDUAL = 3, /* Z_l = Z_{l-1} + alpha*sigmoid(W_l Z_{l-1} + b_l) */
+    DEEPPCR_RELU_MLP = 4,         /* Z_l = max(W_l Z_{l-1} + b_l, 0)                  */
+    DEEPPCR_RELU_RESIDUAL = 5     /* Z_l = Z_{l-1} + alpha*max(W_l Z_{l-1} + b_l, 0)  */
 };
 
 enum { DEEPPCR_OP_PCR = 0, DEEPPCR_OP_FWD = 1, DEEPPCR_OP_BWD = 2 };
@@ -102,8 +109,8 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x,
  *   bias  [L, w]
  *   z0    [B, w]     network input (the fixed state before layer 0)
  *   Z     [B, L, w]  output: Z[:, l] = output of layer l
- *   layer DEEPPCR_TANH_MLP or DEEPPCR_TANH_RESIDUAL; alpha is the residual
- *         branch scale (ignored for TANH_MLP)
+ *   layer one of the DEEPPCR_*_MLP / DEEPPCR_*_RESIDUAL kinds; alpha is the
+ *         residual branch scale (ignored for the plain kinds)
  *   Z_init NULL: every row starts at the first layer's output f_0(z0)
  *         (App. F.2); else [B, L, w] warm start (App. F.2).  May alias Z.
  *   tol   stop once max|dZ| < tol * max(1, max|Z|) after an update; tol = 0
@@ -125,8 +132,8 @@ int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, floa
  * Backward pass by one transposed PCR solve (App. A.2, Eqs. 10-12) for
  * Loss = sum_b <G[b], Z[b, L-1]>.  The layer Jacobians are evaluated at the
  * stored layer inputs Z[:, l-1] (Eq. 11).  With
- * d_l = 1 - tanh(W_l Z_{l-1} + b_l)^2 and c = 1 (TANH_MLP) or alpha
- * (TANH_RESIDUAL), the parameter gradients of Eq. 10 read
+ * d_l = sigma'(W_l Z_{l-1} + b_l) and c = 1 (plain layers) or alpha
+ * (residual layers), the parameter gradients of Eq. 10 read
  *   dW[l] = c * sum_b (d_l * Lambda[b,l]) Z[b,l-1]^T,  db[l] = c * sum_b d_l * Lambda[b,l].
  *   W, bias, z0  as for deeppcr_mlp_forward;  Z [B, L, w] forward states
  *   G      [B, w]     dLoss/dZ[:, L-1]

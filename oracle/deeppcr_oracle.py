@@ -12,9 +12,10 @@ dZ[:, l] / dZ[:, l-1].
 
 Functions and the passages they follow
   step, step_jacobian   App. A.1, Eqs. 7-9 (MLP layer and its Jacobian), in the
-                        post-activation form Z_l = tanh(W_l Z_{l-1} + b_l); and
-                        the residual step Z_l = Z_{l-1} + alpha*tanh(...)
-                        (App. A.3 with a skip of length 1).
+                        post-activation form Z_l = sigma(W_l Z_{l-1} + b_l),
+                        sigma in {tanh, sigmoid, ReLU}; and the residual step
+                        Z_l = Z_{l-1} + alpha*sigma(...) (App. A.3 with a skip
+                        of length 1).
   seq_forward           Sec. 2, Eq. 1: the sequence applied one step at a time;
                         it is the unique root of F(z) = 0.
   seq_solve             Sec. 3: forward substitution of the block-bidiagonal
@@ -40,8 +41,8 @@ design notes of the repository):
   * z0 is an input, so the unknowns are Z[:, 0..L-1] and J_0 couples row 0 to
     an unknown that is identically zero: J[:, 0] is ignored (treated as 0).
   * The Jacobians of the backward pass are evaluated at the stored inputs
-    Z_{l-1} of each layer (Eq. 11); tanh' is recomputed from the
-    pre-activation for both layer kinds.
+    Z_{l-1} of each layer (Eq. 11); sigma' is recomputed from the
+    pre-activation for every layer kind.  ReLU'(0) is taken as 0.
   * Parameter gradients are summed over the batch for
     Loss = sum_b <G_b, Z_{b, L-1}>.
 
@@ -53,8 +54,27 @@ from __future__ import annotations
 
 import numpy as np
 
-TANH_MLP = 0
-TANH_RESIDUAL = 1
+# layer code = 2 * activation + residual; activation 0 tanh, 1 sigmoid, 2 ReLU
+TANH_MLP, TANH_RESIDUAL, SIGMOID_MLP, SIGMOID_RESIDUAL, RELU_MLP, RELU_RESIDUAL = range(6)
+
+
+def is_residual(layer: int) -> bool:
+    return layer % 2 == 1
+
+
+def activation(layer: int, a):
+    """sigma(a) and sigma'(a) for the layer's activation (ReLU' (0) := 0)."""
+    a = _f64(a)
+    act = layer // 2
+    if act == 0:
+        t = np.tanh(a)
+        return t, 1.0 - t * t
+    if act == 1:
+        s = 1.0 / (1.0 + np.exp(-a))
+        return s, s * (1.0 - s)
+    if act == 2:
+        return np.maximum(a, 0.0), (a > 0).astype(np.float64)
+    raise ValueError(f"unknown layer kind {layer}")
 
 
 def _f64(a) -> np.ndarray:
@@ -72,29 +92,22 @@ def preactivation(W_l, b_l, z_prev):
 
 def step(layer: int, alpha: float, W_l, b_l, z_prev):
     """f_l(z_prev) for a batch of states z_prev [B, w]."""
-    t = np.tanh(preactivation(W_l, b_l, z_prev))
-    if layer == TANH_MLP:
-        return t
-    if layer == TANH_RESIDUAL:
-        return _f64(z_prev) + alpha * t
-    raise ValueError(f"unknown layer kind {layer}")
+    y, _ = activation(layer, preactivation(W_l, b_l, z_prev))
+    return _f64(z_prev) + alpha * y if is_residual(layer) else y
 
 
 def step_jacobian(layer: int, alpha: float, W_l, b_l, z_prev):
     """df_l/dz evaluated at z_prev, as explicit [B, w, w] matrices.
 
-    tanh MLP:  J = diag(1 - t^2) W_l                 (Eq. 8 with sigma = tanh)
-    residual:  J = I + alpha * diag(1 - t^2) W_l
+    plain:     J = diag(sigma'(a)) W_l               (Eq. 8)
+    residual:  J = I + alpha * diag(sigma'(a)) W_l
     """
-    t = np.tanh(preactivation(W_l, b_l, z_prev))
-    d = 1.0 - t * t
+    _, d = activation(layer, preactivation(W_l, b_l, z_prev))
     J = d[:, :, None] * _f64(W_l)[None, :, :]
-    if layer == TANH_MLP:
-        return J
-    if layer == TANH_RESIDUAL:
+    if is_residual(layer):
         w = J.shape[-1]
         return np.eye(w)[None] + alpha * J
-    raise ValueError(f"unknown layer kind {layer}")
+    return J
 
 
 def seq_forward(layer: int, alpha: float, W, bias, z0):
@@ -251,7 +264,7 @@ def seq_backward(layer: int, alpha: float, W, bias, z0, Z, G):
 
     lambda_{L-1} = G, lambda_l = J_{l+1}^T lambda_{l+1} (Eq. 11), with J_l
     evaluated at the stored layer input Z_{l-1}; dz0 = J_0^T lambda_0.
-    With d_l = 1 - tanh(W_l Z_{l-1} + b_l)^2 and c = 1 (tanh MLP) or alpha
+    With d_l = sigma'(W_l Z_{l-1} + b_l) and c = 1 (plain) or alpha
     (residual), Eq. 10 in the post-activation form reads
         dW_l = c * sum_b (d_l * lambda_l) Z_{l-1}^T,   db_l = c * sum_b d_l * lambda_l.
     Returns (Lambda [B, L, w], dz0 [B, w], dW [L, w, w], db [L, w]).
@@ -266,12 +279,12 @@ def seq_backward(layer: int, alpha: float, W, bias, z0, Z, G):
         lam[:, l] = np.einsum("bji,bj->bi", J_next, lam[:, l + 1])
     J_0 = step_jacobian(layer, alpha, W[0], bias[0], Zprev[:, 0])
     dz0 = np.einsum("bji,bj->bi", J_0, lam[:, 0])
-    c = 1.0 if layer == TANH_MLP else alpha
+    c = alpha if is_residual(layer) else 1.0
     dW = np.empty((L, w, w))
     db = np.empty((L, w))
     for l in range(L):
-        t = np.tanh(preactivation(W[l], bias[l], Zprev[:, l]))
-        g = c * (1.0 - t * t) * lam[:, l]           # dLoss / d(pre-activation)
+        _, d = activation(layer, preactivation(W[l], bias[l], Zprev[:, l]))
+        g = c * d * lam[:, l]                        # dLoss / d(pre-activation)
         dW[l] = g.T @ Zprev[:, l]
         db[l] = g.sum(axis=0)
     return lam, dz0, dW, db

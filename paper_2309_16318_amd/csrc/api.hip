@@ -320,7 +320,7 @@ int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, floa
                         const float* Z_init, void* workspace, size_t workspace_bytes,
                         int* iters_out, float* last_update_out, void* stream) {
     if (!W || !bias || !z0 || !Z || !workspace || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
-    if (layer != DEEPPCR_TANH_MLP && layer != DEEPPCR_TANH_RESIDUAL) return DEEPPCR_EINVAL;
+    if (layer < 0 || layer >= kNumLayerKinds) return DEEPPCR_EINVAL;
     if (!(tol >= 0.f) || !std::isfinite(tol) || max_iter < 1 || !std::isfinite(alpha))
         return DEEPPCR_EINVAL;
     const Layout lo = layout(DEEPPCR_OP_FWD, B, L, w);
@@ -422,7 +422,7 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
     if (!W || !bias || !z0 || !Z || !G || !Lambda || !dz0 || !dW || !db || !workspace ||
         !sizes_ok(B, L, w))
         return DEEPPCR_EINVAL;
-    if (layer != DEEPPCR_TANH_MLP && layer != DEEPPCR_TANH_RESIDUAL) return DEEPPCR_EINVAL;
+    if (layer < 0 || layer >= kNumLayerKinds) return DEEPPCR_EINVAL;
     if (!std::isfinite(alpha)) return DEEPPCR_EINVAL;
     const Layout lo = layout(DEEPPCR_OP_BWD, B, L, w);
     if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;

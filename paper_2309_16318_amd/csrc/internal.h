@@ -16,6 +16,29 @@ constexpr int kMaxWidth = 128;
 // host takes the max over the slots after its one read-back per iteration.
 constexpr int kRedShards = 256;
 
+// Layer kinds: code = 2 * activation + residual, activation 0 = tanh,
+// 1 = logistic sigmoid, 2 = ReLU (derivative 0 at 0).  The residual form is
+// f(z) = z + alpha * sigma(W z + b), the plain form f(z) = sigma(W z + b).
+constexpr int kNumLayerKinds = 6;
+__host__ __device__ inline bool layer_residual(int layer) { return (layer & 1) != 0; }
+
+// sigma(a) for the layer's activation; *d receives sigma'(a).
+__device__ inline float activate(int layer, float a, float* d) {
+    const int act = layer >> 1;
+    if (act == 0) {
+        const float t = tanhf(a);
+        *d = 1.f - t * t;
+        return t;
+    }
+    if (act == 1) {
+        const float s = 1.f / (1.f + expf(-a));
+        *d = s * (1.f - s);
+        return s;
+    }
+    *d = a > 0.f ? 1.f : 0.f;
+    return a > 0.f ? a : 0.f;
+}
+
 // A batch of w x w blocks addressed as base + b*bstride + m*rstride (floats).
 // Row strides may be negative (the transposed system is stored reversed).
 // trans = 1: element (i, k) of block m is stored at [k*w + i].

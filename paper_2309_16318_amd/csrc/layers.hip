@@ -2,10 +2,9 @@
 // the DeepPCR hot path.
 //
 // Layers (App. A.1, Eqs. 7-9, post-activation form; App. A.3 with a skip of
-// length one):
-//   TANH_MLP      : f_l(z) = tanh(W_l z + b_l),          J_l = diag(1 - t^2) W_l
-//   TANH_RESIDUAL : f_l(z) = z + alpha tanh(W_l z + b_l), J_l = I + alpha diag(1 - t^2) W_l
-// with t = tanh(W_l z + b_l).
+// length one), sigma in {tanh, logistic sigmoid, ReLU}:
+//   plain    : f_l(z) = sigma(W_l z + b_l),          J_l = diag(sigma') W_l
+//   residual : f_l(z) = z + alpha sigma(W_l z + b_l), J_l = I + alpha diag(sigma') W_l
 #include "internal.h"
 
 namespace deeppcr {
@@ -58,12 +57,13 @@ __global__ __launch_bounds__(kThreads) void forward_eval_kernel(
     const float* Wl = W + (long long)l * w * w;
     preactivations(Wl, bias + (long long)l * w, zp, a, w);
     __syncthreads();
+    const bool res = layer_residual(layer);
     for (int i = t; i < w; i += kThreads) {
-        const float th = tanhf(a[i]);
-        const float d = 1.f - th * th;
-        const float f = (layer == 0) ? th : fmaf(alpha, th, zp[i]);
+        float d;
+        const float y = activate(layer, a[i], &d);
+        const float f = res ? fmaf(alpha, y, zp[i]) : y;
         r[row * w + i] = f - Z[row * w + i];
-        dsc[i] = (layer == 0) ? d : alpha * d;
+        dsc[i] = res ? alpha * d : d;
     }
     __syncthreads();
     if (l == 0) return;
@@ -71,7 +71,7 @@ __global__ __launch_bounds__(kThreads) void forward_eval_kernel(
     for (int idx = t; idx < w * w; idx += kThreads) {
         const int i = idx / w, j = idx - (idx / w) * w;
         float v = dsc[i] * Wl[idx];
-        if (layer != 0 && i == j) v += 1.f;
+        if (res && i == j) v += 1.f;
         Ab[idx] = v;
     }
 }
@@ -91,8 +91,9 @@ __global__ __launch_bounds__(kThreads) void initial_guess_kernel(
     preactivations(W, bias, zp, a, w);
     __syncthreads();
     for (int i = t; i < w; i += kThreads) {
-        const float th = tanhf(a[i]);
-        f0[i] = (layer == 0) ? th : fmaf(alpha, th, zp[i]);
+        float d;
+        const float y = activate(layer, a[i], &d);
+        f0[i] = layer_residual(layer) ? fmaf(alpha, y, zp[i]) : y;
     }
     __syncthreads();
     const int l1 = min(L, l0 + rows_per_block);
@@ -153,10 +154,11 @@ __global__ __launch_bounds__(kThreads) void backward_assemble_kernel(
     preactivations(Wl, bias + (long long)l * w, zp, a, w);
     __syncthreads();
     const int m = L - 1 - l;  // reversed row of this layer's adjoint
+    const bool res = layer_residual(layer);
     for (int i = t; i < w; i += kThreads) {
-        const float th = tanhf(a[i]);
-        const float d = 1.f - th * th;
-        const float c = (layer == 0) ? d : alpha * d;
+        float d;
+        activate(layer, a[i], &d);
+        const float c = res ? alpha * d : d;
         dsc[i] = c;
         dscale[row * w + i] = c;
         rrev[((long long)b * L + m) * w + i] = (m == 0) ? G[(long long)b * w + i] : 0.f;
@@ -168,7 +170,7 @@ __global__ __launch_bounds__(kThreads) void backward_assemble_kernel(
     for (int idx = t; idx < w * w; idx += kThreads) {
         const int i = idx / w, k = idx - (idx / w) * w;
         float v = dsc[k] * Wl[(long long)k * w + i];
-        if (layer != 0 && i == k) v += 1.f;
+        if (res && i == k) v += 1.f;
         Ab[idx] = v;
     }
 }
@@ -186,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void dz0_kernel(
     for (int i = t; i < w; i += kThreads) {
         float acc = 0.f;
         for (int k = 0; k < w; ++k) acc = fmaf(W[(long long)k * w + i], g[k], acc);
-        dz0[(long long)b * w + i] = (layer != 0) ? lam[i] + acc : acc;
+        dz0[(long long)b * w + i] = layer_residual(layer) ? lam[i] + acc : acc;
     }
 }
 
@@ -300,14 +302,15 @@ __global__ __launch_bounds__(256) void layer_eval_vec(
 #pragma unroll
         for (int off = 1; off < S::GROUP; off <<= 1) part += __shfl_xor(part, off, 64);
         const float a = part + bias[(long long)l * W + i];
-        const float th = tanhf(a);
-        const float d = 1.f - th * th;
-        const float dsc = (layer == 0) ? d : alpha * d;
+        float d;
+        const float y = activate(layer, a, &d);
+        const bool res = layer_residual(layer);
+        const float dsc = res ? alpha * d : d;
         const bool lead = (f % S::GROUP) == 0;
         if (!BWD) {
             if (lead) {
                 const float zi = zprev[i];
-                const float fv = (layer == 0) ? th : fmaf(alpha, th, zi);
+                const float fv = res ? fmaf(alpha, y, zi) : y;
                 r[row * W + i] = fv - Z[row * W + i];
             }
         } else if (lead) {
@@ -317,7 +320,7 @@ __global__ __launch_bounds__(256) void layer_eval_vec(
         }
         if (l >= 1) {
             v4f j4 = w4 * dsc;
-            if (layer != 0 && i >= c4 && i < c4 + 4) j4[i - c4] += 1.f;
+            if (res && i >= c4 && i < c4 + 4) j4[i - c4] += 1.f;
             *reinterpret_cast<v4f*>(Ab + i * W + c4) = j4;
         }
     }

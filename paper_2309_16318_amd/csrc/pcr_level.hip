@@ -204,9 +204,9 @@ struct WaveLds {
 enum { SRC_MEM = 0, SRC_LAYER = 1 };
 
 // Layer l evaluated at zprev (a row in LDS) for lane (i, g):
-//   a_i = W_l[i, :] zprev + b_i, t = tanh a_i, d = 1 - t^2,
+//   a_i = W_l[i, :] zprev + b_i, y = sigma(a_i), d = sigma'(a_i),
 //   J_l row i = c d_i W_l[i, :] (+ e_i for the residual layer), c = 1 or alpha,
-//   r_i = f_i - zcur_i with f_i = t (tanh MLP) or zprev_i + alpha t (residual).
+//   r_i = f_i - zcur_i with f_i = y (plain) or zprev_i + alpha y (residual).
 // w_in holds W_l[i, col(v)] (layer R) and is turned into J_l[i, col(v)].
 template <int W>
 __device__ inline float eval_layer_row(const NewtonArgs& na, int l, const float* zprev,
@@ -222,11 +222,11 @@ __device__ inline float eval_layer_row(const NewtonArgs& na, int l, const float*
 #pragma unroll
     for (int off = W; off < 64; off <<= 1) part += __shfl_xor(part, off, 64);
     const float a = part + na.bias[(long long)l * W + i];
-    const float th = tanhf(a);
-    const float d = 1.f - th * th;
-    const bool resid = na.layer != 0;
+    float d;
+    const float y = activate(na.layer, a, &d);
+    const bool resid = layer_residual(na.layer);
     const float dsc = resid ? na.alpha * d : d;
-    const float f = resid ? fmaf(na.alpha, th, zprev[i]) : th;
+    const float f = resid ? fmaf(na.alpha, y, zprev[i]) : y;
 #pragma unroll
     for (int v = 0; v < S::NV; ++v) {
         float j = dsc * w_in[v];

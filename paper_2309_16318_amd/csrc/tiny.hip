@@ -40,11 +40,12 @@ __device__ void tiny_eval(const float* __restrict__ W, const float* __restrict__
         float a = 0.f;
         for (int j = 0; j < w; ++j) a = fmaf(Wr[j], zp[j], a);
         a += bias[l * w + i];
-        const float th = tanhf(a);
-        const float d = 1.f - th * th;
-        const float f = (layer == 0) ? th : fmaf(alpha, th, zp[i]);
+        float d;
+        const float y = activate(layer, a, &d);
+        const bool res = layer_residual(layer);
+        const float f = res ? fmaf(alpha, y, zp[i]) : y;
         r[idx] = f - s.Z[idx];
-        s.dsc[idx] = (layer == 0) ? d : alpha * d;
+        s.dsc[idx] = res ? alpha * d : d;
     }
     __syncthreads();
     const int na = B * L * w * w;
@@ -54,7 +55,7 @@ __device__ void tiny_eval(const float* __restrict__ W, const float* __restrict__
         const int bl = idx / (w * w);
         const int l = bl % L;
         float v = s.dsc[bl * w + i] * W[((long long)l * w + i) * w + j];
-        if (layer != 0 && i == j) v += 1.f;
+        if (layer_residual(layer) && i == j) v += 1.f;
         A[idx] = v;
     }
     __syncthreads();
@@ -85,8 +86,9 @@ __global__ __launch_bounds__(kThreads) void newton_tiny_kernel(
             const float* zp = z0 + b * w;
             float a = 0.f;
             for (int j = 0; j < w; ++j) a = fmaf(W[i * w + j], zp[j], a);
-            const float th = tanhf(a + bias[i]);
-            s.Z[idx] = (layer == 0) ? th : fmaf(alpha, th, zp[i]);
+            float d;
+            const float y = activate(layer, a + bias[i], &d);
+            s.Z[idx] = layer_residual(layer) ? fmaf(alpha, y, zp[i]) : y;
         }
     }
     __syncthreads();

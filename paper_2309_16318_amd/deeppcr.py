@@ -12,7 +12,7 @@ import os
 from dataclasses import dataclass
 
 OK, EINVAL, ENOCONV, ENONFINITE, EHIP, EWORKSPACE = range(6)
-TANH_MLP, TANH_RESIDUAL = 0, 1
+TANH_MLP, TANH_RESIDUAL, SIGMOID_MLP, SIGMOID_RESIDUAL, RELU_MLP, RELU_RESIDUAL = range(6)
 OP_PCR, OP_FWD, OP_BWD = 0, 1, 2
 KCLASS_PCR_LEVEL, KCLASS_LAYER, KCLASS_UPDATE, KCLASS_WGRAD, KCLASS_OTHER = range(5)
 KCLASS_NAMES = ("pcr_level", "layer", "update", "wgrad", "other")

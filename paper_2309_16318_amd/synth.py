@@ -17,8 +17,8 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-TANH_MLP = 0       # Z_l = tanh(W_l Z_{l-1} + b_l)
-TANH_RESIDUAL = 1  # Z_l = Z_{l-1} + alpha * tanh(W_l Z_{l-1} + b_l)
+# layer codes (2 * activation + residual; activation 0 tanh, 1 sigmoid, 2 ReLU)
+TANH_MLP, TANH_RESIDUAL, SIGMOID_MLP, SIGMOID_RESIDUAL, RELU_MLP, RELU_RESIDUAL = range(6)
 
 
 @dataclass(frozen=True)

@@ -94,7 +94,8 @@ def test_forward_rejects_invalid_arguments():
     E = deeppcr.EINVAL
     assert _fwd(W=None) == E
     assert _fwd(Z=None) == E
-    assert _fwd(layer=2) == E
+    assert _fwd(layer=6) == E
+    assert _fwd(layer=-1) == E
     assert _fwd(max_iter=0) == E
     assert _fwd(tol=-1.0) == E
     assert _fwd(tol=float("nan")) == E
@@ -124,6 +125,7 @@ def test_backward_rejects_invalid_arguments():
     p[7] = ctypes.c_void_p(P[8].value - 16)  # dW runs into db
     assert _bwd(p) == E
     assert _bwd(layer=-1) == E
+    assert _bwd(layer=6) == E
     assert _bwd(w=0) == E
     assert _bwd(alpha=float("inf")) == E
     assert _bwd(nws=1) == deeppcr.EWORKSPACE

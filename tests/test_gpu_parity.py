@@ -166,6 +166,35 @@ def test_forward_shapes(dev, w, L, B, layer, alpha):
     assert ok and abs(res.iters - k_ref) <= 1
 
 
+ALL_KINDS = [(0, 1.0), (1, 0.1), (2, 1.0), (3, 0.1), (4, 1.0), (5, 0.1)]
+
+
+@pytest.mark.parametrize("w,L,B", [(4, 30, 2), (16, 200, 3), (32, 100, 2), (64, 40, 2),
+                                   (128, 12, 2), (17, 50, 2)])
+@pytest.mark.parametrize("layer,alpha", ALL_KINDS)
+def test_forward_all_layer_kinds(dev, w, L, B, layer, alpha):
+    """tanh, sigmoid and ReLU layers, plain and residual, through every kernel
+    family (single-workgroup, fused w = 16/32, tile w = 64/128, generic)."""
+    _say(f"forward kinds w={w} L={L} B={B} layer={layer}")
+    d = synth.mlp_inputs(B, L, w, seed=700 + w + L + layer)
+    res = _forward(d, dev, layer, alpha)
+    assert res.status == deeppcr.OK
+    ref = oracle.seq_forward(layer, alpha, d["W"], d["bias"], d["z0"])
+    assert normwise_rel_err(h(res.Z), ref) <= TOL
+    _, k_ref, ok, _ = oracle.newton_forward(layer, alpha, d["W"], d["bias"], d["z0"], 1e-5, 20)
+    assert ok and abs(res.iters - k_ref) <= 1
+
+
+@pytest.mark.parametrize("w,L,B", [(4, 30, 2), (16, 200, 3), (32, 100, 2), (64, 40, 2),
+                                   (128, 12, 2), (17, 50, 2)])
+@pytest.mark.parametrize("layer,alpha", ALL_KINDS)
+def test_backward_all_layer_kinds(dev, w, L, B, layer, alpha):
+    _say(f"backward kinds w={w} L={L} B={B} layer={layer}")
+    d = synth.mlp_inputs(B, L, w, seed=800 + w + L + layer)
+    Z32 = oracle.seq_forward(layer, alpha, d["W"], d["bias"], d["z0"]).astype(np.float32)
+    _backward_check(d, Z32, dev, layer, alpha)
+
+
 @pytest.mark.parametrize("w", [8, 16, 32, 64])
 def test_forward_fixed_count_and_prefix_exactness(dev, w):
     """tol = 0 runs exactly max_iter iterations; after k iterations from a
