@@ -180,7 +180,7 @@ def main():
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
     deeppcr.profile_enable(False)
-    prof = {deeppcr.KCLASS_NAMES[c]: deeppcr.profile_read(c) for c in range(5)}
+    prof = {deeppcr.KCLASS_NAMES[c]: deeppcr.profile_read(c) for c in range(len(deeppcr.KCLASS_NAMES))}
 
     ms_step = el * 1e3 / args.steps
     value = wl.B * wl.L / (el / args.steps)

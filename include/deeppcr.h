@@ -149,6 +149,24 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Sequential passes: the layer-by-layer baseline the paper measures DeepPCR
+ * against (Sec. 4.1), on the same GPU.  Forward: Z[:, l] = f_l(Z[:, l-1]) for
+ * l = 0..L-1 (Eq. 1 applied one step at a time).  Backward: the adjoints of
+ * Eq. 11 by back substitution, Lambda[:, L-1] = G, Lambda[:, l-1] =
+ * J_l^T Lambda[:, l], dz0 = J_0^T Lambda[:, 0] (no parameter gradients).
+ * One workgroup walks the layers of one system; launch_per_layer = 0 runs all
+ * layers in one launch, 1 launches once per layer (as an eager framework's
+ * layer loop does).  Arguments as for deeppcr_mlp_forward / _backward; no
+ * workspace.
+ */
+int deeppcr_seq_forward(const float* W, const float* bias, const float* z0, float* Z,
+                        int B, int L, int w, int layer, float alpha, int launch_per_layer,
+                        void* stream);
+int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, const float* Z,
+                         const float* G, float* Lambda, float* dz0, int B, int L, int w,
+                         int layer, float alpha, int launch_per_layer, void* stream);
+
+/*
  * Instrumentation (not part of the numerical path).  While enabled, the
  * library brackets every kernel launch with HIP events on the launch's own
  * stream and records, per kernel class, the launch count, the summed device
@@ -161,7 +179,8 @@ enum {
     DEEPPCR_KCLASS_UPDATE = 2,     /* Newton update and convergence reduction  */
     DEEPPCR_KCLASS_WGRAD = 3,      /* parameter gradients                      */
     DEEPPCR_KCLASS_OTHER = 4,      /* initial guess, copies, dz0               */
-    DEEPPCR_KCLASS_COUNT = 5
+    DEEPPCR_KCLASS_SEQUENTIAL = 5, /* sequential baseline passes               */
+    DEEPPCR_KCLASS_COUNT = 6
 };
 int deeppcr_profile_enable(int on);
 void deeppcr_profile_reset(void);

@@ -158,6 +158,30 @@ hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
 hipError_t launch_copy_rows(const VecSrc& src, const VecDst& dst, int B, int L, int w,
                             hipStream_t stream);
 
+// ----------------------------------------------------------- small widths
+// w <= 8: one PCR level with a lane group per row, and the layer evaluation
+// with one thread per state element (forward and backward layouts as in
+// launch_forward_eval / launch_backward_assemble).
+bool small_width(int w);
+hipError_t launch_pcr_level_small(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
+                                  const VecDst& rout, int B, int L, int w, int s,
+                                  hipStream_t stream);
+hipError_t launch_eval_small(bool bwd, const float* W, const float* bias, const float* z0,
+                             const float* Z, const float* G, float* A, float* r, float* dscale,
+                             unsigned* red, int B, int L, int w, int layer, float alpha,
+                             hipStream_t stream);
+
+// ------------------------------------------------------- sequential passes
+// Layers l0 .. l1-1 of the sequential forward pass (one workgroup per system;
+// reads Z[:, l0-1], or z0 when l0 = 0), and the sequential adjoint pass over
+// layers l1-1 down to l0 (starting from G when l1 = L, else Lambda[:, l1-1]).
+hipError_t launch_seq_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
+                              int L, int w, int layer, float alpha, int l0, int l1,
+                              hipStream_t stream);
+hipError_t launch_seq_backward(const float* W, const float* bias, const float* z0, const float* Z,
+                               const float* G, float* Lambda, float* dz0, int B, int L, int w,
+                               int layer, float alpha, int l0, int l1, hipStream_t stream);
+
 // ------------------------------------------------------------- tiny path
 // Whole Newton + PCR forward solve in one workgroup with everything in LDS,
 // for batches that fit in 64 KiB.  result[0] = status (0 ok, 2 no

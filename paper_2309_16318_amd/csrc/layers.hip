@@ -344,6 +344,9 @@ hipError_t launch_forward_eval(const float* W, const float* bias, const float* z
                                const float* Z, float* A, float* r, unsigned* red,
                                int B, int L, int w, int layer, float alpha,
                                hipStream_t stream) {
+    if (small_width(w))
+        return launch_eval_small(false, W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, w,
+                                 layer, alpha, stream);
     switch (w) {
         case 16: return launch_eval_vec<16, false>(W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, layer, alpha, stream);
         case 32: return launch_eval_vec<32, false>(W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, layer, alpha, stream);
@@ -356,7 +359,9 @@ hipError_t launch_forward_eval(const float* W, const float* bias, const float* z
     return hipGetLastError();
 }
 
-bool backward_blocks_transposed(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
+bool backward_blocks_transposed(int w) {
+    return small_width(w) || w == 16 || w == 32 || w == 64 || w == 128;
+}
 
 hipError_t launch_initial_guess(const float* W, const float* bias, const float* z0, float* Z,
                                 int B, int L, int w, int layer, float alpha,
@@ -383,6 +388,9 @@ hipError_t launch_backward_assemble(const float* W, const float* bias, const flo
                                     const float* Z, const float* G, float* A, float* rrev,
                                     float* dscale, int B, int L, int w, int layer,
                                     float alpha, hipStream_t stream) {
+    if (small_width(w))
+        return launch_eval_small(true, W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, w,
+                                 layer, alpha, stream);
     switch (w) {
         case 16: return launch_eval_vec<16, true>(W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, layer, alpha, stream);
         case 32: return launch_eval_vec<32, true>(W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, layer, alpha, stream);

@@ -16,6 +16,7 @@
 //                segment: the current and previous blocks are staged in LDS
 //                (double buffered), each wave owns 32x32 output tiles, and the
 //                next block is prefetched into registers during the MFMAs.
+//   w <= 8       lane groups of a wave per row (small.hip).
 //   other w      generic path: one workgroup per (system, row), float32 FMA on
 //                the vector ALUs, operands staged through LDS in k-chunks.
 // Block products are formed as C^T = P^T A^T so that the MFMA output of each
@@ -745,6 +746,7 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
         }
         return hipGetLastError();
     }
+    if (small_width(w)) return launch_pcr_level_small(Ain, rin, Aout, rout, B, L, w, s, stream);
     const long long rows = (long long)B * L;
     hipLaunchKernelGGL(pcr_level_generic, dim3((unsigned)rows), dim3(kThreads), 0, stream,
                        Ain, rin, Aout, rout, L, w, s);

@@ -14,8 +14,8 @@ from dataclasses import dataclass
 OK, EINVAL, ENOCONV, ENONFINITE, EHIP, EWORKSPACE = range(6)
 TANH_MLP, TANH_RESIDUAL, SIGMOID_MLP, SIGMOID_RESIDUAL, RELU_MLP, RELU_RESIDUAL = range(6)
 OP_PCR, OP_FWD, OP_BWD = 0, 1, 2
-KCLASS_PCR_LEVEL, KCLASS_LAYER, KCLASS_UPDATE, KCLASS_WGRAD, KCLASS_OTHER = range(5)
-KCLASS_NAMES = ("pcr_level", "layer", "update", "wgrad", "other")
+KCLASS_PCR_LEVEL, KCLASS_LAYER, KCLASS_UPDATE, KCLASS_WGRAD, KCLASS_OTHER, KCLASS_SEQUENTIAL = range(6)
+KCLASS_NAMES = ("pcr_level", "layer", "update", "wgrad", "other", "sequential")
 MAX_WIDTH = 128
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdeeppcr.so")
@@ -37,6 +37,10 @@ SIGNATURES = {
     "deeppcr_mlp_backward": (_c.c_int, [_c.c_void_p] * 9 + [_c.c_int, _c.c_int, _c.c_int,
                                                            _c.c_int, _c.c_float, _c.c_void_p,
                                                            _c.c_size_t, _c.c_void_p]),
+    "deeppcr_seq_forward": (_c.c_int, [_c.c_void_p] * 4 + [_c.c_int] * 4 + [_c.c_float, _c.c_int,
+                                                                          _c.c_void_p]),
+    "deeppcr_seq_backward": (_c.c_int, [_c.c_void_p] * 7 + [_c.c_int] * 4 + [_c.c_float, _c.c_int,
+                                                                           _c.c_void_p]),
     "deeppcr_profile_enable": (_c.c_int, [_c.c_int]),
     "deeppcr_profile_reset": (None, []),
     "deeppcr_profile_read": (_c.c_int, [_c.c_int, _c.POINTER(_c.c_longlong),
@@ -190,6 +194,46 @@ def deeppcr_mlp_backward(W, bias, z0, Z, G, layer: int = TANH_MLP, alpha: float 
     if st != OK:
         raise DeepPCRError(st, "deeppcr_mlp_backward")
     return Lambda, dz0, dW, db
+
+
+def deeppcr_seq_forward(W, bias, z0, Z=None, layer: int = TANH_MLP, alpha: float = 1.0,
+                        launch_per_layer: bool = False, stream=None):
+    """Sequential layer-by-layer forward pass on the GPU (the comparison baseline)."""
+    torch = _torch()
+    L, w, _ = W.shape
+    B = z0.shape[0]
+    for t, shp, n in ((W, (L, w, w), "W"), (bias, (L, w), "bias"), (z0, (B, w), "z0")):
+        _check(t, shp, n)
+    if Z is None:
+        Z = torch.empty((B, L, w), dtype=torch.float32, device=z0.device)
+    _check(Z, (B, L, w), "Z")
+    st = lib().deeppcr_seq_forward(_ptr(W), _ptr(bias), _ptr(z0), _ptr(Z), B, L, w, int(layer),
+                                   float(alpha), int(bool(launch_per_layer)), _stream(stream))
+    if st != OK:
+        raise DeepPCRError(st, "deeppcr_seq_forward")
+    return Z
+
+
+def deeppcr_seq_backward(W, bias, z0, Z, G, layer: int = TANH_MLP, alpha: float = 1.0,
+                         Lambda=None, dz0=None, launch_per_layer: bool = False, stream=None):
+    """Sequential adjoint pass on the GPU; returns (Lambda, dz0)."""
+    torch = _torch()
+    L, w, _ = W.shape
+    B = z0.shape[0]
+    for t, shp, n in ((W, (L, w, w), "W"), (bias, (L, w), "bias"), (z0, (B, w), "z0"),
+                      (Z, (B, L, w), "Z"), (G, (B, w), "G")):
+        _check(t, shp, n)
+    dev = z0.device
+    Lambda = torch.empty((B, L, w), dtype=torch.float32, device=dev) if Lambda is None else Lambda
+    dz0 = torch.empty((B, w), dtype=torch.float32, device=dev) if dz0 is None else dz0
+    _check(Lambda, (B, L, w), "Lambda")
+    _check(dz0, (B, w), "dz0")
+    st = lib().deeppcr_seq_backward(_ptr(W), _ptr(bias), _ptr(z0), _ptr(Z), _ptr(G), _ptr(Lambda),
+                                    _ptr(dz0), B, L, w, int(layer), float(alpha),
+                                    int(bool(launch_per_layer)), _stream(stream))
+    if st != OK:
+        raise DeepPCRError(st, "deeppcr_seq_backward")
+    return Lambda, dz0
 
 
 # ---------------------------------------------------------- instrumentation

@@ -1,0 +1,138 @@
+"""Depth x width sweep: DeepPCR against the sequential pass on the same GPU.
+
+Reproduces the shape of the paper's single-pass experiment (Sec. 4.1 and
+App. C: random MLPs, forward and backward passes, timings over depth L and
+width w, break-even depth) on one MI355X.  For every (w, L):
+
+  * forward  — Newton + PCR (tolerance 1e-5, at most 20 iterations) against
+    the sequential layer loop, both as one fused launch and as one launch per
+    layer (the shape of an eager framework's loop, the paper's baseline);
+  * backward — one transposed PCR solve (adjoints only, as the sequential
+    pass computes) against the sequential adjoint loop, both launch shapes.
+
+Each timing is the minimum over `--reps` runs (the paper's statistic).
+Prints one JSON line per point (so a long run shows progress) and writes the
+whole table to `--out`.
+
+    python -m paper_2309_16318_amd.sweep --layer 0 --batch 1 --out sweep.json
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import time
+
+
+def _time_min(fn, reps, torch):
+    best = float("inf")
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        fn()
+        torch.cuda.synchronize()
+        best = min(best, time.perf_counter() - t0)
+    return best
+
+
+def run_point(w, L, B, layer, alpha, reps, dev):
+    import torch
+
+    from paper_2309_16318_amd import deeppcr, synth
+
+    d = synth.mlp_inputs(B, L, w, seed=0)
+    t = {k: torch.from_numpy(v).to(dev) for k, v in d.items()}
+    Z = torch.empty((B, L, w), dtype=torch.float32, device=dev)
+    Zs = torch.empty_like(Z)
+    lam = torch.empty_like(Z)
+    dz0 = torch.empty((B, w), dtype=torch.float32, device=dev)
+    dW = torch.empty((L, w, w), dtype=torch.float32, device=dev)
+    db = torch.empty((L, w), dtype=torch.float32, device=dev)
+    wsf = torch.empty(deeppcr.workspace_bytes(deeppcr.OP_FWD, B, L, w), dtype=torch.uint8,
+                      device=dev)
+    wsb = torch.empty(deeppcr.workspace_bytes(deeppcr.OP_BWD, B, L, w), dtype=torch.uint8,
+                      device=dev)
+    info = {}
+
+    def fwd():
+        r = deeppcr.deeppcr_mlp_forward(t["W"], t["bias"], t["z0"], Z, layer=layer, alpha=alpha,
+                                        tol=1e-5, max_iter=20, workspace=wsf)
+        info["iters"], info["status"] = r.iters, r.status
+
+    def seq_f(per_layer):
+        return lambda: deeppcr.deeppcr_seq_forward(t["W"], t["bias"], t["z0"], Zs, layer=layer,
+                                                   alpha=alpha, launch_per_layer=per_layer)
+
+    def bwd():
+        deeppcr.deeppcr_mlp_backward(t["W"], t["bias"], t["z0"], Zs, t["G"], layer=layer,
+                                     alpha=alpha, Lambda=lam, dz0=dz0, dW=dW, db=db,
+                                     workspace=wsb)
+
+    def seq_b(per_layer):
+        return lambda: deeppcr.deeppcr_seq_backward(t["W"], t["bias"], t["z0"], Zs, t["G"],
+                                                    layer=layer, alpha=alpha, Lambda=lam,
+                                                    dz0=dz0, launch_per_layer=per_layer)
+
+    out = {"w": w, "L": L, "B": B}
+    out["seq_fwd_fused_ms"] = _time_min(seq_f(False), reps, torch) * 1e3
+    out["seq_fwd_per_layer_ms"] = _time_min(seq_f(True), reps, torch) * 1e3
+    out["deeppcr_fwd_ms"] = _time_min(fwd, reps, torch) * 1e3
+    out["newton_iters"] = info["iters"]
+    out["newton_status"] = info["status"]
+    out["fwd_max_abs_diff"] = float((Z - Zs).abs().max())
+    out["seq_bwd_fused_ms"] = _time_min(seq_b(False), reps, torch) * 1e3
+    out["seq_bwd_per_layer_ms"] = _time_min(seq_b(True), reps, torch) * 1e3
+    out["deeppcr_bwd_ms"] = _time_min(bwd, reps, torch) * 1e3
+    for k in ("fwd", "bwd"):
+        out[f"{k}_speedup_vs_fused"] = out[f"seq_{k}_fused_ms"] / out[f"deeppcr_{k}_ms"]
+        out[f"{k}_speedup_vs_per_layer"] = out[f"seq_{k}_per_layer_ms"] / out[f"deeppcr_{k}_ms"]
+    return out
+
+
+def break_even(rows, key):
+    """Smallest L per w from which DeepPCR stays faster (speedup > 1)."""
+    res = {}
+    for w in sorted({r["w"] for r in rows}):
+        pts = sorted((r for r in rows if r["w"] == w), key=lambda r: r["L"])
+        be = None
+        for i, r in enumerate(pts):
+            if all(p[key] > 1.0 for p in pts[i:]):
+                be = r["L"]
+                break
+        res[w] = be
+    return res
+
+
+def main():
+    import torch
+
+    p = argparse.ArgumentParser()
+    p.add_argument("--layer", type=int, default=0)
+    p.add_argument("--alpha", type=float, default=1.0)
+    p.add_argument("--batch", type=int, default=1)
+    p.add_argument("--widths", default="2,4,8,16,32,64,128")
+    p.add_argument("--depths", default=",".join(str(2 ** k) for k in range(1, 15)))
+    p.add_argument("--reps", type=int, default=3)
+    p.add_argument("--out", required=True)
+    a = p.parse_args()
+    dev = torch.device("cuda:0")
+    rows = []
+    for w in [int(x) for x in a.widths.split(",")]:
+        for L in [int(x) for x in a.depths.split(",")]:
+            r = run_point(w, L, a.batch, a.layer, a.alpha, a.reps, dev)
+            rows.append(r)
+            print(json.dumps(r), flush=True)
+    summary = {"layer": a.layer, "alpha": a.alpha, "batch": a.batch, "reps": a.reps,
+               "break_even_L": {k: break_even(rows, k) for k in
+                                ("fwd_speedup_vs_fused", "fwd_speedup_vs_per_layer",
+                                 "bwd_speedup_vs_fused", "bwd_speedup_vs_per_layer")},
+               "max_speedup": {k: max(r[k] for r in rows) for k in
+                               ("fwd_speedup_vs_fused", "fwd_speedup_vs_per_layer",
+                                "bwd_speedup_vs_fused", "bwd_speedup_vs_per_layer")},
+               "points": rows}
+    with open(a.out, "w") as f:
+        json.dump(summary, f, indent=1)
+    print(json.dumps({k: v for k, v in summary.items() if k != "points"}), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -141,3 +141,17 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(deeppcr, "LIB_PATH", str(tmp_path / "nope.so"))
     with pytest.raises(RuntimeError, match="missing"):
         deeppcr.lib()
+
+
+def test_sequential_passes_reject_invalid_arguments():
+    E = deeppcr.EINVAL
+    f = deeppcr.lib().deeppcr_seq_forward
+    assert f(None, P[1], P[2], P[3], 2, 8, 4, 0, 1.0, 0, None) == E
+    assert f(P[0], P[1], P[2], P[3], 2, 8, 0, 0, 1.0, 0, None) == E
+    assert f(P[0], P[1], P[2], P[3], 2, 8, 4, 6, 1.0, 0, None) == E
+    assert f(P[0], P[1], P[2], P[3], 2, 8, 4, 0, 1.0, 2, None) == E
+    assert f(P[0], P[1], P[2], ctypes.c_void_p(P[0].value + 4), 2, 8, 4, 0, 1.0, 0, None) == E
+    g = deeppcr.lib().deeppcr_seq_backward
+    assert g(*P[:6], None, 2, 8, 4, 0, 1.0, 0, None) == E
+    assert g(*P[:7], 2, 8, 4, -1, 1.0, 0, None) == E
+    assert g(*P[:5], P[3], P[6], 2, 8, 4, 0, 1.0, 0, None) == E   # Lambda over Z

@@ -317,3 +317,22 @@ def test_workspace_too_small_is_rejected(dev):
     ws = torch.empty(16, dtype=torch.uint8, device=dev)
     with pytest.raises(deeppcr.DeepPCRError, match="workspace"):
         deeppcr.pcr_solve_block_bidiag(g(d["J"], dev), g(d["r"], dev), workspace=ws)
+
+
+# ------------------------------------------------------- sequential baseline
+@pytest.mark.parametrize("w,L,B", [(4, 50, 3), (16, 300, 2), (33, 40, 2), (128, 20, 2)])
+@pytest.mark.parametrize("layer,alpha", [(0, 1.0), (3, 0.1), (4, 1.0)])
+@pytest.mark.parametrize("per_layer", [False, True])
+def test_sequential_passes(dev, w, L, B, layer, alpha, per_layer):
+    _say(f"sequential w={w} L={L} B={B} layer={layer} per_layer={per_layer}")
+    d = synth.mlp_inputs(B, L, w, seed=900 + w + L)
+    t = {k: g(v, dev) for k, v in d.items()}
+    Z = deeppcr.deeppcr_seq_forward(t["W"], t["bias"], t["z0"], layer=layer, alpha=alpha,
+                                    launch_per_layer=per_layer)
+    ref = oracle.seq_forward(layer, alpha, d["W"], d["bias"], d["z0"])
+    assert normwise_rel_err(h(Z), ref) <= TOL
+    Z32 = ref.astype(np.float32)
+    lam, dz0 = deeppcr.deeppcr_seq_backward(t["W"], t["bias"], t["z0"], g(Z32, dev), t["G"],
+                                            layer=layer, alpha=alpha, launch_per_layer=per_layer)
+    rl, rz, _, _ = oracle.seq_backward(layer, alpha, d["W"], d["bias"], d["z0"], Z32, d["G"])
+    assert adjoint_err(h(lam), h(dz0), rl, rz) <= TOL
