@@ -8,5 +8,6 @@ from .deeppcr_oracle import (  # noqa: F401
     is_residual, activation, step, step_jacobian, preactivation, seq_forward,
     layer_inputs, all_jacobians, all_steps, seq_solve, pcr_solve,
     reversed_transposed_system, num_levels, initial_guess, newton_forward,
+    residual_norm, newton_forward_residual,
     seq_backward, loss,
 )

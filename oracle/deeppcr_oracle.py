@@ -27,6 +27,10 @@ Functions and the passages they follow
   newton_forward        Sec. 2, Eqs. 2-3: Newton on F with the linear system
                         solved by seq_solve (or pcr_solve); initial guess of
                         App. F.2 (every row set to the first layer's output).
+  newton_forward_residual
+                        the same iteration stopped by the residual rule of the
+                        solver-parameter table of App. F.1 (absolute and
+                        relative infinity-norm thresholds on F(z^k)).
   seq_backward          App. A.2, Eqs. 10-12: adjoints by back substitution and
                         the parameter gradients.
 
@@ -43,6 +47,10 @@ design notes of the repository):
   * The Jacobians of the backward pass are evaluated at the stored inputs
     Z_{l-1} of each layer (Eq. 11); sigma' is recomputed from the
     pre-activation for every layer kind.  ReLU'(0) is taken as 0.
+  * Residual stopping rule: the table gives an absolute and a relative
+    threshold without saying how they combine; either one met stops the
+    iteration (res <= atol or res <= rtol * res_0), checked on the iterate
+    before each solve, and the iteration count is the number of solves.
   * Parameter gradients are summed over the batch for
     Loss = sum_b <G_b, Z_{b, L-1}>.
 
@@ -254,6 +262,45 @@ def newton_forward(layer: int, alpha: float, W, bias, z0, tol: float, max_iter: 
             return Z, k, True, history
     return Z, max_iter, tol == 0, history
 
+
+
+def residual_norm(layer: int, alpha: float, W, bias, z0, Z) -> float:
+    """max |F(Z)| with F_l = f_l(Z_{l-1}) - Z_l: the infinity norm of the
+    Newton solver's residual (Eq. 1 at the iterate)."""
+    W, bias, z0, Z = _f64(W), _f64(bias), _f64(z0), _f64(Z)
+    F = all_steps(layer, alpha, W, bias, layer_inputs(Z, z0)) - Z
+    return float(np.max(np.abs(F))) if F.size else 0.0
+
+
+def newton_forward_residual(layer: int, alpha: float, W, bias, z0, atol: float, rtol: float,
+                            max_iter: int, Z_init=None, solve=seq_solve):
+    """Newton on F(z) = 0 with the residual-based stopping rule of the
+    solver-parameter table (App. F.1): the infinity norm of the residual
+    F(z^k) is compared with an absolute threshold and with a threshold
+    relative to the first iterate's residual norm.
+
+    At k = 0, 1, ...: res_k = max|F(z^k)|; stop with z^k when
+    res_k <= atol or res_k <= rtol * res_0 (either criterion suffices);
+    otherwise, if k == max_iter, stop without convergence; otherwise solve
+    Eq. 3 for dz^k and set z^{k+1} = z^k + dz^k.
+
+    Returns (Z, solves, converged, [res_0, res_1, ...]).
+    """
+    W, bias, z0 = _f64(W), _f64(bias), _f64(z0)
+    Z = initial_guess(layer, alpha, W, bias, z0) if Z_init is None else _f64(Z_init).copy()
+    history = []
+    for k in range(max_iter + 1):
+        Zprev = layer_inputs(Z, z0)
+        F = all_steps(layer, alpha, W, bias, Zprev) - Z
+        res = float(np.max(np.abs(F))) if F.size else 0.0
+        history.append(res)
+        if res <= atol or res <= rtol * history[0]:
+            return Z, k, True, history
+        if k == max_iter:
+            break
+        J = all_jacobians(layer, alpha, W, bias, Zprev)
+        Z = Z + solve(J, F)
+    return Z, max_iter, False, history
 
 # ----------------------------------------------------------------------------
 # Backward pass (App. A.2, Eqs. 10-12)

@@ -334,6 +334,99 @@ def test_newton_zero_weights_converges_in_one_step():
     np.testing.assert_allclose(Z[0], np.tanh(b), rtol=1e-15)
 
 
+
+# --------------------------------------------------------------------------
+# Residual-based stopping rule (solver-parameter table of App. F.1)
+# --------------------------------------------------------------------------
+
+def _residual_by_steps(layer, alpha, W, b, z0, Z):
+    """max |f_l(Z_{l-1}) - Z_l| layer by layer through the pinned step()."""
+    W, b, z0, Z = (np.asarray(a, dtype=np.float64) for a in (W, b, z0, Z))
+    m, zp = 0.0, z0
+    for l in range(W.shape[0]):
+        m = max(m, float(np.max(np.abs(oracle.step(layer, alpha, W[l], b[l], zp) - Z[:, l]))))
+        zp = Z[:, l]
+    return m
+
+
+def test_residual_norm_by_hand():
+    # L = 2, w = 1, tanh MLP: F_0 = tanh(2*0.5 + 0.25) - 0.3, F_1 = tanh(-1*0.3 + 0) - 0.1
+    W = np.array([[[2.0]], [[-1.0]]])
+    b = np.array([[0.25], [0.0]])
+    z0 = np.array([[0.5]])
+    Z = np.array([[[0.3], [0.1]]])
+    want = max(abs(np.tanh(1.25) - 0.3), abs(np.tanh(-0.3) - 0.1))
+    assert oracle.residual_norm(0, 1.0, W, b, z0, Z) == pytest.approx(want, rel=1e-15)
+    # residual layer: F_l = Z_{l-1} + alpha tanh(.) - Z_l
+    want_r = max(abs(0.5 + 0.1 * np.tanh(1.25) - 0.3), abs(0.3 + 0.1 * np.tanh(-0.3) - 0.1))
+    assert oracle.residual_norm(1, 0.1, W, b, z0, Z) == pytest.approx(want_r, rel=1e-15)
+
+
+@pytest.mark.parametrize("layer,alpha", LAYER_KINDS)
+@pytest.mark.parametrize("atol,rtol", [(1e-6, 0.0), (0.0, 1e-3), (1e-4, 1e-4)])
+def test_newton_residual_rule_stops_at_first_iterate_below_threshold(layer, alpha, atol, rtol):
+    """The returned iterate is the first of the plain Newton sequence (the
+    fixed-count iterates of newton_forward) whose residual, evaluated layer
+    by layer, meets either threshold."""
+    B, L, w = 2, 33, 6
+    d = synth.mlp_inputs(B, L, w, seed=41)
+    W, b, z0 = d["W"], d["bias"], d["z0"]
+    Z, k, ok, hist = oracle.newton_forward_residual(layer, alpha, W, b, z0, atol, rtol, 40)
+    assert ok and len(hist) == k + 1
+    res0 = _residual_by_steps(layer, alpha, W, b, z0, oracle.initial_guess(layer, alpha, *(
+        np.asarray(a, dtype=np.float64) for a in (W, b, z0))))
+    for j in range(k + 1):
+        if j == 0:
+            Zj = oracle.initial_guess(layer, alpha, *(np.asarray(a, dtype=np.float64)
+                                                      for a in (W, b, z0)))
+        else:
+            Zj, _, _, _ = oracle.newton_forward(layer, alpha, W, b, z0, 0.0, j)
+        rj = _residual_by_steps(layer, alpha, W, b, z0, Zj)
+        assert hist[j] == pytest.approx(rj, rel=1e-9, abs=1e-300)
+        met = rj <= atol or rj <= rtol * res0
+        assert met == (j == k), (j, rj)
+    np.testing.assert_array_equal(Z, Zj)
+
+
+def test_newton_residual_rule_zero_iterations():
+    wl = synth.WORKLOADS["tiny_fwd"]
+    d = synth.mlp_inputs(wl.B, wl.L, wl.w, wl.seed)
+    W, b, z0 = (d[k].astype(np.float64) for k in ("W", "bias", "z0"))
+    Z, k, ok, hist = oracle.newton_forward_residual(0, 1.0, W, b, z0, 1e9, 0.0, 5)
+    assert (k, ok) == (0, True)
+    np.testing.assert_array_equal(Z, oracle.initial_guess(0, 1.0, W, b, z0))
+    # a warm start at the root: residual below a tight absolute threshold at once
+    ref = oracle.seq_forward(0, 1.0, W, b, z0)
+    Z, k, ok, hist = oracle.newton_forward_residual(0, 1.0, W, b, z0, 1e-14, 0.0, 5, Z_init=ref)
+    assert (k, ok) == (0, True) and hist[0] < 1e-15
+    np.testing.assert_array_equal(Z, ref)
+
+
+def test_newton_residual_rule_exact_zero_residual():
+    """Zero weights and a zero start: one Newton step lands on the root
+    exactly (Z = 0 + tanh(b)), whose residual is exactly 0, which meets a
+    threshold of 0 (the rule is <=)."""
+    L, w = 7, 3
+    rng = np.random.default_rng(3)
+    W = np.zeros((L, w, w))
+    b = rng.standard_normal((L, w))
+    z0 = rng.standard_normal((1, w))
+    Z, k, ok, hist = oracle.newton_forward_residual(0, 1.0, W, b, z0, 0.0, 0.0, 4,
+                                                    Z_init=np.zeros((1, L, w)))
+    assert (k, ok) == (1, True) and hist[0] > 0.0 and hist[1] == 0.0
+    np.testing.assert_array_equal(Z[0], np.tanh(b))
+
+
+def test_newton_residual_rule_max_iter():
+    B, L, w = 1, 40, 5
+    d = synth.mlp_inputs(B, L, w, seed=8)
+    W, b, z0 = d["W"], d["bias"], d["z0"]
+    Z, k, ok, hist = oracle.newton_forward_residual(0, 1.0, W, b, z0, 0.0, 0.0, 3)
+    assert (k, ok) == (3, False) and len(hist) == 4
+    Z3, _, _, _ = oracle.newton_forward(0, 1.0, W, b, z0, 0.0, 3)
+    np.testing.assert_array_equal(Z, Z3)
+    assert hist[3] == pytest.approx(_residual_by_steps(0, 1.0, W, b, z0, Z3), rel=1e-9)
+
 # --------------------------------------------------------------------------
 # Backward pass
 # --------------------------------------------------------------------------
