@@ -20,7 +20,7 @@
  *   - All GPU work is enqueued on `stream` (a hipStream_t passed as void*;
  *     NULL is the default stream).  pcr_solve_block_bidiag and
  *     deeppcr_mlp_backward return without waiting for the GPU;
- *     deeppcr_mlp_forward waits once per Newton iteration to read its
+ *     the two forward entry points wait once per Newton iteration to read their
  *     convergence measure.
  *   - Host out-parameters are plain host pointers.
  *   - Arguments are validated before any HIP call: an invalid argument returns
@@ -127,6 +127,31 @@ int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, floa
                         float tol, int max_iter, const float* Z_init,
                         void* workspace, size_t workspace_bytes,
                         int* iters_out, float* last_update_out, void* stream);
+
+/*
+ * Forward pass by Newton + PCR with the residual stopping rule of the
+ * paper's Newton-solver parameter table (App. F.1): the infinity norm of the
+ * residual F(z^k) = [f_l(Z_{l-1}) - Z_l]_l of Eq. 1 at iterate z^k is tested
+ * against an absolute threshold and against a threshold relative to the
+ * first iterate's residual norm.  For k = 0, 1, ...: the layers are
+ * evaluated at z^k and res_k = max|F(z^k)| is reduced on the fly; the
+ * iteration stops with Z = z^k when res_k <= atol or res_k <= rtol * res_0
+ * (either one suffices), stops with DEEPPCR_ENOCONV when k = max_iter, and
+ * otherwise solves Eq. 3 by PCR and sets z^{k+1} = z^k + dz^k.  (The paper's
+ * defaults for forward passes: atol = rtol = 1e-4, max_iter = 15.)
+ *   W, bias, z0, Z, layer, alpha, Z_init, workspace  as for deeppcr_mlp_forward
+ *   atol, rtol  >= 0 and finite (0 disables the criterion)
+ *   max_iter    >= 0: at most this many PCR solves (0 only tests the start)
+ *   iters_out    (host, may be NULL) number of PCR solves performed
+ *   residual_out (host, may be NULL) res_k of the returned iterate
+ * Returns DEEPPCR_ENONFINITE if the residual is NaN/Inf (Z holds that
+ * iterate).  Waits for the GPU once per iteration, after the evaluation.
+ */
+int deeppcr_mlp_forward_residual(const float* W, const float* bias, const float* z0, float* Z,
+                                 int B, int L, int w, int layer, float alpha,
+                                 float atol, float rtol, int max_iter, const float* Z_init,
+                                 void* workspace, size_t workspace_bytes,
+                                 int* iters_out, float* residual_out, void* stream);
 
 /*
  * Backward pass by one transposed PCR solve (App. A.2, Eqs. 10-12) for

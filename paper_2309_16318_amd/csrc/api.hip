@@ -99,7 +99,7 @@ Layout layout(int op, int B, int L, int w) {
     lo.r[1] = off; off += align_up(nr);
     lo.dscale = off;
     if (op == DEEPPCR_OP_BWD) off += align_up(nr);
-    lo.red = off; off += align_up(2 * kRedShards * sizeof(unsigned));
+    lo.red = off; off += align_up(kRedWords * sizeof(unsigned));
     lo.total = off;
     return lo;
 }
@@ -176,28 +176,23 @@ Ws carve(void* workspace, const Layout& lo) {
     return ws;
 }
 
-// Pinned host copy of the reduction slots for the per-iteration read-back.
+// Pinned host copy of the reduction area for the per-iteration read-back.
 unsigned* host_words() {
     thread_local unsigned* words = nullptr;
     if (!words) {
         void* p = nullptr;
-        if (hipHostMalloc(&p, 2 * kRedShards * sizeof(unsigned), hipHostMallocDefault) !=
-            hipSuccess)
+        if (hipHostMalloc(&p, kRedWords * sizeof(unsigned), hipHostMallocDefault) != hipSuccess)
             return nullptr;
         words = (unsigned*)p;
     }
     return words;
 }
 
-// Max over the slots of the two reductions.
-void reduce_slots(const unsigned* hw, unsigned* mx, unsigned* mz) {
-    unsigned a = 0u, b = 0u;
-    for (int k = 0; k < kRedShards; ++k) {
-        a = hw[k] > a ? hw[k] : a;
-        b = hw[kRedShards + k] > b ? hw[kRedShards + k] : b;
-    }
-    *mx = a;
-    *mz = b;
+// Max over kRedShards slots.
+unsigned max_slots(const unsigned* slots) {
+    unsigned a = 0u;
+    for (int k = 0; k < kRedShards; ++k) a = slots[k] > a ? slots[k] : a;
+    return a;
 }
 
 float bits_to_float(unsigned u) {
@@ -206,26 +201,29 @@ float bits_to_float(unsigned u) {
     return f;
 }
 
-// One Newton linear solve and update with the layer evaluation fused into the
-// first PCR level and the update + reduction fused into the last level
-// (w = 16, 32).  For L <= 2 the solution is written to `x` and applied by the
-// separate update kernel.
-hipError_t newton_solve_fused(const NewtonArgs& na, int B, int L, int w, const Ws& ws,
-                              const VecDst& x, hipStream_t st) {
+// The fused Newton linear solve (w = 16, 32): the layer evaluation runs
+// inside the first PCR level and the update + reduction inside the last.
+// For L <= 2 the first level writes the solution to `x` and the separate
+// update kernel applies it.  Split in two so that a stopping test on the
+// residual (reduced by the first level) can sit between the halves.
+hipError_t fused_first_level(const NewtonArgs& na, int B, int L, int w, const Ws& ws,
+                             const VecDst& x, hipStream_t st) {
     const int K = num_levels(L);
     const double w2 = (double)w * w;
     const long long ld = (long long)L * w;
-    {
-        // level 1 with the layers: W once, Z read twice, products and r written
-        const double na2 = (double)(L - 2 > 0 ? L - 2 : 0);
-        const double bytes = 4.0 * ((double)L * w2 + B * (na2 * w2 + 3.0 * L * w));
-        const double flops = (double)B * (L * 3.0 * w2 + (L - 1) * 2.0 * w2 + na2 * 2.0 * w2 * w);
-        const VecDst out = (K <= 1) ? x : VecDst{ws.r[0], ld, (long long)w};
-        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
-            return launch_first_level_fwd(na, ws.A[0], out, B, L, w, st);
-        });
-        if (e != hipSuccess) return e;
-    }
+    // level 1 with the layers: W once, Z read twice, products and r written
+    const double na2 = (double)(L - 2 > 0 ? L - 2 : 0);
+    const double bytes = 4.0 * ((double)L * w2 + B * (na2 * w2 + 3.0 * L * w));
+    const double flops = (double)B * (L * 3.0 * w2 + (L - 1) * 2.0 * w2 + na2 * 2.0 * w2 * w);
+    const VecDst out = (K <= 1) ? x : VecDst{ws.r[0], ld, (long long)w};
+    return timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st,
+                 [&] { return launch_first_level_fwd(na, ws.A[0], out, B, L, w, st); });
+}
+
+hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws& ws,
+                             const VecDst& x, hipStream_t st) {
+    const int K = num_levels(L);
+    const long long ld = (long long)L * w;
     if (K <= 1) {
         const long long n = (long long)B * L * w;
         return timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
@@ -255,6 +253,138 @@ hipError_t newton_solve_fused(const NewtonArgs& na, int B, int L, int w, const W
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+// Argument checks shared by the two forward entry points.
+int check_forward_args(const float* W, const float* bias, const float* z0, float* Z,
+                       const float* Z_init, void* workspace, size_t workspace_bytes, int B,
+                       int L, int w, int layer, float alpha) {
+    if (!W || !bias || !z0 || !Z || !workspace || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
+    if (layer < 0 || layer >= kNumLayerKinds || !std::isfinite(alpha)) return DEEPPCR_EINVAL;
+    const Layout lo = layout(DEEPPCR_OP_FWD, B, L, w);
+    if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
+    const size_t nv = (size_t)B * L * w * 4;
+    if (overlaps(workspace, lo.total, Z, nv) ||
+        overlaps(workspace, lo.total, W, (size_t)L * w * w * 4) ||
+        overlaps(workspace, lo.total, z0, (size_t)B * w * 4) ||
+        overlaps(workspace, lo.total, bias, (size_t)L * w * 4) ||
+        overlaps(workspace, lo.total, Z_init, Z_init ? nv : 0))
+        return DEEPPCR_EINVAL;
+    if (Z_init && Z_init != Z && overlaps(Z_init, nv, Z, nv)) return DEEPPCR_EINVAL;
+    return DEEPPCR_OK;
+}
+
+// The Newton driver behind both forward entry points (Sec. 2, Eqs. 1-3).
+// Update rule: up to max_iter solves, each followed by the update and the
+// test max|dZ| < tol * max(1, max|Z|) (tol = 0: exactly max_iter solves).
+// Residual rule: for k = 0..max_iter the residual F(z^k) is reduced while
+// the layers are evaluated, and the iteration stops before the solve when
+// max|F| <= atol or max|F| <= rtol * max|F(z^0)|.  One host read-back per
+// iteration either way.  *measure_out = the last max|dZ| or max|F|.
+int newton_forward(const float* W, const float* bias, const float* z0, float* Z, int B, int L,
+                   int w, int layer, float alpha, const StopRule& rule, const float* Z_init,
+                   void* workspace, int* iters_out, float* measure_out, hipStream_t st) {
+    const Layout lo = layout(DEEPPCR_OP_FWD, B, L, w);
+    const size_t nv = (size_t)B * L * w * 4;
+    Ws ws = carve(workspace, lo);
+    unsigned* hw = host_words();
+    if (!hw) return hip_fail(hipErrorOutOfMemory, "hipHostMalloc");
+    if (iters_out) *iters_out = 0;
+    if (measure_out) *measure_out = 0.f;
+
+    if (tiny_eligible(B, L, w)) {
+        // one launch for the whole solve; reads W, bias, z0 (and Z_init), writes Z
+        const double io = 4.0 * ((double)L * w * (w + 1) + B * w + 2.0 * B * L * w);
+        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, io, 0.0, st, [&] {
+            return launch_newton_tiny(W, bias, z0, Z, Z_init, B, L, w, layer, alpha, rule, ws.red,
+                                      st);
+        });
+        if (e != hipSuccess) return hip_fail(e, "newton_tiny");
+        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 3 * sizeof(unsigned), hipMemcpyDeviceToHost, st));
+        DEEPPCR_HIP(hipStreamSynchronize(st));
+        if (iters_out) *iters_out = (int)hw[1];
+        if (measure_out) *measure_out = bits_to_float(hw[2]);
+        if (hw[0] == 3u) return DEEPPCR_ENONFINITE;
+        if (hw[0] == 2u) return DEEPPCR_ENOCONV;
+        return DEEPPCR_OK;
+    }
+    const double w2 = (double)w * w;
+    const double eval_bytes = 4.0 * B * L * (w2 + 2.0 * w);
+    const double eval_flops = (double)B * L * (2.0 * w2 + w2);
+    if (Z_init) {
+        if (Z_init != Z) DEEPPCR_HIP(hipMemcpyAsync(Z, Z_init, nv, hipMemcpyDeviceToDevice, st));
+    } else {
+        hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * B * L * w, 2.0 * B * w * w, st, [&] {
+            return launch_initial_guess(W, bias, z0, Z, B, L, w, layer, alpha, st);
+        });
+        if (e != hipSuccess) return hip_fail(e, "initial_guess");
+    }
+    const long long n = (long long)B * L * w;
+    const VecDst xd{ws.r[(num_levels(L) + 1) & 1], (long long)L * w, (long long)w};
+    const bool fused = fused_newton_levels(w);
+    const NewtonArgs na{W, bias, z0, Z, ws.red, layer, alpha};
+    unsigned* fslots = ws.red + kRedF;
+    if (rule.residual) {
+        hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * kRedShards, 0.0, st,
+                             [&] { return launch_zero_words(fslots, kRedShards, st); });
+        if (e != hipSuccess) return hip_fail(e, "zero_words");
+    }
+    float res0 = 0.f;
+    for (int k = 0; k <= rule.max_iter; ++k) {
+        if (!rule.residual && k == rule.max_iter) break;
+        // Layers, Jacobian blocks (forward order) and residuals at the iterate:
+        // fused into the first PCR level, or evaluated into ws A[1], r[1].
+        hipError_t e;
+        if (fused) {
+            e = fused_first_level(na, B, L, w, ws, xd, st);
+        } else {
+            e = timed(DEEPPCR_KCLASS_LAYER, eval_bytes, eval_flops, st, [&] {
+                return launch_forward_eval(W, bias, z0, Z, ws.A[1], ws.r[1], ws.red, B, L, w,
+                                           layer, alpha, st);
+            });
+        }
+        if (e != hipSuccess) return hip_fail(e, "layer evaluation");
+        if (rule.residual) {
+            DEEPPCR_HIP(hipMemcpyAsync(hw + kRedF, fslots, kRedShards * sizeof(unsigned),
+                                       hipMemcpyDeviceToHost, st));
+            DEEPPCR_HIP(hipStreamSynchronize(st));
+            const unsigned mf = max_slots(hw + kRedF);
+            if (iters_out) *iters_out = k;
+            if (measure_out) *measure_out = bits_to_float(mf);
+            if (mf >= 0x7f800000u) return DEEPPCR_ENONFINITE;
+            const float res = bits_to_float(mf);
+            if (k == 0) res0 = res;
+            if (res <= rule.atol || res <= rule.rtol * res0) return DEEPPCR_OK;
+            if (k == rule.max_iter) return DEEPPCR_ENOCONV;
+            e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * kRedShards, 0.0, st,
+                      [&] { return launch_zero_words(fslots, kRedShards, st); });
+            if (e != hipSuccess) return hip_fail(e, "zero_words");
+        }
+        // The rest of the solve of Eq. 3 and the update Z += dZ.
+        if (fused) {
+            e = fused_rest_levels(na, B, L, w, ws, xd, st);
+            if (e != hipSuccess) return hip_fail(e, "newton levels");
+        } else {
+            e = pcr_sweep(BlockSrc{ws.A[1], (long long)L * w * w, (long long)w * w, 0},
+                          VecSrc{ws.r[1], (long long)L * w, (long long)w}, xd, B, L, w, ws.A,
+                          ws.r, 0, 0, st);
+            if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+            e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
+                      [&] { return launch_update_reduce(Z, xd.base, n, ws.red, st); });
+            if (e != hipSuccess) return hip_fail(e, "update_reduce");
+        }
+        if (rule.residual) continue;
+        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
+                                   hipMemcpyDeviceToHost, st));
+        DEEPPCR_HIP(hipStreamSynchronize(st));
+        const unsigned mx = max_slots(hw + kRedDZ), mz = max_slots(hw + kRedZ);
+        if (iters_out) *iters_out = k + 1;
+        if (measure_out) *measure_out = bits_to_float(mx);
+        if (mx >= 0x7f800000u || mz >= 0x7f800000u) return DEEPPCR_ENONFINITE;
+        const float m = bits_to_float(mx), zmax = bits_to_float(mz);
+        if (rule.tol > 0.f && m < rule.tol * (zmax > 1.f ? zmax : 1.f)) return DEEPPCR_OK;
+    }
+    return rule.tol > 0.f ? DEEPPCR_ENOCONV : DEEPPCR_OK;
 }
 
 }  // namespace
@@ -319,100 +449,29 @@ int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, floa
                         int L, int w, int layer, float alpha, float tol, int max_iter,
                         const float* Z_init, void* workspace, size_t workspace_bytes,
                         int* iters_out, float* last_update_out, void* stream) {
-    if (!W || !bias || !z0 || !Z || !workspace || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
-    if (layer < 0 || layer >= kNumLayerKinds) return DEEPPCR_EINVAL;
-    if (!(tol >= 0.f) || !std::isfinite(tol) || max_iter < 1 || !std::isfinite(alpha))
-        return DEEPPCR_EINVAL;
-    const Layout lo = layout(DEEPPCR_OP_FWD, B, L, w);
-    if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
-    const size_t nv = (size_t)B * L * w * 4;
-    if (overlaps(workspace, lo.total, Z, nv) || overlaps(workspace, lo.total, W, (size_t)L * w * w * 4) ||
-        overlaps(workspace, lo.total, z0, (size_t)B * w * 4) ||
-        overlaps(workspace, lo.total, bias, (size_t)L * w * 4) ||
-        overlaps(workspace, lo.total, Z_init, Z_init ? nv : 0))
-        return DEEPPCR_EINVAL;
-    if (Z_init && Z_init != Z && overlaps(Z_init, nv, Z, nv)) return DEEPPCR_EINVAL;
+    const int c = check_forward_args(W, bias, z0, Z, Z_init, workspace, workspace_bytes, B, L, w,
+                                     layer, alpha);
+    if (c != DEEPPCR_OK) return c;
+    if (!(tol >= 0.f) || !std::isfinite(tol) || max_iter < 1) return DEEPPCR_EINVAL;
+    const StopRule rule{0, tol, 0.f, 0.f, max_iter};
+    return newton_forward(W, bias, z0, Z, B, L, w, layer, alpha, rule, Z_init, workspace,
+                          iters_out, last_update_out, (hipStream_t)stream);
+}
 
-    hipStream_t st = (hipStream_t)stream;
-    Ws ws = carve(workspace, lo);
-    unsigned* hw = host_words();
-    if (!hw) return hip_fail(hipErrorOutOfMemory, "hipHostMalloc");
-    if (iters_out) *iters_out = 0;
-    if (last_update_out) *last_update_out = 0.f;
-
-    if (tiny_eligible(B, L, w)) {
-        // one launch for the whole solve; reads W, bias, z0 (and Z_init), writes Z
-        const double io = 4.0 * ((double)L * w * (w + 1) + B * w + 2.0 * B * L * w);
-        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, io, 0.0, st, [&] {
-            return launch_newton_tiny(W, bias, z0, Z, Z_init, B, L, w, layer, alpha, tol, max_iter,
-                                      ws.red, st);
-        });
-        if (e != hipSuccess) return hip_fail(e, "newton_tiny");
-        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 3 * sizeof(unsigned), hipMemcpyDeviceToHost, st));
-        DEEPPCR_HIP(hipStreamSynchronize(st));
-        if (iters_out) *iters_out = (int)hw[1];
-        if (last_update_out) *last_update_out = bits_to_float(hw[2]);
-        if (hw[0] == 3u) return DEEPPCR_ENONFINITE;
-        if (hw[0] == 2u) return DEEPPCR_ENOCONV;
-        return DEEPPCR_OK;
-    }
-    const double w2 = (double)w * w;
-    const double eval_bytes = 4.0 * B * L * (w2 + 2.0 * w);
-    const double eval_flops = (double)B * L * (2.0 * w2 + w2);
-    if (Z_init) {
-        if (Z_init != Z) DEEPPCR_HIP(hipMemcpyAsync(Z, Z_init, nv, hipMemcpyDeviceToDevice, st));
-    } else {
-        hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * B * L * w, 2.0 * B * w * w, st, [&] {
-            return launch_initial_guess(W, bias, z0, Z, B, L, w, layer, alpha, st);
-        });
-        if (e != hipSuccess) return hip_fail(e, "initial_guess");
-    }
-    const long long n = (long long)B * L * w;
-    const VecDst xd{ws.r[(num_levels(L) + 1) & 1], (long long)L * w, (long long)w};
-    const bool fused = fused_newton_levels(w);
-    const NewtonArgs na{W, bias, z0, Z, ws.red, layer, alpha};
-    for (int k = 1; k <= max_iter; ++k) {
-        if (fused) {
-            hipError_t e = newton_solve_fused(na, B, L, w, ws, xd, st);
-            if (e != hipSuccess) return hip_fail(e, "newton_solve_fused");
-            DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
-                                   hipMemcpyDeviceToHost, st));
-            DEEPPCR_HIP(hipStreamSynchronize(st));
-            unsigned mx, mz;
-            reduce_slots(hw, &mx, &mz);
-            if (iters_out) *iters_out = k;
-            if (last_update_out) *last_update_out = bits_to_float(mx);
-            if (mx >= 0x7f800000u || mz >= 0x7f800000u) return DEEPPCR_ENONFINITE;
-            const float m = bits_to_float(mx), zmax = bits_to_float(mz);
-            if (tol > 0.f && m < tol * (zmax > 1.f ? zmax : 1.f)) return DEEPPCR_OK;
-            continue;
-        }
-        // Layers, Jacobian blocks (forward order) and residuals at the iterate.
-        hipError_t e = timed(DEEPPCR_KCLASS_LAYER, eval_bytes, eval_flops, st, [&] {
-            return launch_forward_eval(W, bias, z0, Z, ws.A[1], ws.r[1], ws.red, B, L, w, layer,
-                                       alpha, st);
-        });
-        if (e != hipSuccess) return hip_fail(e, "forward_eval");
-        // PCR solve of Eq. 3 for the update; level 0 reads ws A[1], r[1].
-        e = pcr_sweep(BlockSrc{ws.A[1], (long long)L * w * w, (long long)w * w, 0},
-                      VecSrc{ws.r[1], (long long)L * w, (long long)w}, xd, B, L, w, ws.A, ws.r,
-                      0, 0, st);
-        if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
-        e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
-                  [&] { return launch_update_reduce(Z, xd.base, n, ws.red, st); });
-        if (e != hipSuccess) return hip_fail(e, "update_reduce");
-        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
-                                   hipMemcpyDeviceToHost, st));
-        DEEPPCR_HIP(hipStreamSynchronize(st));
-        unsigned mx, mz;
-        reduce_slots(hw, &mx, &mz);
-        if (iters_out) *iters_out = k;
-        if (last_update_out) *last_update_out = bits_to_float(mx);
-        if (mx >= 0x7f800000u || mz >= 0x7f800000u) return DEEPPCR_ENONFINITE;
-        const float m = bits_to_float(mx), zmax = bits_to_float(mz);
-        if (tol > 0.f && m < tol * (zmax > 1.f ? zmax : 1.f)) return DEEPPCR_OK;
-    }
-    return tol > 0.f ? DEEPPCR_ENOCONV : DEEPPCR_OK;
+int deeppcr_mlp_forward_residual(const float* W, const float* bias, const float* z0, float* Z,
+                                 int B, int L, int w, int layer, float alpha, float atol,
+                                 float rtol, int max_iter, const float* Z_init, void* workspace,
+                                 size_t workspace_bytes, int* iters_out, float* residual_out,
+                                 void* stream) {
+    const int c = check_forward_args(W, bias, z0, Z, Z_init, workspace, workspace_bytes, B, L, w,
+                                     layer, alpha);
+    if (c != DEEPPCR_OK) return c;
+    if (!(atol >= 0.f) || !std::isfinite(atol) || !(rtol >= 0.f) || !std::isfinite(rtol) ||
+        max_iter < 0)
+        return DEEPPCR_EINVAL;
+    const StopRule rule{1, 0.f, atol, rtol, max_iter};
+    return newton_forward(W, bias, z0, Z, B, L, w, layer, alpha, rule, Z_init, workspace,
+                          iters_out, residual_out, (hipStream_t)stream);
 }
 
 int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, const float* Z,

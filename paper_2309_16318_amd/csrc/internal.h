@@ -14,7 +14,12 @@ constexpr int kMaxWidth = 128;
 // The Newton convergence maxima are reduced into kRedShards slots each
 // (slot = workgroup index mod kRedShards) to keep atomic contention low; the
 // host takes the max over the slots after its one read-back per iteration.
+// Reduction area: max|dZ| slots, then max|Z| slots (both cleared by the
+// forward layer evaluation), then max|F| slots (the residual of the iterate,
+// written by the forward layer evaluation; cleared by launch_zero_words).
 constexpr int kRedShards = 256;
+constexpr int kRedDZ = 0, kRedZ = kRedShards, kRedF = 2 * kRedShards;
+constexpr int kRedWords = 3 * kRedShards;
 
 // Layer kinds: code = 2 * activation + residual, activation 0 = tanh,
 // 1 = logistic sigmoid, 2 = ReLU (derivative 0 at 0).  The residual form is
@@ -82,7 +87,7 @@ struct NewtonArgs {
     const float* z0;     // [B, w]
     float* Z;            // [B, L, w] current iterate (read by the first level,
                          // updated by the last level)
-    unsigned* red;       // kRedShards words of max|dZ| bits, then kRedShards of max|Z|
+    unsigned* red;       // reduction area (kRedDZ, kRedZ and kRedF slots)
     int layer;
     float alpha;
 };
@@ -94,7 +99,8 @@ bool fused_newton_levels(int w);
 // blocks and residuals evaluated on the fly (never stored):
 //   r_l = f_l(Z_{l-1}) - Z_l, J_l = df_l at Z_{l-1};
 //   rout[l] = r_l + J_l r_{l-1} (rout[0] = r_0), Aout[l] = J_l J_{l-1} (l >= 2).
-// Also clears the 2 * kRedShards reduction words.
+// Also clears the max|dZ| and max|Z| slots and reduces max|r| into the
+// kRedF slots.
 hipError_t launch_first_level_fwd(const NewtonArgs& na, float* Aout, const VecDst& rout, int B,
                                   int L, int w, hipStream_t stream);
 
@@ -117,7 +123,8 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
 // Forward Newton step: for every (b, l) evaluate the layer at Zprev = Z[b,l-1]
 // (z0[b] for l = 0), write r[b,l] = f_l(Zprev) - Z[b,l] and, for l >= 1,
 // the Jacobian block J_l into A ([B, L, w, w], forward row order).  The grid
-// also clears the 2 * kRedShards reduction words `red`.
+// also clears the max|dZ| and max|Z| slots of `red` and reduces max|r| into
+// its kRedF slots.
 hipError_t launch_forward_eval(const float* W, const float* bias, const float* z0,
                                const float* Z, float* A, float* r, unsigned* red,
                                int B, int L, int w, int layer, float alpha,
@@ -128,9 +135,9 @@ hipError_t launch_initial_guess(const float* W, const float* bias, const float* 
                                 float* Z, int B, int L, int w, int layer, float alpha,
                                 hipStream_t stream);
 
-// Z += x over n floats; red[slot] = max bits of |x|, red[kRedShards + slot]
-// = max bits of |Z| (atomic max on the IEEE bit patterns of non-negative
-// floats, which orders NaN above Inf).
+// Z += x over n floats; red[kRedDZ + slot] = max bits of |x|,
+// red[kRedZ + slot] = max bits of |Z| (atomic max on the IEEE bit patterns of
+// non-negative floats, which orders NaN above Inf).
 hipError_t launch_update_reduce(float* Z, const float* x, long long n, unsigned* red,
                                 hipStream_t stream);
 
@@ -153,6 +160,9 @@ hipError_t launch_dz0(const float* W, const float* dscale, const float* Lambda, 
 hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
                         const float* Lambda, float* dW, float* db, int B, int L, int w,
                         hipStream_t stream);
+
+// p[0 .. n) = 0 (a kernel, so that the call can sit in a captured graph).
+hipError_t launch_zero_words(unsigned* p, int n, hipStream_t stream);
 
 // dst[b, l] = src[b, l] for every (b, l) (used when L = 1).
 hipError_t launch_copy_rows(const VecSrc& src, const VecDst& dst, int B, int L, int w,
@@ -185,12 +195,19 @@ hipError_t launch_seq_backward(const float* W, const float* bias, const float* z
 // ------------------------------------------------------------- tiny path
 // Whole Newton + PCR forward solve in one workgroup with everything in LDS,
 // for batches that fit in 64 KiB.  result[0] = status (0 ok, 2 no
-// convergence, 3 non-finite), result[1] = iterations, result[2] = bits of the
-// last max|dZ|.  Z_init may be null or alias Z.
+// convergence, 3 non-finite), result[1] = solves, result[2] = bits of the
+// last max|dZ| (update rule) or of the last residual norm (residual rule).
+// Z_init may be null or alias Z.
+struct StopRule {
+    int residual;  // 0: max|dZ| < tol * max(1, max|Z|) after each update;
+                   // 1: max|F| <= atol or <= rtol * max|F_0| before each solve
+    float tol, atol, rtol;
+    int max_iter;
+};
 bool tiny_eligible(int B, int L, int w);
 size_t tiny_lds_bytes(int B, int L, int w);
 hipError_t launch_newton_tiny(const float* W, const float* bias, const float* z0, float* Z,
                               const float* Z_init, int B, int L, int w, int layer, float alpha,
-                              float tol, int max_iter, unsigned* result, hipStream_t stream);
+                              const StopRule& rule, unsigned* result, hipStream_t stream);
 
 }  // namespace deeppcr

@@ -58,12 +58,19 @@ __global__ __launch_bounds__(kThreads) void forward_eval_kernel(
     preactivations(Wl, bias + (long long)l * w, zp, a, w);
     __syncthreads();
     const bool res = layer_residual(layer);
+    unsigned mr = 0u;  // max |r| bits
     for (int i = t; i < w; i += kThreads) {
         float d;
         const float y = activate(layer, a[i], &d);
         const float f = res ? fmaf(alpha, y, zp[i]) : y;
-        r[row * w + i] = f - Z[row * w + i];
+        const float rv = f - Z[row * w + i];
+        r[row * w + i] = rv;
+        mr = max(mr, __float_as_uint(fabsf(rv)));
         dsc[i] = res ? alpha * d : d;
+    }
+    if ((t >> 6) * 64 < w) {  // waves holding residual elements
+        mr = wave_umax(mr);
+        if ((t & 63) == 0) atomicMax(red + kRedF + (int)(row % kRedShards), mr);
     }
     __syncthreads();
     if (l == 0) return;
@@ -130,8 +137,8 @@ __global__ __launch_bounds__(kThreads) void update_reduce_kernel(
             c = max(c, sz[i]);
         }
         const int slot = blockIdx.x % kRedShards;
-        atomicMax(red + slot, a);
-        atomicMax(red + kRedShards + slot, c);
+        atomicMax(red + kRedDZ + slot, a);
+        atomicMax(red + kRedZ + slot, c);
     }
 }
 
@@ -240,6 +247,11 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
     if (t < w) db[(long long)l * w + t] = dbacc;
 }
 
+__global__ __launch_bounds__(kThreads) void zero_words_kernel(unsigned* __restrict__ p, int n) {
+    const int i = blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
 __global__ __launch_bounds__(kThreads) void copy_rows_kernel(VecSrc src, VecDst dst, int L, int w) {
     const long long row = blockIdx.x;
     const int l = (int)(row % L);
@@ -284,6 +296,7 @@ __global__ __launch_bounds__(256) void layer_eval_vec(
     const int l = (int)(row % L);
     const int b = (int)(row / L);
     const int tt = t % S::TPB;
+    unsigned mr = 0u;  // forward: max |r| bits
     const float* zprev = (l == 0) ? z0 + (long long)b * W : Z + (row - 1) * W;
     const float* Wl = W_ + (long long)l * W * W;
     const int m_rev = L - l;  // reversed row of J_l (backward)
@@ -311,7 +324,9 @@ __global__ __launch_bounds__(256) void layer_eval_vec(
             if (lead) {
                 const float zi = zprev[i];
                 const float fv = res ? fmaf(alpha, y, zi) : y;
-                r[row * W + i] = fv - Z[row * W + i];
+                const float rv = fv - Z[row * W + i];
+                r[row * W + i] = rv;
+                mr = max(mr, __float_as_uint(fabsf(rv)));
             }
         } else if (lead) {
             dscale[row * W + i] = dsc;
@@ -323,6 +338,11 @@ __global__ __launch_bounds__(256) void layer_eval_vec(
             if (res && i >= c4 && i < c4 + 4) j4[i - c4] += 1.f;
             *reinterpret_cast<v4f*>(Ab + i * W + c4) = j4;
         }
+    }
+    if (!BWD) {
+        // rows beyond B * L returned above with their whole wave (TPB >= 64)
+        mr = wave_umax(mr);
+        if ((t & 63) == 0) atomicMax(red + kRedF + (int)(row % kRedShards), mr);
     }
 }
 
@@ -416,6 +436,12 @@ hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
                         hipStream_t stream) {
     hipLaunchKernelGGL(wgrad_kernel, dim3((unsigned)L), dim3(kThreads), 0, stream, z0, Z, dscale,
                        Lambda, dW, db, B, L, w);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_words(unsigned* p, int n, hipStream_t stream) {
+    hipLaunchKernelGGL(zero_words_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, stream, p, n);
     return hipGetLastError();
 }
 

@@ -272,6 +272,7 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
     float* zw = na.Z + (long long)sg.b * L * W;
     const float* z0b = na.z0 + (long long)sg.b * W;
     unsigned mx = 0u, mz = 0u;  // UPD reductions
+    unsigned mr = 0u;           // SRC_LAYER: max |r| of the evaluated rows
 
     // Writes solution / next-level row l (lanes with g == 0 hold element i).
     auto emit = [&](int l, float x) {
@@ -295,6 +296,7 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
             float w_in[S::NV];
             load_R<W, false>(na.W, i, g, w_in);
             const float r0 = eval_layer_row<W>(na, 0, lds.z[0], zb[i], i, g, w_in);
+            mr = __float_as_uint(fabsf(r0));
             emit(0, r0);
         } else {
             emit(sg.c, rb[sg.c * rin.rstride + i]);
@@ -358,6 +360,7 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
                     if (lane < W) rnext = zb[(long long)(l + 1) * W + lane];  // Z_{l+1}
                 }
                 ri = eval_layer_row<W>(na, l, zprv, zcur[i], i, g, aR);
+                mr = max(mr, __float_as_uint(fabsf(ri)));
             } else {
                 if constexpr (DEEP) {
                     if (m + 1 < sg.m1) load_R<W, TRANS>(ab + (long long)(l + 2 * s) * Ain.rstride, i, g, aN);
@@ -435,9 +438,13 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
         wave_umax2<W>(mx, mz);
         if (lane == 0) {
             const int slot = blockIdx.x % kRedShards;
-            atomicMax(na.red + slot, mx);
-            atomicMax(na.red + kRedShards + slot, mz);
+            atomicMax(na.red + kRedDZ + slot, mx);
+            atomicMax(na.red + kRedZ + slot, mz);
         }
+    }
+    if constexpr (SRC == SRC_LAYER) {
+        for (int off = 32; off > 0; off >>= 1) mr = max(mr, (unsigned)__shfl_xor((int)mr, off, 64));
+        if (lane == 0) atomicMax(na.red + kRedF + (int)(blockIdx.x % kRedShards), mr);
     }
 }
 

@@ -75,29 +75,37 @@ __global__ __launch_bounds__(kThreads) void eval_small(
     const long long idx = (long long)blockIdx.x * kThreads + threadIdx.x;
     if (!BWD && blockIdx.x == 0)
         for (int k = threadIdx.x; k < 2 * kRedShards; k += kThreads) red[k] = 0u;
-    if (idx >= (long long)B * L * w) return;
-    const int i = (int)(idx % w);
-    const long long row = idx / w;
-    const int l = (int)(row % L);
-    const int b = (int)(row / L);
-    const float* zp = (l == 0) ? z0 + (long long)b * w : Z + (row - 1) * w;
-    const float* Wr = W + ((long long)l * w + i) * w;
-    float acc = 0.f;
-    for (int k = 0; k < w; ++k) acc = fmaf(Wr[k], zp[k], acc);
-    float d;
-    const float y = activate(layer, acc + bias[(long long)l * w + i], &d);
-    const bool res = layer_residual(layer);
-    const float dsc = res ? alpha * d : d;
-    if (!BWD) {
-        r[idx] = (res ? fmaf(alpha, y, zp[i]) : y) - Z[idx];
-    } else {
-        dscale[idx] = dsc;
-        const int mr = L - 1 - l;
-        r[((long long)b * L + mr) * w + i] = (mr == 0) ? G[(long long)b * w + i] : 0.f;
+    unsigned mr = 0u;  // forward: max |r| bits
+    if (idx < (long long)B * L * w) {
+        const int i = (int)(idx % w);
+        const long long row = idx / w;
+        const int l = (int)(row % L);
+        const int b = (int)(row / L);
+        const float* zp = (l == 0) ? z0 + (long long)b * w : Z + (row - 1) * w;
+        const float* Wr = W + ((long long)l * w + i) * w;
+        float acc = 0.f;
+        for (int k = 0; k < w; ++k) acc = fmaf(Wr[k], zp[k], acc);
+        float d;
+        const float y = activate(layer, acc + bias[(long long)l * w + i], &d);
+        const bool res = layer_residual(layer);
+        const float dsc = res ? alpha * d : d;
+        if (!BWD) {
+            const float rv = (res ? fmaf(alpha, y, zp[i]) : y) - Z[idx];
+            r[idx] = rv;
+            mr = __float_as_uint(fabsf(rv));
+        } else {
+            dscale[idx] = dsc;
+            const int mr_row = L - 1 - l;
+            r[((long long)b * L + mr_row) * w + i] = (mr_row == 0) ? G[(long long)b * w + i] : 0.f;
+        }
+        if (l >= 1) {
+            float* Ar = A + ((long long)b * L + (BWD ? L - l : l)) * w * w + (long long)i * w;
+            for (int k = 0; k < w; ++k) Ar[k] = dsc * Wr[k] + ((res && k == i) ? 1.f : 0.f);
+        }
     }
-    if (l >= 1) {
-        float* Ar = A + ((long long)b * L + (BWD ? L - l : l)) * w * w + (long long)i * w;
-        for (int k = 0; k < w; ++k) Ar[k] = dsc * Wr[k] + ((res && k == i) ? 1.f : 0.f);
+    if (!BWD) {
+        for (int off = 32; off > 0; off >>= 1) mr = max(mr, (unsigned)__shfl_xor((int)mr, off, 64));
+        if ((threadIdx.x & 63) == 0) atomicMax(red + kRedF + (int)(blockIdx.x % kRedShards), mr);
     }
 }
 

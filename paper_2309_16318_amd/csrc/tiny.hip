@@ -2,9 +2,10 @@
 // (Sec. 2, Eqs. 1-3; Sec. 3, Alg. 1): the iterate, the Jacobian blocks and
 // the right-hand sides live in LDS, every Newton iteration (layer and
 // Jacobian evaluation, all PCR levels, update, convergence test) runs inside
-// one launch, and the host reads back one status record.  Used when the whole
-// batch fits in 64 KiB of LDS, where a multi-kernel solve would be dominated
-// by launch and synchronisation latency.
+// one launch, and the host reads back one status record.  Both stopping rules
+// of the library are evaluated inside the kernel.  Used when the whole batch
+// fits in 64 KiB of LDS, where a multi-kernel solve would be dominated by
+// launch and synchronisation latency.
 #include "internal.h"
 
 namespace deeppcr {
@@ -17,7 +18,7 @@ struct TinyLds {
     float* A[2];   // [B, L, w, w] ping-pong
     float* r[2];   // [B, L, w] ping-pong
     float* dsc;    // [B, L, w]
-    unsigned* red; // [2 * kThreads / 64]
+    unsigned* red; // [kThreads / 64]
 };
 
 __device__ inline unsigned wave_umax(unsigned v) {
@@ -61,10 +62,22 @@ __device__ void tiny_eval(const float* __restrict__ W, const float* __restrict__
     __syncthreads();
 }
 
+// Max over the workgroup of one value per thread (bit patterns of
+// non-negative floats); every thread receives the result.
+__device__ inline unsigned block_umax(unsigned v, unsigned* red) {
+    v = wave_umax(v);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    unsigned m = 0u;
+    for (int q = 0; q < kThreads / 64; ++q) m = max(m, red[q]);
+    __syncthreads();
+    return m;
+}
+
 __global__ __launch_bounds__(kThreads) void newton_tiny_kernel(
     const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
     float* __restrict__ Zout, const float* __restrict__ Z_init, int B, int L, int w, int layer,
-    float alpha, float tol, int max_iter, unsigned* __restrict__ result) {
+    float alpha, StopRule rule, unsigned* __restrict__ result) {
     extern __shared__ float smem[];
     const int nz = B * L * w, na = nz * w;
     TinyLds s;
@@ -93,10 +106,33 @@ __global__ __launch_bounds__(kThreads) void newton_tiny_kernel(
     }
     __syncthreads();
 
-    unsigned status = 2u;  // no convergence unless tol == 0
-    unsigned mx = 0u, iters = 0u;
-    for (int k = 1; k <= max_iter; ++k) {
+    // Update rule: k counts solves 1..max_iter, tested after each update.
+    // Residual rule: iterates k = 0..max_iter, tested before each solve.
+    unsigned status = 2u;  // no convergence unless stated otherwise
+    unsigned meas = 0u, iters = 0u;
+    float res0 = 0.f;
+    for (int k = 0; k <= rule.max_iter; ++k) {
+        if (!rule.residual && k == rule.max_iter) break;
         tiny_eval(W, bias, z0, s, s.A[0], s.r[0], B, L, w, layer, alpha);
+        if (rule.residual) {
+            unsigned lr = 0u;
+            for (int idx = t; idx < nz; idx += kThreads)
+                lr = max(lr, __float_as_uint(fabsf(s.r[0][idx])));
+            const unsigned gr = block_umax(lr, s.red);
+            iters = (unsigned)k;
+            meas = gr;
+            if (gr >= 0x7f800000u) {
+                status = 3u;
+                break;
+            }
+            const float res = __uint_as_float(gr);
+            if (k == 0) res0 = res;
+            if (res <= rule.atol || res <= rule.rtol * res0) {
+                status = 0u;
+                break;
+            }
+            if (k == rule.max_iter) break;
+        }
         // PCR levels (Alg. 1): read level k-1 buffers, write level k buffers
         int cur = 0;
         for (int st = 1; st < L; st *= 2) {
@@ -137,37 +173,30 @@ __global__ __launch_bounds__(kThreads) void newton_tiny_kernel(
             lmx = max(lmx, __float_as_uint(fabsf(x[idx])));
             lmz = max(lmz, __float_as_uint(fabsf(z)));
         }
-        lmx = wave_umax(lmx);
-        lmz = wave_umax(lmz);
-        if ((t & 63) == 0) {
-            s.red[2 * (t >> 6)] = lmx;
-            s.red[2 * (t >> 6) + 1] = lmz;
+        if (rule.residual) {
+            __syncthreads();  // the next evaluation reads the whole iterate
+            continue;
         }
-        __syncthreads();
-        unsigned gmx = 0u, gmz = 0u;
-        for (int q = 0; q < kThreads / 64; ++q) {
-            gmx = max(gmx, s.red[2 * q]);
-            gmz = max(gmz, s.red[2 * q + 1]);
-        }
-        __syncthreads();
-        mx = gmx;
-        iters = (unsigned)k;
+        const unsigned gmx = block_umax(lmx, s.red);
+        const unsigned gmz = block_umax(lmz, s.red);
+        meas = gmx;
+        iters = (unsigned)(k + 1);
         if (gmx >= 0x7f800000u || gmz >= 0x7f800000u) {
             status = 3u;
             break;
         }
         const float m = __uint_as_float(gmx), zmax = __uint_as_float(gmz);
-        if (tol > 0.f && m < tol * fmaxf(1.f, zmax)) {
+        if (rule.tol > 0.f && m < rule.tol * fmaxf(1.f, zmax)) {
             status = 0u;
             break;
         }
     }
-    if (tol == 0.f && status == 2u) status = 0u;
+    if (!rule.residual && rule.tol == 0.f && status == 2u) status = 0u;
     for (int idx = t; idx < nz; idx += kThreads) Zout[idx] = s.Z[idx];
     if (t == 0) {
         result[0] = status;
         result[1] = iters;
-        result[2] = mx;
+        result[2] = meas;
     }
 }
 
@@ -175,7 +204,7 @@ __global__ __launch_bounds__(kThreads) void newton_tiny_kernel(
 
 size_t tiny_lds_bytes(int B, int L, int w) {
     const size_t nz = (size_t)B * L * w, na = nz * w;
-    return (3 * nz + 2 * na + nz) * sizeof(float) + 2 * (kThreads / 64) * sizeof(unsigned);
+    return (3 * nz + 2 * na + nz) * sizeof(float) + (kThreads / 64) * sizeof(unsigned);
 }
 
 bool tiny_eligible(int B, int L, int w) {
@@ -184,10 +213,10 @@ bool tiny_eligible(int B, int L, int w) {
 
 hipError_t launch_newton_tiny(const float* W, const float* bias, const float* z0, float* Z,
                               const float* Z_init, int B, int L, int w, int layer, float alpha,
-                              float tol, int max_iter, unsigned* result, hipStream_t stream) {
+                              const StopRule& rule, unsigned* result, hipStream_t stream) {
     const size_t lds = tiny_lds_bytes(B, L, w);
     hipLaunchKernelGGL(newton_tiny_kernel, dim3(1), dim3(kThreads), lds, stream, W, bias, z0, Z,
-                       Z_init, B, L, w, layer, alpha, tol, max_iter, result);
+                       Z_init, B, L, w, layer, alpha, rule, result);
     return hipGetLastError();
 }
 

@@ -34,6 +34,12 @@ SIGNATURES = {
                                        _c.c_float, _c.c_int, _c.c_void_p, _c.c_void_p,
                                        _c.c_size_t, _c.POINTER(_c.c_int),
                                        _c.POINTER(_c.c_float), _c.c_void_p]),
+    "deeppcr_mlp_forward_residual": (_c.c_int, [_c.c_void_p, _c.c_void_p, _c.c_void_p,
+                                                _c.c_void_p, _c.c_int, _c.c_int, _c.c_int,
+                                                _c.c_int, _c.c_float, _c.c_float, _c.c_float,
+                                                _c.c_int, _c.c_void_p, _c.c_void_p, _c.c_size_t,
+                                                _c.POINTER(_c.c_int), _c.POINTER(_c.c_float),
+                                                _c.c_void_p]),
     "deeppcr_mlp_backward": (_c.c_int, [_c.c_void_p] * 9 + [_c.c_int, _c.c_int, _c.c_int,
                                                            _c.c_int, _c.c_float, _c.c_void_p,
                                                            _c.c_size_t, _c.c_void_p]),
@@ -168,6 +174,45 @@ def deeppcr_mlp_forward(W, bias, z0, Z=None, layer: int = TANH_MLP, alpha: float
     if st not in (OK, ENOCONV, ENONFINITE):
         raise DeepPCRError(st, "deeppcr_mlp_forward")
     return ForwardResult(Z, iters.value, last.value, st)
+
+
+@dataclass
+class ResidualForwardResult:
+    Z: object
+    iters: int
+    residual: float
+    status: int
+
+
+def deeppcr_mlp_forward_residual(W, bias, z0, Z=None, layer: int = TANH_MLP, alpha: float = 1.0,
+                                 atol: float = 1e-4, rtol: float = 1e-4, max_iter: int = 15,
+                                 Z_init=None, workspace=None,
+                                 stream=None) -> ResidualForwardResult:
+    """Newton + PCR forward pass stopped by the residual rule (defaults: the
+    paper's forward-pass solver settings); raises on EINVAL/EHIP/EWORKSPACE
+    and returns ENOCONV / ENONFINITE in ``status``."""
+    torch = _torch()
+    L, w, _ = W.shape
+    B = z0.shape[0]
+    _check(W, (L, w, w), "W")
+    _check(bias, (L, w), "bias")
+    _check(z0, (B, w), "z0")
+    if Z is None:
+        Z = torch.empty((B, L, w), dtype=torch.float32, device=z0.device)
+    _check(Z, (B, L, w), "Z")
+    if Z_init is not None:
+        _check(Z_init, (B, L, w), "Z_init")
+    ws, nbytes = _workspace(OP_FWD, B, L, w, workspace, z0.device)
+    iters = ctypes.c_int(0)
+    res = ctypes.c_float(0.0)
+    st = lib().deeppcr_mlp_forward_residual(_ptr(W), _ptr(bias), _ptr(z0), _ptr(Z), B, L, w,
+                                            int(layer), float(alpha), float(atol), float(rtol),
+                                            int(max_iter), _ptr(Z_init), _ptr(ws), nbytes,
+                                            ctypes.byref(iters), ctypes.byref(res),
+                                            _stream(stream))
+    if st not in (OK, ENOCONV, ENONFINITE):
+        raise DeepPCRError(st, "deeppcr_mlp_forward_residual")
+    return ResidualForwardResult(Z, iters.value, res.value, st)
 
 
 def deeppcr_mlp_backward(W, bias, z0, Z, G, layer: int = TANH_MLP, alpha: float = 1.0,

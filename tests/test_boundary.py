@@ -20,8 +20,8 @@ def declared_functions():
 
 def test_header_declares_the_entry_points():
     names = declared_functions()
-    for n in ("pcr_solve_block_bidiag", "deeppcr_mlp_forward", "deeppcr_mlp_backward",
-              "deeppcr_workspace_bytes"):
+    for n in ("pcr_solve_block_bidiag", "deeppcr_mlp_forward", "deeppcr_mlp_forward_residual",
+              "deeppcr_mlp_backward", "deeppcr_workspace_bytes"):
         assert n in names
 
 
@@ -38,7 +38,7 @@ def test_workspace_sizes():
     nA = B * L * w * w * 4
     nr = B * L * w * 4
     up = lambda x: (x + 255) // 256 * 256
-    red = 2 * 256 * 4  # two sets of 256 reduction slots
+    red = 3 * 256 * 4  # three sets of 256 reduction slots (max|dZ|, max|Z|, max|F|)
     assert f(deeppcr.OP_PCR, B, L, w) == 2 * up(nA) + 2 * up(nr) + red
     assert f(deeppcr.OP_FWD, B, L, w) == 2 * up(nA) + 2 * up(nr) + red
     assert f(deeppcr.OP_BWD, B, L, w) == 2 * up(nA) + 3 * up(nr) + red
@@ -105,6 +105,35 @@ def test_forward_rejects_invalid_arguments():
     assert _fwd(Zi=ctypes.c_void_p(P[3].value + 4)) == E     # partial overlap with Z
     assert _fwd(ws=ctypes.c_void_p(P[3].value)) == E          # workspace over Z
     assert _fwd(nws=100) == deeppcr.EWORKSPACE
+
+
+def _fwd_res(W=P[0], b=P[1], z0=P[2], Z=P[3], B=2, L=8, w=4, layer=0, alpha=1.0, atol=1e-4,
+             rtol=1e-4, max_iter=15, Zi=None, ws=P[5], nws=BIG):
+    it = ctypes.c_int(-1)
+    res = ctypes.c_float(-1)
+    return deeppcr.lib().deeppcr_mlp_forward_residual(W, b, z0, Z, B, L, w, layer, alpha, atol,
+                                                      rtol, max_iter, Zi, ws, nws,
+                                                      ctypes.byref(it), ctypes.byref(res), None)
+
+
+def test_forward_residual_rejects_invalid_arguments():
+    E = deeppcr.EINVAL
+    assert _fwd_res(W=None) == E
+    assert _fwd_res(b=None) == E
+    assert _fwd_res(z0=None) == E
+    assert _fwd_res(Z=None) == E
+    assert _fwd_res(ws=None) == E
+    assert _fwd_res(layer=6) == E
+    assert _fwd_res(max_iter=-1) == E
+    for bad in (-1.0, float("nan"), float("inf")):
+        assert _fwd_res(atol=bad) == E
+        assert _fwd_res(rtol=bad) == E
+    assert _fwd_res(alpha=float("nan")) == E
+    assert _fwd_res(B=0) == E
+    assert _fwd_res(w=129) == E
+    assert _fwd_res(Zi=ctypes.c_void_p(P[3].value + 4)) == E
+    assert _fwd_res(ws=ctypes.c_void_p(P[0].value)) == E      # workspace over W
+    assert _fwd_res(nws=100) == deeppcr.EWORKSPACE
 
 
 def _bwd(ptrs=None, B=2, L=8, w=4, layer=0, alpha=1.0, ws=P[10], nws=BIG):

@@ -242,6 +242,103 @@ def test_forward_deterministic(dev):
     assert np.array_equal(a, b)
 
 
+
+# ------------------------------------------- residual stopping rule (App. F.1)
+def _forward_res(d, dev, layer, alpha, atol=1e-4, rtol=1e-4, max_iter=15, Z_init=None):
+    return deeppcr.deeppcr_mlp_forward_residual(g(d["W"], dev), g(d["bias"], dev),
+                                                g(d["z0"], dev), layer=layer, alpha=alpha,
+                                                atol=atol, rtol=rtol, max_iter=max_iter,
+                                                Z_init=Z_init)
+
+
+# every kernel family: single workgroup (4, 16), small widths (4, 600), (8, 300),
+# fused w = 16 / 32 (including L <= 2), tile w = 64 / 128, generic (17)
+RES_SHAPES = [(4, 16, 1), (4, 600, 2), (8, 300, 2), (16, 200, 3), (32, 100, 2), (32, 2, 3),
+              (64, 40, 2), (128, 12, 2), (17, 50, 2)]
+
+
+@pytest.mark.parametrize("w,L,B", RES_SHAPES)
+@pytest.mark.parametrize("layer,alpha", [(0, 1.0), (1, 0.1), (4, 1.0)])
+def test_forward_residual_rule(dev, w, L, B, layer, alpha):
+    """Paper defaults (atol = rtol = 1e-4, at most 15 solves): the solve count
+    is within one of the oracle's, the iterate equals the oracle's Newton
+    iterate after the same number of solves, and the reported residual is
+    the residual of the returned iterate and meets a threshold."""
+    _say(f"forward residual rule w={w} L={L} B={B} layer={layer}")
+    d = synth.mlp_inputs(B, L, w, seed=900 + w + L + layer)
+    res = _forward_res(d, dev, layer, alpha)
+    assert res.status == deeppcr.OK
+    Zg = h(res.Z)
+    _, k_ref, ok, hist = oracle.newton_forward_residual(layer, alpha, d["W"], d["bias"], d["z0"],
+                                                        1e-4, 1e-4, 15)
+    _say(f"  gpu solves {res.iters} residual {res.residual:.3e}; oracle {k_ref} {hist[-1]:.3e}")
+    assert ok and abs(res.iters - k_ref) <= 1
+    if res.iters == 0:
+        Zk = oracle.initial_guess(layer, alpha, *(d[k].astype(np.float64)
+                                                  for k in ("W", "bias", "z0")))
+    else:
+        Zk, _, _, _ = oracle.newton_forward(layer, alpha, d["W"], d["bias"], d["z0"], 0.0,
+                                            res.iters)
+    assert normwise_rel_err(Zg, Zk) <= TOL
+    r_own = oracle.residual_norm(layer, alpha, d["W"], d["bias"], d["z0"], Zg)
+    assert abs(res.residual - r_own) <= 1e-5 + 1e-3 * r_own
+    assert res.residual <= max(1e-4, 1e-4 * hist[0]) * (1 + 1e-3) + 1e-6
+    ref = oracle.seq_forward(layer, alpha, d["W"], d["bias"], d["z0"])
+    assert normwise_rel_err(Zg, ref) <= 1e-3
+    if res.iters >= 1:
+        # one solve fewer is not enough: ENOCONV with a residual above both thresholds
+        prev = _forward_res(d, dev, layer, alpha, max_iter=res.iters - 1)
+        assert prev.status == deeppcr.ENOCONV and prev.iters == res.iters - 1
+        assert prev.residual > 1e-4
+
+
+def test_forward_residual_rule_mlp_workload(dev):
+    wl = synth.WORKLOADS["mlp_fwd"]
+    _say(f"mlp forward, residual rule, B={wl.B} L={wl.L} w={wl.w}")
+    d = synth.workload_inputs(wl)
+    res = _forward_res(d, dev, wl.layer, wl.alpha)
+    assert res.status == deeppcr.OK
+    _, k_ref, ok, hist = oracle.newton_forward_residual(wl.layer, wl.alpha, d["W"], d["bias"],
+                                                        d["z0"], 1e-4, 1e-4, 15)
+    _say(f"  gpu solves {res.iters} residual {res.residual:.3e}; oracle {k_ref}")
+    assert ok and abs(res.iters - k_ref) <= 1
+    Zk, _, _, _ = oracle.newton_forward(wl.layer, wl.alpha, d["W"], d["bias"], d["z0"], 0.0,
+                                        res.iters)
+    assert normwise_rel_err(h(res.Z), Zk) <= TOL
+
+
+@pytest.mark.parametrize("w,L,B", [(4, 16, 1), (8, 300, 2), (16, 200, 3), (64, 40, 2),
+                                   (17, 50, 2)])
+def test_forward_residual_rule_zero_solves(dev, w, L, B):
+    d = synth.mlp_inputs(B, L, w, seed=950 + w)
+    res = _forward_res(d, dev, 0, 1.0, atol=1e9)
+    assert res.status == deeppcr.OK and res.iters == 0
+    Z0 = oracle.initial_guess(0, 1.0, *(d[k].astype(np.float64) for k in ("W", "bias", "z0")))
+    assert normwise_rel_err(h(res.Z), Z0) <= 1e-6
+    # warm start at the root: the start already meets the threshold, Z is untouched
+    ref = oracle.seq_forward(0, 1.0, d["W"], d["bias"], d["z0"]).astype(np.float32)
+    res = _forward_res(d, dev, 0, 1.0, atol=1e-4, rtol=0.0, Z_init=g(ref, dev))
+    assert res.status == deeppcr.OK and res.iters == 0 and res.residual <= 1e-4
+    assert np.array_equal(h(res.Z), ref)
+
+
+@pytest.mark.parametrize("w,L,B", [(4, 16, 1), (16, 200, 3), (64, 40, 2), (17, 50, 2)])
+def test_forward_residual_rule_max_iter(dev, w, L, B):
+    d = synth.mlp_inputs(B, L, w, seed=960 + w)
+    res = _forward_res(d, dev, 0, 1.0, atol=0.0, rtol=0.0, max_iter=2)
+    assert res.status == deeppcr.ENOCONV and res.iters == 2
+    Z2, _, _, _ = oracle.newton_forward(0, 1.0, d["W"], d["bias"], d["z0"], 0.0, 2)
+    assert normwise_rel_err(h(res.Z), Z2) <= TOL
+
+
+@pytest.mark.parametrize("w,L,B", [(4, 16, 1), (16, 200, 3), (64, 40, 2)])
+def test_forward_residual_rule_non_finite(dev, w, L, B):
+    d = dict(synth.mlp_inputs(B, L, w, seed=970 + w))
+    d["bias"] = d["bias"].copy()
+    d["bias"][3, 1] = np.nan
+    res = _forward_res(d, dev, 0, 1.0)
+    assert res.status == deeppcr.ENONFINITE and res.iters == 0
+
 # ------------------------------------------------------------------ backward
 def _backward_check(d, Z32, dev, layer, alpha, tol=TOL):
     lam, dz0, dW, db = deeppcr.deeppcr_mlp_backward(g(d["W"], dev), g(d["bias"], dev),
