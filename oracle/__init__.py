@@ -11,3 +11,4 @@ from .deeppcr_oracle import (  # noqa: F401
     residual_norm, newton_forward_residual,
     seq_backward, loss,
 )
+from . import resnet_oracle  # noqa: F401

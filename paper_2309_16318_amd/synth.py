@@ -74,6 +74,27 @@ def mlp_inputs(B: int, L: int, w: int, seed: int = 0) -> dict:
     return {"W": _f32(W), "bias": _f32(bias), "z0": _f32(z0), "G": _f32(G)}
 
 
+def resnet_inputs(B: int, L: int, w: int, seed: int = 0) -> dict:
+    """Random fully connected ResNet parameters (the collapsed-skip network).
+
+    Draw order: W, bias, z0, G.  Weights and biases follow the default
+    initialization of a fully connected layer in PyTorch (uniform on
+    [-1/sqrt(w), 1/sqrt(w)] for both), the usual starting point of the
+    training runs the network is used in:
+      W[L, w, w]  ~ U(-1/sqrt(w), 1/sqrt(w))
+      bias[L, w]  ~ U(-1/sqrt(w), 1/sqrt(w))
+      z0[B, w]    ~ N(0, 1)
+      G[B, w]     ~ N(0, 1)
+    """
+    rng = np.random.default_rng(seed)
+    bound = 1.0 / np.sqrt(w)
+    W = rng.uniform(-bound, bound, size=(L, w, w))
+    bias = rng.uniform(-bound, bound, size=(L, w))
+    z0 = rng.standard_normal((B, w))
+    G = rng.standard_normal((B, w))
+    return {"W": _f32(W), "bias": _f32(bias), "z0": _f32(z0), "G": _f32(G)}
+
+
 def haar_orthogonal(rng: np.random.Generator, shape_prefix: tuple, w: int) -> np.ndarray:
     """Haar-distributed orthogonal w x w matrices: QR of a Gaussian, with the
     signs of R's diagonal folded into Q."""
