@@ -174,6 +174,69 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Collapsed-skip ResNet (App. A.3).  Fully connected layers in the
+ * pre-activation form of the appendix with a skip connection of length
+ * `skip`: for layer j = 0..L-1 (Z[:, -1] := z0)
+ *   Z[:, j] = W_j sigma(Z[:, j-1]) + b_j                 if (j + 1) % skip != 0
+ *   Z[:, j] = W_j sigma(Z[:, j-1]) + b_j + Z[:, j-skip]   if (j + 1) % skip == 0
+ * with sigma one of the DEEPPCR_ACT_* activations and L a multiple of skip.
+ * Collapsing the layers between two skips turns the network into a Markov
+ * chain over the block outputs X_g = Z[:, g*skip + skip - 1],
+ * g = 0..L/skip-1, X_{-1} = z0, with steps
+ *   X_g = F_g(X_{g-1}) = h_{g*skip+skip-1}(... h_{g*skip}(X_{g-1})) + X_{g-1},
+ *   dF_g/dX = I + J_{g*skip+skip-1} ... J_{g*skip},  J_j = W_j diag(sigma'(Z[:, j-1])),
+ * (h_j(z) = W_j sigma(z) + b_j), and DeepPCR runs on that chain: L/skip
+ * unknowns, each Newton step evaluating every block (its skip layers and the
+ * product of their Jacobians) in parallel.
+ */
+enum { DEEPPCR_ACT_TANH = 0, DEEPPCR_ACT_SIGMOID = 1, DEEPPCR_ACT_RELU = 2 };
+
+/* Workspace bytes of deeppcr_resnet_forward (op = DEEPPCR_OP_FWD) or
+ * deeppcr_resnet_backward (DEEPPCR_OP_BWD); 0 for an invalid op or shape. */
+size_t deeppcr_resnet_workspace_bytes(int op, int B, int L, int w, int skip);
+
+/*
+ * Forward pass by Newton + PCR on the block chain (App. A.3; Sec. 2,
+ * Eqs. 1-3).  Each iteration evaluates every block and its Jacobian at the
+ * iterate, solves the block-bidiagonal system of Eq. 3 for the block-output
+ * update by PCR and applies it; stops once max|dX| < tol * max(1, max|X|)
+ * (tol = 0: exactly max_iter iterations).  Start: every X_g = F_0(z0) (the
+ * rule of App. F.2 applied to the blocks), or X_g = Z_init[:, g*skip+skip-1].
+ * After the last iteration the rows inside each block are recomputed from the
+ * block's input X_{g-1}; row g*skip+skip-1 of Z is X_g itself.
+ *   W [L, w, w], bias [L, w], z0 [B, w]; Z [B, L, w] output (every layer)
+ *   skip >= 1 with L % skip == 0; act a DEEPPCR_ACT_* value
+ *   Z_init NULL or [B, L, w] (only its block-output rows are read); may alias Z
+ *   iters_out, last_update_out (host, may be NULL): solves, last max|dX|
+ * Status as for deeppcr_mlp_forward.  Waits for the GPU once per iteration.
+ * workspace_bytes >= deeppcr_resnet_workspace_bytes(DEEPPCR_OP_FWD, B, L, w, skip).
+ */
+int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, float* Z,
+                           int B, int L, int w, int skip, int act, float tol, int max_iter,
+                           const float* Z_init, void* workspace, size_t workspace_bytes,
+                           int* iters_out, float* last_update_out, void* stream);
+
+/*
+ * Backward pass for Loss = sum_b <G[b], Z[b, L-1]> (App. A.3, "a similar
+ * reasoning" for the backward; App. A.2, Eqs. 10-12).  The block-output
+ * adjoints mu_g = dLoss/dX_g solve the transposed block system
+ * mu_{G-1} = G, mu_{g-1} = (dF_g/dX)^T mu_g by one transposed PCR pass with
+ * the block Jacobians evaluated at the stored states Z; the adjoints inside
+ * each block follow by back-propagation through its layers,
+ * Lambda[:, j-1] = diag(sigma'(Z[:, j-1])) W_j^T Lambda[:, j], and
+ *   dW[j] = sum_b Lambda[b, j] sigma(Z[b, j-1])^T,   db[j] = sum_b Lambda[b, j]
+ * (Eq. 10 in the pre-activation form), dz0 = dLoss/dz0.
+ *   W, z0 as for the forward; Z [B, L, w] forward states; G [B, w]
+ *   Lambda [B, L, w], dz0 [B, w], dW [L, w, w], db [L, w]: outputs (overwritten)
+ * Returns without waiting for the GPU.
+ * workspace_bytes >= deeppcr_resnet_workspace_bytes(DEEPPCR_OP_BWD, B, L, w, skip).
+ */
+int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, const float* G,
+                            float* Lambda, float* dz0, float* dW, float* db,
+                            int B, int L, int w, int skip, int act,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Sequential passes: the layer-by-layer baseline the paper measures DeepPCR
  * against (Sec. 4.1), on the same GPU.  Forward: Z[:, l] = f_l(Z[:, l-1]) for
  * l = 0..L-1 (Eq. 1 applied one step at a time).  Backward: the adjoints of

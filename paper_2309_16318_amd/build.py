@@ -15,7 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdeeppcr.so")
 
-SOURCES = ["api.hip", "pcr_level.hip", "layers.hip", "tiny.hip", "sequential.hip", "small.hip"]
+SOURCES = ["api.hip", "pcr_level.hip", "layers.hip", "tiny.hip", "sequential.hip", "small.hip",
+           "resnet.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",

@@ -104,6 +104,28 @@ Layout layout(int op, int B, int L, int w) {
     return lo;
 }
 
+// Collapsed-skip ResNet: the block chain has G = L / skip rows; the forward
+// keeps its iterate X [B, G, w] in the slot of the backward's c*d vectors.
+Layout resnet_layout(int op, int B, int G, int w) {
+    const size_t nA = (size_t)B * G * w * w * sizeof(float);
+    const size_t nr = (size_t)B * G * w * sizeof(float);
+    Layout lo{};
+    size_t off = 0;
+    lo.A[0] = off; off += align_up(nA);
+    lo.A[1] = off; off += align_up(nA);
+    lo.r[0] = off; off += align_up(nr);
+    lo.r[1] = off; off += align_up(nr);
+    lo.dscale = off;
+    if (op == DEEPPCR_OP_FWD) off += align_up(nr);
+    lo.red = off; off += align_up(kRedWords * sizeof(unsigned));
+    lo.total = off;
+    return lo;
+}
+
+bool resnet_shape_ok(int B, int L, int w, int skip, int act) {
+    return sizes_ok(B, L, w) && skip >= 1 && L % skip == 0 && act >= 0 && act <= 2;
+}
+
 int num_levels(int L) {
     int k = 0;
     for (long long s = 1; s < L; s *= 2) ++k;
@@ -521,6 +543,151 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
     if (e != hipSuccess) return hip_fail(e, "dz0");
     e = timed(DEEPPCR_KCLASS_WGRAD, 4.0 * (3.0 * B * L * w + L * (w2 + w)), 2.0 * B * L * w2, st,
               [&] { return launch_wgrad(z0, Z, ws.dscale, Lambda, dW, db, B, L, w, st); });
+    if (e != hipSuccess) return hip_fail(e, "wgrad");
+    return DEEPPCR_OK;
+}
+
+size_t deeppcr_resnet_workspace_bytes(int op, int B, int L, int w, int skip) {
+    if ((op != DEEPPCR_OP_FWD && op != DEEPPCR_OP_BWD) || !resnet_shape_ok(B, L, w, skip, 0))
+        return 0;
+    return resnet_layout(op, B, L / skip, w).total;
+}
+
+int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
+                           int L, int w, int skip, int act, float tol, int max_iter,
+                           const float* Z_init, void* workspace, size_t workspace_bytes,
+                           int* iters_out, float* last_update_out, void* stream) {
+    if (!W || !bias || !z0 || !Z || !workspace || !resnet_shape_ok(B, L, w, skip, act))
+        return DEEPPCR_EINVAL;
+    if (!(tol >= 0.f) || !std::isfinite(tol) || max_iter < 1) return DEEPPCR_EINVAL;
+    const int G = L / skip;
+    const Layout lo = resnet_layout(DEEPPCR_OP_FWD, B, G, w);
+    if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
+    const size_t nv = (size_t)B * L * w * 4;
+    if (overlaps(workspace, lo.total, Z, nv) ||
+        overlaps(workspace, lo.total, W, (size_t)L * w * w * 4) ||
+        overlaps(workspace, lo.total, z0, (size_t)B * w * 4) ||
+        overlaps(workspace, lo.total, bias, (size_t)L * w * 4) ||
+        overlaps(workspace, lo.total, Z_init, Z_init ? nv : 0))
+        return DEEPPCR_EINVAL;
+    if (Z_init && Z_init != Z && overlaps(Z_init, nv, Z, nv)) return DEEPPCR_EINVAL;
+
+    hipStream_t st = (hipStream_t)stream;
+    Ws ws = carve(workspace, lo);
+    float* X = (float*)((char*)workspace + lo.dscale);
+    unsigned* hw = host_words();
+    if (!hw) return hip_fail(hipErrorOutOfMemory, "hipHostMalloc");
+    if (iters_out) *iters_out = 0;
+    if (last_update_out) *last_update_out = 0.f;
+    const long long n = (long long)B * G * w;
+    const double w2 = (double)w * w;
+    if (Z_init) {
+        // X^0[b, g] = Z_init[b, g*skip + skip - 1]
+        const VecSrc src{Z_init + (long long)(skip - 1) * w, (long long)L * w, (long long)skip * w};
+        const VecDst dst{X, (long long)G * w, (long long)w};
+        hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 8.0 * n, 0.0, st,
+                             [&] { return launch_copy_rows(src, dst, B, G, w, st); });
+        if (e != hipSuccess) return hip_fail(e, "copy_rows");
+    } else {
+        hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * n, 2.0 * B * skip * w2, st, [&] {
+            return launch_resnet_initial_guess(W, bias, z0, X, B, G, w, skip, act, st);
+        });
+        if (e != hipSuccess) return hip_fail(e, "resnet_initial_guess");
+    }
+    const VecDst xd{ws.r[(num_levels(G) + 1) & 1], (long long)G * w, (long long)w};
+    // block evaluation: W once, X read twice, blocks and residuals written;
+    // flops: the s - 1 block products and the s mat-vecs per block
+    const double eval_bytes = 4.0 * ((double)L * w2 + (double)B * G * (w2 + 3.0 * w));
+    const double eval_flops = (double)B * G * ((skip - 1) * 2.0 * w2 * w + skip * 2.0 * w2);
+    int status = tol > 0.f ? DEEPPCR_ENOCONV : DEEPPCR_OK;
+    for (int k = 1; k <= max_iter; ++k) {
+        hipError_t e = timed(DEEPPCR_KCLASS_LAYER, eval_bytes, eval_flops, st, [&] {
+            return launch_resnet_block_eval(W, bias, z0, X, ws.A[1], ws.r[1], ws.red, B, G, w,
+                                            skip, act, st);
+        });
+        if (e != hipSuccess) return hip_fail(e, "resnet_block_eval");
+        e = pcr_sweep(BlockSrc{ws.A[1], (long long)G * w * w, (long long)w * w, 0},
+                      VecSrc{ws.r[1], (long long)G * w, (long long)w}, xd, B, G, w, ws.A, ws.r,
+                      0, 0, st);
+        if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+        e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
+                  [&] { return launch_update_reduce(X, xd.base, n, ws.red, st); });
+        if (e != hipSuccess) return hip_fail(e, "update_reduce");
+        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
+                                   hipMemcpyDeviceToHost, st));
+        DEEPPCR_HIP(hipStreamSynchronize(st));
+        const unsigned mx = max_slots(hw + kRedDZ), mz = max_slots(hw + kRedZ);
+        if (iters_out) *iters_out = k;
+        if (last_update_out) *last_update_out = bits_to_float(mx);
+        if (mx >= 0x7f800000u || mz >= 0x7f800000u) {
+            status = DEEPPCR_ENONFINITE;
+            break;
+        }
+        const float m = bits_to_float(mx), zmax = bits_to_float(mz);
+        if (tol > 0.f && m < tol * (zmax > 1.f ? zmax : 1.f)) {
+            status = DEEPPCR_OK;
+            break;
+        }
+    }
+    // every layer output from the block outputs
+    hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * ((double)L * w2 + 2.0 * B * L * w),
+                         2.0 * B * (L - G) * w2, st, [&] {
+                             return launch_resnet_expand(W, bias, z0, X, Z, B, G, w, skip, act,
+                                                         st);
+                         });
+    if (e != hipSuccess) return hip_fail(e, "resnet_expand");
+    return status;
+}
+
+int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, const float* G_,
+                            float* Lambda, float* dz0, float* dW, float* db, int B, int L, int w,
+                            int skip, int act, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+    if (!W || !z0 || !Z || !G_ || !Lambda || !dz0 || !dW || !db || !workspace ||
+        !resnet_shape_ok(B, L, w, skip, act))
+        return DEEPPCR_EINVAL;
+    const int G = L / skip;
+    const Layout lo = resnet_layout(DEEPPCR_OP_BWD, B, G, w);
+    if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
+    const size_t nv = (size_t)B * L * w * 4, nW = (size_t)L * w * w * 4;
+    const void* ins[] = {W, z0, Z, G_};
+    const size_t nins[] = {nW, (size_t)B * w * 4, nv, (size_t)B * w * 4};
+    void* outs[] = {Lambda, dz0, dW, db};
+    const size_t nouts[] = {nv, (size_t)B * w * 4, nW, (size_t)L * w * 4};
+    for (int i = 0; i < 4; ++i) {
+        if (overlaps(workspace, lo.total, outs[i], nouts[i])) return DEEPPCR_EINVAL;
+        if (overlaps(workspace, lo.total, ins[i], nins[i])) return DEEPPCR_EINVAL;
+        for (int j = 0; j < 4; ++j)
+            if (overlaps(outs[i], nouts[i], ins[j], nins[j])) return DEEPPCR_EINVAL;
+        for (int j = i + 1; j < 4; ++j)
+            if (overlaps(outs[i], nouts[i], outs[j], nouts[j])) return DEEPPCR_EINVAL;
+    }
+    hipStream_t st = (hipStream_t)stream;
+    Ws ws = carve(workspace, lo);
+    const double w2 = (double)w * w;
+    // blocks of the transposed block system (reversed rows) and its right-hand side
+    hipError_t e = timed(DEEPPCR_KCLASS_LAYER,
+                         4.0 * ((double)L * w2 + (double)B * L * w + (double)B * G * (w2 + w)),
+                         (double)B * G * (skip - 1) * 2.0 * w2 * w, st, [&] {
+                             return launch_resnet_block_jac(W, z0, Z, G_, ws.A[1], ws.r[1], B, G,
+                                                            w, skip, act, st);
+                         });
+    if (e != hipSuccess) return hip_fail(e, "resnet_block_jac");
+    // block-output adjoints mu (natural order) from the transposed solve
+    float* mu = ws.r[(num_levels(G) + 1) & 1];
+    const VecDst xd{mu + (long long)(G - 1) * w, (long long)G * w, -(long long)w};
+    e = pcr_sweep(BlockSrc{ws.A[1], (long long)G * w * w, (long long)w * w, 1},
+                  VecSrc{ws.r[1], (long long)G * w, (long long)w}, xd, B, G, w, ws.A, ws.r, 0, 0,
+                  st);
+    if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+    e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * ((double)L * w2 + 2.0 * B * L * w),
+              2.0 * B * L * w2, st, [&] {
+                  return launch_resnet_intra_adjoint(W, z0, Z, mu, Lambda, dz0, B, G, w, skip,
+                                                     act, st);
+              });
+    if (e != hipSuccess) return hip_fail(e, "resnet_intra_adjoint");
+    e = timed(DEEPPCR_KCLASS_WGRAD, 4.0 * (2.0 * B * L * w + L * (w2 + w)), 2.0 * B * L * w2, st,
+              [&] { return launch_wgrad_pre(z0, Z, Lambda, dW, db, B, L, w, act, st); });
     if (e != hipSuccess) return hip_fail(e, "wgrad");
     return DEEPPCR_OK;
 }

@@ -22,7 +22,7 @@ constexpr int kRedDZ = 0, kRedZ = kRedShards, kRedF = 2 * kRedShards;
 constexpr int kRedWords = 3 * kRedShards;
 
 // Layer kinds: code = 2 * activation + residual, activation 0 = tanh,
-// 1 = logistic sigmoid, 2 = ReLU (derivative 0 at 0).  The residual form is
+// 1 = logistic sigmoid, 2 = ReLU (derivative 0 at 0; a NaN input gives NaN).  The residual form is
 // f(z) = z + alpha * sigma(W z + b), the plain form f(z) = sigma(W z + b).
 constexpr int kNumLayerKinds = 6;
 __host__ __device__ inline bool layer_residual(int layer) { return (layer & 1) != 0; }
@@ -40,8 +40,9 @@ __device__ inline float activate(int layer, float a, float* d) {
         *d = s * (1.f - s);
         return s;
     }
+    // NaN passes through (as max(a, 0) does in the usual frameworks)
     *d = a > 0.f ? 1.f : 0.f;
-    return a > 0.f ? a : 0.f;
+    return (a > 0.f || __builtin_isnan(a)) ? a : 0.f;
 }
 
 // A batch of w x w blocks addressed as base + b*bstride + m*rstride (floats).
@@ -164,6 +165,12 @@ hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
 // p[0 .. n) = 0 (a kernel, so that the call can sit in a captured graph).
 hipError_t launch_zero_words(unsigned* p, int n, hipStream_t stream);
 
+// dW[l] = sum_b Lambda[b,l] sigma(Zprev[b,l])^T, db[l] = sum_b Lambda[b,l]
+// (pre-activation layers W sigma(z) + b; activation act: 0 tanh, 1 sigmoid,
+// 2 ReLU).
+hipError_t launch_wgrad_pre(const float* z0, const float* Z, const float* Lambda, float* dW,
+                            float* db, int B, int L, int w, int act, hipStream_t stream);
+
 // dst[b, l] = src[b, l] for every (b, l) (used when L = 1).
 hipError_t launch_copy_rows(const VecSrc& src, const VecDst& dst, int B, int L, int w,
                             hipStream_t stream);
@@ -191,6 +198,33 @@ hipError_t launch_seq_forward(const float* W, const float* bias, const float* z0
 hipError_t launch_seq_backward(const float* W, const float* bias, const float* z0, const float* Z,
                                const float* G, float* Lambda, float* dz0, int B, int L, int w,
                                int layer, float alpha, int l0, int l1, hipStream_t stream);
+
+// ------------------------------------------------- collapsed-skip ResNet
+// Blocks of s layers, G = L / s blocks per system, X [B, G, w] the block
+// outputs; act: 0 tanh, 1 sigmoid, 2 ReLU.
+// Block evaluation at the iterate: r[b,g] = F_g(X[b,g-1]) - X[b,g] and, for
+// g >= 1, A[b,g] = I + P_g (forward order); clears the max|dZ|, max|Z| slots.
+hipError_t launch_resnet_block_eval(const float* W, const float* bias, const float* z0,
+                                    const float* X, float* A, float* r, unsigned* red, int B,
+                                    int G, int w, int skip, int act, hipStream_t stream);
+// X[b, g] = F_0(z0[b]) for every g.
+hipError_t launch_resnet_initial_guess(const float* W, const float* bias, const float* z0,
+                                       float* X, int B, int G, int w, int skip, int act,
+                                       hipStream_t stream);
+// Z [B, L, w]: the layers inside each block run from X[b, g-1]; row gs+s-1 = X[b, g].
+hipError_t launch_resnet_expand(const float* W, const float* bias, const float* z0,
+                                const float* X, float* Z, int B, int G, int w, int skip, int act,
+                                hipStream_t stream);
+// Backward blocks at the stored states Z: A[b, G-g] = I + P_g (g >= 1, to be
+// read transposed), rrev[b, m] = G[b] if m == 0 else 0.
+hipError_t launch_resnet_block_jac(const float* W, const float* z0, const float* Z,
+                                   const float* Gv, float* A, float* rrev, int B, int G, int w,
+                                   int skip, int act, hipStream_t stream);
+// Lambda [B, L, w] inside every block from mu [B, G, w] (block-output
+// adjoints, natural order), and dz0.
+hipError_t launch_resnet_intra_adjoint(const float* W, const float* z0, const float* Z,
+                                       const float* mu, float* Lambda, float* dz0, int B, int G,
+                                       int w, int skip, int act, hipStream_t stream);
 
 // ------------------------------------------------------------- tiny path
 // Whole Newton + PCR forward solve in one workgroup with everything in LDS,

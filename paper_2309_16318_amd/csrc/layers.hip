@@ -201,10 +201,14 @@ __global__ __launch_bounds__(kThreads) void dz0_kernel(
 
 constexpr int kWgradBC = 32;  // batch rows staged per LDS chunk
 
+// PRE = false: g = dscale * Lambda and the layer inputs as they are (the
+// post-activation MLP of Eq. 10).  PRE = true: g = Lambda and sigma(layer
+// input) with activation act (the pre-activation layers of the ResNet).
+template <bool PRE>
 __global__ __launch_bounds__(kThreads) void wgrad_kernel(
     const float* __restrict__ z0, const float* __restrict__ Z, const float* __restrict__ dscale,
     const float* __restrict__ Lambda, float* __restrict__ dW, float* __restrict__ db, int B, int L,
-    int w) {
+    int w, int act) {
     const int l = blockIdx.x;
     const int t = threadIdx.x;
     __shared__ float g[kWgradBC][kMaxWidth];
@@ -220,8 +224,15 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
         for (int idx = t; idx < nb * w; idx += kThreads) {
             const int bb = idx / w, i = idx - (idx / w) * w;
             const long long rowi = ((long long)(b0 + bb) * L + l) * w + i;
-            g[bb][i] = dscale[rowi] * Lambda[rowi];
-            zp[bb][i] = (l == 0) ? z0[(long long)(b0 + bb) * w + i] : Z[rowi - w];
+            const float zin = (l == 0) ? z0[(long long)(b0 + bb) * w + i] : Z[rowi - w];
+            if constexpr (PRE) {
+                float d;
+                g[bb][i] = Lambda[rowi];
+                zp[bb][i] = activate(2 * act, zin, &d);
+            } else {
+                g[bb][i] = dscale[rowi] * Lambda[rowi];
+                zp[bb][i] = zin;
+            }
         }
         __syncthreads();
 #pragma unroll
@@ -434,8 +445,15 @@ hipError_t launch_dz0(const float* W, const float* dscale, const float* Lambda, 
 hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
                         const float* Lambda, float* dW, float* db, int B, int L, int w,
                         hipStream_t stream) {
-    hipLaunchKernelGGL(wgrad_kernel, dim3((unsigned)L), dim3(kThreads), 0, stream, z0, Z, dscale,
-                       Lambda, dW, db, B, L, w);
+    hipLaunchKernelGGL(wgrad_kernel<false>, dim3((unsigned)L), dim3(kThreads), 0, stream, z0, Z,
+                       dscale, Lambda, dW, db, B, L, w, 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_wgrad_pre(const float* z0, const float* Z, const float* Lambda, float* dW,
+                            float* db, int B, int L, int w, int act, hipStream_t stream) {
+    hipLaunchKernelGGL(wgrad_kernel<true>, dim3((unsigned)L), dim3(kThreads), 0, stream, z0, Z,
+                       nullptr, Lambda, dW, db, B, L, w, act);
     return hipGetLastError();
 }
 

@@ -1,0 +1,325 @@
+// Collapsed-skip ResNet (App. A.3).  Layer j maps Z_{j-1} to
+//   Z_j = W_j sigma(Z_{j-1}) + b_j            (+ Z_{j-s} when (j+1) % s == 0),
+// Z_{-1} = z0 (the pre-activation MLP layer and residual addition of the
+// appendix).  Collapsing the s layers of a block gives a Markov chain over the
+// block outputs X_g = Z_{gs+s-1}:
+//   X_g = F_g(X_{g-1}) = h_{gs+s-1}(... h_{gs}(X_{g-1}) ...) + X_{g-1},
+//   dF_g/dX = I + J_{gs+s-1} ... J_{gs},   J_j = W_j diag(sigma'(Z_{j-1})),
+// which Newton + PCR solves with L/s unknowns; the backward pass solves the
+// transposed block system for the block-output adjoints and recovers the
+// adjoints inside each block by back-propagating through its s layers.
+//
+// The kernels here work on whole blocks, one workgroup per (system, block),
+// with the state vectors and the w x w running Jacobian product in LDS
+// (dynamic, sized by w).  The PCR levels, the Newton update and its
+// reductions are those of the MLP path.
+#include "internal.h"
+
+namespace deeppcr {
+namespace {
+
+constexpr int kThreads = 256;
+
+// sigma(z) and sigma'(z) for activation act (0 tanh, 1 sigmoid, 2 ReLU with
+// derivative 0 at 0): the MLP layer codes with the residual bit clear.
+__device__ inline float act_fn(int act, float z, float* d) { return activate(2 * act, z, d); }
+
+// One layer on the state z (LDS, length w): z <- W_j sigma(z) + b_j.
+// sg receives sigma(z) of the input.  Starts and ends with a barrier.
+__device__ inline void layer_forward(const float* __restrict__ Wj, const float* __restrict__ bj,
+                                     float* z, float* sg, int w, int act) {
+    const int t = threadIdx.x;
+    __syncthreads();
+    if (t < w) {
+        float d;
+        sg[t] = act_fn(act, z[t], &d);
+    }
+    __syncthreads();
+    float a = 0.f;
+    if (t < w) {
+        for (int k = 0; k < w; ++k) a = fmaf(Wj[(long long)t * w + k], sg[k], a);
+        a += bj[t];
+    }
+    __syncthreads();
+    if (t < w) z[t] = a;
+    __syncthreads();
+}
+
+// Jacobian product of block g, P = J_{gs+s-1} ... J_{gs}, built in two LDS
+// buffers of w x w floats (P and Q, swapped after each layer; the returned
+// pointer holds the product).  J_j P = W_j (diag(sigma'(z)) P) is formed with
+// W_j read from global memory (L2-resident, shared by every system), so no
+// third buffer is needed.  The layer inputs are either recomputed from the
+// block input (FROM_STATES = false: z holds X_{g-1} on entry and the block's
+// last pre-skip output on exit) or read from the stored layer outputs Zb
+// (FROM_STATES = true; Zb = Z + b*L*w).  jac = false skips the product.
+template <bool FROM_STATES>
+__device__ float* block_product(const float* __restrict__ W, const float* __restrict__ bias,
+                                const float* __restrict__ Zb, const float* xin, float* z,
+                                float* sg, float* ds, float* P, float* Q, int g, int w, int skip,
+                                int act, bool jac) {
+    const int t = threadIdx.x;
+    const int ww = w * w;
+    for (int tt = 0; tt < skip; ++tt) {
+        const long long j = (long long)g * skip + tt;
+        const float* Wj = W + j * ww;
+        // the layer input and its activation
+        if (t < w) {
+            const float zin = FROM_STATES ? (tt == 0 ? xin[t] : Zb[(j - 1) * w + t]) : z[t];
+            float d;
+            sg[t] = act_fn(act, zin, &d);
+            ds[t] = d;
+        }
+        __syncthreads();
+        if (jac) {
+            if (tt == 0) {
+                for (int idx = t; idx < ww; idx += kThreads)
+                    P[idx] = Wj[idx] * ds[idx - (idx / w) * w];
+            } else {
+                for (int idx = t; idx < ww; idx += kThreads) {
+                    const int i = idx / w, k = idx - (idx / w) * w;
+                    const float* wr = Wj + (long long)i * w;
+                    float acc = 0.f;
+                    for (int m = 0; m < w; ++m) acc = fmaf(wr[m] * ds[m], P[m * w + k], acc);
+                    Q[idx] = acc;
+                }
+            }
+        }
+        float a = 0.f;
+        if (!FROM_STATES && t < w) {
+            for (int k = 0; k < w; ++k) a = fmaf(Wj[(long long)t * w + k], sg[k], a);
+            a += bias[j * w + t];
+        }
+        __syncthreads();
+        if (jac && tt > 0) {
+            float* tmp = P;
+            P = Q;
+            Q = tmp;
+        }
+        if (!FROM_STATES && t < w) z[t] = a;
+        __syncthreads();
+    }
+    return P;
+}
+
+// Forward Newton step on the block chain: for row (b, g) evaluate the block
+// at the iterate's X_{g-1} (z0 for g = 0): r = F_g(X_{g-1}) - X_g and, for
+// g >= 1, the block A_g = I + P in forward order.  Clears the max|dZ|, max|Z|
+// reduction slots.
+__global__ __launch_bounds__(kThreads) void resnet_block_eval_kernel(
+    const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ X, float* __restrict__ A, float* __restrict__ r,
+    unsigned* __restrict__ red, int G, int w, int skip, int act) {
+    extern __shared__ float smem[];
+    float* xin = smem;
+    float* z = xin + w;
+    float* sg = z + w;
+    float* ds = sg + w;
+    float* P = ds + w;
+    float* Q = P + w * w;
+    const long long row = blockIdx.x;  // b * G + g
+    const int g = (int)(row % G);
+    const int b = (int)(row / G);
+    const int t = threadIdx.x;
+    if (row == 0)
+        for (int k = t; k < 2 * kRedShards; k += kThreads) red[k] = 0u;
+    const float* xp = (g == 0) ? z0 + (long long)b * w : X + (row - 1) * w;
+    if (t < w) {
+        xin[t] = xp[t];
+        z[t] = xp[t];
+    }
+    __syncthreads();
+    const bool jac = g > 0;  // the block of row 0 couples to z0 and is never read
+    const float* Pf = block_product<false>(W, bias, nullptr, xin, z, sg, ds, P, Q, g, w, skip, act,
+                                           jac);
+    if (t < w) r[row * w + t] = (z[t] + xin[t]) - X[row * w + t];
+    if (jac) {
+        float* Ab = A + row * w * w;
+        for (int idx = t; idx < w * w; idx += kThreads)
+            Ab[idx] = Pf[idx] + ((idx / w == idx - (idx / w) * w) ? 1.f : 0.f);
+    }
+}
+
+// X[b, g] = F_0(z0[b]) for every block g (App. F.2 applied to the blocks).
+__global__ __launch_bounds__(kThreads) void resnet_initial_guess_kernel(
+    const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
+    float* __restrict__ X, int G, int w, int skip, int act) {
+    __shared__ float xin[kMaxWidth], z[kMaxWidth], sg[kMaxWidth];
+    const int b = blockIdx.x;
+    const int t = threadIdx.x;
+    if (t < w) {
+        xin[t] = z0[(long long)b * w + t];
+        z[t] = xin[t];
+    }
+    for (int tt = 0; tt < skip; ++tt)
+        layer_forward(W + (long long)tt * w * w, bias + (long long)tt * w, z, sg, w, act);
+    for (long long idx = t; idx < (long long)G * w; idx += kThreads) {
+        const int i = (int)(idx % w);
+        X[(long long)b * G * w + idx] = z[i] + xin[i];
+    }
+}
+
+// All layer outputs from the block outputs: in block g the first s-1 layers
+// run from X_{g-1} (z0 for g = 0), and row gs+s-1 is X_g itself.
+__global__ __launch_bounds__(kThreads) void resnet_expand_kernel(
+    const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ X, float* __restrict__ Z, int G, int w, int skip, int act) {
+    __shared__ float z[kMaxWidth], sg[kMaxWidth];
+    const long long row = blockIdx.x;  // b * G + g
+    const int g = (int)(row % G);
+    const int b = (int)(row / G);
+    const int t = threadIdx.x;
+    const long long L = (long long)G * skip;
+    const float* xp = (g == 0) ? z0 + (long long)b * w : X + (row - 1) * w;
+    if (t < w) z[t] = xp[t];
+    float* Zb = Z + (long long)b * L * w;
+    for (int tt = 0; tt + 1 < skip; ++tt) {
+        const long long j = (long long)g * skip + tt;
+        layer_forward(W + j * w * w, bias + j * w, z, sg, w, act);
+        if (t < w) Zb[j * w + t] = z[t];
+    }
+    if (t < w) Zb[((long long)g * skip + skip - 1) * w + t] = X[row * w + t];
+}
+
+// Backward: blocks of the transposed block system in reversed row order.
+// Reversed row m = G - g holds A_g = I + P_g (g >= 1) with P_g evaluated at
+// the stored layer inputs, stored untransposed (the first PCR level reads it
+// transposed); the right-hand side is G at reversed row 0 and 0 elsewhere.
+__global__ __launch_bounds__(kThreads) void resnet_block_jac_kernel(
+    const float* __restrict__ W, const float* __restrict__ z0, const float* __restrict__ Z,
+    const float* __restrict__ Gv, float* __restrict__ A, float* __restrict__ rrev, int G, int w,
+    int skip, int act) {
+    extern __shared__ float smem[];
+    float* xin = smem;
+    float* z = xin + w;
+    float* sg = z + w;
+    float* ds = sg + w;
+    float* P = ds + w;
+    float* Q = P + w * w;
+    const long long row = blockIdx.x;  // b * G + g
+    const int g = (int)(row % G);
+    const int b = (int)(row / G);
+    const int t = threadIdx.x;
+    const long long L = (long long)G * skip;
+    const float* Zb = Z + (long long)b * L * w;
+    const int m = G - 1 - g;
+    if (t < w) rrev[((long long)b * G + m) * w + t] = (m == 0) ? Gv[(long long)b * w + t] : 0.f;
+    if (g == 0) return;  // uniform over the workgroup
+    if (t < w) xin[t] = Zb[((long long)g * skip - 1) * w + t];
+    __syncthreads();
+    const float* Pf = block_product<true>(W, nullptr, Zb, xin, z, sg, ds, P, Q, g, w, skip, act,
+                                          true);
+    float* Ab = A + ((long long)b * G + (G - g)) * w * w;
+    for (int idx = t; idx < w * w; idx += kThreads)
+        Ab[idx] = Pf[idx] + ((idx / w == idx - (idx / w) * w) ? 1.f : 0.f);
+}
+
+// Adjoints inside block g from the block-output adjoint mu_g (natural order
+// [B, G, w]): Lambda[gs+s-1] = mu_g and, going down the block,
+// lambda_{j-1} = diag(sigma'(Z_{j-1})) W_j^T lambda_j.  Block 0 also gives
+// dz0 = diag(sigma'(z0)) W_0^T lambda_0 + mu_0 (the skip from z0).
+__global__ __launch_bounds__(kThreads) void resnet_intra_adjoint_kernel(
+    const float* __restrict__ W, const float* __restrict__ z0, const float* __restrict__ Z,
+    const float* __restrict__ mu, float* __restrict__ Lambda, float* __restrict__ dz0, int G,
+    int w, int skip, int act) {
+    __shared__ float lam[kMaxWidth];
+    const long long row = blockIdx.x;  // b * G + g
+    const int g = (int)(row % G);
+    const int b = (int)(row / G);
+    const int t = threadIdx.x;
+    const long long L = (long long)G * skip;
+    const float* Zb = Z + (long long)b * L * w;
+    float* Lb = Lambda + (long long)b * L * w;
+    const long long jl = (long long)g * skip + skip - 1;
+    float mu_t = 0.f;
+    if (t < w) {
+        mu_t = mu[row * w + t];
+        lam[t] = mu_t;
+        Lb[jl * w + t] = mu_t;
+    }
+    __syncthreads();
+    const int lo = (g == 0) ? 0 : 1;  // block 0 also goes through layer 0 into z0
+    for (int tt = skip - 1; tt >= lo; --tt) {
+        const long long j = (long long)g * skip + tt;
+        const float* Wj = W + j * w * w;
+        float v = 0.f;
+        if (t < w) {
+            const float zin = (j == 0) ? z0[(long long)b * w + t] : Zb[(j - 1) * w + t];
+            float d;
+            act_fn(act, zin, &d);
+            float s = 0.f;
+            for (int k = 0; k < w; ++k) s = fmaf(Wj[(long long)k * w + t], lam[k], s);
+            v = d * s;
+        }
+        __syncthreads();
+        if (t < w) {
+            if (j >= 1) {
+                lam[t] = v;
+                Lb[(j - 1) * w + t] = v;
+            } else {
+                dz0[(long long)b * w + t] = v + mu_t;
+            }
+        }
+        __syncthreads();
+    }
+}
+
+size_t block_lds_bytes(int w) { return (4 * (size_t)w + 2 * (size_t)w * w) * sizeof(float); }
+
+}  // namespace
+
+// Dynamic LDS beyond 64 KiB (w > 90) must be allowed per kernel first.
+template <class K>
+hipError_t allow_lds(K kernel, size_t bytes) {
+    if (bytes <= 65536) return hipSuccess;
+    return hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)bytes);
+}
+
+hipError_t launch_resnet_block_eval(const float* W, const float* bias, const float* z0,
+                                    const float* X, float* A, float* r, unsigned* red, int B,
+                                    int G, int w, int skip, int act, hipStream_t stream) {
+    const hipError_t e = allow_lds(resnet_block_eval_kernel, block_lds_bytes(w));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(resnet_block_eval_kernel, dim3((unsigned)((long long)B * G)),
+                       dim3(kThreads), block_lds_bytes(w), stream, W, bias, z0, X, A, r, red, G,
+                       w, skip, act);
+    return hipGetLastError();
+}
+
+hipError_t launch_resnet_initial_guess(const float* W, const float* bias, const float* z0,
+                                       float* X, int B, int G, int w, int skip, int act,
+                                       hipStream_t stream) {
+    hipLaunchKernelGGL(resnet_initial_guess_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream,
+                       W, bias, z0, X, G, w, skip, act);
+    return hipGetLastError();
+}
+
+hipError_t launch_resnet_expand(const float* W, const float* bias, const float* z0,
+                                const float* X, float* Z, int B, int G, int w, int skip, int act,
+                                hipStream_t stream) {
+    hipLaunchKernelGGL(resnet_expand_kernel, dim3((unsigned)((long long)B * G)), dim3(kThreads),
+                       0, stream, W, bias, z0, X, Z, G, w, skip, act);
+    return hipGetLastError();
+}
+
+hipError_t launch_resnet_block_jac(const float* W, const float* z0, const float* Z,
+                                   const float* Gv, float* A, float* rrev, int B, int G, int w,
+                                   int skip, int act, hipStream_t stream) {
+    const hipError_t e = allow_lds(resnet_block_jac_kernel, block_lds_bytes(w));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(resnet_block_jac_kernel, dim3((unsigned)((long long)B * G)),
+                       dim3(kThreads), block_lds_bytes(w), stream, W, z0, Z, Gv, A, rrev, G, w,
+                       skip, act);
+    return hipGetLastError();
+}
+
+hipError_t launch_resnet_intra_adjoint(const float* W, const float* z0, const float* Z,
+                                       const float* mu, float* Lambda, float* dz0, int B, int G,
+                                       int w, int skip, int act, hipStream_t stream) {
+    hipLaunchKernelGGL(resnet_intra_adjoint_kernel, dim3((unsigned)((long long)B * G)),
+                       dim3(kThreads), 0, stream, W, z0, Z, mu, Lambda, dz0, G, w, skip, act);
+    return hipGetLastError();
+}
+
+}  // namespace deeppcr

@@ -14,6 +14,7 @@ from dataclasses import dataclass
 OK, EINVAL, ENOCONV, ENONFINITE, EHIP, EWORKSPACE = range(6)
 TANH_MLP, TANH_RESIDUAL, SIGMOID_MLP, SIGMOID_RESIDUAL, RELU_MLP, RELU_RESIDUAL = range(6)
 OP_PCR, OP_FWD, OP_BWD = 0, 1, 2
+ACT_TANH, ACT_SIGMOID, ACT_RELU = 0, 1, 2
 KCLASS_PCR_LEVEL, KCLASS_LAYER, KCLASS_UPDATE, KCLASS_WGRAD, KCLASS_OTHER, KCLASS_SEQUENTIAL = range(6)
 KCLASS_NAMES = ("pcr_level", "layer", "update", "wgrad", "other", "sequential")
 MAX_WIDTH = 128
@@ -43,6 +44,12 @@ SIGNATURES = {
     "deeppcr_mlp_backward": (_c.c_int, [_c.c_void_p] * 9 + [_c.c_int, _c.c_int, _c.c_int,
                                                            _c.c_int, _c.c_float, _c.c_void_p,
                                                            _c.c_size_t, _c.c_void_p]),
+    "deeppcr_resnet_workspace_bytes": (_c.c_size_t, [_c.c_int] * 5),
+    "deeppcr_resnet_forward": (_c.c_int, [_c.c_void_p] * 4 + [_c.c_int] * 5 +
+                               [_c.c_float, _c.c_int, _c.c_void_p, _c.c_void_p, _c.c_size_t,
+                                _c.POINTER(_c.c_int), _c.POINTER(_c.c_float), _c.c_void_p]),
+    "deeppcr_resnet_backward": (_c.c_int, [_c.c_void_p] * 8 + [_c.c_int] * 5 +
+                                [_c.c_void_p, _c.c_size_t, _c.c_void_p]),
     "deeppcr_seq_forward": (_c.c_int, [_c.c_void_p] * 4 + [_c.c_int] * 4 + [_c.c_float, _c.c_int,
                                                                           _c.c_void_p]),
     "deeppcr_seq_backward": (_c.c_int, [_c.c_void_p] * 7 + [_c.c_int] * 4 + [_c.c_float, _c.c_int,
@@ -238,6 +245,70 @@ def deeppcr_mlp_backward(W, bias, z0, Z, G, layer: int = TANH_MLP, alpha: float 
                                     int(layer), float(alpha), _ptr(ws), nbytes, _stream(stream))
     if st != OK:
         raise DeepPCRError(st, "deeppcr_mlp_backward")
+    return Lambda, dz0, dW, db
+
+
+def resnet_workspace_bytes(op: int, B: int, L: int, w: int, skip: int) -> int:
+    return int(lib().deeppcr_resnet_workspace_bytes(op, B, L, w, skip))
+
+
+def deeppcr_resnet_forward(W, bias, z0, skip: int, act: int = ACT_RELU, Z=None,
+                           tol: float = 1e-5, max_iter: int = 20, Z_init=None, workspace=None,
+                           stream=None) -> ForwardResult:
+    """Newton + PCR forward pass of the collapsed-skip ResNet; raises on
+    EINVAL/EHIP/EWORKSPACE and returns ENOCONV / ENONFINITE in ``status``."""
+    torch = _torch()
+    L, w, _ = W.shape
+    B = z0.shape[0]
+    _check(W, (L, w, w), "W")
+    _check(bias, (L, w), "bias")
+    _check(z0, (B, w), "z0")
+    if Z is None:
+        Z = torch.empty((B, L, w), dtype=torch.float32, device=z0.device)
+    _check(Z, (B, L, w), "Z")
+    if Z_init is not None:
+        _check(Z_init, (B, L, w), "Z_init")
+    n = resnet_workspace_bytes(OP_FWD, B, L, w, skip)
+    if workspace is None:
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=z0.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    iters = ctypes.c_int(0)
+    last = ctypes.c_float(0.0)
+    st = lib().deeppcr_resnet_forward(_ptr(W), _ptr(bias), _ptr(z0), _ptr(Z), B, L, w, int(skip),
+                                      int(act), float(tol), int(max_iter), _ptr(Z_init),
+                                      _ptr(workspace), nbytes, ctypes.byref(iters),
+                                      ctypes.byref(last), _stream(stream))
+    if st not in (OK, ENOCONV, ENONFINITE):
+        raise DeepPCRError(st, "deeppcr_resnet_forward")
+    return ForwardResult(Z, iters.value, last.value, st)
+
+
+def deeppcr_resnet_backward(W, z0, Z, G, skip: int, act: int = ACT_RELU, Lambda=None, dz0=None,
+                            dW=None, db=None, workspace=None, stream=None):
+    """Backward pass of the collapsed-skip ResNet; returns (Lambda, dz0, dW, db)."""
+    torch = _torch()
+    L, w, _ = W.shape
+    B = z0.shape[0]
+    for t, shp, n in ((W, (L, w, w), "W"), (z0, (B, w), "z0"), (Z, (B, L, w), "Z"),
+                      (G, (B, w), "G")):
+        _check(t, shp, n)
+    dev = z0.device
+    Lambda = torch.empty((B, L, w), dtype=torch.float32, device=dev) if Lambda is None else Lambda
+    dz0 = torch.empty((B, w), dtype=torch.float32, device=dev) if dz0 is None else dz0
+    dW = torch.empty((L, w, w), dtype=torch.float32, device=dev) if dW is None else dW
+    db = torch.empty((L, w), dtype=torch.float32, device=dev) if db is None else db
+    for t, shp, n in ((Lambda, (B, L, w), "Lambda"), (dz0, (B, w), "dz0"), (dW, (L, w, w), "dW"),
+                      (db, (L, w), "db")):
+        _check(t, shp, n)
+    n = resnet_workspace_bytes(OP_BWD, B, L, w, skip)
+    if workspace is None:
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=dev)
+    nbytes = workspace.numel() * workspace.element_size()
+    st = lib().deeppcr_resnet_backward(_ptr(W), _ptr(z0), _ptr(Z), _ptr(G), _ptr(Lambda),
+                                       _ptr(dz0), _ptr(dW), _ptr(db), B, L, w, int(skip),
+                                       int(act), _ptr(workspace), nbytes, _stream(stream))
+    if st != OK:
+        raise DeepPCRError(st, "deeppcr_resnet_backward")
     return Lambda, dz0, dW, db
 
 

@@ -37,10 +37,13 @@ class Workload:
     transpose: int = 1   # standalone solve: backward-pass (transposed) form
     passes: tuple = field(default=("fwd",))
     seed: int = 0
+    skip: int = 1        # collapsed-skip ResNet: layers per block
+    act: int = 2         # collapsed-skip ResNet activation: 0 tanh, 1 sigmoid, 2 ReLU
 
 
-# The five workloads the build is measured on (tanh MLPs / residual nets with
-# random weights, and a standalone block-bidiagonal solve).
+# The workloads the build is measured on (tanh MLPs / residual nets with
+# random weights, a standalone block-bidiagonal solve, and the collapsed-skip
+# ResNet).
 WORKLOADS = {
     "tiny_fwd": Workload("tiny_fwd", "mlp", B=1, L=16, w=4, passes=("fwd",)),
     "pcr_solve": Workload("pcr_solve", "pcr", B=64, L=1024, w=16, transpose=1,
@@ -50,6 +53,10 @@ WORKLOADS = {
     "resnet_fwd_bwd": Workload("resnet_fwd_bwd", "mlp", B=16, L=1024, w=128,
                                layer=TANH_RESIDUAL, alpha=0.1,
                                passes=("fwd", "bwd")),
+    # the paper's ResNet (App. A.3): width 16, ReLU, a skip every 4 layers,
+    # depth 1024, Newton + PCR forward and the transposed backward
+    "resnet_skip4_fwd_bwd": Workload("resnet_skip4_fwd_bwd", "resnet", B=64, L=1024, w=16,
+                                     passes=("fwd", "bwd"), skip=4, act=2),
 }
 
 
@@ -131,6 +138,8 @@ def random_system(B: int, L: int, w: int, seed: int, scale: float = 1.0) -> dict
 def workload_inputs(wl: Workload) -> dict:
     if wl.kind == "pcr":
         return pcr_inputs(wl.B, wl.L, wl.w, wl.seed)
+    if wl.kind == "resnet":
+        return resnet_inputs(wl.B, wl.L, wl.w, wl.seed)
     return mlp_inputs(wl.B, wl.L, wl.w, wl.seed)
 
 

@@ -184,3 +184,66 @@ def test_sequential_passes_reject_invalid_arguments():
     assert g(*P[:6], None, 2, 8, 4, 0, 1.0, 0, None) == E
     assert g(*P[:7], 2, 8, 4, -1, 1.0, 0, None) == E
     assert g(*P[:5], P[3], P[6], 2, 8, 4, 0, 1.0, 0, None) == E   # Lambda over Z
+
+
+def test_resnet_workspace_sizes():
+    f = deeppcr.resnet_workspace_bytes
+    B, L, w, skip = 3, 12, 5, 4
+    G = L // skip
+    up = lambda x: (x + 255) // 256 * 256
+    nA, nr = B * G * w * w * 4, B * G * w * 4
+    red = 3 * 256 * 4
+    assert f(deeppcr.OP_FWD, B, L, w, skip) == 2 * up(nA) + 3 * up(nr) + red
+    assert f(deeppcr.OP_BWD, B, L, w, skip) == 2 * up(nA) + 2 * up(nr) + red
+    assert f(deeppcr.OP_PCR, B, L, w, skip) == 0
+    for bad in ((B, 10, w, 4), (B, L, w, 0), (0, L, w, 4), (B, L, 129, 4)):
+        assert f(deeppcr.OP_FWD, *bad) == 0
+
+
+def _rfwd(W=P[0], b=P[1], z0=P[2], Z=P[3], B=2, L=8, w=4, skip=4, act=2, tol=1e-5, max_iter=20,
+          Zi=None, ws=P[5], nws=BIG):
+    it = ctypes.c_int(-1)
+    lu = ctypes.c_float(-1)
+    return deeppcr.lib().deeppcr_resnet_forward(W, b, z0, Z, B, L, w, skip, act, tol, max_iter,
+                                                Zi, ws, nws, ctypes.byref(it), ctypes.byref(lu),
+                                                None)
+
+
+def test_resnet_forward_rejects_invalid_arguments():
+    E = deeppcr.EINVAL
+    for k in ("W", "b", "z0", "Z", "ws"):
+        assert _rfwd(**{k: None}) == E
+    assert _rfwd(skip=0) == E
+    assert _rfwd(skip=3) == E            # L = 8 is not a multiple of 3
+    assert _rfwd(act=3) == E
+    assert _rfwd(act=-1) == E
+    assert _rfwd(tol=-1.0) == E
+    assert _rfwd(tol=float("nan")) == E
+    assert _rfwd(max_iter=0) == E
+    assert _rfwd(w=129) == E
+    assert _rfwd(Zi=ctypes.c_void_p(P[3].value + 4)) == E
+    assert _rfwd(ws=ctypes.c_void_p(P[1].value)) == E
+    assert _rfwd(nws=100) == deeppcr.EWORKSPACE
+
+
+def _rbwd(ptrs=None, B=2, L=8, w=4, skip=2, act=0, ws=P[10], nws=BIG):
+    p = list(P[:8]) if ptrs is None else ptrs
+    return deeppcr.lib().deeppcr_resnet_backward(*p, B, L, w, skip, act, ws, nws, None)
+
+
+def test_resnet_backward_rejects_invalid_arguments():
+    E = deeppcr.EINVAL
+    for i in range(8):
+        p = list(P[:8])
+        p[i] = None
+        assert _rbwd(p) == E
+    p = list(P[:8])
+    p[4] = P[2]  # Lambda over Z
+    assert _rbwd(p) == E
+    p = list(P[:8])
+    p[6] = ctypes.c_void_p(P[7].value - 16)  # dW runs into db
+    assert _rbwd(p) == E
+    assert _rbwd(skip=3) == E
+    assert _rbwd(act=5) == E
+    assert _rbwd(ws=ctypes.c_void_p(P[0].value)) == E
+    assert _rbwd(nws=1) == deeppcr.EWORKSPACE

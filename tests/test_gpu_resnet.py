@@ -1,0 +1,156 @@
+"""GPU parity of the collapsed-skip ResNet path (App. A.3) against the CPU
+oracle: forward by Newton + PCR on the block chain, backward by the
+transposed block solve plus back-propagation inside the blocks."""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import resnet_oracle as R
+from paper_2309_16318_amd import deeppcr, synth
+from tests._util import normwise_rel_err
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-4
+
+torch = pytest.importorskip("torch")
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch.device("cuda:0")
+
+
+def g(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+
+def h(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def _fwd(d, dev, skip, act, tol=1e-5, max_iter=20, Z_init=None):
+    return deeppcr.deeppcr_resnet_forward(g(d["W"], dev), g(d["bias"], dev), g(d["z0"], dev),
+                                          skip=skip, act=act, tol=tol, max_iter=max_iter,
+                                          Z_init=Z_init)
+
+
+RELU, TANH, SIG = R.ACT_RELU, R.ACT_TANH, R.ACT_SIGMOID
+FWD_CASES = [(16, 256, 4, 4, RELU), (16, 1024, 8, 4, RELU), (4, 64, 3, 4, TANH),
+             (8, 40, 2, 2, SIG), (32, 96, 2, 3, TANH), (64, 32, 2, 4, RELU),
+             (128, 16, 2, 4, TANH), (17, 30, 2, 5, RELU), (16, 4, 2, 4, RELU),
+             (16, 8, 2, 4, SIG), (3, 9, 2, 1, TANH), (100, 12, 2, 3, RELU), (1, 20, 3, 4, RELU)]
+
+
+@pytest.mark.parametrize("w,L,B,skip,act", FWD_CASES)
+def test_resnet_forward(dev, w, L, B, skip, act):
+    _say(f"resnet forward w={w} L={L} B={B} skip={skip} act={act}")
+    d = synth.resnet_inputs(B, L, w, seed=1000 + w + L + skip + act)
+    res = _fwd(d, dev, skip, act)
+    assert res.status == deeppcr.OK
+    ref = R.resnet_seq_forward(act, skip, d["W"], d["bias"], d["z0"])
+    err = normwise_rel_err(h(res.Z), ref)
+    _, k_ref, ok, _ = R.resnet_newton_forward(act, skip, d["W"], d["bias"], d["z0"], 1e-5, 20)
+    _say(f"  err {err:.2e}; gpu iters {res.iters}, oracle {k_ref}")
+    assert err <= TOL
+    assert ok and abs(res.iters - k_ref) <= 1
+
+
+@pytest.mark.parametrize("w", [4, 16, 64])
+def test_resnet_fixed_count_and_prefix_exactness(dev, w):
+    """tol = 0 runs exactly max_iter solves; from a zero start, k solves make
+    the first k blocks (and the rows computed from them) exact."""
+    skip, G, B = 4, 9, 2
+    L = skip * G
+    d = synth.resnet_inputs(B, L, w, seed=1100 + w)
+    ref = R.resnet_seq_forward(RELU, skip, d["W"], d["bias"], d["z0"])
+    for k in (1, 3, 5):
+        res = _fwd(d, dev, skip, RELU, tol=0.0, max_iter=k,
+                   Z_init=torch.zeros((B, L, w), device=dev))
+        assert res.status == deeppcr.OK and res.iters == k
+        assert normwise_rel_err(h(res.Z)[:, :k * skip], ref[:, :k * skip]) <= 1e-5
+        Zk, _, _, _ = R.resnet_newton_forward(RELU, skip, d["W"], d["bias"], d["z0"], 0.0, k,
+                                              Z_init=np.zeros((B, L, w)))
+        assert normwise_rel_err(h(res.Z), Zk) <= TOL
+
+
+def test_resnet_warm_start_from_solution(dev):
+    d = synth.resnet_inputs(3, 64, 16, seed=1200)
+    ref = R.resnet_seq_forward(RELU, 4, d["W"], d["bias"], d["z0"]).astype(np.float32)
+    res = _fwd(d, dev, 4, RELU, Z_init=g(ref, dev))
+    assert res.status == deeppcr.OK and res.iters == 1
+    assert normwise_rel_err(h(res.Z), ref) <= TOL
+
+
+def test_resnet_reports_no_convergence_and_non_finite(dev):
+    d = dict(synth.resnet_inputs(2, 64, 16, seed=1300))
+    res = _fwd(d, dev, 4, RELU, tol=1e-5, max_iter=1)
+    assert res.status == deeppcr.ENOCONV and res.iters == 1
+    d["bias"] = d["bias"].copy()
+    d["bias"][9, 2] = np.nan
+    res = _fwd(d, dev, 4, RELU)
+    assert res.status == deeppcr.ENONFINITE and res.iters == 1
+
+
+def _bwd_check(d, Z32, dev, skip, act, tol=TOL):
+    lam, dz0, dW, db = deeppcr.deeppcr_resnet_backward(g(d["W"], dev), g(d["z0"], dev),
+                                                       g(Z32, dev), g(d["G"], dev), skip=skip,
+                                                       act=act)
+    rl, rz, rW, rb = R.resnet_seq_backward(act, skip, d["W"], d["bias"], d["z0"], Z32, d["G"])
+    adj = normwise_rel_err(np.concatenate([h(dz0)[:, None], h(lam)], 1),
+                           np.concatenate([rz[:, None], rl], 1))
+    errs = (adj, normwise_rel_err(h(dW), rW, axes="all"), normwise_rel_err(h(db), rb, axes="all"))
+    _say(f"  backward errs adjoints {errs[0]:.2e} dW {errs[1]:.2e} db {errs[2]:.2e}")
+    assert max(errs) <= tol
+
+
+@pytest.mark.parametrize("w,L,B,skip,act", FWD_CASES)
+def test_resnet_backward(dev, w, L, B, skip, act):
+    _say(f"resnet backward w={w} L={L} B={B} skip={skip} act={act}")
+    d = synth.resnet_inputs(B, L, w, seed=1400 + w + L + skip + act)
+    Z32 = R.resnet_seq_forward(act, skip, d["W"], d["bias"], d["z0"]).astype(np.float32)
+    _bwd_check(d, Z32, dev, skip, act)
+
+
+def test_resnet_forward_then_backward_paper_shape(dev):
+    """w = 16, skip 4, ReLU, L = 1024 (the paper's deepest ResNet), B = 64:
+    the GPU backward reads the GPU forward's states."""
+    wl = synth.WORKLOADS["resnet_skip4_fwd_bwd"]
+    _say(f"resnet skip-4 forward + backward B={wl.B} L={wl.L} w={wl.w}")
+    d = synth.workload_inputs(wl)
+    res = _fwd(d, dev, wl.skip, wl.act, wl.tol, wl.max_iter)
+    assert res.status == deeppcr.OK
+    ref = R.resnet_seq_forward(wl.act, wl.skip, d["W"], d["bias"], d["z0"])
+    err = normwise_rel_err(h(res.Z), ref)
+    _say(f"  forward err {err:.2e}, iters {res.iters}")
+    assert err <= TOL and res.iters <= 12
+    lam, dz0, dW, db = deeppcr.deeppcr_resnet_backward(g(d["W"], dev), g(d["z0"], dev), res.Z,
+                                                       g(d["G"], dev), skip=wl.skip, act=wl.act)
+    rl, rz, rW, rb = R.resnet_seq_backward(wl.act, wl.skip, d["W"], d["bias"], d["z0"], ref,
+                                           d["G"])
+    adj = normwise_rel_err(np.concatenate([h(dz0)[:, None], h(lam)], 1),
+                           np.concatenate([rz[:, None], rl], 1))
+    eW = normwise_rel_err(h(dW), rW, axes="all")
+    eb = normwise_rel_err(h(db), rb, axes="all")
+    _say(f"  backward errs adjoints {adj:.2e} dW {eW:.2e} db {eb:.2e}")
+    assert max(adj, eW, eb) <= TOL
+
+
+def test_resnet_deterministic(dev):
+    d = synth.resnet_inputs(4, 128, 16, seed=1500)
+    a = h(_fwd(d, dev, 4, RELU).Z)
+    b = h(_fwd(d, dev, 4, RELU).Z)
+    assert np.array_equal(a, b)
+    Z = g(a, dev)
+    x = [h(t) for t in deeppcr.deeppcr_resnet_backward(g(d["W"], dev), g(d["z0"], dev), Z,
+                                                        g(d["G"], dev), skip=4, act=RELU)]
+    y = [h(t) for t in deeppcr.deeppcr_resnet_backward(g(d["W"], dev), g(d["z0"], dev), Z,
+                                                        g(d["G"], dev), skip=4, act=RELU)]
+    assert all(np.array_equal(p, q) for p, q in zip(x, y))
