@@ -60,6 +60,28 @@ def make_step(wl, dev):
                                            workspace=ws)
         return step, info
 
+    if wl.kind == "resnet":
+        wsf = torch.empty(deeppcr.resnet_workspace_bytes(deeppcr.OP_FWD, B, L, w, wl.skip),
+                          dtype=torch.uint8, device=dev)
+        wsb = torch.empty(deeppcr.resnet_workspace_bytes(deeppcr.OP_BWD, B, L, w, wl.skip),
+                          dtype=torch.uint8, device=dev)
+        Z = torch.empty((B, L, w), dtype=torch.float32, device=dev)
+        outs = dict(Lambda=torch.empty((B, L, w), dtype=torch.float32, device=dev),
+                    dz0=torch.empty((B, w), dtype=torch.float32, device=dev),
+                    dW=torch.empty((L, w, w), dtype=torch.float32, device=dev),
+                    db=torch.empty((L, w), dtype=torch.float32, device=dev))
+
+        def step():
+            res = deeppcr.deeppcr_resnet_forward(t["W"], t["bias"], t["z0"], wl.skip, wl.act, Z,
+                                                 tol=wl.tol, max_iter=wl.max_iter,
+                                                 workspace=wsf)
+            if res.status != deeppcr.OK:
+                raise RuntimeError(f"forward status {res.status}")
+            info["iters"] = res.iters
+            deeppcr.deeppcr_resnet_backward(t["W"], t["z0"], Z, t["G"], wl.skip, wl.act,
+                                            workspace=wsb, **outs)
+        return step, info
+
     op_ws = {}
     Z = torch.empty((B, L, w), dtype=torch.float32, device=dev)
     if "fwd" in wl.passes:
@@ -114,6 +136,11 @@ def cpu_baseline(wl, budget_s):
         if wl.kind == "pcr":
             oracle.seq_solve(d["J"], d["r"], bool(wl.transpose))
             return
+        if wl.kind == "resnet":
+            R = oracle.resnet_oracle
+            Z = R.resnet_seq_forward(wl.act, wl.skip, d["W"], d["bias"], d["z0"])
+            R.resnet_seq_backward(wl.act, wl.skip, d["W"], d["bias"], d["z0"], Z, d["G"])
+            return
         Z = Zs
         if "fwd" in wl.passes:
             Z = oracle.seq_forward(wl.layer, wl.alpha, d["W"], d["bias"], d["z0"])
@@ -129,6 +156,7 @@ def cpu_baseline(wl, budget_s):
         if el >= budget_s:
             break
     parts = "+".join(("seq_solve",) if wl.kind == "pcr" else
+                     ("resnet_seq_forward", "resnet_seq_backward") if wl.kind == "resnet" else
                      tuple(p for p, on in (("seq_forward", "fwd" in wl.passes),
                                            ("seq_backward", "bwd" in wl.passes)) if on))
     return {"value": B * L * reps / el, "unit": "layer-steps/s", "cores": int(cores),
@@ -200,10 +228,19 @@ def main():
     roof["avg_launch_us"] = round(lvl["ms"] * 1e3 / max(lvl["launches"], 1), 3)
     roof["launches"] = lvl["launches"]
 
+    layer_names = ["tanh_mlp", "tanh_residual", "sigmoid_mlp", "sigmoid_residual", "relu_mlp",
+                   "relu_residual"]
+    if wl.kind == "mlp":
+        layer = layer_names[wl.layer]
+    elif wl.kind == "resnet":
+        layer = f"{['tanh', 'sigmoid', 'relu'][wl.act]}_preact_skip{wl.skip}"
+    else:
+        layer = None
     cfg = {"workload": wl.name, "B": wl.B, "L": wl.L, "w": wl.w,
-           "layer": ("tanh_mlp" if wl.layer == 0 else "tanh_residual") if wl.kind == "mlp"
-           else None, "alpha": wl.alpha if wl.kind == "mlp" else None,
+           "layer": layer, "alpha": wl.alpha if wl.kind == "mlp" else None,
            "passes": list(wl.passes), "newton_iters": info["iters"],
+           **({"skip": wl.skip, "unknowns_per_system": wl.L // wl.skip}
+              if wl.kind == "resnet" else {}),
            "newton_tol": wl.tol if "fwd" in wl.passes else None,
            "parallelism": "single-gpu"}
     out = {

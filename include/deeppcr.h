@@ -237,6 +237,21 @@ int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, con
                             void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The collapsed-skip ResNet's sequential passes on the GPU (the baseline of
+ * the paper's ResNet timings, Sec. 4.2): the network of deeppcr_resnet_forward
+ * applied layer after layer, and its reverse-mode adjoints (Lambda, dz0; no
+ * parameter gradients).  One workgroup walks the layers of one system;
+ * launch_per_layer = 0 runs all layers in one launch, 1 launches once per
+ * layer.  No workspace.
+ */
+int deeppcr_resnet_seq_forward(const float* W, const float* bias, const float* z0, float* Z,
+                               int B, int L, int w, int skip, int act, int launch_per_layer,
+                               void* stream);
+int deeppcr_resnet_seq_backward(const float* W, const float* z0, const float* Z, const float* G,
+                                float* Lambda, float* dz0, int B, int L, int w, int skip, int act,
+                                int launch_per_layer, void* stream);
+
+/*
  * Sequential passes: the layer-by-layer baseline the paper measures DeepPCR
  * against (Sec. 4.1), on the same GPU.  Forward: Z[:, l] = f_l(Z[:, l-1]) for
  * l = 0..L-1 (Eq. 1 applied one step at a time).  Backward: the adjoints of

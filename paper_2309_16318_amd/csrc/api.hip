@@ -692,6 +692,59 @@ int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, con
     return DEEPPCR_OK;
 }
 
+int deeppcr_resnet_seq_forward(const float* W, const float* bias, const float* z0, float* Z,
+                               int B, int L, int w, int skip, int act, int launch_per_layer,
+                               void* stream) {
+    if (!W || !bias || !z0 || !Z || !resnet_shape_ok(B, L, w, skip, act) ||
+        (launch_per_layer != 0 && launch_per_layer != 1))
+        return DEEPPCR_EINVAL;
+    const size_t nv = (size_t)B * L * w * 4;
+    if (overlaps(Z, nv, W, (size_t)L * w * w * 4) || overlaps(Z, nv, bias, (size_t)L * w * 4) ||
+        overlaps(Z, nv, z0, (size_t)B * w * 4))
+        return DEEPPCR_EINVAL;
+    hipStream_t st = (hipStream_t)stream;
+    const int step = launch_per_layer ? 1 : L;
+    for (int l0 = 0; l0 < L; l0 += step) {
+        const int l1 = l0 + step;
+        const double n = (double)(l1 - l0);
+        hipError_t e = timed(DEEPPCR_KCLASS_SEQUENTIAL, 4.0 * n * ((double)w * w + 2.0 * B * w),
+                             2.0 * B * n * w * w, st, [&] {
+                                 return launch_resnet_seq_forward(W, bias, z0, Z, B, L, w, skip,
+                                                                  act, l0, l1, st);
+                             });
+        if (e != hipSuccess) return hip_fail(e, "resnet_seq_forward");
+    }
+    return DEEPPCR_OK;
+}
+
+int deeppcr_resnet_seq_backward(const float* W, const float* z0, const float* Z, const float* G,
+                                float* Lambda, float* dz0, int B, int L, int w, int skip, int act,
+                                int launch_per_layer, void* stream) {
+    if (!W || !z0 || !Z || !G || !Lambda || !dz0 || !resnet_shape_ok(B, L, w, skip, act) ||
+        (launch_per_layer != 0 && launch_per_layer != 1))
+        return DEEPPCR_EINVAL;
+    const size_t nv = (size_t)B * L * w * 4, nb = (size_t)B * w * 4;
+    const void* ins[] = {W, z0, Z, G};
+    const size_t nins[] = {(size_t)L * w * w * 4, nb, nv, nb};
+    for (int j = 0; j < 4; ++j)
+        if (overlaps(Lambda, nv, ins[j], nins[j]) || overlaps(dz0, nb, ins[j], nins[j]))
+            return DEEPPCR_EINVAL;
+    if (overlaps(Lambda, nv, dz0, nb)) return DEEPPCR_EINVAL;
+    hipStream_t st = (hipStream_t)stream;
+    const int step = launch_per_layer ? 1 : L;
+    for (int l1 = L; l1 > 0; l1 -= step) {
+        const int l0 = l1 - step;
+        const double n = (double)(l1 - l0);
+        hipError_t e = timed(DEEPPCR_KCLASS_SEQUENTIAL, 4.0 * n * ((double)w * w + 3.0 * B * w),
+                             2.0 * B * n * w * w, st, [&] {
+                                 return launch_resnet_seq_backward(W, z0, Z, G, Lambda, dz0, B, L,
+                                                                   w, skip, act, l0, l1, st);
+                             });
+        if (e != hipSuccess) return hip_fail(e, "resnet_seq_backward");
+    }
+    return DEEPPCR_OK;
+}
+
 int deeppcr_seq_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
                         int L, int w, int layer, float alpha, int launch_per_layer, void* stream) {
     if (!W || !bias || !z0 || !Z || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;

@@ -45,6 +45,13 @@ __device__ inline float activate(int layer, float a, float* d) {
     return (a > 0.f || __builtin_isnan(a)) ? a : 0.f;
 }
 
+// Orders the LDS accesses of one wave (a barrier for the wave only).
+__device__ inline void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // A batch of w x w blocks addressed as base + b*bstride + m*rstride (floats).
 // Row strides may be negative (the transposed system is stored reversed).
 // trans = 1: element (i, k) of block m is stored at [k*w + i].
@@ -225,6 +232,17 @@ hipError_t launch_resnet_block_jac(const float* W, const float* z0, const float*
 hipError_t launch_resnet_intra_adjoint(const float* W, const float* z0, const float* Z,
                                        const float* mu, float* Lambda, float* dz0, int B, int G,
                                        int w, int skip, int act, hipStream_t stream);
+
+// The collapsed-skip ResNet's sequential passes (one workgroup per system):
+// forward layers l0 .. l1-1, and the reverse-mode adjoints over layers l1-1
+// down to l0 (Lambda, and dz0 when l0 = 0).
+hipError_t launch_resnet_seq_forward(const float* W, const float* bias, const float* z0, float* Z,
+                                     int B, int L, int w, int skip, int act, int l0, int l1,
+                                     hipStream_t stream);
+hipError_t launch_resnet_seq_backward(const float* W, const float* z0, const float* Z,
+                                      const float* G, float* Lambda, float* dz0, int B, int L,
+                                      int w, int skip, int act, int l0, int l1,
+                                      hipStream_t stream);
 
 // ------------------------------------------------------------- tiny path
 // Whole Newton + PCR forward solve in one workgroup with everything in LDS,

@@ -140,12 +140,6 @@ __device__ inline Seg decode_segment(long long item, const LevelPlan& p, int L) 
     return g;
 }
 
-__device__ inline void wave_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 // ---- one wave per segment, w = 16 or 32 -----------------------------------
 // Lane layout "R": lane (i = lane % W, g = lane / W) holds row i of a block at
 // the NV columns col(v) = 4*NG*(v/4) + 4*g + v%4 (NG = 64 / W lane groups).

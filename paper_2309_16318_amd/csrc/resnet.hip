@@ -266,6 +266,149 @@ __global__ __launch_bounds__(kThreads) void resnet_intra_adjoint_kernel(
 
 size_t block_lds_bytes(int w) { return (4 * (size_t)w + 2 * (size_t)w * w) * sizeof(float); }
 
+// ---- one wave per (system, block), w = 16 or 32 ----------------------------
+// Lane l owns row i = l / LPR of the running product P and its NC columns
+// c0 = (l % LPR) * NC ..; the next factor's row, W_j[i, :] scaled by
+// sigma'(z), comes from global memory (L2-resident, shared by every system)
+// and the previous product's rows from the wave's LDS copy.  Only wave-level
+// barriers; four independent waves per workgroup.
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <int W>
+struct BlockWaveShape {
+    static constexpr int LPR = 64 / W;     // lanes per product row
+    static constexpr int NC = W / LPR;     // columns per lane (4 for w = 16, 16 for w = 32)
+};
+
+template <int W>
+struct alignas(16) BlockWaveLds {
+    float P[W * W];
+    float xin[W], z[W], sg[W], ds[W];
+};
+
+// BWD = false: the forward block evaluation at the iterate (as
+// resnet_block_eval_kernel).  BWD = true: the backward blocks at the stored
+// states and the reversed right-hand side (as resnet_block_jac_kernel).
+template <int W, bool BWD>
+__global__ __launch_bounds__(256) void resnet_block_wave(
+    const float* __restrict__ Wt, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ S, const float* __restrict__ Gv, float* __restrict__ A,
+    float* __restrict__ r, unsigned* __restrict__ red, int B, int G, int skip, int act) {
+    using SH = BlockWaveShape<W>;
+    constexpr int NC = SH::NC;
+    __shared__ BlockWaveLds<W> lds_all[4];
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    if (!BWD && blockIdx.x == 0)
+        for (int k = threadIdx.x; k < 2 * kRedShards; k += 256) red[k] = 0u;
+    const long long item = (long long)blockIdx.x * 4 + wv;  // b * G + g
+    if (item >= (long long)B * G) return;  // whole wave
+    BlockWaveLds<W>& lds = lds_all[wv];
+    const int g = (int)(item % G);
+    const int b = (int)(item / G);
+    const long long L = (long long)G * skip;
+    const int i = lane / SH::LPR;
+    const int c0 = (lane % SH::LPR) * NC;
+    // S: forward, the iterate X [B, G, W]; backward, the stored states Z [B, L, W]
+    const float* Zb = S + (long long)b * L * W;
+    if (BWD) {
+        const int m = G - 1 - g;
+        if (lane < W) r[((long long)b * G + m) * W + lane] = (m == 0) ? Gv[(long long)b * W + lane] : 0.f;
+        if (g == 0) return;
+    }
+    if (lane < W) {
+        const float x = BWD ? Zb[((long long)g * skip - 1) * W + lane]
+                            : (g == 0 ? z0[(long long)b * W + lane] : S[(item - 1) * W + lane]);
+        lds.xin[lane] = x;
+        lds.z[lane] = x;
+    }
+    const bool jac = g > 0;
+    float pr[NC];
+    for (int tt = 0; tt < skip; ++tt) {
+        const long long j = (long long)g * skip + tt;
+        wave_sync();
+        if (lane < W) {
+            const float zin = BWD ? (tt == 0 ? lds.xin[lane] : Zb[(j - 1) * W + lane]) : lds.z[lane];
+            float d;
+            lds.sg[lane] = act_fn(act, zin, &d);
+            lds.ds[lane] = d;
+        }
+        wave_sync();
+        float wr[W];
+        const float* wrow = Wt + (j * W + i) * W;
+#pragma unroll
+        for (int q = 0; q < W / 4; ++q) {
+            const v4f x = *reinterpret_cast<const v4f*>(wrow + 4 * q);
+            wr[4 * q] = x[0];
+            wr[4 * q + 1] = x[1];
+            wr[4 * q + 2] = x[2];
+            wr[4 * q + 3] = x[3];
+        }
+        if (jac) {
+            if (tt == 0) {
+#pragma unroll
+                for (int c = 0; c < NC; ++c) pr[c] = wr[c0 + c] * lds.ds[c0 + c];
+            } else {
+                float pn[NC];
+#pragma unroll
+                for (int c = 0; c < NC; ++c) pn[c] = 0.f;
+#pragma unroll
+                for (int m = 0; m < W; ++m) {
+                    const float f = wr[m] * lds.ds[m];
+#pragma unroll
+                    for (int q = 0; q < NC / 4; ++q) {
+                        const v4f p4 = *reinterpret_cast<const v4f*>(lds.P + m * W + c0 + 4 * q);
+                        pn[4 * q] = fmaf(f, p4[0], pn[4 * q]);
+                        pn[4 * q + 1] = fmaf(f, p4[1], pn[4 * q + 1]);
+                        pn[4 * q + 2] = fmaf(f, p4[2], pn[4 * q + 2]);
+                        pn[4 * q + 3] = fmaf(f, p4[3], pn[4 * q + 3]);
+                    }
+                }
+#pragma unroll
+                for (int c = 0; c < NC; ++c) pr[c] = pn[c];
+            }
+        }
+        float a = 0.f;
+        if (!BWD) {
+#pragma unroll
+            for (int k = 0; k < W; ++k) a = fmaf(wr[k], lds.sg[k], a);
+            a += bias[j * W + i];
+        }
+        wave_sync();  // every read of P, sg, ds, z of this layer is done
+        if (jac) {
+#pragma unroll
+            for (int q = 0; q < NC / 4; ++q) {
+                v4f x = {pr[4 * q], pr[4 * q + 1], pr[4 * q + 2], pr[4 * q + 3]};
+                *reinterpret_cast<v4f*>(lds.P + i * W + c0 + 4 * q) = x;
+            }
+        }
+        if (!BWD && (lane % SH::LPR) == 0) lds.z[i] = a;
+    }
+    wave_sync();
+    if (!BWD && lane < W) r[item * W + lane] = (lds.z[lane] + lds.xin[lane]) - S[item * W + lane];
+    if (jac) {
+        float* Ab = A + (BWD ? ((long long)b * G + (G - g)) : item) * W * W + i * W + c0;
+#pragma unroll
+        for (int q = 0; q < NC / 4; ++q) {
+            v4f x = {pr[4 * q], pr[4 * q + 1], pr[4 * q + 2], pr[4 * q + 3]};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (c0 + 4 * q + e == i) x[e] += 1.f;
+            *reinterpret_cast<v4f*>(Ab + 4 * q) = x;
+        }
+    }
+}
+
+template <int W, bool BWD>
+hipError_t launch_block_wave(const float* Wt, const float* bias, const float* z0, const float* S,
+                             const float* Gv, float* A, float* r, unsigned* red, int B, int G,
+                             int skip, int act, hipStream_t stream) {
+    const long long items = (long long)B * G;
+    hipLaunchKernelGGL((resnet_block_wave<W, BWD>), dim3((unsigned)((items + 3) / 4)), dim3(256), 0,
+                       stream, Wt, bias, z0, S, Gv, A, r, red, B, G, skip, act);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 // Dynamic LDS beyond 64 KiB (w > 90) must be allowed per kernel first.
@@ -279,6 +422,12 @@ hipError_t allow_lds(K kernel, size_t bytes) {
 hipError_t launch_resnet_block_eval(const float* W, const float* bias, const float* z0,
                                     const float* X, float* A, float* r, unsigned* red, int B,
                                     int G, int w, int skip, int act, hipStream_t stream) {
+    if (w == 16)
+        return launch_block_wave<16, false>(W, bias, z0, X, nullptr, A, r, red, B, G, skip, act,
+                                            stream);
+    if (w == 32)
+        return launch_block_wave<32, false>(W, bias, z0, X, nullptr, A, r, red, B, G, skip, act,
+                                            stream);
     const hipError_t e = allow_lds(resnet_block_eval_kernel, block_lds_bytes(w));
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(resnet_block_eval_kernel, dim3((unsigned)((long long)B * G)),
@@ -306,6 +455,12 @@ hipError_t launch_resnet_expand(const float* W, const float* bias, const float* 
 hipError_t launch_resnet_block_jac(const float* W, const float* z0, const float* Z,
                                    const float* Gv, float* A, float* rrev, int B, int G, int w,
                                    int skip, int act, hipStream_t stream) {
+    if (w == 16)
+        return launch_block_wave<16, true>(W, nullptr, z0, Z, Gv, A, rrev, nullptr, B, G, skip,
+                                           act, stream);
+    if (w == 32)
+        return launch_block_wave<32, true>(W, nullptr, z0, Z, Gv, A, rrev, nullptr, B, G, skip,
+                                           act, stream);
     const hipError_t e = allow_lds(resnet_block_jac_kernel, block_lds_bytes(w));
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(resnet_block_jac_kernel, dim3((unsigned)((long long)B * G)),

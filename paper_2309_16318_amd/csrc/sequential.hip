@@ -132,7 +132,101 @@ __global__ __launch_bounds__(kThreads) void seq_backward_kernel(
     }
 }
 
+// Collapsed-skip ResNet, sequentially: Z_j = W_j sigma(Z_{j-1}) + b_j, plus
+// Z_{j-s} when (j+1) % s == 0, for layers l0 .. l1-1 (reading Z[:, l0-1] and
+// the block input Z[:, s*(l0/s) - 1], or z0).  The skip source (the last
+// block output) stays in LDS between layers.
+__global__ __launch_bounds__(kThreads) void resnet_seq_forward_kernel(
+    const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
+    float* __restrict__ Z, int L, int w, int skip, int act, int l0, int l1) {
+    const int b = blockIdx.x;
+    __shared__ float z[kMaxWidth], xs[kMaxWidth], sg[kMaxWidth], a[kMaxWidth];
+    const RowMap m = row_map(w);
+    const int src = (l0 / skip) * skip - 1;  // the current block's input row
+    for (int i = threadIdx.x; i < w; i += kThreads) {
+        z[i] = (l0 == 0) ? z0[(long long)b * w + i] : Z[((long long)b * L + l0 - 1) * w + i];
+        xs[i] = (src < 0) ? z0[(long long)b * w + i] : Z[((long long)b * L + src) * w + i];
+    }
+    for (int l = l0; l < l1; ++l) {
+        __syncthreads();
+        for (int i = threadIdx.x; i < w; i += kThreads) {
+            float d;
+            sg[i] = activate(2 * act, z[i], &d);
+        }
+        __syncthreads();
+        rows_dot(W + (long long)l * w * w, sg, a, w, m);
+        __syncthreads();
+        const bool sk = (l + 1) % skip == 0;
+        for (int i = threadIdx.x; i < w; i += kThreads) {
+            const float v = a[i] + bias[(long long)l * w + i] + (sk ? xs[i] : 0.f);
+            z[i] = v;
+            Z[((long long)b * L + l) * w + i] = v;
+            if (sk) xs[i] = v;
+        }
+    }
+}
+
+// Its reverse-mode pass over layers l1-1 down to l0, starting from
+// lambda_{l1-1} (G when l1 = L, else Lambda[:, l1-1]): Lambda[:, j] =
+// dLoss/dZ_j; layer j sends diag(sigma'(Z_{j-1})) W_j^T lambda_j to Z_{j-1},
+// and the first layer of a block adds to it the adjoint the block's skip
+// layer (row j+s-1, already final) sends to the block input; dz0 at l = 0.
+__global__ __launch_bounds__(kThreads) void resnet_seq_backward_kernel(
+    const float* __restrict__ W, const float* __restrict__ z0, const float* __restrict__ Z,
+    const float* __restrict__ G, float* __restrict__ Lambda, float* __restrict__ dz0, int L, int w,
+    int skip, int act, int l0, int l1) {
+    const int b = blockIdx.x;
+    __shared__ float lam[kMaxWidth], ds[kMaxWidth], nl[kMaxWidth];
+    const RowMap m = row_map(w);
+    float* Lb = Lambda + (long long)b * L * w;
+    for (int i = threadIdx.x; i < w; i += kThreads) {
+        const float v = (l1 == L) ? G[(long long)b * w + i] : Lb[(long long)(l1 - 1) * w + i];
+        lam[i] = v;
+        if (l1 == L) Lb[(long long)(L - 1) * w + i] = v;
+    }
+    for (int l = l1 - 1; l >= l0; --l) {
+        __syncthreads();
+        for (int i = threadIdx.x; i < w; i += kThreads) {
+            const float zin = (l == 0) ? z0[(long long)b * w + i] : Z[((long long)b * L + l - 1) * w + i];
+            float d;
+            activate(2 * act, zin, &d);
+            ds[i] = d;
+        }
+        __syncthreads();
+        cols_dot(W + (long long)l * w * w, lam, nl, w, m);
+        __syncthreads();
+        const bool first = l % skip == 0;  // first layer of a block: its input took the skip
+        for (int i = threadIdx.x; i < w; i += kThreads) {
+            // the same thread wrote row l + skip - 1 of Lambda earlier
+            const float v = nl[i] * ds[i] + (first ? Lb[(long long)(l + skip - 1) * w + i] : 0.f);
+            if (l >= 1) {
+                lam[i] = v;
+                Lb[(long long)(l - 1) * w + i] = v;
+            } else {
+                dz0[(long long)b * w + i] = v;
+            }
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_resnet_seq_forward(const float* W, const float* bias, const float* z0, float* Z,
+                                     int B, int L, int w, int skip, int act, int l0, int l1,
+                                     hipStream_t stream) {
+    hipLaunchKernelGGL(resnet_seq_forward_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, W,
+                       bias, z0, Z, L, w, skip, act, l0, l1);
+    return hipGetLastError();
+}
+
+hipError_t launch_resnet_seq_backward(const float* W, const float* z0, const float* Z,
+                                      const float* G, float* Lambda, float* dz0, int B, int L,
+                                      int w, int skip, int act, int l0, int l1,
+                                      hipStream_t stream) {
+    hipLaunchKernelGGL(resnet_seq_backward_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream,
+                       W, z0, Z, G, Lambda, dz0, L, w, skip, act, l0, l1);
+    return hipGetLastError();
+}
 
 hipError_t launch_seq_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
                               int L, int w, int layer, float alpha, int l0, int l1,

@@ -50,6 +50,9 @@ SIGNATURES = {
                                 _c.POINTER(_c.c_int), _c.POINTER(_c.c_float), _c.c_void_p]),
     "deeppcr_resnet_backward": (_c.c_int, [_c.c_void_p] * 8 + [_c.c_int] * 5 +
                                 [_c.c_void_p, _c.c_size_t, _c.c_void_p]),
+    "deeppcr_resnet_seq_forward": (_c.c_int, [_c.c_void_p] * 4 + [_c.c_int] * 6 + [_c.c_void_p]),
+    "deeppcr_resnet_seq_backward": (_c.c_int, [_c.c_void_p] * 6 + [_c.c_int] * 6 +
+                                    [_c.c_void_p]),
     "deeppcr_seq_forward": (_c.c_int, [_c.c_void_p] * 4 + [_c.c_int] * 4 + [_c.c_float, _c.c_int,
                                                                           _c.c_void_p]),
     "deeppcr_seq_backward": (_c.c_int, [_c.c_void_p] * 7 + [_c.c_int] * 4 + [_c.c_float, _c.c_int,
@@ -310,6 +313,39 @@ def deeppcr_resnet_backward(W, z0, Z, G, skip: int, act: int = ACT_RELU, Lambda=
     if st != OK:
         raise DeepPCRError(st, "deeppcr_resnet_backward")
     return Lambda, dz0, dW, db
+
+
+def deeppcr_resnet_seq_forward(W, bias, z0, skip: int, act: int = ACT_RELU, Z=None,
+                               launch_per_layer: bool = False, stream=None):
+    """Sequential GPU pass of the collapsed-skip ResNet; returns Z."""
+    torch = _torch()
+    L, w, _ = W.shape
+    B = z0.shape[0]
+    Z = torch.empty((B, L, w), dtype=torch.float32, device=z0.device) if Z is None else Z
+    _check(Z, (B, L, w), "Z")
+    st = lib().deeppcr_resnet_seq_forward(_ptr(W), _ptr(bias), _ptr(z0), _ptr(Z), B, L, w,
+                                          int(skip), int(act), int(bool(launch_per_layer)),
+                                          _stream(stream))
+    if st != OK:
+        raise DeepPCRError(st, "deeppcr_resnet_seq_forward")
+    return Z
+
+
+def deeppcr_resnet_seq_backward(W, z0, Z, G, skip: int, act: int = ACT_RELU, Lambda=None,
+                                dz0=None, launch_per_layer: bool = False, stream=None):
+    """Sequential GPU adjoints of the collapsed-skip ResNet; returns (Lambda, dz0)."""
+    torch = _torch()
+    L, w, _ = W.shape
+    B = z0.shape[0]
+    dev = z0.device
+    Lambda = torch.empty((B, L, w), dtype=torch.float32, device=dev) if Lambda is None else Lambda
+    dz0 = torch.empty((B, w), dtype=torch.float32, device=dev) if dz0 is None else dz0
+    st = lib().deeppcr_resnet_seq_backward(_ptr(W), _ptr(z0), _ptr(Z), _ptr(G), _ptr(Lambda),
+                                           _ptr(dz0), B, L, w, int(skip), int(act),
+                                           int(bool(launch_per_layer)), _stream(stream))
+    if st != OK:
+        raise DeepPCRError(st, "deeppcr_resnet_seq_backward")
+    return Lambda, dz0
 
 
 def deeppcr_seq_forward(W, bias, z0, Z=None, layer: int = TANH_MLP, alpha: float = 1.0,

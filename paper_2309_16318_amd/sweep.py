@@ -10,6 +10,9 @@ width w, break-even depth) on one MI355X.  For every (w, L):
   * backward — one transposed PCR solve (adjoints only, as the sequential
     pass computes) against the sequential adjoint loop, both launch shapes.
 
+With --resnet-skip s the same is done for the collapsed-skip ResNet of
+App. A.3 (DeepPCR on the block chain against the sequential GPU pass).
+
 Each timing is the minimum over `--reps` runs (the paper's statistic).
 Prints one JSON line per point (so a long run shows progress) and writes the
 whole table to `--out`.
@@ -88,6 +91,61 @@ def run_point(w, L, B, layer, alpha, reps, dev):
     return out
 
 
+def run_point_resnet(w, L, B, skip, act, reps, dev):
+    """The collapsed-skip ResNet (App. A.3) at one (w, L): DeepPCR on the
+    block chain against the sequential GPU pass (one launch for all layers)."""
+    import torch
+
+    from paper_2309_16318_amd import deeppcr, synth
+
+    d = synth.resnet_inputs(B, L, w, seed=0)
+    t = {k: torch.from_numpy(v).to(dev) for k, v in d.items()}
+    Z = torch.empty((B, L, w), dtype=torch.float32, device=dev)
+    Zs = torch.empty_like(Z)
+    lam = torch.empty_like(Z)
+    dz0 = torch.empty((B, w), dtype=torch.float32, device=dev)
+    dW = torch.empty((L, w, w), dtype=torch.float32, device=dev)
+    db = torch.empty((L, w), dtype=torch.float32, device=dev)
+    wsf = torch.empty(deeppcr.resnet_workspace_bytes(deeppcr.OP_FWD, B, L, w, skip),
+                      dtype=torch.uint8, device=dev)
+    wsb = torch.empty(deeppcr.resnet_workspace_bytes(deeppcr.OP_BWD, B, L, w, skip),
+                      dtype=torch.uint8, device=dev)
+    info = {}
+
+    def fwd():
+        r = deeppcr.deeppcr_resnet_forward(t["W"], t["bias"], t["z0"], skip, act, Z, tol=1e-5,
+                                           max_iter=20, workspace=wsf)
+        info["iters"], info["status"] = r.iters, r.status
+
+    def seq_f(per_layer):
+        return lambda: deeppcr.deeppcr_resnet_seq_forward(t["W"], t["bias"], t["z0"], skip, act,
+                                                          Zs, launch_per_layer=per_layer)
+
+    def bwd():
+        deeppcr.deeppcr_resnet_backward(t["W"], t["z0"], Zs, t["G"], skip, act, Lambda=lam,
+                                        dz0=dz0, dW=dW, db=db, workspace=wsb)
+
+    def seq_b(per_layer):
+        return lambda: deeppcr.deeppcr_resnet_seq_backward(t["W"], t["z0"], Zs, t["G"], skip, act,
+                                                           Lambda=lam, dz0=dz0,
+                                                           launch_per_layer=per_layer)
+
+    out = {"w": w, "L": L, "B": B, "skip": skip}
+    out["seq_fwd_per_layer_ms"] = _time_min(seq_f(True), reps, torch) * 1e3
+    out["seq_fwd_ms"] = _time_min(seq_f(False), reps, torch) * 1e3
+    out["deeppcr_fwd_ms"] = _time_min(fwd, reps, torch) * 1e3
+    out["newton_iters"] = info["iters"]
+    out["newton_status"] = info["status"]
+    out["fwd_max_abs_diff"] = float((Z - Zs).abs().max())
+    out["seq_bwd_per_layer_ms"] = _time_min(seq_b(True), reps, torch) * 1e3
+    out["seq_bwd_ms"] = _time_min(seq_b(False), reps, torch) * 1e3
+    out["deeppcr_bwd_ms"] = _time_min(bwd, reps, torch) * 1e3
+    for k in ("fwd", "bwd"):
+        out[f"{k}_speedup"] = out[f"seq_{k}_ms"] / out[f"deeppcr_{k}_ms"]
+        out[f"{k}_speedup_vs_per_layer"] = out[f"seq_{k}_per_layer_ms"] / out[f"deeppcr_{k}_ms"]
+    return out
+
+
 def break_even(rows, key):
     """Smallest L per w from which DeepPCR stays faster (speedup > 1)."""
     res = {}
@@ -112,10 +170,31 @@ def main():
     p.add_argument("--widths", default="2,4,8,16,32,64,128")
     p.add_argument("--depths", default=",".join(str(2 ** k) for k in range(1, 15)))
     p.add_argument("--reps", type=int, default=3)
+    p.add_argument("--resnet-skip", type=int, default=0,
+                   help="> 0: the collapsed-skip ResNet with this skip length (activation "
+                        "--act), depths that are multiples of it")
+    p.add_argument("--act", type=int, default=2)
     p.add_argument("--out", required=True)
     a = p.parse_args()
     dev = torch.device("cuda:0")
     rows = []
+    if a.resnet_skip > 0:
+        for w in [int(x) for x in a.widths.split(",")]:
+            for L in [int(x) for x in a.depths.split(",")]:
+                if L % a.resnet_skip:
+                    continue
+                r = run_point_resnet(w, L, a.batch, a.resnet_skip, a.act, a.reps, dev)
+                rows.append(r)
+                print(json.dumps(r), flush=True)
+        keys = ("fwd_speedup", "bwd_speedup", "fwd_speedup_vs_per_layer",
+                "bwd_speedup_vs_per_layer")
+        summary = {"resnet_skip": a.resnet_skip, "act": a.act, "batch": a.batch, "reps": a.reps,
+                   "break_even_L": {k: break_even(rows, k) for k in keys},
+                   "max_speedup": {k: max(r[k] for r in rows) for k in keys}, "points": rows}
+        with open(a.out, "w") as f:
+            json.dump(summary, f, indent=1)
+        print(json.dumps({k: v for k, v in summary.items() if k != "points"}), flush=True)
+        return
     for w in [int(x) for x in a.widths.split(",")]:
         for L in [int(x) for x in a.depths.split(",")]:
             r = run_point(w, L, a.batch, a.layer, a.alpha, a.reps, dev)

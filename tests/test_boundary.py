@@ -247,3 +247,18 @@ def test_resnet_backward_rejects_invalid_arguments():
     assert _rbwd(act=5) == E
     assert _rbwd(ws=ctypes.c_void_p(P[0].value)) == E
     assert _rbwd(nws=1) == deeppcr.EWORKSPACE
+
+
+def test_resnet_sequential_rejects_invalid_arguments():
+    E = deeppcr.EINVAL
+    f = deeppcr.lib().deeppcr_resnet_seq_forward
+    assert f(None, P[1], P[2], P[3], 2, 8, 4, 4, 2, 0, None) == E
+    assert f(P[0], P[1], P[2], P[3], 2, 8, 4, 3, 2, 0, None) == E      # L % skip != 0
+    assert f(P[0], P[1], P[2], P[3], 2, 8, 4, 4, 7, 0, None) == E      # unknown activation
+    assert f(P[0], P[1], P[2], P[0], 2, 8, 4, 4, 2, 0, None) == E      # Z over W
+    assert f(P[0], P[1], P[2], P[3], 2, 8, 4, 4, 2, 2, None) == E      # launch_per_layer
+    fb = deeppcr.lib().deeppcr_resnet_seq_backward
+    assert fb(P[0], P[1], P[2], P[3], None, P[5], 2, 8, 4, 4, 2, 0, None) == E
+    assert fb(P[0], P[1], P[2], P[3], P[2], P[5], 2, 8, 4, 4, 2, 0, None) == E  # Lambda over Z
+    assert fb(P[0], P[1], P[2], P[3], P[4], P[5], 2, 8, 4, 0, 2, 0, None) == E
+    assert fb(P[0], P[1], P[2], P[3], P[4], P[5], 2, 8, 4, 4, 2, -1, None) == E

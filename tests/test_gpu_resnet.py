@@ -154,3 +154,21 @@ def test_resnet_deterministic(dev):
     y = [h(t) for t in deeppcr.deeppcr_resnet_backward(g(d["W"], dev), g(d["z0"], dev), Z,
                                                         g(d["G"], dev), skip=4, act=RELU)]
     assert all(np.array_equal(p, q) for p, q in zip(x, y))
+
+
+@pytest.mark.parametrize("w,L,B,skip,act", [(16, 256, 4, 4, RELU), (3, 9, 2, 1, TANH),
+                                            (33, 60, 2, 3, SIG), (128, 16, 2, 4, RELU)])
+@pytest.mark.parametrize("per_layer", [False, True])
+def test_resnet_sequential_passes(dev, w, L, B, skip, act, per_layer):
+    d = synth.resnet_inputs(B, L, w, seed=1600 + w + L)
+    Z = deeppcr.deeppcr_resnet_seq_forward(g(d["W"], dev), g(d["bias"], dev), g(d["z0"], dev),
+                                           skip=skip, act=act, launch_per_layer=per_layer)
+    ref = R.resnet_seq_forward(act, skip, d["W"], d["bias"], d["z0"])
+    assert normwise_rel_err(h(Z), ref) <= TOL
+    Z32 = ref.astype(np.float32)
+    lam, dz0 = deeppcr.deeppcr_resnet_seq_backward(g(d["W"], dev), g(d["z0"], dev), g(Z32, dev),
+                                                   g(d["G"], dev), skip=skip, act=act,
+                                                   launch_per_layer=per_layer)
+    rl, rz, _, _ = R.resnet_seq_backward(act, skip, d["W"], d["bias"], d["z0"], Z32, d["G"])
+    assert normwise_rel_err(np.concatenate([h(dz0)[:, None], h(lam)], 1),
+                            np.concatenate([rz[:, None], rl], 1)) <= TOL
