@@ -271,10 +271,13 @@ int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, con
 
 /*
  * Instrumentation (not part of the numerical path).  While enabled, the
- * library brackets every kernel launch with HIP events on the launch's own
+ * library brackets its kernel launches with HIP events on the launch's own
  * stream and records, per kernel class, the launch count, the summed device
- * time and the algorithmic bytes and flops of each launch.  Enabling adds a
- * few microseconds per launch.  Not thread-safe.
+ * time and the algorithmic bytes and flops of each launch.  Consecutive
+ * launches of one class on one stream (no host wait or other class between
+ * them, e.g. the levels of one PCR sweep) share one event pair, so the time
+ * of such a run includes the gaps between its kernels but no event overhead
+ * per kernel.  Not thread-safe.
  */
 enum {
     DEEPPCR_KCLASS_PCR_LEVEL = 0,  /* one PCR level (Alg. 1 inner parfor)      */

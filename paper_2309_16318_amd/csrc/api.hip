@@ -30,14 +30,21 @@ int hip_fail(hipError_t e, const char* where) {
     } while (0)
 
 // ------------------------------------------------------------ instrumentation
+// One record per span: consecutive launches of one kernel class on one
+// stream, with no host synchronisation or other class in between, share one
+// event pair (the end event is recorded again after each launch), so that
+// short kernels are not charged the cost of an event pair each.
 struct ProfRec {
     int kclass;
+    hipStream_t st;
     hipEvent_t e0, e1;
+    long long n;
     double bytes, flops;
 };
 
 struct Prof {
     bool on = false;
+    bool open = false;  // the last record may be extended
     std::vector<ProfRec> pending;
     std::vector<hipEvent_t> pool;
     long long launches[DEEPPCR_KCLASS_COUNT] = {};
@@ -58,11 +65,27 @@ hipEvent_t take_event() {
     return e;
 }
 
+// Ends the current span (at every entry point and after every host wait).
+void prof_break() { g_prof.open = false; }
+
 // Runs `launch` (which enqueues one kernel on `st` and returns its
 // hipGetLastError), bracketed by events when instrumentation is on.
 template <class F>
 hipError_t timed(int kclass, double bytes, double flops, hipStream_t st, F&& launch) {
     if (!g_prof.on) return launch();
+    if (g_prof.open && !g_prof.pending.empty()) {
+        ProfRec& r = g_prof.pending.back();
+        if (r.kclass == kclass && r.st == st) {
+            hipError_t e = launch();
+            if (e != hipSuccess) return e;
+            e = hipEventRecord(r.e1, st);
+            if (e != hipSuccess) return e;
+            r.n += 1;
+            r.bytes += bytes;
+            r.flops += flops;
+            return hipSuccess;
+        }
+    }
     hipEvent_t e0 = take_event(), e1 = take_event();
     if (!e0 || !e1) return launch();
     hipError_t e = hipEventRecord(e0, st);
@@ -71,8 +94,15 @@ hipError_t timed(int kclass, double bytes, double flops, hipStream_t st, F&& lau
     if (e != hipSuccess) return e;
     e = hipEventRecord(e1, st);
     if (e != hipSuccess) return e;
-    g_prof.pending.push_back({kclass, e0, e1, bytes, flops});
+    g_prof.pending.push_back({kclass, st, e0, e1, 1, bytes, flops});
+    g_prof.open = true;
     return hipSuccess;
+}
+
+// Waits for the stream (ending the instrumentation span).
+hipError_t host_wait(hipStream_t st) {
+    prof_break();
+    return hipStreamSynchronize(st);
 }
 
 // ------------------------------------------------------------------ sizes
@@ -323,7 +353,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
         });
         if (e != hipSuccess) return hip_fail(e, "newton_tiny");
         DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 3 * sizeof(unsigned), hipMemcpyDeviceToHost, st));
-        DEEPPCR_HIP(hipStreamSynchronize(st));
+        DEEPPCR_HIP(host_wait(st));
         if (iters_out) *iters_out = (int)hw[1];
         if (measure_out) *measure_out = bits_to_float(hw[2]);
         if (hw[0] == 3u) return DEEPPCR_ENONFINITE;
@@ -369,7 +399,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
         if (rule.residual) {
             DEEPPCR_HIP(hipMemcpyAsync(hw + kRedF, fslots, kRedShards * sizeof(unsigned),
                                        hipMemcpyDeviceToHost, st));
-            DEEPPCR_HIP(hipStreamSynchronize(st));
+            DEEPPCR_HIP(host_wait(st));
             const unsigned mf = max_slots(hw + kRedF);
             if (iters_out) *iters_out = k;
             if (measure_out) *measure_out = bits_to_float(mf);
@@ -398,7 +428,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
         if (rule.residual) continue;
         DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
                                    hipMemcpyDeviceToHost, st));
-        DEEPPCR_HIP(hipStreamSynchronize(st));
+        DEEPPCR_HIP(host_wait(st));
         const unsigned mx = max_slots(hw + kRedDZ), mz = max_slots(hw + kRedZ);
         if (iters_out) *iters_out = k + 1;
         if (measure_out) *measure_out = bits_to_float(mx);
@@ -435,6 +465,7 @@ const char* deeppcr_last_error(void) { return g_last_error; }
 int pcr_solve_block_bidiag(const float* J, const float* r, float* x, int B, int L, int w,
                            int transpose, void* workspace, size_t workspace_bytes,
                            void* stream) {
+    prof_break();
     if (!J || !r || !x || !workspace || !sizes_ok(B, L, w) || (transpose != 0 && transpose != 1))
         return DEEPPCR_EINVAL;
     const Layout lo = layout(DEEPPCR_OP_PCR, B, L, w);
@@ -471,6 +502,7 @@ int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, floa
                         int L, int w, int layer, float alpha, float tol, int max_iter,
                         const float* Z_init, void* workspace, size_t workspace_bytes,
                         int* iters_out, float* last_update_out, void* stream) {
+    prof_break();
     const int c = check_forward_args(W, bias, z0, Z, Z_init, workspace, workspace_bytes, B, L, w,
                                      layer, alpha);
     if (c != DEEPPCR_OK) return c;
@@ -485,6 +517,7 @@ int deeppcr_mlp_forward_residual(const float* W, const float* bias, const float*
                                  float rtol, int max_iter, const float* Z_init, void* workspace,
                                  size_t workspace_bytes, int* iters_out, float* residual_out,
                                  void* stream) {
+    prof_break();
     const int c = check_forward_args(W, bias, z0, Z, Z_init, workspace, workspace_bytes, B, L, w,
                                      layer, alpha);
     if (c != DEEPPCR_OK) return c;
@@ -500,6 +533,7 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
                          const float* G, float* Lambda, float* dz0, float* dW, float* db, int B,
                          int L, int w, int layer, float alpha, void* workspace,
                          size_t workspace_bytes, void* stream) {
+    prof_break();
     if (!W || !bias || !z0 || !Z || !G || !Lambda || !dz0 || !dW || !db || !workspace ||
         !sizes_ok(B, L, w))
         return DEEPPCR_EINVAL;
@@ -557,6 +591,7 @@ int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, f
                            int L, int w, int skip, int act, float tol, int max_iter,
                            const float* Z_init, void* workspace, size_t workspace_bytes,
                            int* iters_out, float* last_update_out, void* stream) {
+    prof_break();
     if (!W || !bias || !z0 || !Z || !workspace || !resnet_shape_ok(B, L, w, skip, act))
         return DEEPPCR_EINVAL;
     if (!(tol >= 0.f) || !std::isfinite(tol) || max_iter < 1) return DEEPPCR_EINVAL;
@@ -615,7 +650,7 @@ int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, f
         if (e != hipSuccess) return hip_fail(e, "update_reduce");
         DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
                                    hipMemcpyDeviceToHost, st));
-        DEEPPCR_HIP(hipStreamSynchronize(st));
+        DEEPPCR_HIP(host_wait(st));
         const unsigned mx = max_slots(hw + kRedDZ), mz = max_slots(hw + kRedZ);
         if (iters_out) *iters_out = k;
         if (last_update_out) *last_update_out = bits_to_float(mx);
@@ -643,6 +678,7 @@ int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, con
                             float* Lambda, float* dz0, float* dW, float* db, int B, int L, int w,
                             int skip, int act, void* workspace, size_t workspace_bytes,
                             void* stream) {
+    prof_break();
     if (!W || !z0 || !Z || !G_ || !Lambda || !dz0 || !dW || !db || !workspace ||
         !resnet_shape_ok(B, L, w, skip, act))
         return DEEPPCR_EINVAL;
@@ -695,6 +731,7 @@ int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, con
 int deeppcr_resnet_seq_forward(const float* W, const float* bias, const float* z0, float* Z,
                                int B, int L, int w, int skip, int act, int launch_per_layer,
                                void* stream) {
+    prof_break();
     if (!W || !bias || !z0 || !Z || !resnet_shape_ok(B, L, w, skip, act) ||
         (launch_per_layer != 0 && launch_per_layer != 1))
         return DEEPPCR_EINVAL;
@@ -720,6 +757,7 @@ int deeppcr_resnet_seq_forward(const float* W, const float* bias, const float* z
 int deeppcr_resnet_seq_backward(const float* W, const float* z0, const float* Z, const float* G,
                                 float* Lambda, float* dz0, int B, int L, int w, int skip, int act,
                                 int launch_per_layer, void* stream) {
+    prof_break();
     if (!W || !z0 || !Z || !G || !Lambda || !dz0 || !resnet_shape_ok(B, L, w, skip, act) ||
         (launch_per_layer != 0 && launch_per_layer != 1))
         return DEEPPCR_EINVAL;
@@ -747,6 +785,7 @@ int deeppcr_resnet_seq_backward(const float* W, const float* z0, const float* Z,
 
 int deeppcr_seq_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
                         int L, int w, int layer, float alpha, int launch_per_layer, void* stream) {
+    prof_break();
     if (!W || !bias || !z0 || !Z || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
     if (layer < 0 || layer >= kNumLayerKinds || !std::isfinite(alpha)) return DEEPPCR_EINVAL;
     if (launch_per_layer != 0 && launch_per_layer != 1) return DEEPPCR_EINVAL;
@@ -771,6 +810,7 @@ int deeppcr_seq_forward(const float* W, const float* bias, const float* z0, floa
 int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, const float* Z,
                          const float* G, float* Lambda, float* dz0, int B, int L, int w, int layer,
                          float alpha, int launch_per_layer, void* stream) {
+    prof_break();
     if (!W || !bias || !z0 || !Z || !G || !Lambda || !dz0 || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
     if (layer < 0 || layer >= kNumLayerKinds || !std::isfinite(alpha)) return DEEPPCR_EINVAL;
     if (launch_per_layer != 0 && launch_per_layer != 1) return DEEPPCR_EINVAL;
@@ -823,7 +863,7 @@ int deeppcr_profile_read(int kclass, long long* launches, double* total_ms, doub
         float ms = 0.f;
         e = hipEventElapsedTime(&ms, p.e0, p.e1);
         if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
-        g_prof.launches[p.kclass] += 1;
+        g_prof.launches[p.kclass] += p.n;
         g_prof.ms[p.kclass] += ms;
         g_prof.bytes[p.kclass] += p.bytes;
         g_prof.flops[p.kclass] += p.flops;
