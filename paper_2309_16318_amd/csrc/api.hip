@@ -162,6 +162,13 @@ int num_levels(int L) {
     return k;
 }
 
+// Kernel launches of a PCR sweep: pairs of levels where the width has the
+// two-level kernel, plus a single last level when the level count is odd.
+int num_passes(int L, int w) {
+    const int K = num_levels(L);
+    return two_level_width(w) ? (K + 1) / 2 : K;
+}
+
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
     if (!a || !b || na == 0 || nb == 0) return false;
     const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
@@ -178,6 +185,19 @@ void level_work(int B, int L, int w, int s, double* bytes, double* flops) {
     *flops = (double)B * (nr * 2.0 * w2 + na * 2.0 * w2 * w);
 }
 
+// Algorithmic work of a fused pair of levels (strides s, 2s): the flops of
+// both levels; the bytes the fused pass must move: A_l read for l >= s, the
+// level-2s operators written for l >= 4s, r read and written once.
+void level2_work(int B, int L, int w, int s, double* bytes, double* flops) {
+    double b1, f1, b2, f2;
+    level_work(B, L, w, s, &b1, &f1);
+    level_work(B, L, w, 2 * s, &b2, &f2);
+    const double nr = (double)(L - s), na = (double)(L - 4 * s > 0 ? L - 4 * s : 0);
+    const double w2 = (double)w * w;
+    *bytes = 4.0 * B * (nr * w2 + na * w2 + 2.0 * L * w);
+    *flops = f1 + f2;
+}
+
 // Runs all PCR levels.  Level 0 reads (A0, r0); level k writes operators to
 // ws A buffer (k + a_first) % 2 and vectors to ws r buffer (k + r_first) % 2,
 // except the last level, which writes the solution to `x`.
@@ -189,22 +209,36 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
         return timed(DEEPPCR_KCLASS_OTHER, bytes, 0.0, st,
                      [&] { return launch_copy_rows(r0, x, B, L, w, st); });
     }
+    const bool two = two_level_width(w);
     BlockSrc Ain = A0;
     VecSrc rin = r0;
     int s = 1;
-    for (int k = 0; k < K; ++k, s *= 2) {
-        const bool last = (k == K - 1);
-        float* Aout = wsA[(k + a_first) & 1];
+    // pass p writes operators to ws A buffer (p + a_first) % 2 and vectors to
+    // ws r buffer (p + r_first) % 2; the last pass writes the solution to x
+    for (int k = 0, p = 0; k < K; ++p) {
+        const bool pair = two && k + 1 < K;
+        const bool last = (k + (pair ? 1 : 0)) == K - 1;
+        float* Aout = wsA[(p + a_first) & 1];
         VecDst rout = last ? x
-                           : VecDst{wsr[(k + r_first) & 1], (long long)L * w, (long long)w};
+                           : VecDst{wsr[(p + r_first) & 1], (long long)L * w, (long long)w};
         double bytes, flops;
-        level_work(B, L, w, s, &bytes, &flops);
-        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
-            return launch_pcr_level(Ain, rin, Aout, rout, B, L, w, s, st);
-        });
+        hipError_t e;
+        if (pair) {
+            level2_work(B, L, w, s, &bytes, &flops);
+            e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+                return launch_pcr_level2(Ain, rin, Aout, rout, B, L, w, s, st);
+            });
+        } else {
+            level_work(B, L, w, s, &bytes, &flops);
+            e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+                return launch_pcr_level(Ain, rin, Aout, rout, B, L, w, s, st);
+            });
+        }
         if (e != hipSuccess) return e;
         Ain = BlockSrc{Aout, (long long)L * w * w, (long long)w * w, 0};
         rin = VecSrc{rout.base, rout.bstride, rout.rstride};
+        s *= pair ? 4 : 2;
+        k += pair ? 2 : 1;
     }
     return hipSuccess;
 }
@@ -283,28 +317,39 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
     }
     BlockSrc Ain{ws.A[0], (long long)L * w * w, (long long)w * w, 0};
     VecSrc rin{ws.r[0], ld, (long long)w};
-    int s = 2;
-    for (int k = 1; k < K; ++k, s *= 2) {
+    // the middle levels 1 .. K-2, two per pass where possible; pass p writes
+    // ws buffers p % 2 (the first level wrote buffers 0)
+    int s = 2, p = 1;
+    for (int k = 1; k < K - 1; ++p) {
+        const bool pair = two_level_width(w) && k + 1 < K - 1;
+        float* Aout = ws.A[p & 1];
+        const VecDst rout{ws.r[p & 1], ld, (long long)w};
         double bytes, flops;
-        level_work(B, L, w, s, &bytes, &flops);
         hipError_t e;
-        if (k == K - 1) {
-            bytes += 8.0 * B * L * w;  // the iterate is read and written
+        if (pair) {
+            level2_work(B, L, w, s, &bytes, &flops);
             e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
-                return launch_last_level_update(Ain, rin, na, B, L, w, s, st);
+                return launch_pcr_level2(Ain, rin, Aout, rout, B, L, w, s, st);
             });
         } else {
-            float* Aout = ws.A[k & 1];
-            const VecDst rout{ws.r[k & 1], ld, (long long)w};
+            level_work(B, L, w, s, &bytes, &flops);
             e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
                 return launch_pcr_level(Ain, rin, Aout, rout, B, L, w, s, st);
             });
-            Ain = BlockSrc{Aout, (long long)L * w * w, (long long)w * w, 0};
-            rin = VecSrc{rout.base, rout.bstride, rout.rstride};
         }
         if (e != hipSuccess) return e;
+        Ain = BlockSrc{Aout, (long long)L * w * w, (long long)w * w, 0};
+        rin = VecSrc{rout.base, rout.bstride, rout.rstride};
+        s *= pair ? 4 : 2;
+        k += pair ? 2 : 1;
     }
-    return hipSuccess;
+    // the last level with the update Z += x and the convergence reduction
+    double bytes, flops;
+    level_work(B, L, w, s, &bytes, &flops);
+    bytes += 8.0 * B * L * w;  // the iterate is read and written
+    return timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+        return launch_last_level_update(Ain, rin, na, B, L, w, s, st);
+    });
 }
 
 // Argument checks shared by the two forward entry points.
@@ -372,7 +417,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
         if (e != hipSuccess) return hip_fail(e, "initial_guess");
     }
     const long long n = (long long)B * L * w;
-    const VecDst xd{ws.r[(num_levels(L) + 1) & 1], (long long)L * w, (long long)w};
+    const VecDst xd{ws.r[(num_passes(L, w) + 1) & 1], (long long)L * w, (long long)w};
     const bool fused = fused_newton_levels(w);
     const NewtonArgs na{W, bias, z0, Z, ws.red, layer, alpha};
     unsigned* fslots = ws.red + kRedF;
@@ -629,7 +674,7 @@ int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, f
         });
         if (e != hipSuccess) return hip_fail(e, "resnet_initial_guess");
     }
-    const VecDst xd{ws.r[(num_levels(G) + 1) & 1], (long long)G * w, (long long)w};
+    const VecDst xd{ws.r[(num_passes(G, w) + 1) & 1], (long long)G * w, (long long)w};
     // block evaluation: W once, X read twice, blocks and residuals written;
     // flops: the s - 1 block products and the s mat-vecs per block
     const double eval_bytes = 4.0 * ((double)L * w2 + (double)B * G * (w2 + 3.0 * w));
@@ -710,7 +755,7 @@ int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, con
                          });
     if (e != hipSuccess) return hip_fail(e, "resnet_block_jac");
     // block-output adjoints mu (natural order) from the transposed solve
-    float* mu = ws.r[(num_levels(G) + 1) & 1];
+    float* mu = ws.r[(num_passes(G, w) + 1) & 1];
     const VecDst xd{mu + (long long)(G - 1) * w, (long long)G * w, -(long long)w};
     e = pcr_sweep(BlockSrc{ws.A[1], (long long)G * w * w, (long long)w * w, 1},
                   VecSrc{ws.r[1], (long long)G * w, (long long)w}, xd, B, G, w, ws.A, ws.r, 0, 0,

@@ -127,6 +127,14 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
                             const VecDst& rout, int B, int L, int w, int s,
                             hipStream_t stream);
 
+// Two levels (strides s and 2s) in one pass, for the widths two_level_width
+// accepts: rout[l] and Aout[l] hold what level 2s would have written
+// (operators for rows l >= 4s).  Aout must not be the buffer Ain reads.
+bool two_level_width(int w);
+hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
+                             const VecDst& rout, int B, int L, int w, int s,
+                             hipStream_t stream);
+
 // ------------------------------------------------------------ layer kernels
 // Forward Newton step: for every (b, l) evaluate the layer at Zprev = Z[b,l-1]
 // (z0[b] for l = 0), write r[b,l] = f_l(Zprev) - Z[b,l] and, for l >= 1,

@@ -12,7 +12,7 @@
 //                level, the block product runs on fp32 MFMA
 //                (16x16x4 / 32x32x2) and the previous block is kept, transposed
 //                through LDS, as the next row's right operand.
-//   w = 64, 128  the same chain walk with a 4-wave workgroup per chain
+//   w = 64, 128  the same chain walk with one workgroup per chain
 //                segment: the current and previous blocks are staged in LDS
 //                (double buffered), each wave owns 32x32 output tiles, and the
 //                next block is prefetched into registers during the MFMAs.
@@ -442,10 +442,13 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
     }
 }
 
-// ---- 4-wave workgroup per segment, w = 64 or 128 --------------------------
+// ---- one workgroup per segment, w = 64 (4 waves) or 128 (16 waves) -------
+// Each wave owns one 32x32 tile of the product (w = 128: 4 waves per SIMD,
+// which hides the LDS and memory latency better than 8 waves with two tiles
+// each) or, for w = 64, one 32-row tile by two column tiles.
 template <int W>
 struct TileShape {
-    static constexpr int NT = (W == 128) ? 512 : 256;  // threads per workgroup
+    static constexpr int NT = (W == 128) ? 1024 : 256;  // threads per workgroup
     static constexpr int NWV = NT / 64;                 // waves
     static constexpr int PITCH = W + 4;
     static constexpr int NL = W * W / 4 / NT;           // float4 loads per thread per block
@@ -686,6 +689,168 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
     }
 }
 
+// ---- two levels per pass, w = 16 or 32 ------------------------------------
+// Levels with strides s and 2s fused: the chains of stride 2s are the even and
+// odd elements of the chains of stride s, so one wave walking a chain of
+// stride s (elements m = 0, 1, 2, ... at rows l = c + m s) applies level s to
+// element m,  r'_m = r_m + A_m r_{m-1},  A'_m = A_m A_{m-1}  (m >= 1 / m >= 2),
+// and then level 2s,  r''_m = r'_m + A'_m r'_{m-2},  A''_m = A'_m A'_{m-2}
+// (m >= 2 / m >= 4), with A'_{m-1}, A'_{m-2} and r'_{m-1}, r'_{m-2} kept in
+// the wave's LDS.  Every read of level 2s sees level s's result, as Alg. 1
+// requires, and the arithmetic per row is that of two separate levels; but
+// each operator block is read from HBM and each product written once per
+// two levels.  A segment starting at element m0 > 0 first walks elements
+// m0-3 .. m0-1 again to rebuild that state; element 0 (row c < s) is final
+// and its block is never read.
+template <int W>
+struct Wave2Lds {
+    float tr[W * WaveShape<W>::PITCH];       // transpose of the raw block / product staging
+    float ring[2][W * WaveShape<W>::PITCH];  // A'_m row-major in slot m & 1
+    float r[2][W];                           // raw r_m in slot m & 1
+    float rp[2][W];                          // r'_m in slot m & 1
+};
+
+// acc = (A P)^T in layout R from pT (T layout of P) and aR (R layout of A).
+template <int W>
+__device__ inline void wave_product(const float* pT, const float* aR, float* out) {
+    if constexpr (W == 16) {
+        v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(pT[v], aR[v], acc, 0, 0, 0);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) out[v] = acc[v];
+    } else {
+        v16f acc = {};
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(pT[v], aR[v], acc, 0, 0, 0);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) out[v] = acc[v];
+    }
+}
+
+// sum over the row of a layout-R block times a vector in LDS; every lane of
+// row i receives the full sum.
+template <int W>
+__device__ inline float wave_matvec(const float* aR, const float* x, int g) {
+    using S = WaveShape<W>;
+    float part = 0.f;
+#pragma unroll
+    for (int q = 0; q < S::NV / 4; ++q) {
+        const v4f xv = *reinterpret_cast<const v4f*>(x + S::col(4 * q, g));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) part = fmaf(aR[4 * q + e], xv[e], part);
+    }
+#pragma unroll
+    for (int off = W; off < 64; off <<= 1) part += __shfl_xor(part, off, 64);
+    return part;
+}
+
+// Writes a layout-R block row-major at dst (pitch PITCH, LDS).
+template <int W>
+__device__ inline void lds_put_R(float* dst, const float* aR, int i, int g) {
+    using S = WaveShape<W>;
+#pragma unroll
+    for (int q = 0; q < S::NV / 4; ++q) {
+        v4f x = {aR[4 * q], aR[4 * q + 1], aR[4 * q + 2], aR[4 * q + 3]};
+        *reinterpret_cast<v4f*>(dst + i * S::PITCH + S::col(4 * q, g)) = x;
+    }
+}
+
+// Stores a layout-R block to global memory (w = 32 through the staging area
+// so that each store instruction writes 1 KiB contiguously).
+template <int W>
+__device__ inline void store_R(float* blk, const float* cR, float* stg, int i, int g, int lane) {
+    using S = WaveShape<W>;
+    if constexpr (W == 16) {
+        v4f x = {cR[0], cR[1], cR[2], cR[3]};
+        *reinterpret_cast<v4f*>(blk + i * W + S::col(0, g)) = x;
+    } else {
+        wave_sync();
+        lds_put_R<W>(stg, cR, i, g);
+        wave_sync();
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const int e = 4 * (lane + 64 * p);
+            *reinterpret_cast<v4f*>(blk + e) =
+                *reinterpret_cast<const v4f*>(stg + (e / W) * S::PITCH + e % W);
+        }
+    }
+}
+
+template <int W, bool TRANS>
+__global__ __launch_bounds__(256) void pcr_level2_wave(BlockSrc Ain, VecSrc rin,
+                                                       float* __restrict__ Aout, VecDst rout,
+                                                       int L, LevelPlan plan) {
+    using S = WaveShape<W>;
+    constexpr int NV = S::NV;
+    __shared__ Wave2Lds<W> lds_all[4];
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    const long long item = (long long)blockIdx.x * 4 + wv;
+    if (item >= plan.total) return;
+    const int s = plan.s;
+    const long long per_b = (long long)s * plan.segs_per_class;
+    const int b = (int)(item / per_b);
+    const long long rem = item - (long long)b * per_b;
+    const int c = (int)(rem / plan.segs_per_class);
+    const int j = (int)(rem - (long long)c * plan.segs_per_class);
+    const int count = (L - 1 - c) / s;  // elements m = 0 .. count
+    const int m0 = j * plan.n;
+    if (m0 > count) return;  // whole wave
+    const int m1 = min(count, m0 + plan.n - 1);
+    const int mw = max(0, m0 - 3);
+    Wave2Lds<W>& lds = lds_all[wv];
+    const int i = lane % W;
+    const int g = lane / W;
+    const float* ab = Ain.base + b * Ain.bstride;
+    const float* rb = rin.base + b * rin.bstride;
+    float* ob = rout.base + b * rout.bstride;
+    float* Ob = Aout + (long long)b * L * W * W;
+
+    float aR[NV], pT[NV], aN[NV], ap[NV], pT2[NV], app[NV];
+    int l = c + s * mw;
+    if (lane < W) lds.r[mw & 1][lane] = rb[(long long)l * rin.rstride + lane];
+    if (mw >= 1) load_R<W, TRANS>(ab + (long long)l * Ain.rstride, i, g, aR);
+    for (int m = mw; m <= m1; ++m, l += s) {
+        const bool more = m < m1;
+        const bool have_prev = m > mw;  // state of element m-1 is valid
+        const bool out_row = m >= m0;
+        float rnext = 0.f;
+        if (more) {
+            load_R<W, TRANS>(ab + (long long)(l + s) * Ain.rstride, i, g, aN);
+            if (lane < W) rnext = rb[(long long)(l + s) * rin.rstride + lane];
+        }
+        wave_sync();
+        // level s: r'_m and A'_m
+        float rp = lds.r[m & 1][i];
+        if (m >= 1 && have_prev) rp += wave_matvec<W>(aR, lds.r[(m + 1) & 1], g);
+        const bool prod1 = m >= 2 && have_prev;
+        if (prod1) wave_product<W>(pT, aR, ap);
+        // level 2s: r''_m and A''_m (A'_{m-2} and r'_{m-2} are in slot m & 1)
+        float rpp = rp;
+        if (m >= 2 && out_row) rpp += wave_matvec<W>(ap, lds.rp[m & 1], g);
+        const bool prod2 = m >= 4 && out_row;
+        if (prod2) {
+#pragma unroll
+            for (int v = 0; v < NV; ++v) pT2[v] = lds.ring[m & 1][S::col(v, g) * S::PITCH + i];
+            wave_product<W>(pT2, ap, app);
+        }
+        if (out_row && g == 0) ob[(long long)l * rout.rstride + i] = rpp;
+        if (prod2) store_R<W>(Ob + (long long)l * W * W, app, lds.tr, i, g, lane);
+        // state for element m+1 and m+2
+        wave_sync();
+        if (g == 0) lds.rp[m & 1][i] = rp;
+        if (prod1) lds_put_R<W>(lds.ring[m & 1], ap, i, g);
+        if (more) {
+            if (m >= 1) lds_transpose<W>(lds.tr, aR, i, g, pT);  // begins with a wave sync
+            if (lane < W) lds.r[(m + 1) & 1][lane] = rnext;
+#pragma unroll
+            for (int v = 0; v < NV; ++v) aR[v] = aN[v];
+        }
+    }
+}
+
 }  // namespace
 
 LevelPlan plan_level(int B, int L, int s, long long target_items, int n_max) {
@@ -729,7 +894,8 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
     }
     if (w == 64 || w == 128) {
         const LevelPlan p = plan_level(B, L, s, w == 64 ? 4096 : 1024, 64);
-        const dim3 grid((unsigned)p.total), block(w == 64 ? 256 : 512);
+        const dim3 grid((unsigned)p.total),
+            block(w == 64 ? TileShape<64>::NT : TileShape<128>::NT);
         if (w == 64) {
             if (Ain.trans)
                 hipLaunchKernelGGL((pcr_level_tile<64, true>), grid, block, 0, stream, Ain, rin,
@@ -751,6 +917,49 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
     const long long rows = (long long)B * L;
     hipLaunchKernelGGL(pcr_level_generic, dim3((unsigned)rows), dim3(kThreads), 0, stream,
                        Ain, rin, Aout, rout, L, w, s);
+    return hipGetLastError();
+}
+
+bool two_level_width(int w) { return w == 16 || w == 32; }
+
+// Segments of the fused pair cover elements m = 0 .. (L-1-c)/s of each chain;
+// n rows each, at least 8 so that the 3-row warm-up stays a small share.
+LevelPlan plan_level2(int B, int L, int s, long long target_items) {
+    LevelPlan p;
+    p.s = s;
+    const int E = (L - 1) / s + 1;  // elements of the longest chain
+    const long long rows = (long long)B * s * E;
+    long long n = (rows + target_items - 1) / target_items;
+    if (n < 8) n = 8;
+    if (n > 64) n = 64;
+    p.n = (int)n;
+    p.segs_per_class = (E + p.n - 1) / p.n;
+    p.total = (long long)B * s * p.segs_per_class;
+    return p;
+}
+
+hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
+                             const VecDst& rout, int B, int L, int w, int s,
+                             hipStream_t stream) {
+    const LevelPlan p = plan_level2(B, L, s, 4096);
+    const dim3 g3((unsigned)((p.total + 3) / 4)), block(256);
+    if (w == 16) {
+        if (Ain.trans)
+            hipLaunchKernelGGL((pcr_level2_wave<16, true>), g3, block, 0, stream, Ain, rin, Aout,
+                               rout, L, p);
+        else
+            hipLaunchKernelGGL((pcr_level2_wave<16, false>), g3, block, 0, stream, Ain, rin, Aout,
+                               rout, L, p);
+    } else if (w == 32) {
+        if (Ain.trans)
+            hipLaunchKernelGGL((pcr_level2_wave<32, true>), g3, block, 0, stream, Ain, rin, Aout,
+                               rout, L, p);
+        else
+            hipLaunchKernelGGL((pcr_level2_wave<32, false>), g3, block, 0, stream, Ain, rin, Aout,
+                               rout, L, p);
+    } else {
+        return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
