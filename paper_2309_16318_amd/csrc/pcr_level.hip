@@ -704,10 +704,9 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
 // and its block is never read.
 template <int W>
 struct Wave2Lds {
-    float tr[W * WaveShape<W>::PITCH];       // transpose of the raw block / product staging
-    float ring[2][W * WaveShape<W>::PITCH];  // A'_m row-major in slot m & 1
-    float r[2][W];                           // raw r_m in slot m & 1
-    float rp[2][W];                          // r'_m in slot m & 1
+    float tr[W * WaveShape<W>::PITCH];  // transposes and product staging
+    float r[2][W];                      // raw r_m in slot m & 1
+    float rp[2][W];                     // r'_m in slot m & 1
 };
 
 // acc = (A P)^T in layout R from pT (T layout of P) and aR (R layout of A).
@@ -808,11 +807,14 @@ __global__ __launch_bounds__(256) void pcr_level2_wave(BlockSrc Ain, VecSrc rin,
     float* ob = rout.base + b * rout.bstride;
     float* Ob = Aout + (long long)b * L * W * W;
 
-    float aR[NV], pT[NV], aN[NV], ap[NV], pT2[NV], app[NV];
+    // aR: raw A_m (layout R); pT: raw A_{m-1} transposed; ringE / ringO: the
+    // level-s products A'_m of even / odd elements, transposed (T layout)
+    float aR[NV], pT[NV], aN[NV], ap[NV], app[NV], ringE[NV], ringO[NV];
     int l = c + s * mw;
     if (lane < W) lds.r[mw & 1][lane] = rb[(long long)l * rin.rstride + lane];
     if (mw >= 1) load_R<W, TRANS>(ab + (long long)l * Ain.rstride, i, g, aR);
-    for (int m = mw; m <= m1; ++m, l += s) {
+    // one element of the walk; `ring` holds A'_{m-2} on entry and A'_m on exit
+    auto element = [&](int m, float (&ring)[NV]) {
         const bool more = m < m1;
         const bool have_prev = m > mw;  // state of element m-1 is valid
         const bool out_row = m >= m0;
@@ -827,27 +829,30 @@ __global__ __launch_bounds__(256) void pcr_level2_wave(BlockSrc Ain, VecSrc rin,
         if (m >= 1 && have_prev) rp += wave_matvec<W>(aR, lds.r[(m + 1) & 1], g);
         const bool prod1 = m >= 2 && have_prev;
         if (prod1) wave_product<W>(pT, aR, ap);
-        // level 2s: r''_m and A''_m (A'_{m-2} and r'_{m-2} are in slot m & 1)
+        // level 2s: r''_m and A''_m (A'_{m-2} in ring, r'_{m-2} in slot m & 1)
         float rpp = rp;
         if (m >= 2 && out_row) rpp += wave_matvec<W>(ap, lds.rp[m & 1], g);
         const bool prod2 = m >= 4 && out_row;
-        if (prod2) {
-#pragma unroll
-            for (int v = 0; v < NV; ++v) pT2[v] = lds.ring[m & 1][S::col(v, g) * S::PITCH + i];
-            wave_product<W>(pT2, ap, app);
-        }
+        if (prod2) wave_product<W>(ring, ap, app);
         if (out_row && g == 0) ob[(long long)l * rout.rstride + i] = rpp;
         if (prod2) store_R<W>(Ob + (long long)l * W * W, app, lds.tr, i, g, lane);
-        // state for element m+1 and m+2
+        // state for elements m+1 and m+2
         wave_sync();
         if (g == 0) lds.rp[m & 1][i] = rp;
-        if (prod1) lds_put_R<W>(lds.ring[m & 1], ap, i, g);
+        if (prod1) lds_transpose<W>(lds.tr, ap, i, g, ring);  // begins with a wave sync
         if (more) {
-            if (m >= 1) lds_transpose<W>(lds.tr, aR, i, g, pT);  // begins with a wave sync
+            if (m >= 1) lds_transpose<W>(lds.tr, aR, i, g, pT);
             if (lane < W) lds.r[(m + 1) & 1][lane] = rnext;
 #pragma unroll
             for (int v = 0; v < NV; ++v) aR[v] = aN[v];
         }
+        l += s;
+    };
+    for (int m = mw; m <= m1; ++m) {
+        if (m & 1)
+            element(m, ringO);
+        else
+            element(m, ringE);
     }
 }
 
@@ -941,7 +946,7 @@ LevelPlan plan_level2(int B, int L, int s, long long target_items) {
 hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
                              const VecDst& rout, int B, int L, int w, int s,
                              hipStream_t stream) {
-    const LevelPlan p = plan_level2(B, L, s, 4096);
+    const LevelPlan p = plan_level2(B, L, s, w == 16 ? 8192 : 4096);
     const dim3 g3((unsigned)((p.total + 3) / 4)), block(256);
     if (w == 16) {
         if (Ain.trans)
