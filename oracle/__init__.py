@@ -12,3 +12,4 @@ from .deeppcr_oracle import (  # noqa: F401
     seq_backward, loss,
 )
 from . import resnet_oracle  # noqa: F401
+from . import diffusion_oracle  # noqa: F401

@@ -102,6 +102,30 @@ def resnet_inputs(B: int, L: int, w: int, seed: int = 0) -> dict:
     return {"W": _f32(W), "bias": _f32(bias), "z0": _f32(z0), "G": _f32(G)}
 
 
+def diffusion_inputs(B: int, L: int, w: int, h: int, seed: int = 0) -> dict:
+    """A synthetic, untrained one-hidden-layer denoiser and the noise of one
+    denoising run.
+
+    Draw order: W1, b1, W2, b2, temb, zT, eps.
+      W1[h, w], b1[h]  ~ U(-1/sqrt(w), 1/sqrt(w))   (default fully connected init)
+      W2[w, h], b2[w]  ~ U(-1/sqrt(h), 1/sqrt(h))
+      temb[L, h]       ~ N(0, 1)    (time embedding of schedule index t = 1..L)
+      zT[B, w]         ~ N(0, 1)    (the starting noise)
+      eps[B, L, w]     ~ N(0, 1)    (the normal sample each step adds)
+    """
+    rng = np.random.default_rng(seed)
+    bw, bh = 1.0 / np.sqrt(w), 1.0 / np.sqrt(h)
+    W1 = rng.uniform(-bw, bw, size=(h, w))
+    b1 = rng.uniform(-bw, bw, size=(h,))
+    W2 = rng.uniform(-bh, bh, size=(w, h))
+    b2 = rng.uniform(-bh, bh, size=(w,))
+    temb = rng.standard_normal((L, h))
+    zT = rng.standard_normal((B, w))
+    eps = rng.standard_normal((B, L, w))
+    return {"W1": _f32(W1), "b1": _f32(b1), "W2": _f32(W2), "b2": _f32(b2),
+            "temb": _f32(temb), "zT": _f32(zT), "eps": _f32(eps)}
+
+
 def haar_orthogonal(rng: np.random.Generator, shape_prefix: tuple, w: int) -> np.ndarray:
     """Haar-distributed orthogonal w x w matrices: QR of a Gaussian, with the
     signs of R's diagonal folded into Q."""
