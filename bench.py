@@ -60,6 +60,22 @@ def make_step(wl, dev):
                                            workspace=ws)
         return step, info
 
+    if wl.kind == "diffusion":
+        from paper_2309_16318_amd import generic
+
+        p = {k: t[k] for k in ("W1", "b1", "W2", "b2", "temb")}
+        step_fn, jac_fn = generic.denoising_steps(p, t["eps"])
+        ws = torch.empty(deeppcr.workspace_bytes(deeppcr.OP_PCR, B, L, w), dtype=torch.uint8,
+                         device=dev)
+
+        def step():
+            res = generic.newton_generic(step_fn, jac_fn, t["zT"], L, tol=wl.tol,
+                                         max_iter=wl.max_iter, workspace=ws)
+            if res.status != deeppcr.OK:
+                raise RuntimeError(f"sampler status {res.status}")
+            info["iters"] = res.iters
+        return step, info
+
     if wl.kind == "resnet":
         wsf = torch.empty(deeppcr.resnet_workspace_bytes(deeppcr.OP_FWD, B, L, w, wl.skip),
                           dtype=torch.uint8, device=dev)
@@ -136,6 +152,9 @@ def cpu_baseline(wl, budget_s):
         if wl.kind == "pcr":
             oracle.seq_solve(d["J"], d["r"], bool(wl.transpose))
             return
+        if wl.kind == "diffusion":
+            oracle.diffusion_oracle.seq_sample(d, d["zT"], d["eps"])
+            return
         if wl.kind == "resnet":
             R = oracle.resnet_oracle
             Z = R.resnet_seq_forward(wl.act, wl.skip, d["W"], d["bias"], d["z0"])
@@ -157,6 +176,7 @@ def cpu_baseline(wl, budget_s):
             break
     parts = "+".join(("seq_solve",) if wl.kind == "pcr" else
                      ("resnet_seq_forward", "resnet_seq_backward") if wl.kind == "resnet" else
+                     ("diffusion seq_sample",) if wl.kind == "diffusion" else
                      tuple(p for p, on in (("seq_forward", "fwd" in wl.passes),
                                            ("seq_backward", "bwd" in wl.passes)) if on))
     return {"value": B * L * reps / el, "unit": "layer-steps/s", "cores": int(cores),
@@ -234,6 +254,8 @@ def main():
         layer = layer_names[wl.layer]
     elif wl.kind == "resnet":
         layer = f"{['tanh', 'sigmoid', 'relu'][wl.act]}_preact_skip{wl.skip}"
+    elif wl.kind == "diffusion":
+        layer = f"denoising_step_tanh_denoiser_h{wl.hidden}"
     else:
         layer = None
     cfg = {"workload": wl.name, "B": wl.B, "L": wl.L, "w": wl.w,

@@ -100,6 +100,25 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x,
                            void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * One Newton iteration for a step function the caller evaluates (Sec. 2,
+ * Eqs. 1-3; the paper's general setting of z_l = f_l(z_{l-1}), e.g. the
+ * denoising steps of App. A.4 whose Jacobians come from autograd).  At the
+ * current iterate Z the caller supplies, for every step in parallel, the step
+ * values F[b, l] = f_l(Z[b, l-1]) (Z[b, -1] being the fixed start) and the
+ * Jacobians J[b, l] = df_l/dz at Z[b, l-1]; the library forms the residual
+ * r = F - Z, solves the block-bidiagonal system of Eq. 3 for dZ by PCR and
+ * applies Z += dZ.  J[b, 0] is never read.
+ *   J [B, L, w, w], F [B, L, w]  inputs;  Z [B, L, w] input and output
+ *   residual_out   (host, may be NULL) max |F - Z| before the update
+ *   max_update_out (host, may be NULL) max |dZ|;  max_abs_out: max |Z| after it
+ * Returns DEEPPCR_ENONFINITE if any of the three is NaN/Inf.  Waits for the GPU
+ * once.  workspace_bytes >= deeppcr_workspace_bytes(DEEPPCR_OP_PCR, B, L, w).
+ */
+int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, int w,
+                        void* workspace, size_t workspace_bytes, float* residual_out,
+                        float* max_update_out, float* max_abs_out, void* stream);
+
+/*
  * Forward pass of a depth-L network by Newton + PCR (Sec. 2, Eqs. 1-3).
  * Each Newton iteration evaluates every layer and its Jacobian at the current
  * iterate in parallel (App. A.1, Eq. 8), forms the residual

@@ -543,6 +543,50 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x, int B, int 
     return DEEPPCR_OK;
 }
 
+int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, int w,
+                        void* workspace, size_t workspace_bytes, float* residual_out,
+                        float* max_update_out, float* max_abs_out, void* stream) {
+    prof_break();
+    if (!J || !F || !Z || !workspace || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
+    const Layout lo = layout(DEEPPCR_OP_PCR, B, L, w);
+    if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
+    const size_t nJ = (size_t)B * L * w * w * 4, nv = (size_t)B * L * w * 4;
+    if (overlaps(Z, nv, J, nJ) || overlaps(Z, nv, F, nv) || overlaps(workspace, lo.total, J, nJ) ||
+        overlaps(workspace, lo.total, F, nv) || overlaps(workspace, lo.total, Z, nv))
+        return DEEPPCR_EINVAL;
+    hipStream_t st = (hipStream_t)stream;
+    Ws ws = carve(workspace, lo);
+    unsigned* hw = host_words();
+    if (!hw) return hip_fail(hipErrorOutOfMemory, "hipHostMalloc");
+    const long long n = (long long)B * L * w;
+    // all reduction slots cleared, then r = F - Z with max |r|
+    hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * kRedWords, 0.0, st,
+                         [&] { return launch_zero_words(ws.red, kRedWords, st); });
+    if (e != hipSuccess) return hip_fail(e, "zero_words");
+    e = timed(DEEPPCR_KCLASS_LAYER, 12.0 * n, (double)n, st,
+              [&] { return launch_residual(F, Z, ws.r[1], n, ws.red, st); });
+    if (e != hipSuccess) return hip_fail(e, "residual");
+    // Eq. 3 with the caller's blocks (J[:, 0] unused) by PCR, then Z += dZ
+    const VecDst xd{ws.r[(num_passes(L, w) + 1) & 1], (long long)L * w, (long long)w};
+    e = pcr_sweep(BlockSrc{J, (long long)L * w * w, (long long)w * w, 0},
+                  VecSrc{ws.r[1], (long long)L * w, (long long)w}, xd, B, L, w, ws.A, ws.r, 0, 0,
+                  st);
+    if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+    e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
+              [&] { return launch_update_reduce(Z, xd.base, n, ws.red, st); });
+    if (e != hipSuccess) return hip_fail(e, "update_reduce");
+    DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, kRedWords * sizeof(unsigned), hipMemcpyDeviceToHost,
+                               st));
+    DEEPPCR_HIP(host_wait(st));
+    const unsigned mr = max_slots(hw + kRedF), mx = max_slots(hw + kRedDZ),
+                   mz = max_slots(hw + kRedZ);
+    if (residual_out) *residual_out = bits_to_float(mr);
+    if (max_update_out) *max_update_out = bits_to_float(mx);
+    if (max_abs_out) *max_abs_out = bits_to_float(mz);
+    if (mr >= 0x7f800000u || mx >= 0x7f800000u || mz >= 0x7f800000u) return DEEPPCR_ENONFINITE;
+    return DEEPPCR_OK;
+}
+
 int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
                         int L, int w, int layer, float alpha, float tol, int max_iter,
                         const float* Z_init, void* workspace, size_t workspace_bytes,

@@ -177,6 +177,10 @@ hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
                         const float* Lambda, float* dW, float* db, int B, int L, int w,
                         hipStream_t stream);
 
+// r = F - Z over n floats; max |r| bits into the kRedF slots of red.
+hipError_t launch_residual(const float* F, const float* Z, float* r, long long n, unsigned* red,
+                           hipStream_t stream);
+
 // p[0 .. n) = 0 (a kernel, so that the call can sit in a captured graph).
 hipError_t launch_zero_words(unsigned* p, int n, hipStream_t stream);
 

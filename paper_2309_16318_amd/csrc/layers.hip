@@ -258,6 +258,22 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
     if (t < w) db[(long long)l * w + t] = dbacc;
 }
 
+// r = F - Z over n floats, max |r| bits into the kRedF slots of red.
+__global__ __launch_bounds__(kThreads) void residual_kernel(const float* __restrict__ F,
+                                                           const float* __restrict__ Z,
+                                                           float* __restrict__ r, long long n,
+                                                           unsigned* __restrict__ red) {
+    unsigned mr = 0u;
+    for (long long k = (long long)blockIdx.x * kThreads + threadIdx.x; k < n;
+         k += (long long)gridDim.x * kThreads) {
+        const float v = F[k] - Z[k];
+        r[k] = v;
+        mr = max(mr, __float_as_uint(fabsf(v)));
+    }
+    mr = wave_umax(mr);
+    if ((threadIdx.x & 63) == 0) atomicMax(red + kRedF + (int)(blockIdx.x % kRedShards), mr);
+}
+
 __global__ __launch_bounds__(kThreads) void zero_words_kernel(unsigned* __restrict__ p, int n) {
     const int i = blockIdx.x * kThreads + threadIdx.x;
     if (i < n) p[i] = 0u;
@@ -454,6 +470,16 @@ hipError_t launch_wgrad_pre(const float* z0, const float* Z, const float* Lambda
                             float* db, int B, int L, int w, int act, hipStream_t stream) {
     hipLaunchKernelGGL(wgrad_kernel<true>, dim3((unsigned)L), dim3(kThreads), 0, stream, z0, Z,
                        nullptr, Lambda, dW, db, B, L, w, act);
+    return hipGetLastError();
+}
+
+hipError_t launch_residual(const float* F, const float* Z, float* r, long long n, unsigned* red,
+                           hipStream_t stream) {
+    long long blocks = (n + kThreads - 1) / kThreads;
+    if (blocks > 4096) blocks = 4096;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(residual_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, F, Z, r,
+                       n, red);
     return hipGetLastError();
 }
 

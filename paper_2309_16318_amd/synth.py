@@ -39,6 +39,7 @@ class Workload:
     seed: int = 0
     skip: int = 1        # collapsed-skip ResNet: layers per block
     act: int = 2         # collapsed-skip ResNet activation: 0 tanh, 1 sigmoid, 2 ReLU
+    hidden: int = 0      # diffusion-style sampler: denoiser width
 
 
 # The workloads the build is measured on (tanh MLPs / residual nets with
@@ -57,6 +58,10 @@ WORKLOADS = {
     # depth 1024, Newton + PCR forward and the transposed backward
     "resnet_skip4_fwd_bwd": Workload("resnet_skip4_fwd_bwd", "resnet", B=64, L=1024, w=16,
                                      passes=("fwd", "bwd"), skip=4, act=2),
+    # a diffusion-style sampler (App. A.4): 1024 denoising steps of a 64-wide
+    # latent with a synthetic 128-wide denoiser, steps evaluated by the caller
+    "diffusion_generic": Workload("diffusion_generic", "diffusion", B=16, L=1024, w=64,
+                                  passes=("fwd",), hidden=128, max_iter=30),
 }
 
 
@@ -164,6 +169,8 @@ def workload_inputs(wl: Workload) -> dict:
         return pcr_inputs(wl.B, wl.L, wl.w, wl.seed)
     if wl.kind == "resnet":
         return resnet_inputs(wl.B, wl.L, wl.w, wl.seed)
+    if wl.kind == "diffusion":
+        return diffusion_inputs(wl.B, wl.L, wl.w, wl.hidden, wl.seed)
     return mlp_inputs(wl.B, wl.L, wl.w, wl.seed)
 
 

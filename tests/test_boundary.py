@@ -262,3 +262,21 @@ def test_resnet_sequential_rejects_invalid_arguments():
     assert fb(P[0], P[1], P[2], P[3], P[2], P[5], 2, 8, 4, 4, 2, 0, None) == E  # Lambda over Z
     assert fb(P[0], P[1], P[2], P[3], P[4], P[5], 2, 8, 4, 0, 2, 0, None) == E
     assert fb(P[0], P[1], P[2], P[3], P[4], P[5], 2, 8, 4, 4, 2, -1, None) == E
+
+
+def test_newton_step_rejects_invalid_arguments():
+    E = deeppcr.EINVAL
+    f = deeppcr.lib().deeppcr_newton_step
+
+    def call(J=P[0], F=P[1], Z=P[2], B=2, L=8, w=4, ws=P[3], nws=BIG):
+        return f(J, F, Z, B, L, w, ws, nws, None, None, None, None)
+
+    assert call(J=None) == E
+    assert call(F=None) == E
+    assert call(Z=None) == E
+    assert call(ws=None) == E
+    assert call(w=129) == E
+    assert call(Z=ctypes.c_void_p(P[0].value + 64)) == E   # Z over J
+    assert call(Z=P[1]) == E                                # Z over F
+    assert call(ws=ctypes.c_void_p(P[2].value - 16)) == E   # workspace runs into Z
+    assert call(nws=deeppcr.workspace_bytes(deeppcr.OP_PCR, 2, 8, 4) - 1) == deeppcr.EWORKSPACE
