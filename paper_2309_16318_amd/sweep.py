@@ -11,7 +11,9 @@ width w, break-even depth) on one MI355X.  For every (w, L):
     pass computes) against the sequential adjoint loop, both launch shapes.
 
 With --resnet-skip s the same is done for the collapsed-skip ResNet of
-App. A.3 (DeepPCR on the block chain against the sequential GPU pass).
+App. A.3 (DeepPCR on the block chain against the sequential GPU pass), and
+with --diffusion for the diffusion-style sampler of App. A.4 (DeepPCR with
+PyTorch-evaluated steps against a PyTorch step loop).
 
 Each timing is the minimum over `--reps` runs (the paper's statistic).
 Prints one JSON line per point (so a long run shows progress) and writes the
@@ -146,6 +148,61 @@ def run_point_resnet(w, L, B, skip, act, reps, dev):
     return out
 
 
+def run_point_diffusion(w, L, B, reps, dev):
+    """The diffusion-style sampler (App. A.4) at one (w, L): DeepPCR with the
+    step values and Jacobians evaluated in PyTorch against the same step
+    applied L times in a PyTorch loop (the shape of the paper's baseline)."""
+    import torch
+
+    from paper_2309_16318_amd import deeppcr, generic, synth
+
+    hd = 2 * w
+    d = synth.diffusion_inputs(B, L, w, hd, seed=0)
+    t = {k: torch.from_numpy(v).to(dev) for k, v in d.items()}
+    p = {k: t[k] for k in ("W1", "b1", "W2", "b2", "temb")}
+    step_fn, jac_fn = generic.denoising_steps(p, t["eps"])
+    ws = torch.empty(deeppcr.workspace_bytes(deeppcr.OP_PCR, B, L, w), dtype=torch.uint8,
+                     device=dev)
+    info = {}
+
+    def dpcr():
+        r = generic.newton_generic(step_fn, jac_fn, t["zT"], L, tol=1e-5, max_iter=30,
+                                   workspace=ws)
+        info["iters"], info["status"], info["Z"] = r.iters, r.status, r.Z
+
+    # the same step applied one at a time (schedule coefficients on the host,
+    # so the loop never waits for the GPU)
+    import numpy as np
+
+    beta = np.linspace(1e-4, 0.02, L) if L > 1 else np.array([1e-4])
+    alpha = 1.0 - beta
+    alphabar = np.cumprod(alpha)
+    coef = []
+    for l in range(L):
+        ti = L - l
+        coef.append(((1.0 - alpha[ti - 1]) / np.sqrt(1.0 - alphabar[ti - 1]),
+                     1.0 / np.sqrt(alpha[ti - 1]), np.sqrt(beta[ti - 1])))
+    W1t, W2t = p["W1"].t().contiguous(), p["W2"].t().contiguous()
+    out = torch.empty((B, L, w), dtype=torch.float32, device=dev)
+
+    def seq():
+        z = t["zT"]
+        for l in range(L):
+            c, isa, sb = coef[l]
+            g = torch.tanh(z @ W1t + p["b1"] + p["temb"][L - l - 1]) @ W2t + p["b2"]
+            z = (z - c * g) * isa + sb * t["eps"][:, l]
+            out[:, l] = z
+
+    res = {"w": w, "L": L, "B": B, "hidden": hd}
+    res["seq_ms"] = _time_min(seq, reps, torch) * 1e3
+    res["deeppcr_ms"] = _time_min(dpcr, reps, torch) * 1e3
+    res["newton_iters"] = info["iters"]
+    res["newton_status"] = info["status"]
+    res["max_abs_diff"] = float((info["Z"] - out).abs().max())
+    res["speedup"] = res["seq_ms"] / res["deeppcr_ms"]
+    return res
+
+
 def break_even(rows, key):
     """Smallest L per w from which DeepPCR stays faster (speedup > 1)."""
     res = {}
@@ -174,10 +231,26 @@ def main():
                    help="> 0: the collapsed-skip ResNet with this skip length (activation "
                         "--act), depths that are multiples of it")
     p.add_argument("--act", type=int, default=2)
+    p.add_argument("--diffusion", action="store_true",
+                   help="the diffusion-style sampler (denoiser width 2w) against a PyTorch "
+                        "step loop")
     p.add_argument("--out", required=True)
     a = p.parse_args()
     dev = torch.device("cuda:0")
     rows = []
+    if a.diffusion:
+        for w in [int(x) for x in a.widths.split(",")]:
+            for L in [int(x) for x in a.depths.split(",")]:
+                r = run_point_diffusion(w, L, a.batch, a.reps, dev)
+                rows.append(r)
+                print(json.dumps(r), flush=True)
+        summary = {"diffusion": True, "batch": a.batch, "reps": a.reps,
+                   "break_even_L": {"speedup": break_even(rows, "speedup")},
+                   "max_speedup": {"speedup": max(r["speedup"] for r in rows)}, "points": rows}
+        with open(a.out, "w") as f:
+            json.dump(summary, f, indent=1)
+        print(json.dumps({k: v for k, v in summary.items() if k != "points"}), flush=True)
+        return
     if a.resnet_skip > 0:
         for w in [int(x) for x in a.widths.split(",")]:
             for L in [int(x) for x in a.depths.split(",")]:
