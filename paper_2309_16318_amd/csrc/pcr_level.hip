@@ -442,21 +442,25 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
     }
 }
 
-// ---- one workgroup per segment, w = 64 (4 waves) or 128 (16 waves) -------
-// Each wave owns one 32x32 tile of the product (w = 128: 4 waves per SIMD,
-// which hides the LDS and memory latency better than 8 waves with two tiles
-// each) or, for w = 64, one 32-row tile by two column tiles.
+// ---- one workgroup per segment, w = 64 or 128 ----------------------------
+// The waves form a WGR x WGC grid over the product; each owns TW_R x TW_C
+// 32x32 tiles.  w = 64: 4 waves, one tile each.  w = 128: 16 waves, one tile
+// each (4 waves per SIMD); 8 waves of 64x32 or 32x64 tiles and 4 waves of
+// 64x64 tiles measured within 3% of it.
 template <int W>
 struct TileShape {
     static constexpr int NT = (W == 128) ? 1024 : 256;  // threads per workgroup
-    static constexpr int NWV = NT / 64;                 // waves
+    static constexpr int NWV = NT / 64;                        // waves
     static constexpr int PITCH = W + 4;
-    static constexpr int NL = W * W / 4 / NT;           // float4 loads per thread per block
-    static constexpr int T = W / 32;                    // 32x32 tiles per side
-    static constexpr int WPR = NWV / T;                 // waves per tile row
-    static constexpr int TW_C = T / WPR;                // column tiles per wave (one row tile)
-    static constexpr int NQ = W / 8;                    // k-steps of 8 (4 per lane half)
-    static constexpr int NST = 4 * TW_C;                // float4 stores per lane per product
+    static constexpr int NL = W * W / 4 / NT;  // float4 loads per thread per block
+    static constexpr int T = W / 32;           // 32x32 tiles per side
+    static constexpr int TW_R = 1;  // row tiles per wave
+    static constexpr int TW_C = 1;  // column tiles per wave
+    static constexpr int WGR = T / TW_R;                       // waves along the rows
+    static constexpr int WGC = T / TW_C;                       // waves along the columns
+    static constexpr int NQ = W / 8;             // k-steps of 8 (4 per lane half)
+    static constexpr int NST = 4 * TW_R * TW_C;  // float4 stores per lane per product
+    static_assert(WGR * WGC == NWV, "the wave grid covers the product");
     static_assert(NL <= NQ && NST <= NQ, "prefetch/stores are spread over the k-steps");
 };
 
@@ -512,28 +516,37 @@ __device__ inline void stage_tile(float* stg, const v16f& acc, int i, int h, v4f
     }
 }
 
+template <int W>
+using TileAcc = v16f[TileShape<W>::TW_R][TileShape<W>::TW_C];
+
 template <int W, bool PROD, bool STORE>
 __device__ __forceinline__ void tile_row(const float* cur, const float* prv, const float* rprv,
                                          const float* next_blk, v4f (&pre)[TileShape<W>::NL],
-                                         v16f (&acc)[TileShape<W>::TW_C],
-                                         const v16f (&acc_old)[TileShape<W>::TW_C], float* old_dst,
-                                         int tr, int tc0, int i, int h, float& part, float* stg) {
+                                         TileAcc<W>& acc, const TileAcc<W>& acc_old,
+                                         float* old_dst, int tr0, int tc0, int i, int h,
+                                         float (&part)[TileShape<W>::TW_R], float* stg) {
     using S = TileShape<W>;
     // w = 64: the previous row's product goes out through the staging area
     // (old_dst is then the tile's first element in the product block).
     constexpr bool STAGED = (W == 64);
     v4f cst[4];
-    if constexpr (STORE && STAGED) stage_tile(stg, acc_old[0], i, h, cst);
+    if constexpr (STORE && STAGED) stage_tile(stg, acc_old[0][0], i, h, cst);
 #pragma unroll
-    for (int bb = 0; bb < S::TW_C; ++bb) acc[bb] = v16f{};
-    part = 0.f;
-    v4f av[2], rv[2];
+    for (int a = 0; a < S::TW_R; ++a) {
+        part[a] = 0.f;
+#pragma unroll
+        for (int bb = 0; bb < S::TW_C; ++bb) acc[a][bb] = v16f{};
+    }
+    v4f av[2][S::TW_R], rv[2];
     float pv[2][S::TW_C][4];
 #pragma unroll
     for (int q = 0; q <= S::NQ; ++q) {
         if (q < S::NQ) {
             const int k = 8 * q + 4 * h;
-            av[q & 1] = *reinterpret_cast<const v4f*>(cur + (tr * 32 + i) * S::PITCH + k);
+#pragma unroll
+            for (int a = 0; a < S::TW_R; ++a)
+                av[q & 1][a] =
+                    *reinterpret_cast<const v4f*>(cur + ((tr0 + a) * 32 + i) * S::PITCH + k);
             rv[q & 1] = *reinterpret_cast<const v4f*>(rprv + k);
             if (PROD) {
 #pragma unroll
@@ -553,10 +566,10 @@ __device__ __forceinline__ void tile_row(const float* cur, const float* prv, con
                 const int t = threadIdx.x & 63;
                 *reinterpret_cast<v4f*>(old_dst + (8 * q + t / 8) * W + 4 * (t % 8)) = cst[q];
             } else {
-                const int bb = q / 4, qq = q % 4;
-                const v16f& x = acc_old[bb];
+                const int a = q / (4 * S::TW_C), bb = (q / 4) % S::TW_C, qq = q % 4;
+                const v16f& x = acc_old[a][bb];
                 v4f y = {x[4 * qq], x[4 * qq + 1], x[4 * qq + 2], x[4 * qq + 3]};
-                *reinterpret_cast<v4f*>(old_dst + (tc0 + bb) * 32 + 8 * qq) = y;
+                *reinterpret_cast<v4f*>(old_dst + a * 32 * W + (tc0 + bb) * 32 + 8 * qq) = y;
             }
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -566,15 +579,20 @@ __device__ __forceinline__ void tile_row(const float* cur, const float* prv, con
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
 #pragma unroll
-                    for (int bb = 0; bb < S::TW_C; ++bb)
-                        acc[bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[qb][bb][e], av[qb][e],
-                                                                       acc[bb], 0, 0, 0);
+                    for (int a = 0; a < S::TW_R; ++a)
+#pragma unroll
+                        for (int bb = 0; bb < S::TW_C; ++bb)
+                            acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                                pv[qb][bb][e], av[qb][a][e], acc[a][bb], 0, 0, 0);
             }
 #pragma unroll
-            for (int e = 0; e < 4; ++e) part = fmaf(av[qb][e], rv[qb][e], part);
+            for (int a = 0; a < S::TW_R; ++a)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) part[a] = fmaf(av[qb][a][e], rv[qb][e], part[a]);
         }
     }
-    part += __shfl_xor(part, 32, 64);
+#pragma unroll
+    for (int a = 0; a < S::TW_R; ++a) part[a] += __shfl_xor(part[a], 32, 64);
 }
 
 // Chain walk with a double-buffered LDS block pair per workgroup: at the u-th
@@ -604,10 +622,10 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
     float* Ob = Aout + (long long)sg.b * L * W * W;
     const int lane = t & 63, wv = t >> 6;
     const int i = lane & 31, h = lane >> 5;
-    const int tr = wv / S::WPR, tc0 = (wv % S::WPR) * S::TW_C;
-    const bool writes_r = (wv % S::WPR) == 0 && h == 0;
+    const int tr0 = (wv / S::WGC) * S::TW_R, tc0 = (wv % S::WGC) * S::TW_C;
+    const bool writes_r = (wv % S::WGC) == 0 && h == 0;
     // this lane's place in a product block (staged: the wave's tile origin)
-    const int orow_off = STAGED ? tr * 32 * W + tc0 * 32 : (tr * 32 + i) * W + 4 * h;
+    const int orow_off = STAGED ? tr0 * 32 * W + tc0 * 32 : (tr0 * 32 + i) * W + 4 * h;
 
     int l = sg.c + s * sg.m0;
     {
@@ -623,10 +641,10 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
         if (t < W) rpv[0][t] = rb[(long long)l * rin.rstride + t];
     }
 
-    v16f accA[S::TW_C], accB[S::TW_C];
+    TileAcc<W> accA, accB;
     float* pending = nullptr;  // destination of the product held in the "old" set
     int m = sg.m0, u = 0;
-    auto row = [&](v16f (&an)[S::TW_C], v16f (&ao)[S::TW_C]) -> bool {
+    auto row = [&](TileAcc<W>& an, TileAcc<W>& ao) -> bool {
         const float* cur = bufs[u & 1];
         float* prv = bufs[(u + 1) & 1];
         const float* rcur = rpv[u & 1];
@@ -637,16 +655,22 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
         float rl_next = 0.f;
         if (more && t < W) rl_next = rb[(long long)(l + s) * rin.rstride + t];
         v4f pre[S::NL];
-        float part;
+        float part[S::TW_R];
         // without a next row the prefetch rereads the current block (unused)
         const float* nb = ab + (long long)(more ? l + s : l) * Ain.rstride;
         if (prod && pending)
-            tile_row<W, true, true>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part, stg);
+            tile_row<W, true, true>(cur, prv, rprv, nb, pre, an, ao, pending, tr0, tc0, i, h, part, stg);
         else if (prod)
-            tile_row<W, true, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part, stg);
+            tile_row<W, true, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr0, tc0, i, h, part, stg);
         else
-            tile_row<W, false, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr, tc0, i, h, part, stg);
-        if (writes_r) ob[(long long)l * rout.rstride + tr * 32 + i] = rcur[tr * 32 + i] + part;
+            tile_row<W, false, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr0, tc0, i, h, part, stg);
+        if (writes_r) {
+#pragma unroll
+            for (int a = 0; a < S::TW_R; ++a) {
+                const int rr = (tr0 + a) * 32 + i;
+                ob[(long long)l * rout.rstride + rr] = rcur[rr] + part[a];
+            }
+        }
         pending = prod ? Ob + (long long)l * W * W + orow_off : nullptr;
         __syncthreads();  // every wave is done with prv and rprv
         if (more) {
@@ -664,10 +688,10 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
         if (!row(accB, accA)) { last_in_A = false; break; }
     }
     if (pending) {
-        auto flush = [&](const v16f (&acc)[S::TW_C]) {
+        auto flush = [&](const TileAcc<W>& acc) {
             if constexpr (STAGED) {
                 v4f cst[4];
-                stage_tile(stg, acc[0], i, h, cst);
+                stage_tile(stg, acc[0][0], i, h, cst);
                 const int tl = t & 63;
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
@@ -675,10 +699,10 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
             } else {
 #pragma unroll
                 for (int q = 0; q < S::NST; ++q) {
-                    const int bb = q / 4, qq = q % 4;
-                    v4f y = {acc[bb][4 * qq], acc[bb][4 * qq + 1], acc[bb][4 * qq + 2],
-                             acc[bb][4 * qq + 3]};
-                    *reinterpret_cast<v4f*>(pending + (tc0 + bb) * 32 + 8 * qq) = y;
+                    const int a = q / (4 * S::TW_C), bb = (q / 4) % S::TW_C, qq = q % 4;
+                    const v16f& x = acc[a][bb];
+                    v4f y = {x[4 * qq], x[4 * qq + 1], x[4 * qq + 2], x[4 * qq + 3]};
+                    *reinterpret_cast<v4f*>(pending + a * 32 * W + (tc0 + bb) * 32 + 8 * qq) = y;
                 }
             }
         };
