@@ -287,11 +287,12 @@ float bits_to_float(unsigned u) {
     return f;
 }
 
-// The fused Newton linear solve (w = 16, 32): the layer evaluation runs
-// inside the first PCR level and the update + reduction inside the last.
-// For L <= 2 the first level writes the solution to `x` and the separate
-// update kernel applies it.  Split in two so that a stopping test on the
-// residual (reduced by the first level) can sit between the halves.
+// The fused Newton linear solve (w = 16, 32, 64, 128): the layer evaluation
+// runs inside the first PCR level; for w = 16, 32 the update + reduction runs
+// inside the last, for w = 64, 128 the last level writes the solution to `x`
+// as do the first for L <= 2, and the separate update kernel applies it.
+// Split in two so that a stopping test on the residual (reduced by the first
+// level) can sit between the halves.
 hipError_t fused_first_level(const NewtonArgs& na, int B, int L, int w, const Ws& ws,
                              const VecDst& x, hipStream_t st) {
     const int K = num_levels(L);
@@ -346,6 +347,15 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
     // the last level with the update Z += x and the convergence reduction
     double bytes, flops;
     level_work(B, L, w, s, &bytes, &flops);
+    if (!fused_newton_levels(w)) {
+        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+            return launch_pcr_level(Ain, rin, ws.A[p & 1], x, B, L, w, s, st);
+        });
+        if (e != hipSuccess) return e;
+        const long long n = (long long)B * L * w;
+        return timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
+                     [&] { return launch_update_reduce(na.Z, x.base, n, na.red, st); });
+    }
     bytes += 8.0 * B * L * w;  // the iterate is read and written
     return timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
         return launch_last_level_update(Ain, rin, na, B, L, w, s, st);
@@ -418,7 +428,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
     }
     const long long n = (long long)B * L * w;
     const VecDst xd{ws.r[(num_passes(L, w) + 1) & 1], (long long)L * w, (long long)w};
-    const bool fused = fused_newton_levels(w);
+    const bool fused = layer_first_level(w);
     const NewtonArgs na{W, bias, z0, Z, ws.red, layer, alpha};
     unsigned* fslots = ws.red + kRedF;
     if (rule.residual) {

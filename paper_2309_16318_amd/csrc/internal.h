@@ -100,8 +100,10 @@ struct NewtonArgs {
     float alpha;
 };
 
-// Whether the fused first/last level kernels exist for width w.
+// Whether the first level with the layer evaluation (layer_first_level) and
+// the last level with the update (fused_newton_levels) exist for width w.
 bool fused_newton_levels(int w);
+bool layer_first_level(int w);
 
 // First level (s = 1) of the Newton linear solve with the layers, Jacobian
 // blocks and residuals evaluated on the fly (never stored):

@@ -713,6 +713,241 @@ __attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile
     }
 }
 
+// ---- first Newton level with the layers, w = 64 or 128 ---------------------
+// The first PCR level (s = 1) of a Newton iteration for the MLP layer kinds,
+// with the Jacobian blocks and residuals formed on the fly from the raw
+// weights: J_l = D_l W_l (+ I), D_l = c diag(sigma'(W_l Z_{l-1} + b_l)).  At
+// row l the current LDS block is the raw W_l (the weights are shared by every
+// system, so they mostly come from L2) and the previous one J_{l-1}; the
+// k-loop forms P = W_l J_{l-1} and W_l r_{l-1}, and then
+//   r_l   = f_l(Z_{l-1}) - Z_l,
+//   r'_l  = r_l + J_l r_{l-1}     = r_l + D_l (W_l r_{l-1}) (+ r_{l-1}),
+//   A'_l  = J_l J_{l-1}           = D_l P (+ J_{l-1}).
+// The pre-activation W_l Z_{l-1} of row l is summed from the prefetched raw
+// block while it is still in registers (during row l-1).  After the row, W_l
+// becomes J_l in place: the right operand of the next row.  A segment starting
+// at row l first evaluates layer l-1 for r_{l-1} and J_{l-1}.  Also clears
+// the max|dZ|, max|Z| slots and reduces max|r| into the kRedF slots.
+template <int W>
+__device__ inline float layer_out(const NewtonArgs& na, float a, float zin, float* dsc) {
+    float d;
+    const float y = activate(na.layer, a, &d);
+    const bool res = layer_residual(na.layer);
+    *dsc = res ? na.alpha * d : d;
+    return res ? fmaf(na.alpha, y, zin) : y;
+}
+
+// blk (in registers as load_block_regs holds it) times the vector x in LDS,
+// into y (LDS); W/4 consecutive threads share a row of the block.
+template <int W>
+__device__ inline void regs_matvec(const v4f* blk, const float* x, float* y) {
+    using S = TileShape<W>;
+    constexpr int LPR = W / 4;
+    const int t = threadIdx.x;
+    const v4f x4 = *reinterpret_cast<const v4f*>(x + (4 * t) % W);
+#pragma unroll
+    for (int p = 0; p < S::NL; ++p) {
+        float d = blk[p][0] * x4[0];
+#pragma unroll
+        for (int e = 1; e < 4; ++e) d = fmaf(blk[p][e], x4[e], d);
+#pragma unroll
+        for (int off = 1; off < LPR; off <<= 1) d += __shfl_xor(d, off, 64);
+        if (t % LPR == 0) y[(4 * (t + S::NT * p)) / W] = d;
+    }
+}
+
+// buf (a raw W_l in LDS) becomes diag(dsc) buf (+ I).
+template <int W>
+__device__ inline void lds_to_jacobian(float* buf, const float* dsc, bool res) {
+    using S = TileShape<W>;
+#pragma unroll
+    for (int p = 0; p < S::NL; ++p) {
+        const int f = 4 * (threadIdx.x + S::NT * p);
+        const int row = f / W, col = f % W;
+        v4f x = *reinterpret_cast<v4f*>(buf + row * S::PITCH + col);
+        x *= dsc[row];
+        if (res && row >= col && row < col + 4) x[row - col] += 1.f;
+        *reinterpret_cast<v4f*>(buf + row * S::PITCH + col) = x;
+    }
+}
+
+template <int W>
+__global__ __launch_bounds__(TileShape<W>::NT)
+__attribute__((amdgpu_waves_per_eu(TileShape<W>::NT / 256))) void pcr_level_tile_layer(
+    float* __restrict__ Aout, VecDst rout, int L, LevelPlan plan, NewtonArgs na) {
+    using S = TileShape<W>;
+    __shared__ float bufs[2][W * S::PITCH];
+    __shared__ float rpv[2][W];  // r_{l-1} / r_l
+    __shared__ float zv[2][W];   // Z_{l-1} / Z_l
+    __shared__ float zt[W];      // Z_{l-2} of the segment's first row
+    __shared__ float pz[W];      // W_l Z_{l-1} of the coming row
+    __shared__ float pzp[W];     // W_{l-1} Z_{l-2} of the segment's first row
+    __shared__ float dv[W];      // D_l of the row just done
+    constexpr bool STAGED = (W == 64);
+    __shared__ float stg_all[STAGED ? S::NWV : 1][STAGED ? 32 * 32 : 1];
+    const int t = threadIdx.x;
+    if (blockIdx.x == 0)
+        for (int k = t; k < 2 * kRedShards; k += S::NT) na.red[k] = 0u;
+    const Seg sg = decode_segment(blockIdx.x, plan, L);  // s = 1: one chain (c = 0)
+    const bool res = layer_residual(na.layer);
+    const float* Zb = na.Z + (long long)sg.b * L * W;
+    const float* z0b = na.z0 + (long long)sg.b * W;
+    float* ob = rout.base + sg.b * rout.bstride;
+    float* Ob = Aout + (long long)sg.b * L * W * W;
+    const int lane = t & 63, wv = t >> 6;
+    unsigned mr = 0u;
+    auto finish = [&]() {
+        for (int off = 32; off > 0; off >>= 1)
+            mr = max(mr, (unsigned)__shfl_xor((int)mr, off, 64));
+        if (lane == 0) atomicMax(na.red + kRedF + (int)(blockIdx.x % kRedShards), mr);
+    };
+    if (sg.m0 > sg.count) {  // uniform over the workgroup; only L = 1 gets here
+        if (sg.j == 0 && t < W) {
+            float a = na.bias[t];
+            for (int k = 0; k < W; ++k) a = fmaf(na.W[t * W + k], z0b[k], a);
+            float dsc;
+            const float r = layer_out<W>(na, a, z0b[t], &dsc) - Zb[t];
+            ob[t] = r;
+            mr = __float_as_uint(fabsf(r));
+        }
+        finish();
+        return;
+    }
+    float* stg = stg_all[STAGED ? (t >> 6) : 0];
+    const int i = lane & 31, h = lane >> 5;
+    const int tr0 = (wv / S::WGC) * S::TW_R, tc0 = (wv % S::WGC) * S::TW_C;
+    const bool writes_r = (wv % S::WGC) == 0 && h == 0;
+    const int orow_off = STAGED ? tr0 * 32 * W + tc0 * 32 : (tr0 * 32 + i) * W + 4 * h;
+
+    int l = sg.m0;
+    {
+        // layer l-1 at Z_{l-2} from the raw W_{l-1} (bufs[1]); W_l to bufs[0]
+        if (t < W) {
+            zt[t] = (l >= 2) ? Zb[(long long)(l - 2) * W + t] : z0b[t];
+            zv[1][t] = Zb[(long long)(l - 1) * W + t];
+            zv[0][t] = Zb[(long long)l * W + t];
+        }
+        v4f pre[S::NL];
+        load_block_regs<W>(na.W + (long long)(l - 1) * W * W, pre);
+        regs_to_lds<W>(pre, bufs[1], false);
+        __syncthreads();
+        regs_matvec<W>(pre, zt, pzp);
+        load_block_regs<W>(na.W + (long long)l * W * W, pre);
+        regs_to_lds<W>(pre, bufs[0], false);
+        regs_matvec<W>(pre, zv[1], pz);
+        __syncthreads();
+        if (t < W) {
+            float dsc;
+            const float f =
+                layer_out<W>(na, pzp[t] + na.bias[(long long)(l - 1) * W + t], zt[t], &dsc);
+            const float r = f - zv[1][t];
+            rpv[1][t] = r;
+            dv[t] = dsc;
+            mr = __float_as_uint(fabsf(r));
+            if (sg.j == 0) ob[t] = r;  // row 0 (< s) is final
+        }
+        __syncthreads();
+        if (sg.m0 >= 2) lds_to_jacobian<W>(bufs[1], dv, res);
+    }
+
+    TileAcc<W> accA, accB;
+    float* pending = nullptr;  // destination of the product held in the "old" set
+    int m = sg.m0, u = 0;
+    auto row = [&](TileAcc<W>& an, TileAcc<W>& ao) -> bool {
+        float* cur = bufs[u & 1];        // raw W_l
+        float* prv = bufs[(u + 1) & 1];  // J_{l-1}
+        const float* rprv = rpv[(u + 1) & 1];
+        const float* zp = zv[(u + 1) & 1];
+        const float* zc = zv[u & 1];
+        const bool more = m < sg.m1;
+        const bool prod = m >= 2;
+        __syncthreads();
+        float z_next = 0.f;
+        if (more && t < W) z_next = Zb[(long long)(l + 1) * W + t];
+        v4f pre[S::NL];
+        float part[S::TW_R];
+        const float* nb = na.W + (long long)(more ? l + 1 : l) * W * W;
+        if (prod && pending)
+            tile_row<W, true, true>(cur, prv, rprv, nb, pre, an, ao, pending, tr0, tc0, i, h,
+                                    part, stg);
+        else if (prod)
+            tile_row<W, true, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr0, tc0, i, h,
+                                     part, stg);
+        else
+            tile_row<W, false, false>(cur, prv, rprv, nb, pre, an, ao, pending, tr0, tc0, i, h,
+                                      part, stg);
+#pragma unroll
+        for (int a = 0; a < S::TW_R; ++a) {
+            const int R = (tr0 + a) * 32 + i;
+            float dsc;
+            const float f = layer_out<W>(na, pz[R] + na.bias[(long long)l * W + R], zp[R], &dsc);
+            if (writes_r) {
+                const float r = f - zc[R];
+                ob[(long long)l * rout.rstride + R] = r + fmaf(dsc, part[a], res ? rprv[R] : 0.f);
+                rpv[u & 1][R] = r;
+                dv[R] = dsc;
+                mr = max(mr, __float_as_uint(fabsf(r)));
+            }
+            if (prod) {
+                // lane row R, columns (tc0 + bb) * 32 + 8 qq + 4 h + e
+#pragma unroll
+                for (int bb = 0; bb < S::TW_C; ++bb)
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq) {
+                        const int col = (tc0 + bb) * 32 + 8 * qq + 4 * h;
+                        v4f jp = {0.f, 0.f, 0.f, 0.f};
+                        if (res) jp = *reinterpret_cast<const v4f*>(prv + R * S::PITCH + col);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            an[a][bb][4 * qq + e] = fmaf(dsc, an[a][bb][4 * qq + e], jp[e]);
+                    }
+            }
+        }
+        pending = prod ? Ob + (long long)l * W * W + orow_off : nullptr;
+        __syncthreads();  // cur, prv, rprv, pz are read; dv is complete
+        if (more) {
+            regs_to_lds<W>(pre, prv, false);   // raw W_{l+1}
+            regs_matvec<W>(pre, zc, pz);       // W_{l+1} Z_l
+            lds_to_jacobian<W>(cur, dv, res);  // J_l
+            if (t < W) zv[(u + 1) & 1][t] = z_next;
+        }
+        ++m;
+        ++u;
+        ++l;
+        return more;
+    };
+    bool last_in_A = true;
+    for (;;) {
+        if (!row(accA, accB)) { last_in_A = true; break; }
+        if (!row(accB, accA)) { last_in_A = false; break; }
+    }
+    if (pending) {
+        auto flush = [&](const TileAcc<W>& acc) {
+            if constexpr (STAGED) {
+                v4f cst[4];
+                stage_tile(stg, acc[0][0], i, h, cst);
+                const int tl = t & 63;
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    *reinterpret_cast<v4f*>(pending + (8 * q + tl / 8) * W + 4 * (tl % 8)) = cst[q];
+            } else {
+#pragma unroll
+                for (int q = 0; q < S::NST; ++q) {
+                    const int a = q / (4 * S::TW_C), bb = (q / 4) % S::TW_C, qq = q % 4;
+                    const v16f& x = acc[a][bb];
+                    v4f y = {x[4 * qq], x[4 * qq + 1], x[4 * qq + 2], x[4 * qq + 3]};
+                    *reinterpret_cast<v4f*>(pending + a * 32 * W + (tc0 + bb) * 32 + 8 * qq) = y;
+                }
+            }
+        };
+        if (last_in_A)
+            flush(accA);
+        else
+            flush(accB);
+    }
+    finish();
+}
+
 // ---- two levels per pass, w = 16 or 32 ------------------------------------
 // Levels with strides s and 2s fused: the chains of stride 2s are the even and
 // odd elements of the chains of stride s, so one wave walking a chain of
@@ -993,9 +1228,22 @@ hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout
 }
 
 bool fused_newton_levels(int w) { return w == 16 || w == 32; }
+bool layer_first_level(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
 
 hipError_t launch_first_level_fwd(const NewtonArgs& na, float* Aout, const VecDst& rout, int B,
                                   int L, int w, hipStream_t stream) {
+    if (w == 64 || w == 128) {
+        const LevelPlan p = plan_level(B, L, 1, w == 64 ? 4096 : 1024, 64);
+        const dim3 grid((unsigned)p.total),
+            block(w == 64 ? TileShape<64>::NT : TileShape<128>::NT);
+        if (w == 64)
+            hipLaunchKernelGGL((pcr_level_tile_layer<64>), grid, block, 0, stream, Aout, rout, L,
+                               p, na);
+        else
+            hipLaunchKernelGGL((pcr_level_tile_layer<128>), grid, block, 0, stream, Aout, rout, L,
+                               p, na);
+        return hipGetLastError();
+    }
     const LevelPlan p = plan_level(B, L, 1, 8192, 64);
     const dim3 g3((unsigned)((p.total + 3) / 4)), block(256);
     const BlockSrc noA{nullptr, 0, 0, 0};

@@ -185,6 +185,19 @@ def test_forward_all_layer_kinds(dev, w, L, B, layer, alpha):
     assert ok and abs(res.iters - k_ref) <= 1
 
 
+# Tile widths with several rows per workgroup segment: w = 64, B = 40 gives
+# 2-row segments, w = 128, B = 16, L = 203 gives 4-row ones with a 2-row tail.
+@pytest.mark.parametrize("w,L,B", [(64, 130, 40), (128, 203, 16)])
+@pytest.mark.parametrize("layer,alpha", ALL_KINDS)
+def test_forward_tile_segments(dev, w, L, B, layer, alpha):
+    _say(f"forward tile segments w={w} L={L} B={B} layer={layer}")
+    d = synth.mlp_inputs(B, L, w, seed=1100 + w + L + layer)
+    res = _forward(d, dev, layer, alpha)
+    assert res.status == deeppcr.OK
+    ref = oracle.seq_forward(layer, alpha, d["W"], d["bias"], d["z0"])
+    assert normwise_rel_err(h(res.Z), ref) <= TOL
+
+
 @pytest.mark.parametrize("w,L,B", [(4, 30, 2), (16, 200, 3), (32, 100, 2), (64, 40, 2),
                                    (128, 12, 2), (17, 50, 2)])
 @pytest.mark.parametrize("layer,alpha", ALL_KINDS)
