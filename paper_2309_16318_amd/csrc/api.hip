@@ -316,13 +316,16 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
         return timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
                      [&] { return launch_update_reduce(na.Z, x.base, n, na.red, st); });
     }
+    // w = 16, 32: the last level applies the update itself
+    const bool upd = fused_newton_levels(w);
+    const int Kp = upd ? K - 1 : K;
     BlockSrc Ain{ws.A[0], (long long)L * w * w, (long long)w * w, 0};
     VecSrc rin{ws.r[0], ld, (long long)w};
-    // the middle levels 1 .. K-2, two per pass where possible; pass p writes
-    // ws buffers p % 2 (the first level wrote buffers 0)
+    // levels 1 .. Kp-1, two per pass where possible; pass p writes ws
+    // buffers p % 2 (the first level wrote buffers 0)
     int s = 2, p = 1;
-    for (int k = 1; k < K - 1; ++p) {
-        const bool pair = two_level_width(w) && k + 1 < K - 1;
+    for (int k = 1; k < Kp; ++p) {
+        const bool pair = two_level_width(w) && k + 1 < Kp;
         float* Aout = ws.A[p & 1];
         const VecDst rout{ws.r[p & 1], ld, (long long)w};
         double bytes, flops;
@@ -344,18 +347,15 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
         s *= pair ? 4 : 2;
         k += pair ? 2 : 1;
     }
+    if (!upd) {
+        // the last pass wrote the solution to ws r buffer (p - 1) % 2
+        const long long n = (long long)B * L * w;
+        return timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
+                     [&] { return launch_update_reduce(na.Z, rin.base, n, na.red, st); });
+    }
     // the last level with the update Z += x and the convergence reduction
     double bytes, flops;
     level_work(B, L, w, s, &bytes, &flops);
-    if (!fused_newton_levels(w)) {
-        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
-            return launch_pcr_level(Ain, rin, ws.A[p & 1], x, B, L, w, s, st);
-        });
-        if (e != hipSuccess) return e;
-        const long long n = (long long)B * L * w;
-        return timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
-                     [&] { return launch_update_reduce(na.Z, x.base, n, na.red, st); });
-    }
     bytes += 8.0 * B * L * w;  // the iterate is read and written
     return timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
         return launch_last_level_update(Ain, rin, na, B, L, w, s, st);

@@ -1115,6 +1115,220 @@ __global__ __launch_bounds__(256) void pcr_level2_wave(BlockSrc Ain, VecSrc rin,
     }
 }
 
+// ---- two levels per pass, w = 64 or 128 ---------------------------------
+// The chain walk of pcr_level2_wave with one workgroup per segment and one
+// wave per 32-row strip of the blocks.  A lane (i, h) of wave v holds row
+// R = 32 v + i of a block at the columns 8q + 4h .. +3 (q = 0 .. W/8-1): the
+// left MFMA operand, read straight from HBM into registers, and also the
+// layout in which the MFMA leaves a strip of the product (tile tc, float4
+// qq at q = 4 tc + qq).  So A'_m = A_m A_{m-1} stays in registers as the left
+// operand of A''_m = A'_m A'_{m-2}; only the right operands A_{m-1} and
+// A'_{m-2} go through LDS (two blocks), and each element costs one block
+// read and one block write for two levels.
+template <int W>
+struct Tile2Shape {
+    static constexpr int NWV = W / 32;  // waves, one 32-row strip each
+    static constexpr int NT = 64 * NWV;
+    static constexpr int PITCH = W + 4;
+    static constexpr int NQ = W / 8;  // k-steps of 8 (4 per lane half)
+    static constexpr int T = W / 32;  // 32-column tiles of a strip
+};
+
+template <int W>
+using StripA = v4f[Tile2Shape<W>::NQ];
+template <int W>
+using StripC = v16f[Tile2Shape<W>::T];
+
+template <int W, bool TRANS>
+__device__ __forceinline__ void strip_load(const float* blk, StripA<W>& a, int R, int h) {
+#pragma unroll
+    for (int q = 0; q < Tile2Shape<W>::NQ; ++q) {
+        if constexpr (!TRANS) {
+            a[q] = *reinterpret_cast<const v4f*>(blk + R * W + 8 * q + 4 * h);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) a[q][e] = blk[(8 * q + 4 * h + e) * W + R];
+        }
+    }
+}
+
+template <int W>
+__device__ __forceinline__ v4f strip_quad(const StripA<W>& a, int q) {
+    return a[q];
+}
+template <int W>
+__device__ __forceinline__ v4f strip_quad(const StripC<W>& c, int q) {
+    const v16f& x = c[q / 4];
+    const int o = 4 * (q % 4);
+    return v4f{x[o], x[o + 1], x[o + 2], x[o + 3]};
+}
+
+// acc = (strip of M) X, X in LDS transposed (XT[col][k], pitch PITCH): the
+// right operand of k-step q for column tile tc is one 16-byte read, and all
+// offsets fit the immediate field of one base address.
+template <int W, class M>
+__device__ __forceinline__ void strip_product(const float* XT, const M& a, StripC<W>& acc, int i,
+                                              int h) {
+    using S = Tile2Shape<W>;
+#pragma unroll
+    for (int tc = 0; tc < S::T; ++tc) acc[tc] = v16f{};
+    const float* xb = XT + i * S::PITCH + 4 * h;
+    v4f pv[2][S::T];
+#pragma unroll
+    for (int q = 0; q <= S::NQ; ++q) {
+        if (q < S::NQ) {
+#pragma unroll
+            for (int tc = 0; tc < S::T; ++tc)
+                pv[q & 1][tc] = *reinterpret_cast<const v4f*>(xb + 32 * tc * S::PITCH + 8 * q);
+        }
+        // keeps the operand reads of step q beside the MFMAs of step q-1
+        __builtin_amdgcn_sched_barrier(0);
+        if (q > 0) {
+            const int qb = (q - 1) & 1;
+            const v4f av = strip_quad<W>(a, q - 1);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int tc = 0; tc < S::T; ++tc)
+                    acc[tc] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[qb][tc][e], av[e], acc[tc],
+                                                                   0, 0, 0);
+        }
+    }
+}
+
+template <int W>
+__device__ __forceinline__ void strip_zero(StripC<W>& c) {
+#pragma unroll
+    for (int tc = 0; tc < Tile2Shape<W>::T; ++tc) c[tc] = v16f{};
+}
+
+// (strip of M) x for x in LDS; every lane of the row gets the sum.
+template <int W, class M>
+__device__ __forceinline__ float strip_matvec(const M& a, const float* x, int h) {
+    float part = 0.f;
+#pragma unroll
+    for (int q = 0; q < Tile2Shape<W>::NQ; ++q) {
+        const v4f xv = *reinterpret_cast<const v4f*>(x + 8 * q + 4 * h);
+        const v4f av = strip_quad<W>(a, q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) part = fmaf(av[e], xv[e], part);
+    }
+    return part + __shfl_xor(part, 32, 64);
+}
+
+// A strip to a row-major block in global memory.
+template <int W, class M>
+__device__ __forceinline__ void strip_store(float* dst, const M& a, int R, int h) {
+#pragma unroll
+    for (int q = 0; q < Tile2Shape<W>::NQ; ++q)
+        *reinterpret_cast<v4f*>(dst + R * W + 8 * q + 4 * h) = strip_quad<W>(a, q);
+}
+
+// A strip to a transposed block in LDS (XT[col][row], pitch PITCH).  The
+// empty asm statements keep the writes single (not paired into two-offset
+// writes, whose short offsets would need a base register per pair of rows):
+// every offset then fits the immediate field of one base address.
+template <int W, class M>
+__device__ __forceinline__ void strip_put_T(float* XT, const M& a, int R, int h) {
+    using S = Tile2Shape<W>;
+    float* xb = XT + 4 * h * S::PITCH + R;
+#pragma unroll
+    for (int q = 0; q < S::NQ; ++q) {
+        const v4f x = strip_quad<W>(a, q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            xb[(8 * q + e) * S::PITCH] = x[e];
+            asm volatile("" ::: "memory");
+        }
+    }
+}
+
+template <int W, bool TRANS>
+__global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ain, VecSrc rin,
+                                                                     float* __restrict__ Aout,
+                                                                     VecDst rout, int L,
+                                                                     LevelPlan plan) {
+    using S = Tile2Shape<W>;
+    __shared__ float X[W * S::PITCH];  // A_{m-1}, transposed
+    __shared__ float Y[W * S::PITCH];  // A'_{m-2}, transposed
+    __shared__ float rv[2][W];         // r_m in slot m & 1, r_{m-1} in the other
+    __shared__ float rp[2][W];         // r'_{m-2} in slot m & 1, r'_{m-1} in the other
+    const int t = threadIdx.x;
+    const int lane = t & 63, i = lane & 31, h = lane >> 5;
+    const int R = 32 * (t >> 6) + i;
+    const int s = plan.s;
+    const long long item = blockIdx.x;
+    const long long per_b = (long long)s * plan.segs_per_class;
+    const int b = (int)(item / per_b);
+    const long long rem = item - (long long)b * per_b;
+    const int c = (int)(rem / plan.segs_per_class);
+    const int j = (int)(rem - (long long)c * plan.segs_per_class);
+    const int count = (L - 1 - c) / s;  // elements m = 0 .. count
+    const int m0 = j * plan.n;
+    if (m0 > count) return;  // uniform over the workgroup
+    const int m1 = min(count, m0 + plan.n - 1);
+    const int mw = max(0, m0 - 3);
+    const float* ab = Ain.base + b * Ain.bstride;
+    const float* rb = rin.base + b * rin.bstride;
+    float* ob = rout.base + b * rout.bstride;
+    float* Ob = Aout + (long long)b * L * W * W;
+
+    StripA<W> a;             // A_m, then A_{m+1}
+    StripC<W> pE, pO, app;   // A'_m of even / odd elements; A''_m
+    int l = c + s * mw;
+    if (t < W) rv[mw & 1][t] = rb[(long long)l * rin.rstride + t];
+    if (mw >= 1) strip_load<W, TRANS>(ab + (long long)l * Ain.rstride, a, R, h);
+    __syncthreads();
+    // element m: a = A_m on entry and A_{m+1} on exit, pC <- A'_m, pP =
+    // A'_{m-1}.  A_m replaces A_{m-1} in X as soon as the first product is
+    // done, and only then is A_{m+1} requested into the same registers.
+    auto element = [&](int m, StripC<W>& pC, StripC<W>& pP) {
+        const bool more = m < m1;
+        const bool have_prev = m > mw;  // state of element m-1 is valid
+        const bool out_row = m >= m0;
+        // level s: r'_m and A'_m
+        float r1 = rv[m & 1][R];
+        if (m >= 1 && have_prev) r1 += strip_matvec<W>(a, rv[(m + 1) & 1], h);
+        // (the strips are set on every path, so that no old value of a
+        // register set stays live across elements)
+        const bool prod1 = m >= 2 && have_prev;
+        if (prod1)
+            strip_product<W>(X, a, pC, i, h);
+        else
+            strip_zero<W>(pC);
+        __syncthreads();  // X and rv are read
+        if (more && m >= 1) strip_put_T<W>(X, a, R, h);  // A_m
+        // without a next element this rereads the current block (unused)
+        strip_load<W, TRANS>(ab + (long long)(more ? l + s : l) * Ain.rstride, a, R, h);
+        float rnext = 0.f;
+        if (more && t < W) rnext = rb[(long long)(l + s) * rin.rstride + t];
+        // level 2s: r''_m and A''_m
+        float r2 = r1;
+        if (m >= 2 && out_row) r2 += strip_matvec<W>(pC, rp[m & 1], h);
+        const bool prod2 = m >= 4 && out_row;
+        if (prod2)
+            strip_product<W>(Y, pC, app, i, h);
+        else
+            strip_zero<W>(app);
+        if (out_row && h == 0) ob[(long long)l * rout.rstride + R] = r2;
+        __syncthreads();  // Y and rp are read
+        if (prod2) strip_store<W>(Ob + (long long)l * W * W, app, R, h);
+        if (h == 0) rp[m & 1][R] = r1;
+        if (more) {
+            if (m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
+            if (t < W) rv[(m + 1) & 1][t] = rnext;
+        }
+        __syncthreads();
+        l += s;
+    };
+    for (int m = mw; m <= m1; ++m) {
+        if (m & 1)
+            element(m, pO, pE);
+        else
+            element(m, pE, pO);
+    }
+}
+
 }  // namespace
 
 LevelPlan plan_level(int B, int L, int s, long long target_items, int n_max) {
@@ -1184,10 +1398,28 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
     return hipGetLastError();
 }
 
-bool two_level_width(int w) { return w == 16 || w == 32; }
+bool two_level_width(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
 
 // Segments of the fused pair cover elements m = 0 .. (L-1-c)/s of each chain;
 // n rows each, at least 8 so that the 3-row warm-up stays a small share.
+// Tile pairs: about target_wgs workgroups (one segment each), segments of at
+// least 8 elements where the chains allow (a segment re-walks up to 3
+// elements before its first).
+LevelPlan plan_level2_tile(int B, int L, int s, long long target_wgs) {
+    LevelPlan p;
+    p.s = s;
+    const int E = (L - 1) / s + 1;
+    const long long chains = (long long)B * s;
+    long long segs = target_wgs / chains;
+    if (segs < 1) segs = 1;
+    long long n = (E + segs - 1) / segs;
+    if (n < 8) n = 8;
+    p.n = (int)n;
+    p.segs_per_class = (int)((E + n - 1) / n);
+    p.total = chains * p.segs_per_class;
+    return p;
+}
+
 LevelPlan plan_level2(int B, int L, int s, long long target_items) {
     LevelPlan p;
     p.s = s;
@@ -1221,6 +1453,26 @@ hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout
         else
             hipLaunchKernelGGL((pcr_level2_wave<32, false>), g3, block, 0, stream, Ain, rin, Aout,
                                rout, L, p);
+    } else if (w == 64 || w == 128) {
+        const LevelPlan q = plan_level2_tile(B, L, s, w == 64 ? 1024 : 256);
+        const dim3 grid((unsigned)q.total);
+        if (w == 64) {
+            const dim3 blk(Tile2Shape<64>::NT);
+            if (Ain.trans)
+                hipLaunchKernelGGL((pcr_level2_tile<64, true>), grid, blk, 0, stream, Ain, rin,
+                                   Aout, rout, L, q);
+            else
+                hipLaunchKernelGGL((pcr_level2_tile<64, false>), grid, blk, 0, stream, Ain, rin,
+                                   Aout, rout, L, q);
+        } else {
+            const dim3 blk(Tile2Shape<128>::NT);
+            if (Ain.trans)
+                hipLaunchKernelGGL((pcr_level2_tile<128, true>), grid, blk, 0, stream, Ain, rin,
+                                   Aout, rout, L, q);
+            else
+                hipLaunchKernelGGL((pcr_level2_tile<128, false>), grid, blk, 0, stream, Ain, rin,
+                                   Aout, rout, L, q);
+        }
     } else {
         return hipErrorInvalidValue;
     }
