@@ -288,9 +288,10 @@ float bits_to_float(unsigned u) {
 }
 
 // The fused Newton linear solve (w = 16, 32, 64, 128): the layer evaluation
-// runs inside the first PCR level; for w = 16, 32 the update + reduction runs
-// inside the last, for w = 64, 128 the last level writes the solution to `x`
-// as do the first for L <= 2, and the separate update kernel applies it.
+// runs inside the first PCR pass (level 1, or levels 1 and 2 for w = 64, 128
+// and L > 2); for w = 16, 32 the update + reduction runs inside the last
+// level, for w = 64, 128 the last pass writes the solution (as does the
+// first for L <= 2, to `x`) and the separate update kernel applies it.
 // Split in two so that a stopping test on the residual (reduced by the first
 // level) can sit between the halves.
 hipError_t fused_first_level(const NewtonArgs& na, int B, int L, int w, const Ws& ws,
@@ -298,10 +299,18 @@ hipError_t fused_first_level(const NewtonArgs& na, int B, int L, int w, const Ws
     const int K = num_levels(L);
     const double w2 = (double)w * w;
     const long long ld = (long long)L * w;
-    // level 1 with the layers: W once, Z read twice, products and r written
-    const double na2 = (double)(L - 2 > 0 ? L - 2 : 0);
+    // the first level (or two) with the layers: W once, Z read twice,
+    // products and r written
+    const int nl = first_level_count(L, w);
+    const double na2 = (double)(L - 2 * nl > 0 ? L - 2 * nl : 0);
     const double bytes = 4.0 * ((double)L * w2 + B * (na2 * w2 + 3.0 * L * w));
-    const double flops = (double)B * (L * 3.0 * w2 + (L - 1) * 2.0 * w2 + na2 * 2.0 * w2 * w);
+    double flops = (double)B * (L * 3.0 * w2 + (L - 1) * 2.0 * w2 +
+                                (L - 2 > 0 ? L - 2 : 0) * 2.0 * w2 * w);
+    if (nl == 2) {
+        double b2, f2;
+        level_work(B, L, w, 2, &b2, &f2);
+        flops += f2;
+    }
     const VecDst out = (K <= 1) ? x : VecDst{ws.r[0], ld, (long long)w};
     return timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st,
                  [&] { return launch_first_level_fwd(na, ws.A[0], out, B, L, w, st); });
@@ -321,10 +330,11 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
     const int Kp = upd ? K - 1 : K;
     BlockSrc Ain{ws.A[0], (long long)L * w * w, (long long)w * w, 0};
     VecSrc rin{ws.r[0], ld, (long long)w};
-    // levels 1 .. Kp-1, two per pass where possible; pass p writes ws
-    // buffers p % 2 (the first level wrote buffers 0)
-    int s = 2, p = 1;
-    for (int k = 1; k < Kp; ++p) {
+    // the levels after the first one (or two) up to Kp-1, two per pass where
+    // possible; pass p writes ws buffers p % 2 (the first pass wrote buffers 0)
+    const int k0 = first_level_count(L, w);
+    int s = 1 << k0, p = 1;
+    for (int k = k0; k < Kp; ++p) {
         const bool pair = two_level_width(w) && k + 1 < Kp;
         float* Aout = ws.A[p & 1];
         const VecDst rout{ws.r[p & 1], ld, (long long)w};

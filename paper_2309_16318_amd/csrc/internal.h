@@ -105,10 +105,16 @@ struct NewtonArgs {
 bool fused_newton_levels(int w);
 bool layer_first_level(int w);
 
+// Number of PCR levels launch_first_level_fwd runs (1, or 2 for w = 64, 128
+// when the solve has two levels or more).
+int first_level_count(int L, int w);
+
 // First level (s = 1) of the Newton linear solve with the layers, Jacobian
 // blocks and residuals evaluated on the fly (never stored):
 //   r_l = f_l(Z_{l-1}) - Z_l, J_l = df_l at Z_{l-1};
-//   rout[l] = r_l + J_l r_{l-1} (rout[0] = r_0), Aout[l] = J_l J_{l-1} (l >= 2).
+//   rout[l] = r_l + J_l r_{l-1} (rout[0] = r_0), Aout[l] = J_l J_{l-1} (l >= 2);
+// or, when first_level_count says 2, the first two levels: rout and Aout
+// then hold what the level s = 2 writes.
 // Also clears the max|dZ| and max|Z| slots and reduces max|r| into the
 // kRedF slots.
 hipError_t launch_first_level_fwd(const NewtonArgs& na, float* Aout, const VecDst& rout, int B,

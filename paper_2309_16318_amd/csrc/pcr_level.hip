@@ -1163,39 +1163,6 @@ __device__ __forceinline__ v4f strip_quad(const StripC<W>& c, int q) {
     return v4f{x[o], x[o + 1], x[o + 2], x[o + 3]};
 }
 
-// acc = (strip of M) X, X in LDS transposed (XT[col][k], pitch PITCH): the
-// right operand of k-step q for column tile tc is one 16-byte read, and all
-// offsets fit the immediate field of one base address.
-template <int W, class M>
-__device__ __forceinline__ void strip_product(const float* XT, const M& a, StripC<W>& acc, int i,
-                                              int h) {
-    using S = Tile2Shape<W>;
-#pragma unroll
-    for (int tc = 0; tc < S::T; ++tc) acc[tc] = v16f{};
-    const float* xb = XT + i * S::PITCH + 4 * h;
-    v4f pv[2][S::T];
-#pragma unroll
-    for (int q = 0; q <= S::NQ; ++q) {
-        if (q < S::NQ) {
-#pragma unroll
-            for (int tc = 0; tc < S::T; ++tc)
-                pv[q & 1][tc] = *reinterpret_cast<const v4f*>(xb + 32 * tc * S::PITCH + 8 * q);
-        }
-        // keeps the operand reads of step q beside the MFMAs of step q-1
-        __builtin_amdgcn_sched_barrier(0);
-        if (q > 0) {
-            const int qb = (q - 1) & 1;
-            const v4f av = strip_quad<W>(a, q - 1);
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-#pragma unroll
-                for (int tc = 0; tc < S::T; ++tc)
-                    acc[tc] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[qb][tc][e], av[e], acc[tc],
-                                                                   0, 0, 0);
-        }
-    }
-}
-
 template <int W>
 __device__ __forceinline__ void strip_zero(StripC<W>& c) {
 #pragma unroll
@@ -1214,6 +1181,84 @@ __device__ __forceinline__ float strip_matvec(const M& a, const float* x, int h)
         for (int e = 0; e < 4; ++e) part = fmaf(av[e], xv[e], part);
     }
     return part + __shfl_xor(part, 32, 64);
+}
+
+// acc[0 .. NTC-1] = column tiles TC0 .. TC0+NTC-1 of (strip of M) X, X in
+// LDS transposed (XT[col][k], pitch PITCH): the right operand of k-step q for
+// one column tile is one 16-byte read, and all offsets fit the immediate
+// field of one base address.  With MV also returns (strip of M) x for the
+// vector x in LDS (every lane of the row gets the sum), from the left
+// operands as they pass (for accumulator strips this avoids copying the
+// whole strip out of the accumulation registers at once).
+template <int W, int TC0, int NTC, bool MV, class M>
+__device__ __forceinline__ float strip_product(const float* XT, const M& a, v16f (&acc)[NTC],
+                                               int i, int h, const float* x = nullptr) {
+    using S = Tile2Shape<W>;
+#pragma unroll
+    for (int tc = 0; tc < NTC; ++tc) acc[tc] = v16f{};
+    const float* xb = XT + (32 * TC0 + i) * S::PITCH + 4 * h;
+    v4f pv[2][NTC], xv[2];
+    float part = 0.f;
+#pragma unroll
+    for (int q = 0; q <= S::NQ; ++q) {
+        if (q < S::NQ) {
+#pragma unroll
+            for (int tc = 0; tc < NTC; ++tc)
+                pv[q & 1][tc] = *reinterpret_cast<const v4f*>(xb + 32 * tc * S::PITCH + 8 * q);
+            if constexpr (MV) xv[q & 1] = *reinterpret_cast<const v4f*>(x + 8 * q + 4 * h);
+        }
+        // keeps the operand reads of step q beside the MFMAs of step q-1
+        __builtin_amdgcn_sched_barrier(0);
+        if (q > 0) {
+            const int qb = (q - 1) & 1;
+            const v4f av = strip_quad<W>(a, q - 1);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int tc = 0; tc < NTC; ++tc)
+                    acc[tc] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[qb][tc][e], av[e], acc[tc],
+                                                                   0, 0, 0);
+            if constexpr (MV) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) part = fmaf(av[e], xv[qb][e], part);
+            }
+        }
+    }
+    if constexpr (MV) return part + __shfl_xor(part, 32, 64);
+    return 0.f;
+}
+
+// Stores column tiles TC0 .. TC0+NTC-1 of a product strip (row-major block
+// in global memory).
+template <int W, int TC0, int NTC>
+__device__ __forceinline__ void tiles_store(float* dst, const v16f (&acc)[NTC], int R, int h) {
+#pragma unroll
+    for (int tc = 0; tc < NTC; ++tc)
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+            const v16f& x = acc[tc];
+            *reinterpret_cast<v4f*>(dst + R * W + 32 * (TC0 + tc) + 8 * qq + 4 * h) =
+                v4f{x[4 * qq], x[4 * qq + 1], x[4 * qq + 2], x[4 * qq + 3]};
+        }
+}
+
+// Level-2s product of an element, A''_m = A'_m A'_{m-2} (A'_{m-2} in YT),
+// two column tiles at a time, each pair stored as soon as it is done (so no
+// whole product strip is held); returns A'_m r'_{m-2} (r'_{m-2} in LDS).
+template <int W>
+__device__ __forceinline__ float second_product(const float* YT, const StripC<W>& pC,
+                                                const float* rpp, float* dst, int i, int h,
+                                                int R) {
+    constexpr int T = Tile2Shape<W>::T;
+    v16f acc[2];
+    const float part = strip_matvec<W>(pC, rpp, h);
+    strip_product<W, 0, 2, false>(YT, pC, acc, i, h);
+    tiles_store<W, 0, 2>(dst, acc, R, h);
+    if constexpr (T == 4) {
+        strip_product<W, 2, 2, false>(YT, pC, acc, i, h);
+        tiles_store<W, 2, 2>(dst, acc, R, h);
+    }
+    return part;
 }
 
 // A strip to a row-major block in global memory.
@@ -1274,7 +1319,7 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
     float* Ob = Aout + (long long)b * L * W * W;
 
     StripA<W> a;             // A_m, then A_{m+1}
-    StripC<W> pE, pO, app;   // A'_m of even / odd elements; A''_m
+    StripC<W> pE, pO;        // A'_m of even / odd elements
     int l = c + s * mw;
     if (t < W) rv[mw & 1][t] = rb[(long long)l * rin.rstride + t];
     if (mw >= 1) strip_load<W, TRANS>(ab + (long long)l * Ain.rstride, a, R, h);
@@ -1286,16 +1331,16 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
         const bool more = m < m1;
         const bool have_prev = m > mw;  // state of element m-1 is valid
         const bool out_row = m >= m0;
-        // level s: r'_m and A'_m
+        // level s: r'_m and A'_m (the strips are set on every path, so that no
+        // old value of a register set stays live across elements)
         float r1 = rv[m & 1][R];
-        if (m >= 1 && have_prev) r1 += strip_matvec<W>(a, rv[(m + 1) & 1], h);
-        // (the strips are set on every path, so that no old value of a
-        // register set stays live across elements)
         const bool prod1 = m >= 2 && have_prev;
-        if (prod1)
-            strip_product<W>(X, a, pC, i, h);
-        else
+        if (prod1) {
+            r1 += strip_product<W, 0, S::T, true>(X, a, pC, i, h, rv[(m + 1) & 1]);
+        } else {
+            if (m >= 1 && have_prev) r1 += strip_matvec<W>(a, rv[(m + 1) & 1], h);
             strip_zero<W>(pC);
+        }
         __syncthreads();  // X and rv are read
         if (more && m >= 1) strip_put_T<W>(X, a, R, h);  // A_m
         // without a next element this rereads the current block (unused)
@@ -1304,15 +1349,13 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
         if (more && t < W) rnext = rb[(long long)(l + s) * rin.rstride + t];
         // level 2s: r''_m and A''_m
         float r2 = r1;
-        if (m >= 2 && out_row) r2 += strip_matvec<W>(pC, rp[m & 1], h);
         const bool prod2 = m >= 4 && out_row;
         if (prod2)
-            strip_product<W>(Y, pC, app, i, h);
-        else
-            strip_zero<W>(app);
+            r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)l * W * W, i, h, R);
+        else if (m >= 2 && out_row)
+            r2 += strip_matvec<W>(pC, rp[m & 1], h);
         if (out_row && h == 0) ob[(long long)l * rout.rstride + R] = r2;
         __syncthreads();  // Y and rp are read
-        if (prod2) strip_store<W>(Ob + (long long)l * W * W, app, R, h);
         if (h == 0) rp[m & 1][R] = r1;
         if (more) {
             if (m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
@@ -1327,6 +1370,117 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
         else
             element(m, pE, pO);
     }
+}
+
+// The first two levels (s = 1, 2) of a Newton iteration as one pass of the
+// walk above, with the layers evaluated on the fly: element m loads the raw
+// W_m strip, forms the pre-activation W_m Z_{m-1} from it, then
+// r_m = f_m(Z_{m-1}) - Z_m and, scaling its own row, the strip of
+// J_m = D_m W_m (+ I); the walk goes on with A_m = J_m.  Also clears the
+// max|dZ|, max|Z| slots and reduces max|r| into the kRedF slots.
+template <int W>
+__global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile_layer(
+    float* __restrict__ Aout, VecDst rout, int L, LevelPlan plan, NewtonArgs na) {
+    using S = Tile2Shape<W>;
+    __shared__ float X[W * S::PITCH];  // J_{m-1}, transposed
+    __shared__ float Y[W * S::PITCH];  // A'_{m-2}, transposed
+    __shared__ float rv[2][W];         // r_{m-1} in slot (m+1) & 1
+    __shared__ float rp[2][W];         // r'_{m-2} in slot m & 1
+    __shared__ float zv[2][W];         // Z_m in slot m & 1, Z_{m-1} in the other
+    const int t = threadIdx.x;
+    if (blockIdx.x == 0)
+        for (int k = t; k < 2 * kRedShards; k += S::NT) na.red[k] = 0u;
+    const int lane = t & 63, i0 = lane & 31, h0 = lane >> 5;
+    const int R0 = 32 * (t >> 6) + i0;
+    const int b = (int)(blockIdx.x / plan.segs_per_class);  // s = 1: one chain per system
+    const int j = (int)(blockIdx.x - (long long)b * plan.segs_per_class);
+    const int count = L - 1;
+    const int m0 = j * plan.n;
+    unsigned mr = 0u;
+    if (m0 <= count) {  // uniform over the workgroup
+        const int m1 = min(count, m0 + plan.n - 1);
+        const int mw = max(0, m0 - 3);
+        const bool res = layer_residual(na.layer);
+        const float* Zb = na.Z + (long long)b * L * W;
+        float* ob = rout.base + b * rout.bstride;
+        float* Ob = Aout + (long long)b * L * W * W;
+        StripA<W> a;            // W_m, then J_m; then W_{m+1}
+        StripC<W> pE, pO;       // A'_m of even / odd elements
+        if (t < W) {
+            zv[(mw + 1) & 1][t] =
+                mw >= 1 ? Zb[(long long)(mw - 1) * W + t] : na.z0[(long long)b * W + t];
+            zv[mw & 1][t] = Zb[(long long)mw * W + t];
+        }
+        strip_load<W, false>(na.W + (long long)mw * W * W, a, R0, h0);
+        __syncthreads();
+        auto element = [&](int m, StripC<W>& pC, StripC<W>& pP) {
+            const bool more = m < m1;
+            const bool have_prev = m > mw;
+            const bool out_row = m >= m0;
+            // The lane's row and half as opaque values: the LDS and global
+            // addresses derived from them are formed per element instead of
+            // being held (or spilled) across the whole walk.
+            int R = R0, h = h0, i = i0;
+            asm volatile("" : "+v"(R), "+v"(h), "+v"(i));
+            // layer m at Z_{m-1}: r_m and the strip of J_m
+            const float* zp = zv[(m + 1) & 1];
+            float dsc;
+            const float f = layer_out<W>(
+                na, strip_matvec<W>(a, zp, h) + na.bias[(long long)m * W + R], zp[R], &dsc);
+            const float rm = f - zv[m & 1][R];
+            mr = max(mr, __float_as_uint(fabsf(rm)));
+            // the diagonal is column k = R, at 8q + e = R - 4h (the empty asm
+            // keeps the compiler from holding 64 precomputed selects)
+            int dk = res ? R - 4 * h : -1;
+            asm volatile("" : "+v"(dk));
+#pragma unroll
+            for (int q = 0; q < S::NQ; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    a[q][e] = fmaf(dsc, a[q][e], dk == 8 * q + e ? 1.f : 0.f);
+            // level 1: r'_m and A'_m
+            float r1 = rm;
+            const bool prod1 = m >= 2 && have_prev;
+            if (prod1) {
+                r1 += strip_product<W, 0, S::T, true>(X, a, pC, i, h, rv[(m + 1) & 1]);
+            } else {
+                if (m >= 1 && have_prev) r1 += strip_matvec<W>(a, rv[(m + 1) & 1], h);
+                strip_zero<W>(pC);
+            }
+            __syncthreads();  // X, rv and zv are read
+            if (more && m >= 1) strip_put_T<W>(X, a, R, h);  // J_m
+            // without a next element this rereads the current block (unused)
+            strip_load<W, false>(na.W + (long long)(more ? m + 1 : m) * W * W, a, R, h);
+            float znext = 0.f;
+            if (more && t < W) znext = Zb[(long long)(m + 1) * W + t];
+            // level 2: r''_m and A''_m
+            float r2 = r1;
+            const bool prod2 = m >= 4 && out_row;
+            if (prod2)
+                r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)m * W * W, i, h, R);
+            else if (m >= 2 && out_row)
+                r2 += strip_matvec<W>(pC, rp[m & 1], h);
+            if (out_row && h == 0) ob[(long long)m * rout.rstride + R] = r2;
+            __syncthreads();  // Y and rp are read
+            if (h == 0) {
+                rp[m & 1][R] = r1;
+                rv[m & 1][R] = rm;
+            }
+            if (more) {
+                if (m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
+                if (t < W) zv[(m + 1) & 1][t] = znext;
+            }
+            __syncthreads();
+        };
+        for (int m = mw; m <= m1; ++m) {
+            if (m & 1)
+                element(m, pO, pE);
+            else
+                element(m, pE, pO);
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) mr = max(mr, (unsigned)__shfl_xor((int)mr, off, 64));
+    if (lane == 0) atomicMax(na.red + kRedF + (int)(blockIdx.x % kRedShards), mr);
 }
 
 }  // namespace
@@ -1480,10 +1634,23 @@ hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout
 }
 
 bool fused_newton_levels(int w) { return w == 16 || w == 32; }
+
+int first_level_count(int L, int w) { return (w == 64 || w == 128) && L > 2 ? 2 : 1; }
 bool layer_first_level(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
 
 hipError_t launch_first_level_fwd(const NewtonArgs& na, float* Aout, const VecDst& rout, int B,
                                   int L, int w, hipStream_t stream) {
+    if (first_level_count(L, w) == 2) {
+        const LevelPlan q = plan_level2_tile(B, L, 1, w == 64 ? 1024 : 256);
+        const dim3 grid((unsigned)q.total);
+        if (w == 64)
+            hipLaunchKernelGGL((pcr_level2_tile_layer<64>), grid, dim3(Tile2Shape<64>::NT), 0,
+                               stream, Aout, rout, L, q, na);
+        else
+            hipLaunchKernelGGL((pcr_level2_tile_layer<128>), grid, dim3(Tile2Shape<128>::NT), 0,
+                               stream, Aout, rout, L, q, na);
+        return hipGetLastError();
+    }
     if (w == 64 || w == 128) {
         const LevelPlan p = plan_level(B, L, 1, w == 64 ? 4096 : 1024, 64);
         const dim3 grid((unsigned)p.total),
