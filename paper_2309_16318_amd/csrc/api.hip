@@ -198,6 +198,16 @@ void level2_work(int B, int L, int w, int s, double* bytes, double* flops) {
     *flops = f1 + f2;
 }
 
+// Algorithmic work of the last two levels as mat-vecs only (strides s, 2s,
+// 4s >= L): A_l read once for l >= s; mat-vecs A_l r_{l-s} and
+// A_l r'_{l-s} for l >= s, A_l t_{l-s} for l >= 2s; r read and written once.
+void last2_work(int B, int L, int w, int s, double* bytes, double* flops) {
+    const double n1 = (double)(L - s), n2 = (double)(L - 2 * s > 0 ? L - 2 * s : 0);
+    const double w2 = (double)w * w;
+    *bytes = 4.0 * B * (n1 * w2 + 2.0 * L * w);
+    *flops = (double)B * 2.0 * w2 * (2.0 * n1 + n2);
+}
+
 // Runs all PCR levels.  Level 0 reads (A0, r0); level k writes operators to
 // ws A buffer (k + a_first) % 2 and vectors to ws r buffer (k + r_first) % 2,
 // except the last level, which writes the solution to `x`.
@@ -223,7 +233,12 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
                            : VecDst{wsr[(p + r_first) & 1], (long long)L * w, (long long)w};
         double bytes, flops;
         hipError_t e;
-        if (pair) {
+        if (pair && last && last_pair_width(w)) {
+            last2_work(B, L, w, s, &bytes, &flops);
+            e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+                return launch_pcr_level2_last(Ain, rin, rout, B, L, w, s, st);
+            });
+        } else if (pair) {
             level2_work(B, L, w, s, &bytes, &flops);
             e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
                 return launch_pcr_level2(Ain, rin, Aout, rout, B, L, w, s, st);
@@ -340,7 +355,12 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
         const VecDst rout{ws.r[p & 1], ld, (long long)w};
         double bytes, flops;
         hipError_t e;
-        if (pair) {
+        if (pair && !upd && k + 1 == K - 1 && last_pair_width(w)) {
+            last2_work(B, L, w, s, &bytes, &flops);
+            e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+                return launch_pcr_level2_last(Ain, rin, rout, B, L, w, s, st);
+            });
+        } else if (pair) {
             level2_work(B, L, w, s, &bytes, &flops);
             e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
                 return launch_pcr_level2(Ain, rin, Aout, rout, B, L, w, s, st);

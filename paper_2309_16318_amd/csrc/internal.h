@@ -139,6 +139,13 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
 // accepts: rout[l] and Aout[l] hold what level 2s would have written
 // (operators for rows l >= 4s).  Aout must not be the buffer Ain reads.
 bool two_level_width(int w);
+
+// The last two levels of a solve (strides s, 2s with 4s >= L) in one pass
+// without operator products (mat-vecs only), for the widths last_pair_width
+// accepts; rout gets the solution.
+bool last_pair_width(int w);
+hipError_t launch_pcr_level2_last(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
+                                  int B, int L, int w, int s, hipStream_t stream);
 hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
                              const VecDst& rout, int B, int L, int w, int s,
                              hipStream_t stream);

@@ -1372,6 +1372,98 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
     }
 }
 
+// The last two levels of a solve (strides s and 2s, 4s >= L): no operator
+// is written, and the one product the walk would form, A'_m = A_m A_{m-1},
+// only ever meets the vector r'_{m-2}, so A'_m r'_{m-2} is taken as
+// A_m (A_{m-1} r'_{m-2}) = A_m t_{m-1}, with t_m = A_m r'_{m-1} formed by the
+// element before: three mat-vecs per element and no MFMA work.  The strips
+// are double-buffered in registers (the next one is requested before the
+// mat-vecs of the current one).
+template <int W, bool TRANS>
+__global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile_last(BlockSrc Ain,
+                                                                          VecSrc rin,
+                                                                          VecDst rout, int L,
+                                                                          LevelPlan plan) {
+    using S = Tile2Shape<W>;
+    __shared__ float rv[2][W];  // r_m in slot m & 1, r_{m-1} in the other
+    __shared__ float rp[2][W];  // r'_{m-1} in slot (m+1) & 1
+    __shared__ float tv[2][W];  // t_{m-1} = A_{m-1} r'_{m-2} in slot (m+1) & 1
+    const int t = threadIdx.x;
+    const int lane = t & 63, h = lane >> 5;
+    const int R = 32 * (t >> 6) + (lane & 31);
+    const int s = plan.s;
+    const long long item = blockIdx.x;
+    const long long per_b = (long long)s * plan.segs_per_class;
+    const int b = (int)(item / per_b);
+    const long long rem = item - (long long)b * per_b;
+    const int c = (int)(rem / plan.segs_per_class);
+    const int j = (int)(rem - (long long)c * plan.segs_per_class);
+    const int count = (L - 1 - c) / s;  // elements m = 0 .. count
+    const int m0 = j * plan.n;
+    if (m0 > count) return;  // uniform over the workgroup
+    const int m1 = min(count, m0 + plan.n - 1);
+    const int mw = max(0, m0 - 3);
+    const float* ab = Ain.base + b * Ain.bstride;
+    const float* rb = rin.base + b * rin.bstride;
+    float* ob = rout.base + b * rout.bstride;
+
+    StripA<W> aE, aO;  // A_m of even / odd elements
+    int l = c + s * mw;
+    if (t < W) rv[mw & 1][t] = rb[(long long)l * rin.rstride + t];
+    if (mw & 1)
+        strip_load<W, TRANS>(ab + (long long)l * Ain.rstride, aO, R, h);
+    else
+        strip_load<W, TRANS>(ab + (long long)l * Ain.rstride, aE, R, h);
+    __syncthreads();
+    auto element = [&](int m, StripA<W>& aC, StripA<W>& aN) {
+        const bool more = m < m1;
+        const bool have_prev = m > mw;
+        const bool out_row = m >= m0;
+        // the next strip (without a next element the current block again)
+        strip_load<W, TRANS>(ab + (long long)(more ? l + s : l) * Ain.rstride, aN, R, h);
+        float rnext = 0.f;
+        if (more && t < W) rnext = rb[(long long)(l + s) * rin.rstride + t];
+        const float* rm1 = rv[(m + 1) & 1];
+        const float* rpm1 = rp[(m + 1) & 1];
+        const float* tm1 = tv[(m + 1) & 1];
+        float u1 = 0.f, u2 = 0.f, u3 = 0.f;  // A_m r_{m-1}, A_m r'_{m-1}, A_m t_{m-1}
+#pragma unroll
+        for (int q = 0; q < S::NQ; ++q) {
+            const int k = 8 * q + 4 * h;
+            const v4f x1 = *reinterpret_cast<const v4f*>(rm1 + k);
+            const v4f x2 = *reinterpret_cast<const v4f*>(rpm1 + k);
+            const v4f x3 = *reinterpret_cast<const v4f*>(tm1 + k);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                u1 = fmaf(aC[q][e], x1[e], u1);
+                u2 = fmaf(aC[q][e], x2[e], u2);
+                u3 = fmaf(aC[q][e], x3[e], u3);
+            }
+        }
+        u1 += __shfl_xor(u1, 32, 64);
+        u2 += __shfl_xor(u2, 32, 64);
+        u3 += __shfl_xor(u3, 32, 64);
+        float r1 = rv[m & 1][R];
+        if (m >= 1 && have_prev) r1 += u1;
+        const float r2 = (m >= 2 && out_row) ? r1 + u3 : r1;
+        if (out_row && h == 0) ob[(long long)l * rout.rstride + R] = r2;
+        __syncthreads();  // rv, rp and tv are read
+        if (h == 0) {
+            rp[m & 1][R] = r1;
+            tv[m & 1][R] = u2;
+        }
+        if (more && t < W) rv[(m + 1) & 1][t] = rnext;
+        __syncthreads();
+        l += s;
+    };
+    for (int m = mw; m <= m1; ++m) {
+        if (m & 1)
+            element(m, aO, aE);
+        else
+            element(m, aE, aO);
+    }
+}
+
 // The first two levels (s = 1, 2) of a Newton iteration as one pass of the
 // walk above, with the layers evaluated on the fly: element m loads the raw
 // W_m strip, forms the pre-activation W_m Z_{m-1} from it, then
@@ -1632,6 +1724,34 @@ hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout
     }
     return hipGetLastError();
 }
+
+hipError_t launch_pcr_level2_last(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
+                                  int B, int L, int w, int s, hipStream_t stream) {
+    const LevelPlan q = plan_level2_tile(B, L, s, w == 64 ? 4096 : 2048);
+    const dim3 grid((unsigned)q.total);
+    if (w == 64) {
+        const dim3 blk(Tile2Shape<64>::NT);
+        if (Ain.trans)
+            hipLaunchKernelGGL((pcr_level2_tile_last<64, true>), grid, blk, 0, stream, Ain, rin,
+                               rout, L, q);
+        else
+            hipLaunchKernelGGL((pcr_level2_tile_last<64, false>), grid, blk, 0, stream, Ain, rin,
+                               rout, L, q);
+    } else if (w == 128) {
+        const dim3 blk(Tile2Shape<128>::NT);
+        if (Ain.trans)
+            hipLaunchKernelGGL((pcr_level2_tile_last<128, true>), grid, blk, 0, stream, Ain, rin,
+                               rout, L, q);
+        else
+            hipLaunchKernelGGL((pcr_level2_tile_last<128, false>), grid, blk, 0, stream, Ain, rin,
+                               rout, L, q);
+    } else {
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+bool last_pair_width(int w) { return w == 64 || w == 128; }
 
 bool fused_newton_levels(int w) { return w == 16 || w == 32; }
 
