@@ -1327,10 +1327,15 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
     // element m: a = A_m on entry and A_{m+1} on exit, pC <- A'_m, pP =
     // A'_{m-1}.  A_m replaces A_{m-1} in X as soon as the first product is
     // done, and only then is A_{m+1} requested into the same registers.
+    // Two barriers per element: B0 after the reads of X and rv, B1 after
+    // those of Y and rp.  X and rv are rewritten between B0 and B1 (read
+    // again after B1), Y and rp after B1 (read again after the next B0).
     auto element = [&](int m, StripC<W>& pC, StripC<W>& pP) {
         const bool more = m < m1;
         const bool have_prev = m > mw;  // state of element m-1 is valid
         const bool out_row = m >= m0;
+        float rnext = 0.f;
+        if (more && t < W) rnext = rb[(long long)(l + s) * rin.rstride + t];
         // level s: r'_m and A'_m (the strips are set on every path, so that no
         // old value of a register set stays live across elements)
         float r1 = rv[m & 1][R];
@@ -1341,12 +1346,11 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
             if (m >= 1 && have_prev) r1 += strip_matvec<W>(a, rv[(m + 1) & 1], h);
             strip_zero<W>(pC);
         }
-        __syncthreads();  // X and rv are read
+        __syncthreads();  // B0: X and rv are read
         if (more && m >= 1) strip_put_T<W>(X, a, R, h);  // A_m
+        if (more && t < W) rv[(m + 1) & 1][t] = rnext;
         // without a next element this rereads the current block (unused)
         strip_load<W, TRANS>(ab + (long long)(more ? l + s : l) * Ain.rstride, a, R, h);
-        float rnext = 0.f;
-        if (more && t < W) rnext = rb[(long long)(l + s) * rin.rstride + t];
         // level 2s: r''_m and A''_m
         float r2 = r1;
         const bool prod2 = m >= 4 && out_row;
@@ -1355,13 +1359,9 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
         else if (m >= 2 && out_row)
             r2 += strip_matvec<W>(pC, rp[m & 1], h);
         if (out_row && h == 0) ob[(long long)l * rout.rstride + R] = r2;
-        __syncthreads();  // Y and rp are read
+        __syncthreads();  // B1: Y and rp are read
         if (h == 0) rp[m & 1][R] = r1;
-        if (more) {
-            if (m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
-            if (t < W) rv[(m + 1) & 1][t] = rnext;
-        }
-        __syncthreads();
+        if (more && m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
         l += s;
     };
     for (int m = mw; m <= m1; ++m) {
@@ -1505,10 +1505,14 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile_layer(
         }
         strip_load<W, false>(na.W + (long long)mw * W * W, a, R0, h0);
         __syncthreads();
+        // Two barriers per element as in pcr_level2_tile; zv and rv are
+        // rewritten before B1, rp and Y after it.
         auto element = [&](int m, StripC<W>& pC, StripC<W>& pP) {
             const bool more = m < m1;
             const bool have_prev = m > mw;
             const bool out_row = m >= m0;
+            float znext = 0.f;
+            if (more && t < W) znext = Zb[(long long)(m + 1) * W + t];
             // The lane's row and half as opaque values: the LDS and global
             // addresses derived from them are formed per element instead of
             // being held (or spilled) across the whole walk.
@@ -1539,12 +1543,12 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile_layer(
                 if (m >= 1 && have_prev) r1 += strip_matvec<W>(a, rv[(m + 1) & 1], h);
                 strip_zero<W>(pC);
             }
-            __syncthreads();  // X, rv and zv are read
+            __syncthreads();  // B0: X, rv and zv are read
             if (more && m >= 1) strip_put_T<W>(X, a, R, h);  // J_m
+            if (h == 0) rv[m & 1][R] = rm;
+            if (more && t < W) zv[(m + 1) & 1][t] = znext;
             // without a next element this rereads the current block (unused)
             strip_load<W, false>(na.W + (long long)(more ? m + 1 : m) * W * W, a, R, h);
-            float znext = 0.f;
-            if (more && t < W) znext = Zb[(long long)(m + 1) * W + t];
             // level 2: r''_m and A''_m
             float r2 = r1;
             const bool prod2 = m >= 4 && out_row;
@@ -1553,16 +1557,9 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile_layer(
             else if (m >= 2 && out_row)
                 r2 += strip_matvec<W>(pC, rp[m & 1], h);
             if (out_row && h == 0) ob[(long long)m * rout.rstride + R] = r2;
-            __syncthreads();  // Y and rp are read
-            if (h == 0) {
-                rp[m & 1][R] = r1;
-                rv[m & 1][R] = rm;
-            }
-            if (more) {
-                if (m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
-                if (t < W) zv[(m + 1) & 1][t] = znext;
-            }
-            __syncthreads();
+            __syncthreads();  // B1: Y and rp are read
+            if (h == 0) rp[m & 1][R] = r1;
+            if (more && m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
         };
         for (int m = mw; m <= m1; ++m) {
             if (m & 1)
