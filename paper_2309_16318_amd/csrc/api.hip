@@ -211,8 +211,11 @@ void last2_work(int B, int L, int w, int s, double* bytes, double* flops) {
 // Runs all PCR levels.  Level 0 reads (A0, r0); level k writes operators to
 // ws A buffer (k + a_first) % 2 and vectors to ws r buffer (k + r_first) % 2,
 // except the last level, which writes the solution to `x`.
+// With bwd the first pass (levels 1 and 2) forms the backward's blocks from
+// the weights instead of reading A0 (w = 64, 128 and L > 2 only).
 hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int B, int L, int w,
-                     float* wsA[2], float* wsr[2], int a_first, int r_first, hipStream_t st) {
+                     float* wsA[2], float* wsr[2], int a_first, int r_first, hipStream_t st,
+                     const BwdArgs* bwd = nullptr) {
     const int K = num_levels(L);
     if (K == 0) {
         const double bytes = 8.0 * B * L * w;
@@ -233,7 +236,14 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
                            : VecDst{wsr[(p + r_first) & 1], (long long)L * w, (long long)w};
         double bytes, flops;
         hipError_t e;
-        if (pair && last && last_pair_width(w)) {
+        if (bwd && k == 0) {
+            // blocks from the weights (read from L2): the products and r
+            level2_work(B, L, w, s, &bytes, &flops);
+            bytes -= 4.0 * B * (L - 1) * (double)w * w;
+            e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+                return launch_pcr_level2_bwd(*bwd, rin, Aout, rout, B, L, w, st);
+            });
+        } else if (pair && last && last_pair_width(w)) {
             last2_work(B, L, w, s, &bytes, &flops);
             e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
                 return launch_pcr_level2_last(Ain, rin, rout, B, L, w, s, st);
@@ -688,17 +698,22 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
     hipStream_t st = (hipStream_t)stream;
     Ws ws = carve(workspace, lo);
     const double w2 = (double)w * w;
-    hipError_t e = timed(DEEPPCR_KCLASS_LAYER, 4.0 * B * L * (w2 + 3.0 * w),
-                         (double)B * L * 3.0 * w2, st, [&] {
-        return launch_backward_assemble(W, bias, z0, Z, G, ws.A[1], ws.r[1], ws.dscale, B, L, w,
-                                        layer, alpha, st);
+    // w = 64, 128 (L > 2): the first PCR pass forms the blocks from the
+    // weights and c d, so the assembly writes only c d and the right-hand side
+    const bool from_weights = (w == 64 || w == 128) && L > 2;
+    const BwdArgs bw{W, ws.dscale, layer_residual(layer) ? 1 : 0};
+    const double jbytes = from_weights ? 0.0 : 4.0 * B * L * w2;
+    hipError_t e = timed(DEEPPCR_KCLASS_LAYER, jbytes + 4.0 * B * L * 3.0 * w,
+                         (double)B * L * (from_weights ? 2.0 : 3.0) * w2, st, [&] {
+        return launch_backward_assemble(W, bias, z0, Z, G, from_weights ? nullptr : ws.A[1],
+                                        ws.r[1], ws.dscale, B, L, w, layer, alpha, st);
     });
     if (e != hipSuccess) return hip_fail(e, "backward_assemble");
     const VecDst lam{Lambda + (long long)(L - 1) * w, (long long)L * w, -(long long)w};
     e = pcr_sweep(BlockSrc{ws.A[1], (long long)L * w * w, (long long)w * w,
                            backward_blocks_transposed(w) ? 1 : 0},
                   VecSrc{ws.r[1], (long long)L * w, (long long)w}, lam, B, L, w, ws.A, ws.r, 0, 0,
-                  st);
+                  st, from_weights ? &bw : nullptr);
     if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
     e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * (w2 + 3.0 * B * w), 2.0 * B * w2, st, [&] {
         return launch_dz0(W, ws.dscale, Lambda, dz0, B, L, w, layer, st);

@@ -87,6 +87,15 @@ struct LevelPlan {
 };
 LevelPlan plan_level(int B, int L, int s, long long target_items, int n_max);
 
+// The blocks of the backward's reversed transposed system formed from the
+// weights instead of read from memory: row m >= 1 holds J_{L-m}^T with
+// J_l = diag(dscale_l) W_l (+ I for residual layers), dscale [B, L, w].
+struct BwdArgs {
+    const float* W;       // [L, w, w]
+    const float* dscale;  // [B, L, w]
+    int residual;
+};
+
 // Inputs of the layer evaluation fused into the first PCR level of a Newton
 // iteration, and of the Newton update fused into the last level.
 struct NewtonArgs {
@@ -140,6 +149,12 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
 // (operators for rows l >= 4s).  Aout must not be the buffer Ain reads.
 bool two_level_width(int w);
 
+// The first two levels (s = 1, 2) of the backward solve with the blocks
+// formed from the weights (w = 64, 128, L > 2); rout and Aout as for
+// launch_pcr_level2.
+hipError_t launch_pcr_level2_bwd(const BwdArgs& bw, const VecSrc& rin, float* Aout,
+                                 const VecDst& rout, int B, int L, int w, hipStream_t stream);
+
 // The last two levels of a solve (strides s, 2s with 4s >= L) in one pass
 // without operator products (mat-vecs only), for the widths last_pair_width
 // accepts; rout gets the solution.
@@ -176,7 +191,7 @@ hipError_t launch_update_reduce(float* Z, const float* x, long long n, unsigned*
 // blocks[m = L-l] = J_l^T for l >= 1 (stored as J_l itself, i.e. to be read
 // transposed, when backward_blocks_transposed(w)), right-hand side
 // rrev[m] = G if m == 0 else 0, and dscale[b, l] = c * (1 - tanh(a_l)^2) in
-// natural order.
+// natural order.  For w = 16, 32, 64, 128 a null `blocks` skips the blocks.
 bool backward_blocks_transposed(int w);
 hipError_t launch_backward_assemble(const float* W, const float* bias, const float* z0,
                                     const float* Z, const float* G, float* A, float* rrev,

@@ -295,8 +295,8 @@ __global__ __launch_bounds__(kThreads) void copy_rows_kernel(VecSrc src, VecDst 
 // a_i = W_l[i,:] z + b_i is reduced by lane shuffles inside the group and
 // every lane of the group then holds a_i.  The Jacobian rows are written with
 // float4 stores.  Mode FWD writes J_l at row l and the residual; mode BWD
-// writes J_l (not transposed) at reversed row L - l, c * d_l and the
-// reversed right-hand side (G at reversed row 0).
+// writes J_l (not transposed) at reversed row L - l (unless A is null),
+// c * d_l and the reversed right-hand side (G at reversed row 0).
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 template <int W>
@@ -360,7 +360,7 @@ __global__ __launch_bounds__(256) void layer_eval_vec(
             const int mr = L - 1 - l;
             r[((long long)b * L + mr) * W + i] = (mr == 0) ? G[(long long)b * W + i] : 0.f;
         }
-        if (l >= 1) {
+        if (l >= 1 && A != nullptr) {
             v4f j4 = w4 * dsc;
             if (res && i >= c4 && i < c4 + 4) j4[i - c4] += 1.f;
             *reinterpret_cast<v4f*>(Ab + i * W + c4) = j4;

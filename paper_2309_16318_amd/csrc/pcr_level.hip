@@ -1288,11 +1288,36 @@ __device__ __forceinline__ void strip_put_T(float* XT, const M& a, int R, int h)
     }
 }
 
-template <int W, bool TRANS>
+// The strip of row m of the backward's reversed transposed system, formed
+// from the weights: J_{L-m}^T[R][k] = dscale_k W_{L-m}[k][R] (+ 1 if k = R);
+// rows m < 1 (never read) are formed as row 1.
+template <int W>
+__device__ __forceinline__ void strip_load_bwd(const BwdArgs& bw, int b, int L, int m,
+                                               StripA<W>& a, int R, int h) {
+    const int lay = L - max(m, 1);
+    const float* Wl = bw.W + (long long)lay * W * W;
+    const float* dl = bw.dscale + ((long long)b * L + lay) * W;
+    // the diagonal is column k = R, at 8q + e = R - 4h (opaque, so that the
+    // compiler forms the selects here instead of holding them all)
+    int dk = bw.residual ? R - 4 * h : -1;
+    asm volatile("" : "+v"(dk));
+#pragma unroll
+    for (int q = 0; q < Tile2Shape<W>::NQ; ++q) {
+        const v4f d4 = *reinterpret_cast<const v4f*>(dl + 8 * q + 4 * h);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            a[q][e] = fmaf(d4[e], Wl[(8 * q + 4 * h + e) * W + R], dk == 8 * q + e ? 1.f : 0.f);
+    }
+}
+
+// SRCB: the blocks are the backward's, formed from the weights (bw; Ain is
+// unused; s = 1).
+template <int W, bool TRANS, bool SRCB = false>
 __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ain, VecSrc rin,
                                                                      float* __restrict__ Aout,
                                                                      VecDst rout, int L,
-                                                                     LevelPlan plan) {
+                                                                     LevelPlan plan,
+                                                                     BwdArgs bw = {}) {
     using S = Tile2Shape<W>;
     __shared__ float X[W * S::PITCH];  // A_{m-1}, transposed
     __shared__ float Y[W * S::PITCH];  // A'_{m-2}, transposed
@@ -1320,9 +1345,15 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
 
     StripA<W> a;             // A_m, then A_{m+1}
     StripC<W> pE, pO;        // A'_m of even / odd elements
+    auto load = [&](int row) {
+        if constexpr (SRCB)
+            strip_load_bwd<W>(bw, b, L, row, a, R, h);
+        else
+            strip_load<W, TRANS>(ab + (long long)row * Ain.rstride, a, R, h);
+    };
     int l = c + s * mw;
     if (t < W) rv[mw & 1][t] = rb[(long long)l * rin.rstride + t];
-    if (mw >= 1) strip_load<W, TRANS>(ab + (long long)l * Ain.rstride, a, R, h);
+    if (mw >= 1) load(l);
     __syncthreads();
     // element m: a = A_m on entry and A_{m+1} on exit, pC <- A'_m, pP =
     // A'_{m-1}.  A_m replaces A_{m-1} in X as soon as the first product is
@@ -1350,7 +1381,7 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ai
         if (more && m >= 1) strip_put_T<W>(X, a, R, h);  // A_m
         if (more && t < W) rv[(m + 1) & 1][t] = rnext;
         // without a next element this rereads the current block (unused)
-        strip_load<W, TRANS>(ab + (long long)(more ? l + s : l) * Ain.rstride, a, R, h);
+        load(more ? l + s : l);
         // level 2s: r''_m and A''_m
         float r2 = r1;
         const bool prod2 = m >= 4 && out_row;
@@ -1407,20 +1438,26 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile_last(BlockS
     const float* rb = rin.base + b * rin.bstride;
     float* ob = rout.base + b * rout.bstride;
 
-    StripA<W> aE, aO;  // A_m of even / odd elements
+    StripA<W> aE, aO;  // A_m of even / odd elements (A_0 is never read)
     int l = c + s * mw;
     if (t < W) rv[mw & 1][t] = rb[(long long)l * rin.rstride + t];
-    if (mw & 1)
-        strip_load<W, TRANS>(ab + (long long)l * Ain.rstride, aO, R, h);
-    else
-        strip_load<W, TRANS>(ab + (long long)l * Ain.rstride, aE, R, h);
+    if (mw >= 1) {
+        if (mw & 1)
+            strip_load<W, TRANS>(ab + (long long)l * Ain.rstride, aO, R, h);
+        else
+            strip_load<W, TRANS>(ab + (long long)l * Ain.rstride, aE, R, h);
+    } else {
+#pragma unroll
+        for (int q = 0; q < S::NQ; ++q) aE[q] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
     __syncthreads();
     auto element = [&](int m, StripA<W>& aC, StripA<W>& aN) {
         const bool more = m < m1;
         const bool have_prev = m > mw;
         const bool out_row = m >= m0;
-        // the next strip (without a next element the current block again)
-        strip_load<W, TRANS>(ab + (long long)(more ? l + s : l) * Ain.rstride, aN, R, h);
+        // the next strip; with chains of a few elements, as here, the
+        // segments are short, so no block is read that is not used
+        if (more) strip_load<W, TRANS>(ab + (long long)(l + s) * Ain.rstride, aN, R, h);
         float rnext = 0.f;
         if (more && t < W) rnext = rb[(long long)(l + s) * rin.rstride + t];
         const float* rm1 = rv[(m + 1) & 1];
@@ -1719,6 +1756,22 @@ hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout
     } else {
         return hipErrorInvalidValue;
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_pcr_level2_bwd(const BwdArgs& bw, const VecSrc& rin, float* Aout,
+                                 const VecDst& rout, int B, int L, int w, hipStream_t stream) {
+    const LevelPlan q = plan_level2_tile(B, L, 1, w == 64 ? 1024 : 256);
+    const dim3 grid((unsigned)q.total);
+    const BlockSrc none{nullptr, 0, 0, 0};
+    if (w == 64)
+        hipLaunchKernelGGL((pcr_level2_tile<64, false, true>), grid, dim3(Tile2Shape<64>::NT), 0,
+                           stream, none, rin, Aout, rout, L, q, bw);
+    else if (w == 128)
+        hipLaunchKernelGGL((pcr_level2_tile<128, false, true>), grid, dim3(Tile2Shape<128>::NT),
+                           0, stream, none, rin, Aout, rout, L, q, bw);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

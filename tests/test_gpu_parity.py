@@ -185,9 +185,10 @@ def test_forward_all_layer_kinds(dev, w, L, B, layer, alpha):
     assert ok and abs(res.iters - k_ref) <= 1
 
 
-# Tile widths with several rows per workgroup segment: w = 64, B = 40 gives
-# 2-row segments, w = 128, B = 16, L = 203 gives 4-row ones with a 2-row tail.
-@pytest.mark.parametrize("w,L,B", [(64, 130, 40), (128, 203, 16)])
+# Tile widths with several elements per workgroup segment in every pass
+# (w = 64, B = 40 and w = 128, B = 16), even and odd level counts (L = 130
+# and 203: 8 levels, L = 300: 9, the last one a single level).
+@pytest.mark.parametrize("w,L,B", [(64, 130, 40), (64, 300, 8), (128, 203, 16)])
 @pytest.mark.parametrize("layer,alpha", ALL_KINDS)
 def test_forward_tile_segments(dev, w, L, B, layer, alpha):
     _say(f"forward tile segments w={w} L={L} B={B} layer={layer}")
@@ -379,6 +380,18 @@ def adjoint_err(lam, dz0, rl, rz):
 def test_backward_shapes(dev, w, L, B, layer, alpha):
     _say(f"backward shapes w={w} L={L} B={B} layer={layer}")
     d = synth.mlp_inputs(B, L, w, seed=500 + w + L)
+    Z32 = oracle.seq_forward(layer, alpha, d["W"], d["bias"], d["z0"]).astype(np.float32)
+    _backward_check(d, Z32, dev, layer, alpha)
+
+
+# Tile widths with several elements per workgroup segment in every pass of
+# the transposed sweep (the first pass forms its blocks from the weights),
+# odd and even level counts (L = 130: 8 levels; L = 203 and 300: 8 and 9).
+@pytest.mark.parametrize("w,L,B", [(64, 130, 40), (64, 300, 8), (128, 203, 16)])
+@pytest.mark.parametrize("layer,alpha", ALL_KINDS)
+def test_backward_tile_segments(dev, w, L, B, layer, alpha):
+    _say(f"backward tile segments w={w} L={L} B={B} layer={layer}")
+    d = synth.mlp_inputs(B, L, w, seed=1200 + w + L + layer)
     Z32 = oracle.seq_forward(layer, alpha, d["W"], d["bias"], d["z0"]).astype(np.float32)
     _backward_check(d, Z32, dev, layer, alpha)
 
