@@ -164,9 +164,9 @@ int num_levels(int L) {
 
 // Kernel launches of a PCR sweep: pairs of levels where the width has the
 // two-level kernel, plus a single last level when the level count is odd.
-int num_passes(int L, int w) {
+int num_passes(int B, int L, int w) {
     const int K = num_levels(L);
-    return two_level_width(w) ? (K + 1) / 2 : K;
+    return two_level(B, L, w) ? (K + 1) / 2 : K;
 }
 
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
@@ -222,7 +222,7 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
         return timed(DEEPPCR_KCLASS_OTHER, bytes, 0.0, st,
                      [&] { return launch_copy_rows(r0, x, B, L, w, st); });
     }
-    const bool two = two_level_width(w);
+    const bool two = two_level(B, L, w);
     BlockSrc Ain = A0;
     VecSrc rin = r0;
     int s = 1;
@@ -313,10 +313,11 @@ float bits_to_float(unsigned u) {
 }
 
 // The fused Newton linear solve (w = 16, 32, 64, 128): the layer evaluation
-// runs inside the first PCR pass (level 1, or levels 1 and 2 for w = 64, 128
-// and L > 2); for w = 16, 32 the update + reduction runs inside the last
-// level, for w = 64, 128 the last pass writes the solution (as does the
-// first for L <= 2, to `x`) and the separate update kernel applies it.
+// runs inside the first PCR pass (level 1, or levels 1 and 2 where
+// first_level_count says so); for w = 16, 32 the update + reduction runs
+// inside the last level, for w = 64, 128 the last pass writes the solution
+// (as does the first for L <= 2, to `x`) and the separate update kernel
+// applies it.
 // Split in two so that a stopping test on the residual (reduced by the first
 // level) can sit between the halves.
 hipError_t fused_first_level(const NewtonArgs& na, int B, int L, int w, const Ws& ws,
@@ -326,7 +327,7 @@ hipError_t fused_first_level(const NewtonArgs& na, int B, int L, int w, const Ws
     const long long ld = (long long)L * w;
     // the first level (or two) with the layers: W once, Z read twice,
     // products and r written
-    const int nl = first_level_count(L, w);
+    const int nl = first_level_count(B, L, w);
     const double na2 = (double)(L - 2 * nl > 0 ? L - 2 * nl : 0);
     const double bytes = 4.0 * ((double)L * w2 + B * (na2 * w2 + 3.0 * L * w));
     double flops = (double)B * (L * 3.0 * w2 + (L - 1) * 2.0 * w2 +
@@ -357,10 +358,10 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
     VecSrc rin{ws.r[0], ld, (long long)w};
     // the levels after the first one (or two) up to Kp-1, two per pass where
     // possible; pass p writes ws buffers p % 2 (the first pass wrote buffers 0)
-    const int k0 = first_level_count(L, w);
+    const int k0 = first_level_count(B, L, w);
     int s = 1 << k0, p = 1;
     for (int k = k0; k < Kp; ++p) {
-        const bool pair = two_level_width(w) && k + 1 < Kp;
+        const bool pair = two_level(B, L, w) && k + 1 < Kp;
         float* Aout = ws.A[p & 1];
         const VecDst rout{ws.r[p & 1], ld, (long long)w};
         double bytes, flops;
@@ -467,7 +468,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
         if (e != hipSuccess) return hip_fail(e, "initial_guess");
     }
     const long long n = (long long)B * L * w;
-    const VecDst xd{ws.r[(num_passes(L, w) + 1) & 1], (long long)L * w, (long long)w};
+    const VecDst xd{ws.r[(num_passes(B, L, w) + 1) & 1], (long long)L * w, (long long)w};
     const bool fused = layer_first_level(w);
     const NewtonArgs na{W, bias, z0, Z, ws.red, layer, alpha};
     unsigned* fslots = ws.red + kRedF;
@@ -617,7 +618,7 @@ int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, 
               [&] { return launch_residual(F, Z, ws.r[1], n, ws.red, st); });
     if (e != hipSuccess) return hip_fail(e, "residual");
     // Eq. 3 with the caller's blocks (J[:, 0] unused) by PCR, then Z += dZ
-    const VecDst xd{ws.r[(num_passes(L, w) + 1) & 1], (long long)L * w, (long long)w};
+    const VecDst xd{ws.r[(num_passes(B, L, w) + 1) & 1], (long long)L * w, (long long)w};
     e = pcr_sweep(BlockSrc{J, (long long)L * w * w, (long long)w * w, 0},
                   VecSrc{ws.r[1], (long long)L * w, (long long)w}, xd, B, L, w, ws.A, ws.r, 0, 0,
                   st);
@@ -698,9 +699,10 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
     hipStream_t st = (hipStream_t)stream;
     Ws ws = carve(workspace, lo);
     const double w2 = (double)w * w;
-    // w = 64, 128 (L > 2): the first PCR pass forms the blocks from the
-    // weights and c d, so the assembly writes only c d and the right-hand side
-    const bool from_weights = (w == 64 || w == 128) && L > 2;
+    // w = 64, 128 with paired levels: the first PCR pass forms the blocks
+    // from the weights and c d, so the assembly writes only c d and the
+    // right-hand side
+    const bool from_weights = first_level_count(B, L, w) == 2;
     const BwdArgs bw{W, ws.dscale, layer_residual(layer) ? 1 : 0};
     const double jbytes = from_weights ? 0.0 : 4.0 * B * L * w2;
     hipError_t e = timed(DEEPPCR_KCLASS_LAYER, jbytes + 4.0 * B * L * 3.0 * w,
@@ -773,7 +775,7 @@ int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, f
         });
         if (e != hipSuccess) return hip_fail(e, "resnet_initial_guess");
     }
-    const VecDst xd{ws.r[(num_passes(G, w) + 1) & 1], (long long)G * w, (long long)w};
+    const VecDst xd{ws.r[(num_passes(B, G, w) + 1) & 1], (long long)G * w, (long long)w};
     // block evaluation: W once, X read twice, blocks and residuals written;
     // flops: the s - 1 block products and the s mat-vecs per block
     const double eval_bytes = 4.0 * ((double)L * w2 + (double)B * G * (w2 + 3.0 * w));
@@ -854,7 +856,7 @@ int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, con
                          });
     if (e != hipSuccess) return hip_fail(e, "resnet_block_jac");
     // block-output adjoints mu (natural order) from the transposed solve
-    float* mu = ws.r[(num_passes(G, w) + 1) & 1];
+    float* mu = ws.r[(num_passes(B, G, w) + 1) & 1];
     const VecDst xd{mu + (long long)(G - 1) * w, (long long)G * w, -(long long)w};
     e = pcr_sweep(BlockSrc{ws.A[1], (long long)G * w * w, (long long)w * w, 1},
                   VecSrc{ws.r[1], (long long)G * w, (long long)w}, xd, B, G, w, ws.A, ws.r, 0, 0,

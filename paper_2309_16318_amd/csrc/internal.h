@@ -115,8 +115,8 @@ bool fused_newton_levels(int w);
 bool layer_first_level(int w);
 
 // Number of PCR levels launch_first_level_fwd runs (1, or 2 for w = 64, 128
-// when the solve has two levels or more).
-int first_level_count(int L, int w);
+// when the solve has two levels or more and two_level accepts the shape).
+int first_level_count(int B, int L, int w);
 
 // First level (s = 1) of the Newton linear solve with the layers, Jacobian
 // blocks and residuals evaluated on the fly (never stored):
@@ -144,10 +144,10 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
                             const VecDst& rout, int B, int L, int w, int s,
                             hipStream_t stream);
 
-// Two levels (strides s and 2s) in one pass, for the widths two_level_width
-// accepts: rout[l] and Aout[l] hold what level 2s would have written
+// Two levels (strides s and 2s) in one pass, where two_level accepts the
+// shape: rout[l] and Aout[l] hold what level 2s would have written
 // (operators for rows l >= 4s).  Aout must not be the buffer Ain reads.
-bool two_level_width(int w);
+bool two_level(int B, int L, int w);
 
 // The first two levels (s = 1, 2) of the backward solve with the blocks
 // formed from the weights (w = 64, 128, L > 2); rout and Aout as for

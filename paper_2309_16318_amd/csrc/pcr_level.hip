@@ -1678,7 +1678,14 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
     return hipGetLastError();
 }
 
-bool two_level_width(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
+// Tile widths pair their levels only for B L >= 2048 chain elements: the
+// pair kernels walk segments of at least 8 elements, so below that they
+// would run fewer workgroups than the chip has CUs, where single levels
+// (segments of one row) keep it busy.
+bool two_level(int B, int L, int w) {
+    if (w == 16 || w == 32) return true;
+    return (w == 64 || w == 128) && (long long)B * L >= 2048;
+}
 
 // Segments of the fused pair cover elements m = 0 .. (L-1-c)/s of each chain;
 // n rows each, at least 8 so that the 3-row warm-up stays a small share.
@@ -1805,12 +1812,14 @@ bool last_pair_width(int w) { return w == 64 || w == 128; }
 
 bool fused_newton_levels(int w) { return w == 16 || w == 32; }
 
-int first_level_count(int L, int w) { return (w == 64 || w == 128) && L > 2 ? 2 : 1; }
+int first_level_count(int B, int L, int w) {
+    return (w == 64 || w == 128) && L > 2 && two_level(B, L, w) ? 2 : 1;
+}
 bool layer_first_level(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
 
 hipError_t launch_first_level_fwd(const NewtonArgs& na, float* Aout, const VecDst& rout, int B,
                                   int L, int w, hipStream_t stream) {
-    if (first_level_count(L, w) == 2) {
+    if (first_level_count(B, L, w) == 2) {
         const LevelPlan q = plan_level2_tile(B, L, 1, w == 64 ? 1024 : 256);
         const dim3 grid((unsigned)q.total);
         if (w == 64)
