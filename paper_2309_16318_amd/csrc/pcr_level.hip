@@ -1312,8 +1312,12 @@ __device__ __forceinline__ void strip_load_bwd(const BwdArgs& bw, int b, int L, 
 
 // SRCB: the blocks are the backward's, formed from the weights (bw; Ain is
 // unused; s = 1).
+// (w = 64: two waves per SIMD; for the blocks from memory the register
+// budget allows that without spilling, the backward's source spills a few
+// registers and is still faster: 3% on a w = 64 backward in all)
 template <int W, bool TRANS, bool SRCB = false>
-__global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile(BlockSrc Ain, VecSrc rin,
+__global__ __launch_bounds__(Tile2Shape<W>::NT)
+__attribute__((amdgpu_waves_per_eu(W == 64 ? 2 : 1))) void pcr_level2_tile(BlockSrc Ain, VecSrc rin,
                                                                      float* __restrict__ Aout,
                                                                      VecDst rout, int L,
                                                                      LevelPlan plan,
