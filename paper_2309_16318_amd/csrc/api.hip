@@ -165,8 +165,9 @@ int num_levels(int L) {
 // Kernel launches of a PCR sweep: pairs of levels where the width has the
 // two-level kernel, plus a single last level when the level count is odd.
 int num_passes(int B, int L, int w) {
-    const int K = num_levels(L);
-    return two_level(B, L, w) ? (K + 1) / 2 : K;
+    const int kt = tail_levels(B, L, w);
+    const int K1 = num_levels(L) - kt;
+    return (two_level(B, L, w) ? (K1 + 1) / 2 : K1) + (kt > 0 ? 1 : 0);
 }
 
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
@@ -208,6 +209,16 @@ void last2_work(int B, int L, int w, int s, double* bytes, double* flops) {
     *flops = (double)B * 2.0 * w2 * (2.0 * n1 + n2);
 }
 
+// Algorithmic work of the last kt levels as products with vectors: A_l read
+// once for l >= s; per row 2^kt - 1 mat-vecs (the composite operators of the
+// kt levels applied to their vectors); r read and the solution written.
+void tail_work(int B, int L, int w, int kt, double* bytes, double* flops) {
+    const int s = 1 << (num_levels(L) - kt);
+    const double w2 = (double)w * w;
+    *bytes = 4.0 * B * ((double)(L - s) * w2 + 2.0 * L * w);
+    *flops = (double)B * (L - s) * ((1 << kt) - 1) * 2.0 * w2;
+}
+
 // Runs all PCR levels.  Level 0 reads (A0, r0); level k writes operators to
 // ws A buffer (k + a_first) % 2 and vectors to ws r buffer (k + r_first) % 2,
 // except the last level, which writes the solution to `x`.
@@ -223,14 +234,18 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
                      [&] { return launch_copy_rows(r0, x, B, L, w, st); });
     }
     const bool two = two_level(B, L, w);
+    const int kt = tail_levels(B, L, w);
+    const int K1 = K - kt;  // levels before the tail
     BlockSrc Ain = A0;
     VecSrc rin = r0;
     int s = 1;
     // pass p writes operators to ws A buffer (p + a_first) % 2 and vectors to
     // ws r buffer (p + r_first) % 2; the last pass writes the solution to x
-    for (int k = 0, p = 0; k < K; ++p) {
-        const bool pair = two && k + 1 < K;
-        const bool last = (k + (pair ? 1 : 0)) == K - 1;
+    // (the tail pass, when there is one, after the levels below K1)
+    const int Kend = kt > 0 ? K1 : K;
+    for (int k = 0, p = 0; k < Kend; ++p) {
+        const bool pair = two && k + 1 < Kend;
+        const bool last = kt == 0 && (k + (pair ? 1 : 0)) == K - 1;
         float* Aout = wsA[(p + a_first) & 1];
         VecDst rout = last ? x
                            : VecDst{wsr[(p + r_first) & 1], (long long)L * w, (long long)w};
@@ -265,7 +280,11 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
         s *= pair ? 4 : 2;
         k += pair ? 2 : 1;
     }
-    return hipSuccess;
+    if (kt == 0) return hipSuccess;
+    double bytes, flops;
+    tail_work(B, L, w, kt, &bytes, &flops);
+    return timed(DEEPPCR_KCLASS_PCR_TAIL, bytes, flops, st,
+                 [&] { return launch_pcr_level_tail(Ain, rin, x, B, L, w, kt, st); });
 }
 
 struct Ws {
@@ -351,9 +370,11 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
         return timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
                      [&] { return launch_update_reduce(na.Z, x.base, n, na.red, st); });
     }
-    // w = 16, 32: the last level applies the update itself
+    // w = 16, 32: the last level applies the update itself; w = 64, 128: the
+    // last levels may go to one tail pass
     const bool upd = fused_newton_levels(w);
-    const int Kp = upd ? K - 1 : K;
+    const int kt = upd ? 0 : tail_levels(B, L, w);
+    const int Kp = upd ? K - 1 : K - kt;
     BlockSrc Ain{ws.A[0], (long long)L * w * w, (long long)w * w, 0};
     VecSrc rin{ws.r[0], ld, (long long)w};
     // the levels after the first one (or two) up to Kp-1, two per pass where
@@ -366,7 +387,7 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
         const VecDst rout{ws.r[p & 1], ld, (long long)w};
         double bytes, flops;
         hipError_t e;
-        if (pair && !upd && k + 1 == K - 1 && last_pair_width(w)) {
+        if (pair && !upd && kt == 0 && k + 1 == K - 1 && last_pair_width(w)) {
             last2_work(B, L, w, s, &bytes, &flops);
             e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
                 return launch_pcr_level2_last(Ain, rin, rout, B, L, w, s, st);
@@ -388,8 +409,19 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
         s *= pair ? 4 : 2;
         k += pair ? 2 : 1;
     }
+    if (kt > 0) {
+        // the last kt levels in one pass: the solution to ws r buffer p % 2
+        double bytes, flops;
+        tail_work(B, L, w, kt, &bytes, &flops);
+        const VecDst xo{ws.r[p & 1], ld, (long long)w};
+        hipError_t e = timed(DEEPPCR_KCLASS_PCR_TAIL, bytes, flops, st, [&] {
+            return launch_pcr_level_tail(Ain, rin, xo, B, L, w, kt, st);
+        });
+        if (e != hipSuccess) return e;
+        rin = VecSrc{xo.base, xo.bstride, xo.rstride};
+    }
     if (!upd) {
-        // the last pass wrote the solution to ws r buffer (p - 1) % 2
+        // the last pass wrote the solution to the ws r buffer rin reads
         const long long n = (long long)B * L * w;
         return timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
                      [&] { return launch_update_reduce(na.Z, rin.base, n, na.red, st); });

@@ -155,6 +155,15 @@ bool two_level(int B, int L, int w);
 hipError_t launch_pcr_level2_bwd(const BwdArgs& bw, const VecSrc& rin, float* Aout,
                                  const VecDst& rout, int B, int L, int w, hipStream_t stream);
 
+// The number of last levels that one tail pass does (0: none), for the
+// problem shape: 3 to 6 levels at w = 64, 128 when the levels pair.
+int tail_levels(int B, int L, int w);
+// The last kt = tail_levels(B, L, w) levels of a solve in one pass that
+// writes no operator: the solution goes to rout.  Ain holds the operators of
+// the level before (rows l >= s, s = 2^(levels - kt)), not transposed.
+hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
+                                 int B, int L, int w, int kt, hipStream_t stream);
+
 // The last two levels of a solve (strides s, 2s with 4s >= L) in one pass
 // without operator products (mat-vecs only), for the widths last_pair_width
 // accepts; rout gets the solution.

@@ -1407,6 +1407,108 @@ __attribute__((amdgpu_waves_per_eu(W == 64 ? 2 : 1))) void pcr_level2_tile(Block
     }
 }
 
+// ---- the last KT levels of a solve, w = 64 or 128 -------------------------
+// After the levels below stride s the system is s independent chains per
+// system, and the last KT levels (strides s .. s 2^{KT-1}, s 2^KT >= L) write
+// no operator: their products only ever meet vectors.  Level i updates
+//   r^{i+1}_m = r^i_m + A_m A_{m-1} ... A_{m-2^i+1} r^i_{m-2^i}   (m >= 2^i)
+// along a chain of stride s (A the blocks this pass reads).  Walking the
+// chain, element m keeps, per level i, the vectors g^i_{j,m} =
+// A_m g^i_{j-1,m-1} (g^i_{0,m} = r^i_m), j = 1 .. 2^i, so that g^i_{2^i,m}
+// is the term of the update.  All of them are A_m times vectors of element
+// m-1, so one product per element, A_m V_{m-1} with V the W x (2^KT - 1)
+// matrix of the carried vectors, does every level's work on MFMA.  Column
+// 2^i - 1 + j of V holds g^i_{j} (j = 0 .. 2^i - 1, j = 0 being r^i); the
+// same column of the product is then g^i_{j+1}.  One workgroup walks one
+// whole chain (at most 2^KT elements), so no segment warm-up is needed; the
+// r chain of an element and the new V are formed by one thread per row.
+template <int W, int KT>
+struct TailShape {
+    static constexpr int NP = 1 << KT;   // columns of V, padded (2^KT - 1 used)
+    static constexpr int NTC = NP / 32;  // 32-column tiles of the product
+    // tiles per wave: as many waves as SIMDs where the tiles allow (more
+    // waves would not add MFMA throughput, only strip reloads)
+    static constexpr int TPW = (W / 32) * NTC >= 8 ? (W / 32) * NTC / 4 : 1;
+    static constexpr int NWV = (W / 32) * NTC / TPW;
+    static constexpr int NT = 64 * NWV;
+    static_assert(NP % 32 == 0 && NTC % TPW == 0, "whole tiles");
+};
+
+template <int W, int KT>
+__global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSrc Ain, VecSrc rin,
+                                                                       VecDst rout, int L,
+                                                                       int s) {
+    using S = Tile2Shape<W>;
+    using T = TailShape<W, KT>;
+    __shared__ float VT[2][T::NP * S::PITCH];  // V_{m-1} / V_m, transposed (VT[n][k])
+    __shared__ float UP[KT][W];                // g^lv_{2^lv, m}: the terms of the updates
+    const int t = threadIdx.x;
+    const int lane = t & 63, i = lane & 31, h = lane >> 5, wv = t >> 6;
+    const int tc0 = T::TPW * (wv / (W / 32));  // the wave's first column tile
+    const int R = 32 * (wv % (W / 32)) + i;    // the lane's row
+    const int b = (int)(blockIdx.x / s);
+    const int c = (int)(blockIdx.x - (long long)b * s);
+    const int count = (L - 1 - c) / s;  // elements m = 0 .. count
+    const float* ab = Ain.base + b * Ain.bstride;
+    const float* rb = rin.base + b * rin.bstride;
+    float* ob = rout.base + b * rout.bstride;
+
+    // A_m of even / odd elements: the strip of element m+1 is requested when
+    // element m starts, a whole element ahead of its use (A_0 is never read)
+    StripA<W> aE, aO;
+    v16f acc[T::TPW];
+    if (count >= 1) strip_load<W, false>(ab + (long long)(c + s) * Ain.rstride, aO, R, h);
+    int l = c;
+    // r_m of the element (threads t < W), requested an element ahead too
+    float rcur = t < W ? rb[(long long)c * rin.rstride + t] : 0.f;
+    auto element = [&](int m, StripA<W>& aC, StripA<W>& aN) {
+        const float* Vp = VT[(m + 1) & 1];
+        float* Vn = VT[m & 1];
+        float rnext = 0.f;
+        if (m < count && t < W) rnext = rb[(long long)(l + s) * rin.rstride + t];
+        if (m >= 1 && m < count)
+            strip_load<W, false>(ab + (long long)(l + s) * Ain.rstride, aN, R, h);
+        // Column n of the product (level lv, n = 2^lv - 1 + j) is g^lv_{j+1};
+        // it goes to column n + 1 of V_m, or, for j + 1 = 2^lv, to the update
+        // terms.  Element 0 has no block: its g columns are 0.
+        if (m >= 1) strip_product<W, 0, T::TPW, false>(Vp + 32 * tc0 * S::PITCH, aC, acc, i, h);
+#pragma unroll
+        for (int tt = 0; tt < T::TPW; ++tt)
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int n = 32 * (tc0 + tt) + 8 * qq + 4 * h + e;
+                    if (n >= T::NP - 1) continue;
+                    const int lv = 31 - __builtin_clz(n + 1);
+                    const float v = m >= 1 ? acc[tt][4 * qq + e] : 0.f;
+                    if (n + 1 < (2 << lv) - 1)
+                        Vn[(n + 1) * S::PITCH + R] = v;
+                    else if (m >= 1)
+                        UP[lv][R] = v;
+                }
+        __syncthreads();  // the g columns of V_m and the update terms are written
+        if (t < W) {
+            float r = rcur;
+#pragma unroll
+            for (int lv = 0; lv < KT; ++lv) {
+                Vn[((1 << lv) - 1) * S::PITCH + t] = r;  // r^lv_m
+                if (m >= (1 << lv)) r += UP[lv][t];
+            }
+            ob[(long long)l * rout.rstride + t] = r;
+        }
+        rcur = rnext;
+        __syncthreads();  // V_m is complete, UP is read
+        l += s;
+    };
+    for (int m = 0; m <= count; ++m) {
+        if (m & 1)
+            element(m, aO, aE);
+        else
+            element(m, aE, aO);
+    }
+}
+
 // The last two levels of a solve (strides s and 2s, 4s >= L): no operator
 // is written, and the one product the walk would form, A'_m = A_m A_{m-1},
 // only ever meets the vector r'_{m-2}, so A'_m r'_{m-2} is taken as
@@ -1813,6 +1915,58 @@ hipError_t launch_pcr_level2_last(const BlockSrc& Ain, const VecSrc& rin, const 
 }
 
 bool last_pair_width(int w) { return w == 64 || w == 128; }
+
+namespace {
+int num_levels_of(int L) {
+    int k = 0;
+    for (long long s = 1; s < L; s *= 2) ++k;
+    return k;
+}
+}  // namespace
+
+int tail_levels(int B, int L, int w) {
+    const int K = num_levels_of(L);
+    if (!(w == 64 || w == 128) || !two_level(B, L, w) || K < 4) return 0;
+    // the first tail level: at least 2 (the first pass is a pair), even (the
+    // passes before it are pairs), with B s >= 256 chains so that every CU
+    // walks one, and at most 6 levels in the tail (chains of 64 elements)
+    int k0 = 2;
+    while (k0 < K - 6 || ((long long)B << k0) < 256) k0 += 2;
+    return K - k0 >= 3 ? K - k0 : 0;
+}
+
+hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
+                                 int B, int L, int w, int kt, hipStream_t stream) {
+    // KT = 5 serves 3 to 5 levels (one 32-column tile; the levels above
+    // the chain length never update, since m < 2^lv there)
+    const int s = 1 << (num_levels_of(L) - kt);
+    const dim3 grid((unsigned)((long long)B * s));
+    if (Ain.trans) return hipErrorInvalidValue;
+#define DEEPPCR_TAIL(WW, KK)                                                             \
+    hipLaunchKernelGGL((pcr_level_tail<WW, KK>), grid, dim3((TailShape<WW, KK>::NT)), 0, \
+                       stream, Ain, rin, rout, L, s)
+    if (w == 64) {
+        switch (kt) {
+            case 3: DEEPPCR_TAIL(64, 5); break;
+            case 4: DEEPPCR_TAIL(64, 5); break;
+            case 5: DEEPPCR_TAIL(64, 5); break;
+            case 6: DEEPPCR_TAIL(64, 6); break;
+            default: return hipErrorInvalidValue;
+        }
+    } else if (w == 128) {
+        switch (kt) {
+            case 3: DEEPPCR_TAIL(128, 5); break;
+            case 4: DEEPPCR_TAIL(128, 5); break;
+            case 5: DEEPPCR_TAIL(128, 5); break;
+            case 6: DEEPPCR_TAIL(128, 6); break;
+            default: return hipErrorInvalidValue;
+        }
+    } else {
+        return hipErrorInvalidValue;
+    }
+#undef DEEPPCR_TAIL
+    return hipGetLastError();
+}
 
 bool fused_newton_levels(int w) { return w == 16 || w == 32; }
 

@@ -15,8 +15,9 @@ OK, EINVAL, ENOCONV, ENONFINITE, EHIP, EWORKSPACE = range(6)
 TANH_MLP, TANH_RESIDUAL, SIGMOID_MLP, SIGMOID_RESIDUAL, RELU_MLP, RELU_RESIDUAL = range(6)
 OP_PCR, OP_FWD, OP_BWD = 0, 1, 2
 ACT_TANH, ACT_SIGMOID, ACT_RELU = 0, 1, 2
-KCLASS_PCR_LEVEL, KCLASS_LAYER, KCLASS_UPDATE, KCLASS_WGRAD, KCLASS_OTHER, KCLASS_SEQUENTIAL = range(6)
-KCLASS_NAMES = ("pcr_level", "layer", "update", "wgrad", "other", "sequential")
+(KCLASS_PCR_LEVEL, KCLASS_LAYER, KCLASS_UPDATE, KCLASS_WGRAD, KCLASS_OTHER, KCLASS_SEQUENTIAL,
+ KCLASS_PCR_TAIL) = range(7)
+KCLASS_NAMES = ("pcr_level", "layer", "update", "wgrad", "other", "sequential", "pcr_tail")
 MAX_WIDTH = 128
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdeeppcr.so")
