@@ -234,7 +234,7 @@ def main():
     value = wl.B * wl.L / (el / args.steps)
     lvl = prof["pcr_level"]
     intensity = lvl["flops"] / max(lvl["bytes"], 1.0)
-    if intensity >= RIDGE * 0.75 or wl.w >= 64:
+    if intensity >= RIDGE or wl.w >= 64:
         achieved = lvl["flops"] / (lvl["ms"] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4)}

@@ -165,7 +165,7 @@ int num_levels(int L) {
 // Kernel launches of a PCR sweep: pairs of levels where the width has the
 // two-level kernel, plus a single last level when the level count is odd.
 int num_passes(int B, int L, int w) {
-    const int kt = tail_levels(B, L, w);
+    const int kt = tail_levels(B, L, w, 0);
     const int K1 = num_levels(L) - kt;
     return (two_level(B, L, w) ? (K1 + 1) / 2 : K1) + (kt > 0 ? 1 : 0);
 }
@@ -234,7 +234,7 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
                      [&] { return launch_copy_rows(r0, x, B, L, w, st); });
     }
     const bool two = two_level(B, L, w);
-    const int kt = tail_levels(B, L, w);
+    const int kt = tail_levels(B, L, w, 0);
     const int K1 = K - kt;  // levels before the tail
     BlockSrc Ain = A0;
     VecSrc rin = r0;
@@ -370,16 +370,16 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
         return timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
                      [&] { return launch_update_reduce(na.Z, x.base, n, na.red, st); });
     }
-    // w = 16, 32: the last level applies the update itself; w = 64, 128: the
-    // last levels may go to one tail pass
-    const bool upd = fused_newton_levels(w);
-    const int kt = upd ? 0 : tail_levels(B, L, w);
+    // the last levels go to one tail pass where tail_levels says so; else for
+    // w = 16, 32 the last level applies the update itself
+    const int k0 = first_level_count(B, L, w);
+    const int kt = tail_levels(B, L, w, k0);
+    const bool upd = fused_newton_levels(w) && kt == 0;
     const int Kp = upd ? K - 1 : K - kt;
     BlockSrc Ain{ws.A[0], (long long)L * w * w, (long long)w * w, 0};
     VecSrc rin{ws.r[0], ld, (long long)w};
     // the levels after the first one (or two) up to Kp-1, two per pass where
     // possible; pass p writes ws buffers p % 2 (the first pass wrote buffers 0)
-    const int k0 = first_level_count(B, L, w);
     int s = 1 << k0, p = 1;
     for (int k = k0; k < Kp; ++p) {
         const bool pair = two_level(B, L, w) && k + 1 < Kp;

@@ -156,9 +156,10 @@ hipError_t launch_pcr_level2_bwd(const BwdArgs& bw, const VecSrc& rin, float* Ao
                                  const VecDst& rout, int B, int L, int w, hipStream_t stream);
 
 // The number of last levels that one tail pass does (0: none), for the
-// problem shape: 3 to 6 levels at w = 64, 128 when the levels pair.
-int tail_levels(int B, int L, int w);
-// The last kt = tail_levels(B, L, w) levels of a solve in one pass that
+// problem shape and the number of levels `first` the solve's first pass
+// does (then pairs up to the tail): 3 to 6 levels at w = 32, 64, 128.
+int tail_levels(int B, int L, int w, int first);
+// The last kt = tail_levels(...) levels of a solve in one pass that
 // writes no operator: the solution goes to rout.  Ain holds the operators of
 // the level before (rows l >= s, s = 2^(levels - kt)), not transposed.
 hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,

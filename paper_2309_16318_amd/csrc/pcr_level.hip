@@ -1924,15 +1924,21 @@ int num_levels_of(int L) {
 }
 }  // namespace
 
-int tail_levels(int B, int L, int w) {
+int tail_levels(int B, int L, int w, int first) {
+    if (!(w == 32 || w == 64 || w == 128) || !two_level(B, L, w)) return 0;
     const int K = num_levels_of(L);
-    if (!(w == 64 || w == 128) || !two_level(B, L, w) || K < 4) return 0;
-    // the first tail level: at least 2 (the first pass is a pair), even (the
-    // passes before it are pairs), with B s >= 256 chains so that every CU
-    // walks one, and at most 6 levels in the tail (chains of 64 elements)
-    int k0 = 2;
-    while (k0 < K - 6 || ((long long)B << k0) < 256) k0 += 2;
-    return K - k0 >= 3 ? K - k0 : 0;
+    // the most levels (6 down to 3) such that the levels before the tail are
+    // the first pass plus pairs, the tail reads operators written by this
+    // solve (not the caller's possibly transposed blocks), and B s >= 256
+    // chains keep every CU walking one (chains of at most 64 elements)
+    const int kmin = first == 1 ? 1 : 2;
+    for (int kt = 6; kt >= 3; --kt) {
+        const int k0 = K - kt;
+        if (k0 < kmin || k0 < first || ((k0 - first) & 1)) continue;
+        if (((long long)B << k0) < 256) continue;
+        return kt;
+    }
+    return 0;
 }
 
 hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
@@ -1945,7 +1951,15 @@ hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const V
 #define DEEPPCR_TAIL(WW, KK)                                                             \
     hipLaunchKernelGGL((pcr_level_tail<WW, KK>), grid, dim3((TailShape<WW, KK>::NT)), 0, \
                        stream, Ain, rin, rout, L, s)
-    if (w == 64) {
+    if (w == 32) {
+        switch (kt) {
+            case 3: DEEPPCR_TAIL(32, 5); break;
+            case 4: DEEPPCR_TAIL(32, 5); break;
+            case 5: DEEPPCR_TAIL(32, 5); break;
+            case 6: DEEPPCR_TAIL(32, 6); break;
+            default: return hipErrorInvalidValue;
+        }
+    } else if (w == 64) {
         switch (kt) {
             case 3: DEEPPCR_TAIL(64, 5); break;
             case 4: DEEPPCR_TAIL(64, 5); break;

@@ -187,8 +187,11 @@ def test_forward_all_layer_kinds(dev, w, L, B, layer, alpha):
 
 # Tile widths with several elements per workgroup segment in every pass
 # (w = 64, B = 40 and w = 128, B = 16), even and odd level counts (L = 130
-# and 203: 8 levels, L = 300: 9, the last one a single level).
-@pytest.mark.parametrize("w,L,B", [(64, 130, 40), (64, 300, 8), (128, 203, 16)])
+# and 203: 8 levels, L = 300: 9), and the one-pass tail of the last levels
+# at w = 32 (B = 64: 5 tail levels after the first level and one pair), 64
+# (4 and 3 levels) and 128 (4 levels).
+@pytest.mark.parametrize("w,L,B", [(64, 130, 40), (64, 300, 8), (128, 203, 16), (32, 130, 64),
+                                   (32, 300, 40)])
 @pytest.mark.parametrize("layer,alpha", ALL_KINDS)
 def test_forward_tile_segments(dev, w, L, B, layer, alpha):
     _say(f"forward tile segments w={w} L={L} B={B} layer={layer}")
@@ -386,8 +389,10 @@ def test_backward_shapes(dev, w, L, B, layer, alpha):
 
 # Tile widths with several elements per workgroup segment in every pass of
 # the transposed sweep (the first pass forms its blocks from the weights),
-# odd and even level counts (L = 130: 8 levels; L = 203 and 300: 8 and 9).
-@pytest.mark.parametrize("w,L,B", [(64, 130, 40), (64, 300, 8), (128, 203, 16)])
+# odd and even level counts (L = 130: 8 levels; L = 203 and 300: 8 and 9),
+# and the tail of the last levels at w = 32, 64, 128.
+@pytest.mark.parametrize("w,L,B", [(64, 130, 40), (64, 300, 8), (128, 203, 16), (32, 130, 64),
+                                   (32, 300, 40)])
 @pytest.mark.parametrize("layer,alpha", ALL_KINDS)
 def test_backward_tile_segments(dev, w, L, B, layer, alpha):
     _say(f"backward tile segments w={w} L={L} B={B} layer={layer}")
