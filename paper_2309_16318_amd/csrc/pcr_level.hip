@@ -1442,6 +1442,7 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
     using T = TailShape<W, KT>;
     __shared__ float VT[2][T::NP * S::PITCH];  // V_{m-1} / V_m, transposed (VT[n][k])
     __shared__ float UP[KT][W];                // g^lv_{2^lv, m}: the terms of the updates
+    __shared__ float RS[2][W];                 // r_m of the element in slot m & 1
     const int t = threadIdx.x;
     const int lane = t & 63, i = lane & 31, h = lane >> 5, wv = t >> 6;
     const int tc0 = T::TPW * (wv / (W / 32));  // the wave's first column tile
@@ -1459,8 +1460,9 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
     v16f acc[T::TPW];
     if (count >= 1) strip_load<W, false>(ab + (long long)(c + s) * Ain.rstride, aO, R, h);
     int l = c;
-    // r_m of the element (threads t < W), requested an element ahead too
-    float rcur = t < W ? rb[(long long)c * rin.rstride + t] : 0.f;
+    // r_m is requested an element ahead too and parked in LDS (consumed in
+    // the element that loads it, so no wait spans the loop's back edge)
+    if (t < W) RS[0][t] = rb[(long long)c * rin.rstride + t];
     auto element = [&](int m, StripA<W>& aC, StripA<W>& aN) {
         const float* Vp = VT[(m + 1) & 1];
         float* Vn = VT[m & 1];
@@ -1489,23 +1491,23 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
                 }
         __syncthreads();  // the g columns of V_m and the update terms are written
         if (t < W) {
-            float r = rcur;
+            float r = RS[m & 1][t];
 #pragma unroll
             for (int lv = 0; lv < KT; ++lv) {
                 Vn[((1 << lv) - 1) * S::PITCH + t] = r;  // r^lv_m
                 if (m >= (1 << lv)) r += UP[lv][t];
             }
             ob[(long long)l * rout.rstride + t] = r;
+            RS[(m + 1) & 1][t] = rnext;
         }
-        rcur = rnext;
-        __syncthreads();  // V_m is complete, UP is read
+        __syncthreads();  // V_m and r_{m+1} are in place, UP is read
         l += s;
     };
-    for (int m = 0; m <= count; ++m) {
-        if (m & 1)
-            element(m, aO, aE);
-        else
-            element(m, aE, aO);
+    // two elements per trip, so that the strips keep their registers and a
+    // request stays in flight across the loop's back edge
+    for (int m = 0; m <= count; m += 2) {
+        element(m, aE, aO);
+        if (m + 1 <= count) element(m + 1, aO, aE);
     }
 }
 
