@@ -89,9 +89,12 @@ def main():
         kernels[name] = {"launches": n,
                          "read_bytes_per_launch": fetch[name][1] * ff / n,
                          "write_bytes_per_launch": write[name][1] * wf / write[name][0]}
-    n_all = sum(v["launches"] for v in kernels.values())
-    rd = sum(v["read_bytes_per_launch"] * v["launches"] for v in kernels.values()) / n_all
-    wr = sum(v["write_bytes_per_launch"] * v["launches"] for v in kernels.values()) / n_all
+    # The tail pass is timed as a class of its own, so the per-launch average
+    # that goes with the PCR-level roofline leaves it out.
+    level = {k: v for k, v in kernels.items() if not k.startswith("pcr_level_tail")}
+    n_all = sum(v["launches"] for v in level.values())
+    rd = sum(v["read_bytes_per_launch"] * v["launches"] for v in level.values()) / n_all
+    wr = sum(v["write_bytes_per_launch"] * v["launches"] for v in level.values()) / n_all
     out = {"workload": a.workload, "kernel_source_sha256": kernel_source_sha256(),
            "fetch_bytes_per_counter_unit": ff, "write_bytes_per_counter_unit": wf,
            "pcr_level_launches": n_all, "read_bytes_per_launch": rd,
