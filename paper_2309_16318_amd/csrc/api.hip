@@ -333,10 +333,10 @@ float bits_to_float(unsigned u) {
 
 // The fused Newton linear solve (w = 16, 32, 64, 128): the layer evaluation
 // runs inside the first PCR pass (level 1, or levels 1 and 2 where
-// first_level_count says so); for w = 16, 32 the update + reduction runs
-// inside the last level, for w = 64, 128 the last pass writes the solution
-// (as does the first for L <= 2, to `x`) and the separate update kernel
-// applies it.
+// first_level_count says so); for w = 16, 32 without a tail pass the update
+// + reduction runs inside the last level, otherwise the last pass writes the
+// solution (as does the first for L <= 2, to `x`) and the separate update
+// kernel applies it.
 // Split in two so that a stopping test on the residual (reduced by the first
 // level) can sit between the halves.
 hipError_t fused_first_level(const NewtonArgs& na, int B, int L, int w, const Ws& ws,
@@ -374,7 +374,7 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
     // w = 16, 32 the last level applies the update itself
     const int k0 = first_level_count(B, L, w);
     const int kt = tail_levels(B, L, w, k0);
-    const bool upd = fused_newton_levels(w) && kt == 0;
+    const bool upd = fused_newton_levels(w) && kt == 0 && k0 < K;
     const int Kp = upd ? K - 1 : K - kt;
     BlockSrc Ain{ws.A[0], (long long)L * w * w, (long long)w * w, 0};
     VecSrc rin{ws.r[0], ld, (long long)w};
@@ -731,7 +731,7 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
     hipStream_t st = (hipStream_t)stream;
     Ws ws = carve(workspace, lo);
     const double w2 = (double)w * w;
-    // w = 64, 128 with paired levels: the first PCR pass forms the blocks
+    // w = 32, 64, 128 with paired levels: the first PCR pass forms the blocks
     // from the weights and c d, so the assembly writes only c d and the
     // right-hand side
     const bool from_weights = first_level_count(B, L, w) == 2;

@@ -114,8 +114,9 @@ struct NewtonArgs {
 bool fused_newton_levels(int w);
 bool layer_first_level(int w);
 
-// Number of PCR levels launch_first_level_fwd runs (1, or 2 for w = 64, 128
-// when the solve has two levels or more and two_level accepts the shape).
+// Number of PCR levels launch_first_level_fwd runs (1, or 2 for w = 32, 64,
+// 128 when the solve has two levels or more and two_level accepts the
+// shape).
 int first_level_count(int B, int L, int w);
 
 // First level (s = 1) of the Newton linear solve with the layers, Jacobian
@@ -150,7 +151,7 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
 bool two_level(int B, int L, int w);
 
 // The first two levels (s = 1, 2) of the backward solve with the blocks
-// formed from the weights (w = 64, 128, L > 2); rout and Aout as for
+// formed from the weights (w = 32, 64, 128, L > 2); rout and Aout as for
 // launch_pcr_level2.
 hipError_t launch_pcr_level2_bwd(const BwdArgs& bw, const VecSrc& rin, float* Aout,
                                  const VecDst& rout, int B, int L, int w, hipStream_t stream);

@@ -24,6 +24,8 @@
 // is consumed in the layout it is loaded in.
 #include "internal.h"
 
+#include <type_traits>
+
 namespace deeppcr {
 namespace {
 
@@ -1250,10 +1252,11 @@ __device__ __forceinline__ float second_product(const float* YT, const StripC<W>
                                                 const float* rpp, float* dst, int i, int h,
                                                 int R) {
     constexpr int T = Tile2Shape<W>::T;
-    v16f acc[2];
+    constexpr int N0 = T < 2 ? T : 2;
+    v16f acc[N0];
     const float part = strip_matvec<W>(pC, rpp, h);
-    strip_product<W, 0, 2, false>(YT, pC, acc, i, h);
-    tiles_store<W, 0, 2>(dst, acc, R, h);
+    strip_product<W, 0, N0, false>(YT, pC, acc, i, h);
+    tiles_store<W, 0, N0>(dst, acc, R, h);
     if constexpr (T == 4) {
         strip_product<W, 2, 2, false>(YT, pC, acc, i, h);
         tiles_store<W, 2, 2>(dst, acc, R, h);
@@ -1317,7 +1320,7 @@ __device__ __forceinline__ void strip_load_bwd(const BwdArgs& bw, int b, int L, 
 // registers and is still faster: 3% on a w = 64 backward in all)
 template <int W, bool TRANS, bool SRCB = false>
 __global__ __launch_bounds__(Tile2Shape<W>::NT)
-__attribute__((amdgpu_waves_per_eu(W == 64 ? 2 : 1))) void pcr_level2_tile(BlockSrc Ain, VecSrc rin,
+__attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_level2_tile(BlockSrc Ain, VecSrc rin,
                                                                      float* __restrict__ Aout,
                                                                      VecDst rout, int L,
                                                                      LevelPlan plan,
@@ -1431,8 +1434,23 @@ struct TailShape {
     static constexpr int TPW = (W / 32) * NTC >= 8 ? (W / 32) * NTC / 4 : 1;
     static constexpr int NWV = (W / 32) * NTC / TPW;
     static constexpr int NT = 64 * NWV;
+    // elements whose block and right-hand side are in flight: an element's
+    // product is short at small w, so the loads are issued D elements ahead
+    // (a ring of D + 1 strips in registers)
+    static constexpr int D = W == 32 ? 3 : W == 64 ? 2 : 1;
+    static constexpr int NB = D + 1;
     static_assert(NP % 32 == 0 && NTC % TPW == 0, "whole tiles");
 };
+
+// f(integral_constant<0>), ..., f(integral_constant<N-1>): ring slots as
+// compile-time indices, so that the ring stays in registers.
+template <int I, int N, class F>
+__device__ __forceinline__ void unroll_each(F& f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        unroll_each<I + 1, N>(f);
+    }
+}
 
 template <int W, int KT>
 __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSrc Ain, VecSrc rin,
@@ -1440,8 +1458,10 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
                                                                        int s) {
     using S = Tile2Shape<W>;
     using T = TailShape<W, KT>;
+    constexpr int NB = T::NB, D = T::D;
     __shared__ float VT[2][T::NP * S::PITCH];  // V_{m-1} / V_m, transposed (VT[n][k])
-    __shared__ float UP[KT][W];                // g^lv_{2^lv, m}: the terms of the updates
+    __shared__ float UP[KT + 1][W];            // g^lv_{2^lv, m}: the terms of the updates
+                                               // (row KT: the padding column, unused)
     __shared__ float RS[2][W];                 // r_m of the element in slot m & 1
     const int t = threadIdx.x;
     const int lane = t & 63, i = lane & 31, h = lane >> 5, wv = t >> 6;
@@ -1454,60 +1474,79 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
     const float* rb = rin.base + b * rin.bstride;
     float* ob = rout.base + b * rout.bstride;
 
-    // A_m of even / odd elements: the strip of element m+1 is requested when
-    // element m starts, a whole element ahead of its use (A_0 is never read)
-    StripA<W> aE, aO;
+    // Ring slot m % NB holds A_m (A_0 is never read) and r_m; element m
+    // requests A_{m+D} and r_{m+D}, and r_{m+1} goes to LDS at the end of
+    // element m.  Every thread issues the same loads on every element (rows
+    // past the chain's end are clamped to its last row and never used), so
+    // the compiler can count the requests in flight instead of waiting for
+    // all of them where a branch would merge.
+    StripA<W> a[NB];
+    float rq[NB];
     v16f acc[T::TPW];
-    if (count >= 1) strip_load<W, false>(ab + (long long)(c + s) * Ain.rstride, aO, R, h);
-    int l = c;
-    // r_m is requested an element ahead too and parked in LDS (consumed in
-    // the element that loads it, so no wait spans the loop's back edge)
+    const int tw = t & (W - 1);
+#pragma unroll
+    for (int j = 1; j < D; ++j) {
+        const long long lj = c + (long long)min(j, count) * s;
+        strip_load<W, false>(ab + lj * Ain.rstride, a[j], R, h);
+        rq[j] = rb[lj * rin.rstride + tw];
+    }
     if (t < W) RS[0][t] = rb[(long long)c * rin.rstride + t];
-    auto element = [&](int m, StripA<W>& aC, StripA<W>& aN) {
+    auto element = [&](int m, auto U) {
+        constexpr int u = decltype(U)::value;  // m % NB
+        constexpr int un = (u + D) % NB, u1 = (u + 1) % NB;
         const float* Vp = VT[(m + 1) & 1];
         float* Vn = VT[m & 1];
-        float rnext = 0.f;
-        if (m < count && t < W) rnext = rb[(long long)(l + s) * rin.rstride + t];
-        if (m >= 1 && m < count)
-            strip_load<W, false>(ab + (long long)(l + s) * Ain.rstride, aN, R, h);
+        const long long l = c + (long long)m * s;
+        {
+            const long long ln = c + (long long)min(m + D, count) * s;
+            strip_load<W, false>(ab + ln * Ain.rstride, a[un], R, h);
+            rq[un] = rb[ln * rin.rstride + tw];
+        }
         // Column n of the product (level lv, n = 2^lv - 1 + j) is g^lv_{j+1};
-        // it goes to column n + 1 of V_m, or, for j + 1 = 2^lv, to the update
-        // terms.  Element 0 has no block: its g columns are 0.
-        if (m >= 1) strip_product<W, 0, T::TPW, false>(Vp + 32 * tc0 * S::PITCH, aC, acc, i, h);
+        // it goes to column n + 1 of V_m, or, for j + 1 = 2^lv (n + 2 a power
+        // of two), to the update terms; the padding column n = 2^KT - 1 goes
+        // to the spare row.  The destination is computed, not branched on.
+        // Element 0 has no block: its g columns are 0.
+        if (m >= 1) strip_product<W, 0, T::TPW, false>(Vp + 32 * tc0 * S::PITCH, a[u], acc, i, h);
 #pragma unroll
         for (int tt = 0; tt < T::TPW; ++tt)
 #pragma unroll
-            for (int qq = 0; qq < 4; ++qq)
+            for (int qq = 0; qq < 4; ++qq) {
+                const int n0 = 32 * (tc0 + tt) + 8 * qq + 4 * h;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const int n = 32 * (tc0 + tt) + 8 * qq + 4 * h + e;
-                    if (n >= T::NP - 1) continue;
-                    const int lv = 31 - __builtin_clz(n + 1);
-                    const float v = m >= 1 ? acc[tt][4 * qq + e] : 0.f;
-                    if (n + 1 < (2 << lv) - 1)
-                        Vn[(n + 1) * S::PITCH + R] = v;
-                    else if (m >= 1)
-                        UP[lv][R] = v;
+                    const int n = n0 + e;
+                    const int lv = 30 - __builtin_clz(n + 2);
+                    float* dst = n == T::NP - 1         ? &UP[KT][R]
+                                 : ((n + 2) & (n + 1)) ? &Vn[(n + 1) * S::PITCH + R]
+                                                       : &UP[lv][R];
+                    *dst = m >= 1 ? acc[tt][4 * qq + e] : 0.f;
                 }
+            }
         __syncthreads();  // the g columns of V_m and the update terms are written
         if (t < W) {
+            // all update terms are read before the sums that need them
+            float up[KT];
+#pragma unroll
+            for (int lv = 0; lv < KT; ++lv) up[lv] = UP[lv][t];
             float r = RS[m & 1][t];
 #pragma unroll
             for (int lv = 0; lv < KT; ++lv) {
                 Vn[((1 << lv) - 1) * S::PITCH + t] = r;  // r^lv_m
-                if (m >= (1 << lv)) r += UP[lv][t];
+                r += m >= (1 << lv) ? up[lv] : 0.f;
             }
-            ob[(long long)l * rout.rstride + t] = r;
-            RS[(m + 1) & 1][t] = rnext;
+            ob[l * rout.rstride + t] = r;
+            if (m < count) RS[(m + 1) & 1][t] = rq[u1];
         }
         __syncthreads();  // V_m and r_{m+1} are in place, UP is read
-        l += s;
     };
-    // two elements per trip, so that the strips keep their registers and a
-    // request stays in flight across the loop's back edge
-    for (int m = 0; m <= count; m += 2) {
-        element(m, aE, aO);
-        if (m + 1 <= count) element(m + 1, aO, aE);
+    // NB elements per trip, so that every ring index is a constant
+    for (int mb = 0; mb <= count; mb += NB) {
+        auto trip = [&](auto U) {
+            const int m = mb + decltype(U)::value;
+            if (m <= count) element(m, U);
+        };
+        unroll_each<0, NB>(trip);
     }
 }
 
@@ -1616,7 +1655,8 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile_last(BlockS
 // J_m = D_m W_m (+ I); the walk goes on with A_m = J_m.  Also clears the
 // max|dZ|, max|Z| slots and reduces max|r| into the kRedF slots.
 template <int W>
-__global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile_layer(
+__global__ __launch_bounds__(Tile2Shape<W>::NT)
+__attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer(
     float* __restrict__ Aout, VecDst rout, int L, LevelPlan plan, NewtonArgs na) {
     using S = Tile2Shape<W>;
     __shared__ float X[W * S::PITCH];  // J_{m-1}, transposed
@@ -1815,6 +1855,10 @@ LevelPlan plan_level2_tile(int B, int L, int s, long long target_wgs) {
     return p;
 }
 
+// Workgroups per tile pass: w = 128 and 64 fill the CUs with one or two
+// workgroups of 4 or 2 waves each; a w = 32 workgroup is one wave.
+long long pair_tile_target(int w) { return w == 32 ? 8192 : w == 64 ? 1024 : 256; }
+
 LevelPlan plan_level2(int B, int L, int s, long long target_items) {
     LevelPlan p;
     p.s = s;
@@ -1849,7 +1893,7 @@ hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout
             hipLaunchKernelGGL((pcr_level2_wave<32, false>), g3, block, 0, stream, Ain, rin, Aout,
                                rout, L, p);
     } else if (w == 64 || w == 128) {
-        const LevelPlan q = plan_level2_tile(B, L, s, w == 64 ? 1024 : 256);
+        const LevelPlan q = plan_level2_tile(B, L, s, pair_tile_target(w));
         const dim3 grid((unsigned)q.total);
         if (w == 64) {
             const dim3 blk(Tile2Shape<64>::NT);
@@ -1876,10 +1920,13 @@ hipError_t launch_pcr_level2(const BlockSrc& Ain, const VecSrc& rin, float* Aout
 
 hipError_t launch_pcr_level2_bwd(const BwdArgs& bw, const VecSrc& rin, float* Aout,
                                  const VecDst& rout, int B, int L, int w, hipStream_t stream) {
-    const LevelPlan q = plan_level2_tile(B, L, 1, w == 64 ? 1024 : 256);
+    const LevelPlan q = plan_level2_tile(B, L, 1, pair_tile_target(w));
     const dim3 grid((unsigned)q.total);
     const BlockSrc none{nullptr, 0, 0, 0};
-    if (w == 64)
+    if (w == 32)
+        hipLaunchKernelGGL((pcr_level2_tile<32, false, true>), grid, dim3(Tile2Shape<32>::NT), 0,
+                           stream, none, rin, Aout, rout, L, q, bw);
+    else if (w == 64)
         hipLaunchKernelGGL((pcr_level2_tile<64, false, true>), grid, dim3(Tile2Shape<64>::NT), 0,
                            stream, none, rin, Aout, rout, L, q, bw);
     else if (w == 128)
@@ -1987,16 +2034,19 @@ hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const V
 bool fused_newton_levels(int w) { return w == 16 || w == 32; }
 
 int first_level_count(int B, int L, int w) {
-    return (w == 64 || w == 128) && L > 2 && two_level(B, L, w) ? 2 : 1;
+    return (w == 32 || w == 64 || w == 128) && L > 2 && two_level(B, L, w) ? 2 : 1;
 }
 bool layer_first_level(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
 
 hipError_t launch_first_level_fwd(const NewtonArgs& na, float* Aout, const VecDst& rout, int B,
                                   int L, int w, hipStream_t stream) {
     if (first_level_count(B, L, w) == 2) {
-        const LevelPlan q = plan_level2_tile(B, L, 1, w == 64 ? 1024 : 256);
+        const LevelPlan q = plan_level2_tile(B, L, 1, pair_tile_target(w));
         const dim3 grid((unsigned)q.total);
-        if (w == 64)
+        if (w == 32)
+            hipLaunchKernelGGL((pcr_level2_tile_layer<32>), grid, dim3(Tile2Shape<32>::NT), 0,
+                               stream, Aout, rout, L, q, na);
+        else if (w == 64)
             hipLaunchKernelGGL((pcr_level2_tile_layer<64>), grid, dim3(Tile2Shape<64>::NT), 0,
                                stream, Aout, rout, L, q, na);
         else
