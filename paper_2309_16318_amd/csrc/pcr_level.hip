@@ -1430,8 +1430,13 @@ struct TailShape {
     static constexpr int NP = 1 << KT;   // columns of V, padded (2^KT - 1 used)
     static constexpr int NTC = NP / 32;  // 32-column tiles of the product
     // tiles per wave: as many waves as SIMDs where the tiles allow (more
-    // waves would not add MFMA throughput, only strip reloads)
-    static constexpr int TPW = (W / 32) * NTC >= 8 ? (W / 32) * NTC / 4 : 1;
+    // waves would not add MFMA throughput, only strip reloads); at w = 64
+    // one wave per row strip with all its column tiles, whose independent
+    // accumulators interleave (measured 15% faster than a wave per tile,
+    // which at w = 32 is the faster choice)
+    static constexpr int TPW = W == 64                 ? NTC
+                               : (W / 32) * NTC >= 8 ? (W / 32) * NTC / 4
+                                                     : 1;
     static constexpr int NWV = (W / 32) * NTC / TPW;
     static constexpr int NT = 64 * NWV;
     // elements whose block and right-hand side are in flight: an element's
@@ -1452,6 +1457,45 @@ __device__ __forceinline__ void unroll_each(F& f) {
     }
 }
 
+// acc[tt] = (strip of A) x (column tile tc0 + tt of V): lane i supplies
+// column i of each tile from col[tt] (its k = 4h .. rows, contiguous).
+template <int W, int NTC>
+__device__ __forceinline__ void tail_product(const float* const (&col)[NTC], const StripA<W>& a,
+                                             v16f (&acc)[NTC]) {
+    constexpr int NQ = Tile2Shape<W>::NQ;
+#pragma unroll
+    for (int tc = 0; tc < NTC; ++tc) acc[tc] = v16f{};
+    v4f pv[2][NTC];
+#pragma unroll
+    for (int q = 0; q <= NQ; ++q) {
+        if (q < NQ) {
+#pragma unroll
+            for (int tc = 0; tc < NTC; ++tc)
+                pv[q & 1][tc] = *reinterpret_cast<const v4f*>(col[tc] + 8 * q);
+        }
+        // keeps the operand reads of step q beside the MFMAs of step q-1
+        __builtin_amdgcn_sched_barrier(0);
+        if (q > 0) {
+            const int qb = (q - 1) & 1;
+            const v4f av = a[q - 1];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int tc = 0; tc < NTC; ++tc)
+                    acc[tc] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[qb][tc][e], av[e], acc[tc],
+                                                                   0, 0, 0);
+        }
+    }
+}
+
+// One barrier per element.  The r columns of V (n = 2^lv - 1, all in column
+// tile 0) are the only part of V that depends on the r chain, so every wave
+// that computes tile 0 forms the r chain of all W rows itself and keeps
+// those columns in its own LDS rows (RC), which its product reads in place
+// of V's; V's r-column slots hold the update terms of the element instead.
+// What the r chain reads (update terms of V_m) is next overwritten by
+// element m+2, after the barrier of element m+1, which every wave reaches
+// after its r chain of element m.
 template <int W, int KT>
 __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSrc Ain, VecSrc rin,
                                                                        VecDst rout, int L,
@@ -1459,10 +1503,9 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
     using S = Tile2Shape<W>;
     using T = TailShape<W, KT>;
     constexpr int NB = T::NB, D = T::D;
+    constexpr int RPL = W > 64 ? W / 64 : 1;  // rows of the r chain per lane
     __shared__ float VT[2][T::NP * S::PITCH];  // V_{m-1} / V_m, transposed (VT[n][k])
-    __shared__ float UP[KT + 1][W];            // g^lv_{2^lv, m}: the terms of the updates
-                                               // (row KT: the padding column, unused)
-    __shared__ float RS[2][W];                 // r_m of the element in slot m & 1
+    __shared__ float RC[T::NWV][KT][S::PITCH];  // per wave: r^lv_m, lv = 0 .. KT-1
     const int t = threadIdx.x;
     const int lane = t & 63, i = lane & 31, h = lane >> 5, wv = t >> 6;
     const int tc0 = T::TPW * (wv / (W / 32));  // the wave's first column tile
@@ -1473,41 +1516,54 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
     const float* ab = Ain.base + b * Ain.bstride;
     const float* rb = rin.base + b * rin.bstride;
     float* ob = rout.base + b * rout.bstride;
+    // lane i's column of tile 0 is r column lv_i (or no r column: -1)
+    const int lv_i = ((i + 1) & i) == 0 && i + 1 < (1 << KT) ? 31 - __builtin_clz(i + 1) : -1;
 
-    // Ring slot m % NB holds A_m (A_0 is never read) and r_m; element m
-    // requests A_{m+D} and r_{m+D}, and r_{m+1} goes to LDS at the end of
-    // element m.  Every thread issues the same loads on every element (rows
-    // past the chain's end are clamped to its last row and never used), so
-    // the compiler can count the requests in flight instead of waiting for
-    // all of them where a branch would merge.
+    // Ring slot m % NB holds A_m (A_0 is never read) and, per r-chain row of
+    // the lane, r_m; element m requests A_{m+D} and r_{m+D}.  Every thread
+    // issues the same loads on every element (rows past the chain's end are
+    // clamped to its last row and never used), so the compiler can count the
+    // requests in flight instead of waiting for all of them where a branch
+    // would merge.
     StripA<W> a[NB];
-    float rq[NB];
+    float rq[NB][RPL];
     v16f acc[T::TPW];
-    const int tw = t & (W - 1);
+    auto load_r = [&](float (&dst)[RPL], long long row) {
 #pragma unroll
-    for (int j = 1; j < D; ++j) {
+        for (int rr = 0; rr < RPL; ++rr) dst[rr] = rb[row * rin.rstride + ((lane + 64 * rr) & (W - 1))];
+    };
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
         const long long lj = c + (long long)min(j, count) * s;
-        strip_load<W, false>(ab + lj * Ain.rstride, a[j], R, h);
-        rq[j] = rb[lj * rin.rstride + tw];
+        if (j >= 1) strip_load<W, false>(ab + lj * Ain.rstride, a[j], R, h);
+        load_r(rq[j], lj);
     }
-    if (t < W) RS[0][t] = rb[(long long)c * rin.rstride + t];
     auto element = [&](int m, auto U) {
         constexpr int u = decltype(U)::value;  // m % NB
-        constexpr int un = (u + D) % NB, u1 = (u + 1) % NB;
+        constexpr int un = (u + D) % NB;
         const float* Vp = VT[(m + 1) & 1];
         float* Vn = VT[m & 1];
         const long long l = c + (long long)m * s;
         {
             const long long ln = c + (long long)min(m + D, count) * s;
             strip_load<W, false>(ab + ln * Ain.rstride, a[un], R, h);
-            rq[un] = rb[ln * rin.rstride + tw];
+            load_r(rq[un], ln);
+        }
+        if (m >= 1) {
+            const float* col[T::TPW];
+#pragma unroll
+            for (int tt = 0; tt < T::TPW; ++tt)
+                col[tt] = (tc0 + tt == 0 && lv_i >= 0 ? RC[wv][lv_i]
+                                                      : Vp + (32 * (tc0 + tt) + i) * S::PITCH) +
+                          4 * h;
+            tail_product<W, T::TPW>(col, a[u], acc);
         }
         // Column n of the product (level lv, n = 2^lv - 1 + j) is g^lv_{j+1};
         // it goes to column n + 1 of V_m, or, for j + 1 = 2^lv (n + 2 a power
-        // of two), to the update terms; the padding column n = 2^KT - 1 goes
-        // to the spare row.  The destination is computed, not branched on.
-        // Element 0 has no block: its g columns are 0.
-        if (m >= 1) strip_product<W, 0, T::TPW, false>(Vp + 32 * tc0 * S::PITCH, a[u], acc, i, h);
+        // of two), to the update term of level lv, kept in V_m's r-column slot
+        // 2^lv - 1; the padding column goes to the padding column.  The
+        // destination is computed, not branched on.  Element 0 has no block:
+        // its g columns are 0.
 #pragma unroll
         for (int tt = 0; tt < T::TPW; ++tt)
 #pragma unroll
@@ -1517,28 +1573,32 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
                 for (int e = 0; e < 4; ++e) {
                     const int n = n0 + e;
                     const int lv = 30 - __builtin_clz(n + 2);
-                    float* dst = n == T::NP - 1         ? &UP[KT][R]
-                                 : ((n + 2) & (n + 1)) ? &Vn[(n + 1) * S::PITCH + R]
-                                                       : &UP[lv][R];
-                    *dst = m >= 1 ? acc[tt][4 * qq + e] : 0.f;
+                    const int col = n == T::NP - 1         ? n
+                                    : ((n + 2) & (n + 1)) ? n + 1
+                                                          : (1 << lv) - 1;
+                    Vn[col * S::PITCH + R] = m >= 1 ? acc[tt][4 * qq + e] : 0.f;
                 }
             }
         __syncthreads();  // the g columns of V_m and the update terms are written
-        if (t < W) {
-            // all update terms are read before the sums that need them
-            float up[KT];
+        if (tc0 == 0) {
 #pragma unroll
-            for (int lv = 0; lv < KT; ++lv) up[lv] = UP[lv][t];
-            float r = RS[m & 1][t];
+            for (int rr = 0; rr < RPL; ++rr) {
+                const int k = lane + 64 * rr;
+                if (k < W) {
+                    // all update terms are read before the sums that need them
+                    float up[KT];
 #pragma unroll
-            for (int lv = 0; lv < KT; ++lv) {
-                Vn[((1 << lv) - 1) * S::PITCH + t] = r;  // r^lv_m
-                r += m >= (1 << lv) ? up[lv] : 0.f;
+                    for (int lv = 0; lv < KT; ++lv) up[lv] = Vn[((1 << lv) - 1) * S::PITCH + k];
+                    float r = rq[u][rr];
+#pragma unroll
+                    for (int lv = 0; lv < KT; ++lv) {
+                        RC[wv][lv][k] = r;  // r^lv_m
+                        r += m >= (1 << lv) ? up[lv] : 0.f;
+                    }
+                    if (wv == 0) ob[l * rout.rstride + k] = r;
+                }
             }
-            ob[l * rout.rstride + t] = r;
-            if (m < count) RS[(m + 1) & 1][t] = rq[u1];
         }
-        __syncthreads();  // V_m and r_{m+1} are in place, UP is read
     };
     // NB elements per trip, so that every ring index is a constant
     for (int mb = 0; mb <= count; mb += NB) {
