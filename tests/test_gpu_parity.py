@@ -152,7 +152,8 @@ def test_forward_residual_workload(dev):
 @pytest.mark.parametrize("w,L,B", [(1, 5, 2), (3, 40, 3), (16, 100, 2), (17, 33, 2),
                                    (32, 64, 2), (64, 20, 2), (128, 9, 2),
                                    (16, 1, 3), (16, 2, 3), (16, 3, 2), (32, 1, 2), (32, 2, 5),
-                                   (32, 3, 2), (32, 5, 3), (16, 257, 4), (32, 130, 3),
+                                   (32, 3, 2), (32, 4, 2), (32, 5, 3), (32, 9, 3), (16, 257, 4),
+                                   (32, 130, 3), (64, 3, 2), (128, 4, 2),
                                    (4, 600, 2), (2, 3000, 1)])
 @pytest.mark.parametrize("layer,alpha", [(0, 1.0), (1, 0.1)])
 def test_forward_shapes(dev, w, L, B, layer, alpha):
@@ -188,8 +189,9 @@ def test_forward_all_layer_kinds(dev, w, L, B, layer, alpha):
 # Tile widths with several elements per workgroup segment in every pass
 # (w = 64, B = 40 and w = 128, B = 16), even and odd level counts (L = 130
 # and 203: 8 levels, L = 300: 9), and the one-pass tail of the last levels
-# at w = 32 (B = 64: 5 tail levels after the first level and one pair), 64
-# (4 and 3 levels) and 128 (4 levels).
+# at w = 32 (L = 130, B = 64: 6 tail levels right after the first pair with
+# the layers; L = 300, B = 40: that pair, one more pair and 5 tail levels),
+# 64 and 128.
 @pytest.mark.parametrize("w,L,B", [(64, 130, 40), (64, 300, 8), (128, 203, 16), (32, 130, 64),
                                    (32, 300, 40)])
 @pytest.mark.parametrize("layer,alpha", ALL_KINDS)
@@ -378,7 +380,9 @@ def adjoint_err(lam, dz0, rl, rz):
 
 
 @pytest.mark.parametrize("w,L,B", [(1, 1, 1), (2, 2, 3), (4, 16, 1), (3, 37, 4), (16, 100, 3),
-                                   (33, 65, 2), (64, 30, 3), (128, 17, 2)])
+                                   (33, 65, 2), (64, 30, 3), (128, 17, 2),
+                                   (32, 2, 2), (32, 3, 2), (32, 4, 3), (32, 5, 2), (32, 9, 2),
+                                   (64, 3, 2), (128, 5, 2)])
 @pytest.mark.parametrize("layer,alpha", [(0, 1.0), (1, 0.1)])
 def test_backward_shapes(dev, w, L, B, layer, alpha):
     _say(f"backward shapes w={w} L={L} B={B} layer={layer}")
