@@ -31,9 +31,11 @@ int hip_fail(hipError_t e, const char* where) {
 
 // ------------------------------------------------------------ instrumentation
 // One record per span: consecutive launches of one kernel class on one
-// stream, with no host synchronisation or other class in between, share one
-// event pair (the end event is recorded again after each launch), so that
-// short kernels are not charged the cost of an event pair each.
+// stream, with nothing else enqueued in between, share one event pair, so
+// that short kernels are not charged the cost of an event pair each.  The
+// end event is recorded when the span ends (the next launch of another
+// class, any other enqueue of the library, or the return of an entry point),
+// so that no event sits between the kernels of a span.
 struct ProfRec {
     int kclass;
     hipStream_t st;
@@ -44,7 +46,7 @@ struct ProfRec {
 
 struct Prof {
     bool on = false;
-    bool open = false;  // the last record may be extended
+    bool open = false;  // the last record may be extended; its end event is not recorded yet
     std::vector<ProfRec> pending;
     std::vector<hipEvent_t> pool;
     long long launches[DEEPPCR_KCLASS_COUNT] = {};
@@ -65,26 +67,41 @@ hipEvent_t take_event() {
     return e;
 }
 
-// Ends the current span (at every entry point and after every host wait).
-void prof_break() { g_prof.open = false; }
+// Ends the current span: its end event is recorded now, right behind its
+// last launch.  Called before every enqueue that is not a timed launch and
+// when an entry point returns.
+hipError_t prof_break() {
+    if (!g_prof.open) return hipSuccess;
+    g_prof.open = false;
+    const ProfRec& r = g_prof.pending.back();
+    return hipEventRecord(r.e1, r.st);
+}
+
+// Ends the span at every exit of an entry point.
+struct SpanGuard {
+    SpanGuard() { (void)prof_break(); }
+    ~SpanGuard() { (void)prof_break(); }
+    SpanGuard(const SpanGuard&) = delete;
+    SpanGuard& operator=(const SpanGuard&) = delete;
+};
 
 // Runs `launch` (which enqueues one kernel on `st` and returns its
 // hipGetLastError), bracketed by events when instrumentation is on.
 template <class F>
 hipError_t timed(int kclass, double bytes, double flops, hipStream_t st, F&& launch) {
     if (!g_prof.on) return launch();
-    if (g_prof.open && !g_prof.pending.empty()) {
+    if (g_prof.open) {
         ProfRec& r = g_prof.pending.back();
         if (r.kclass == kclass && r.st == st) {
             hipError_t e = launch();
-            if (e != hipSuccess) return e;
-            e = hipEventRecord(r.e1, st);
             if (e != hipSuccess) return e;
             r.n += 1;
             r.bytes += bytes;
             r.flops += flops;
             return hipSuccess;
         }
+        hipError_t e = prof_break();
+        if (e != hipSuccess) return e;
     }
     hipEvent_t e0 = take_event(), e1 = take_event();
     if (!e0 || !e1) return launch();
@@ -92,16 +109,22 @@ hipError_t timed(int kclass, double bytes, double flops, hipStream_t st, F&& lau
     if (e != hipSuccess) return e;
     e = launch();
     if (e != hipSuccess) return e;
-    e = hipEventRecord(e1, st);
-    if (e != hipSuccess) return e;
     g_prof.pending.push_back({kclass, st, e0, e1, 1, bytes, flops});
     g_prof.open = true;
     return hipSuccess;
 }
 
+// An asynchronous copy on the stream (ending the instrumentation span).
+hipError_t copy_async(void* dst, const void* src, size_t n, hipMemcpyKind kind, hipStream_t st) {
+    hipError_t e = prof_break();
+    if (e != hipSuccess) return e;
+    return hipMemcpyAsync(dst, src, n, kind, st);
+}
+
 // Waits for the stream (ending the instrumentation span).
 hipError_t host_wait(hipStream_t st) {
-    prof_break();
+    hipError_t e = prof_break();
+    if (e != hipSuccess) return e;
     return hipStreamSynchronize(st);
 }
 
@@ -480,7 +503,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
                                       st);
         });
         if (e != hipSuccess) return hip_fail(e, "newton_tiny");
-        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 3 * sizeof(unsigned), hipMemcpyDeviceToHost, st));
+        DEEPPCR_HIP(copy_async(hw, ws.red, 3 * sizeof(unsigned), hipMemcpyDeviceToHost, st));
         DEEPPCR_HIP(host_wait(st));
         if (iters_out) *iters_out = (int)hw[1];
         if (measure_out) *measure_out = bits_to_float(hw[2]);
@@ -492,7 +515,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
     const double eval_bytes = 4.0 * B * L * (w2 + 2.0 * w);
     const double eval_flops = (double)B * L * (2.0 * w2 + w2);
     if (Z_init) {
-        if (Z_init != Z) DEEPPCR_HIP(hipMemcpyAsync(Z, Z_init, nv, hipMemcpyDeviceToDevice, st));
+        if (Z_init != Z) DEEPPCR_HIP(copy_async(Z, Z_init, nv, hipMemcpyDeviceToDevice, st));
     } else {
         hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * B * L * w, 2.0 * B * w * w, st, [&] {
             return launch_initial_guess(W, bias, z0, Z, B, L, w, layer, alpha, st);
@@ -525,7 +548,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
         }
         if (e != hipSuccess) return hip_fail(e, "layer evaluation");
         if (rule.residual) {
-            DEEPPCR_HIP(hipMemcpyAsync(hw + kRedF, fslots, kRedShards * sizeof(unsigned),
+            DEEPPCR_HIP(copy_async(hw + kRedF, fslots, kRedShards * sizeof(unsigned),
                                        hipMemcpyDeviceToHost, st));
             DEEPPCR_HIP(host_wait(st));
             const unsigned mf = max_slots(hw + kRedF);
@@ -554,7 +577,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
             if (e != hipSuccess) return hip_fail(e, "update_reduce");
         }
         if (rule.residual) continue;
-        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
+        DEEPPCR_HIP(copy_async(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
                                    hipMemcpyDeviceToHost, st));
         DEEPPCR_HIP(host_wait(st));
         const unsigned mx = max_slots(hw + kRedDZ), mz = max_slots(hw + kRedZ);
@@ -593,7 +616,7 @@ const char* deeppcr_last_error(void) { return g_last_error; }
 int pcr_solve_block_bidiag(const float* J, const float* r, float* x, int B, int L, int w,
                            int transpose, void* workspace, size_t workspace_bytes,
                            void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     if (!J || !r || !x || !workspace || !sizes_ok(B, L, w) || (transpose != 0 && transpose != 1))
         return DEEPPCR_EINVAL;
     const Layout lo = layout(DEEPPCR_OP_PCR, B, L, w);
@@ -629,7 +652,7 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x, int B, int 
 int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, int w,
                         void* workspace, size_t workspace_bytes, float* residual_out,
                         float* max_update_out, float* max_abs_out, void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     if (!J || !F || !Z || !workspace || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
     const Layout lo = layout(DEEPPCR_OP_PCR, B, L, w);
     if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
@@ -658,7 +681,7 @@ int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, 
     e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
               [&] { return launch_update_reduce(Z, xd.base, n, ws.red, st); });
     if (e != hipSuccess) return hip_fail(e, "update_reduce");
-    DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, kRedWords * sizeof(unsigned), hipMemcpyDeviceToHost,
+    DEEPPCR_HIP(copy_async(hw, ws.red, kRedWords * sizeof(unsigned), hipMemcpyDeviceToHost,
                                st));
     DEEPPCR_HIP(host_wait(st));
     const unsigned mr = max_slots(hw + kRedF), mx = max_slots(hw + kRedDZ),
@@ -674,7 +697,7 @@ int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, floa
                         int L, int w, int layer, float alpha, float tol, int max_iter,
                         const float* Z_init, void* workspace, size_t workspace_bytes,
                         int* iters_out, float* last_update_out, void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     const int c = check_forward_args(W, bias, z0, Z, Z_init, workspace, workspace_bytes, B, L, w,
                                      layer, alpha);
     if (c != DEEPPCR_OK) return c;
@@ -689,7 +712,7 @@ int deeppcr_mlp_forward_residual(const float* W, const float* bias, const float*
                                  float rtol, int max_iter, const float* Z_init, void* workspace,
                                  size_t workspace_bytes, int* iters_out, float* residual_out,
                                  void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     const int c = check_forward_args(W, bias, z0, Z, Z_init, workspace, workspace_bytes, B, L, w,
                                      layer, alpha);
     if (c != DEEPPCR_OK) return c;
@@ -705,7 +728,7 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
                          const float* G, float* Lambda, float* dz0, float* dW, float* db, int B,
                          int L, int w, int layer, float alpha, void* workspace,
                          size_t workspace_bytes, void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     if (!W || !bias || !z0 || !Z || !G || !Lambda || !dz0 || !dW || !db || !workspace ||
         !sizes_ok(B, L, w))
         return DEEPPCR_EINVAL;
@@ -769,7 +792,7 @@ int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, f
                            int L, int w, int skip, int act, float tol, int max_iter,
                            const float* Z_init, void* workspace, size_t workspace_bytes,
                            int* iters_out, float* last_update_out, void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     if (!W || !bias || !z0 || !Z || !workspace || !resnet_shape_ok(B, L, w, skip, act))
         return DEEPPCR_EINVAL;
     if (!(tol >= 0.f) || !std::isfinite(tol) || max_iter < 1) return DEEPPCR_EINVAL;
@@ -826,7 +849,7 @@ int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, f
         e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
                   [&] { return launch_update_reduce(X, xd.base, n, ws.red, st); });
         if (e != hipSuccess) return hip_fail(e, "update_reduce");
-        DEEPPCR_HIP(hipMemcpyAsync(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
+        DEEPPCR_HIP(copy_async(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
                                    hipMemcpyDeviceToHost, st));
         DEEPPCR_HIP(host_wait(st));
         const unsigned mx = max_slots(hw + kRedDZ), mz = max_slots(hw + kRedZ);
@@ -856,7 +879,7 @@ int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, con
                             float* Lambda, float* dz0, float* dW, float* db, int B, int L, int w,
                             int skip, int act, void* workspace, size_t workspace_bytes,
                             void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     if (!W || !z0 || !Z || !G_ || !Lambda || !dz0 || !dW || !db || !workspace ||
         !resnet_shape_ok(B, L, w, skip, act))
         return DEEPPCR_EINVAL;
@@ -909,7 +932,7 @@ int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, con
 int deeppcr_resnet_seq_forward(const float* W, const float* bias, const float* z0, float* Z,
                                int B, int L, int w, int skip, int act, int launch_per_layer,
                                void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     if (!W || !bias || !z0 || !Z || !resnet_shape_ok(B, L, w, skip, act) ||
         (launch_per_layer != 0 && launch_per_layer != 1))
         return DEEPPCR_EINVAL;
@@ -935,7 +958,7 @@ int deeppcr_resnet_seq_forward(const float* W, const float* bias, const float* z
 int deeppcr_resnet_seq_backward(const float* W, const float* z0, const float* Z, const float* G,
                                 float* Lambda, float* dz0, int B, int L, int w, int skip, int act,
                                 int launch_per_layer, void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     if (!W || !z0 || !Z || !G || !Lambda || !dz0 || !resnet_shape_ok(B, L, w, skip, act) ||
         (launch_per_layer != 0 && launch_per_layer != 1))
         return DEEPPCR_EINVAL;
@@ -963,7 +986,7 @@ int deeppcr_resnet_seq_backward(const float* W, const float* z0, const float* Z,
 
 int deeppcr_seq_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
                         int L, int w, int layer, float alpha, int launch_per_layer, void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     if (!W || !bias || !z0 || !Z || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
     if (layer < 0 || layer >= kNumLayerKinds || !std::isfinite(alpha)) return DEEPPCR_EINVAL;
     if (launch_per_layer != 0 && launch_per_layer != 1) return DEEPPCR_EINVAL;
@@ -988,7 +1011,7 @@ int deeppcr_seq_forward(const float* W, const float* bias, const float* z0, floa
 int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, const float* Z,
                          const float* G, float* Lambda, float* dz0, int B, int L, int w, int layer,
                          float alpha, int launch_per_layer, void* stream) {
-    prof_break();
+    const SpanGuard span_guard;
     if (!W || !bias || !z0 || !Z || !G || !Lambda || !dz0 || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
     if (layer < 0 || layer >= kNumLayerKinds || !std::isfinite(alpha)) return DEEPPCR_EINVAL;
     if (launch_per_layer != 0 && launch_per_layer != 1) return DEEPPCR_EINVAL;
@@ -1015,11 +1038,13 @@ int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, con
 }
 
 int deeppcr_profile_enable(int on) {
+    (void)prof_break();
     g_prof.on = on != 0;
     return DEEPPCR_OK;
 }
 
 void deeppcr_profile_reset(void) {
+    (void)prof_break();
     for (auto& p : g_prof.pending) {
         (void)hipEventSynchronize(p.e1);
         g_prof.pool.push_back(p.e0);
@@ -1035,6 +1060,10 @@ void deeppcr_profile_reset(void) {
 int deeppcr_profile_read(int kclass, long long* launches, double* total_ms, double* alg_bytes,
                          double* alg_flops) {
     if (kclass < 0 || kclass >= DEEPPCR_KCLASS_COUNT) return DEEPPCR_EINVAL;
+    {
+        hipError_t e = prof_break();
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
     for (auto& p : g_prof.pending) {
         hipError_t e = hipEventSynchronize(p.e1);
         if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
