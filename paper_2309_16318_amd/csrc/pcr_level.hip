@@ -1741,23 +1741,56 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
         const float* Zb = na.Z + (long long)b * L * W;
         float* ob = rout.base + b * rout.bstride;
         float* Ob = Aout + (long long)b * L * W * W;
-        StripA<W> a;            // W_m, then J_m; then W_{m+1}
+        // PF (w = 32, where an element's products are short): the weight
+        // strip, iterate row and bias of later elements are requested at the
+        // start of an element, into the other slot of a two-slot ring (by
+        // element parity), and every request is issued on every element
+        // (clamped to the chain's last row), so no branch makes the compiler
+        // wait for all of them.  Otherwise (w = 64, 128, no registers to
+        // spare) one strip buffer is refilled after J_m has gone to LDS.
+        constexpr bool PF = W == 32;
+        StripA<W> aE, aO;       // W_m, then J_m (PF: by element parity)
         StripC<W> pE, pO;       // A'_m of even / odd elements
+        float zq0 = 0.f, zq1 = 0.f, bq0 = 0.f, bq1 = 0.f;  // PF: Z and bias ring
+        const int tw = t & (W - 1);
         if (t < W) {
             zv[(mw + 1) & 1][t] =
                 mw >= 1 ? Zb[(long long)(mw - 1) * W + t] : na.z0[(long long)b * W + t];
             zv[mw & 1][t] = Zb[(long long)mw * W + t];
         }
-        strip_load<W, false>(na.W + (long long)mw * W * W, a, R0, h0);
+        strip_load<W, false>(na.W + (long long)mw * W * W, (PF && (mw & 1)) ? aO : aE, R0, h0);
+        if constexpr (PF) {
+            const float zn = Zb[(long long)min(mw + 1, count) * W + tw];  // Z_{mw+1}
+            const float bn = na.bias[(long long)mw * W + R0];
+            if (mw & 1) {
+                zq0 = zn;
+                bq1 = bn;
+            } else {
+                zq1 = zn;
+                bq0 = bn;
+            }
+        }
         __syncthreads();
         // Two barriers per element as in pcr_level2_tile; zv and rv are
-        // rewritten before B1, rp and Y after it.
-        auto element = [&](int m, StripC<W>& pC, StripC<W>& pP) {
+        // rewritten before B1, rp and Y after it.  aC holds the strip of
+        // element m; with PF, aN receives that of m+1, zS (slot m & 1)
+        // Z_{m+2} and bO the bias of m+1, while zO holds Z_{m+1} and bS the
+        // bias of m.
+        auto element = [&](int m, StripC<W>& pC, StripC<W>& pP, StripA<W>& aC, StripA<W>& aN,
+                           float& zS, float& zO, float& bS, float& bO) {
             const bool more = m < m1;
             const bool have_prev = m > mw;
             const bool out_row = m >= m0;
-            float znext = 0.f;
-            if (more && t < W) znext = Zb[(long long)(m + 1) * W + t];
+            float znext = 0.f, bm;
+            if constexpr (PF) {
+                strip_load<W, false>(na.W + (long long)min(m + 1, count) * W * W, aN, R0, h0);
+                zS = Zb[(long long)min(m + 2, count) * W + tw];
+                bO = na.bias[(long long)min(m + 1, count) * W + R0];
+                bm = bS;
+            } else {
+                if (more && t < W) znext = Zb[(long long)(m + 1) * W + t];
+                bm = na.bias[(long long)m * W + R0];
+            }
             // The lane's row and half as opaque values: the LDS and global
             // addresses derived from them are formed per element instead of
             // being held (or spilled) across the whole walk.
@@ -1766,8 +1799,7 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
             // layer m at Z_{m-1}: r_m and the strip of J_m
             const float* zp = zv[(m + 1) & 1];
             float dsc;
-            const float f = layer_out<W>(
-                na, strip_matvec<W>(a, zp, h) + na.bias[(long long)m * W + R], zp[R], &dsc);
+            const float f = layer_out<W>(na, strip_matvec<W>(aC, zp, h) + bm, zp[R], &dsc);
             const float rm = f - zv[m & 1][R];
             mr = max(mr, __float_as_uint(fabsf(rm)));
             // the diagonal is column k = R, at 8q + e = R - 4h (the empty asm
@@ -1778,22 +1810,26 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
             for (int q = 0; q < S::NQ; ++q)
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    a[q][e] = fmaf(dsc, a[q][e], dk == 8 * q + e ? 1.f : 0.f);
+                    aC[q][e] = fmaf(dsc, aC[q][e], dk == 8 * q + e ? 1.f : 0.f);
             // level 1: r'_m and A'_m
             float r1 = rm;
             const bool prod1 = m >= 2 && have_prev;
             if (prod1) {
-                r1 += strip_product<W, 0, S::T, true>(X, a, pC, i, h, rv[(m + 1) & 1]);
+                r1 += strip_product<W, 0, S::T, true>(X, aC, pC, i, h, rv[(m + 1) & 1]);
             } else {
-                if (m >= 1 && have_prev) r1 += strip_matvec<W>(a, rv[(m + 1) & 1], h);
+                if (m >= 1 && have_prev) r1 += strip_matvec<W>(aC, rv[(m + 1) & 1], h);
                 strip_zero<W>(pC);
             }
             __syncthreads();  // B0: X, rv and zv are read
-            if (more && m >= 1) strip_put_T<W>(X, a, R, h);  // J_m
+            if (more && m >= 1) strip_put_T<W>(X, aC, R, h);  // J_m
             if (h == 0) rv[m & 1][R] = rm;
-            if (more && t < W) zv[(m + 1) & 1][t] = znext;
-            // without a next element this rereads the current block (unused)
-            strip_load<W, false>(na.W + (long long)(more ? m + 1 : m) * W * W, a, R, h);
+            if constexpr (PF) {
+                if (more && t < W) zv[(m + 1) & 1][t] = zO;
+            } else {
+                if (more && t < W) zv[(m + 1) & 1][t] = znext;
+                // without a next element this rereads the current block (unused)
+                strip_load<W, false>(na.W + (long long)(more ? m + 1 : m) * W * W, aC, R, h);
+            }
             // level 2: r''_m and A''_m
             float r2 = r1;
             const bool prod2 = m >= 4 && out_row;
@@ -1807,10 +1843,17 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
             if (more && m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
         };
         for (int m = mw; m <= m1; ++m) {
-            if (m & 1)
-                element(m, pO, pE);
-            else
-                element(m, pE, pO);
+            if constexpr (PF) {
+                if (m & 1)
+                    element(m, pO, pE, aO, aE, zq1, zq0, bq1, bq0);
+                else
+                    element(m, pE, pO, aE, aO, zq0, zq1, bq0, bq1);
+            } else {
+                if (m & 1)
+                    element(m, pO, pE, aE, aE, zq1, zq0, bq1, bq0);
+                else
+                    element(m, pE, pO, aE, aE, zq0, zq1, bq0, bq1);
+            }
         }
     }
     for (int off = 32; off > 0; off >>= 1) mr = max(mr, (unsigned)__shfl_xor((int)mr, off, 64));
