@@ -246,7 +246,7 @@ void tail_work(int B, int L, int w, int kt, double* bytes, double* flops) {
 // ws A buffer (k + a_first) % 2 and vectors to ws r buffer (k + r_first) % 2,
 // except the last level, which writes the solution to `x`.
 // With bwd the first pass (levels 1 and 2) forms the backward's blocks from
-// the weights instead of reading A0 (w = 64, 128 and L > 2 only).
+// the weights instead of reading A0 (w = 32, 64, 128 and L > 2 only).
 hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int B, int L, int w,
                      float* wsA[2], float* wsr[2], int a_first, int r_first, hipStream_t st,
                      const BwdArgs* bwd = nullptr) {

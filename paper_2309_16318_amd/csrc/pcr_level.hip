@@ -6,16 +6,21 @@
 // Rows s <= l < 2s need no operator update: their new operator would multiply
 // a row index below zero, whose unknown is identically zero.
 //
-// Three implementations, chosen by width:
+// Implementations, chosen by width:
 //   w = 16, 32   one wave walks a chain of rows l, l+s, l+2s, ... of one
 //                residue class: each operator block is read from HBM once per
 //                level, the block product runs on fp32 MFMA
 //                (16x16x4 / 32x32x2) and the previous block is kept, transposed
-//                through LDS, as the next row's right operand.
-//   w = 64, 128  the same chain walk with one workgroup per chain
-//                segment: the current and previous blocks are staged in LDS
-//                (double buffered), each wave owns 32x32 output tiles, and the
-//                next block is prefetched into registers during the MFMAs.
+//                through LDS, as the next row's right operand; two levels per
+//                pass where the chains allow.
+//   w = 64, 128  the same chain walk with one workgroup per chain segment,
+//                one wave per 32-row strip of the blocks (left MFMA operand in
+//                registers, right operands in LDS), two levels per pass; the
+//                strip kernels also serve w = 32 for the first two levels of
+//                a Newton iteration or backward solve.
+//   tail         the last 3-6 levels of a solve at w = 32, 64, 128 in one
+//                pass, one workgroup per independent chain, the level
+//                products applied to vectors.
 //   w <= 8       lane groups of a wave per row (small.hip).
 //   other w      generic path: one workgroup per (system, row), float32 FMA on
 //                the vector ALUs, operands staged through LDS in k-chunks.
@@ -1117,7 +1122,7 @@ __global__ __launch_bounds__(256) void pcr_level2_wave(BlockSrc Ain, VecSrc rin,
     }
 }
 
-// ---- two levels per pass, w = 64 or 128 ---------------------------------
+// ---- two levels per pass, w = 32 (first levels only), 64, 128 ------------
 // The chain walk of pcr_level2_wave with one workgroup per segment and one
 // wave per 32-row strip of the blocks.  A lane (i, h) of wave v holds row
 // R = 32 v + i of a block at the columns 8q + 4h .. +3 (q = 0 .. W/8-1): the
@@ -1410,7 +1415,7 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
     }
 }
 
-// ---- the last KT levels of a solve, w = 64 or 128 -------------------------
+// ---- the last KT levels of a solve, w = 32, 64, 128 -----------------------
 // After the levels below stride s the system is s independent chains per
 // system, and the last KT levels (strides s .. s 2^{KT-1}, s 2^KT >= L) write
 // no operator: their products only ever meet vectors.  Level i updates
@@ -1424,7 +1429,7 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
 // 2^i - 1 + j of V holds g^i_{j} (j = 0 .. 2^i - 1, j = 0 being r^i); the
 // same column of the product is then g^i_{j+1}.  One workgroup walks one
 // whole chain (at most 2^KT elements), so no segment warm-up is needed; the
-// r chain of an element and the new V are formed by one thread per row.
+// r chain of an element (r^{i+1} = r^i + g^i_{2^i}) takes KT adds per row.
 template <int W, int KT>
 struct TailShape {
     static constexpr int NP = 1 << KT;   // columns of V, padded (2^KT - 1 used)
