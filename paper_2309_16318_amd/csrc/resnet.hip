@@ -14,6 +14,7 @@
 // (dynamic, sized by w).  The PCR levels, the Newton update and its
 // reductions are those of the MLP path.
 #include "internal.h"
+#include "strip.h"
 
 namespace deeppcr {
 namespace {
@@ -272,8 +273,6 @@ size_t block_lds_bytes(int w) { return (4 * (size_t)w + 2 * (size_t)w * w) * siz
 // sigma'(z), comes from global memory (L2-resident, shared by every system)
 // and the previous product's rows from the wave's LDS copy.  Only wave-level
 // barriers; four independent waves per workgroup.
-typedef float v4f __attribute__((ext_vector_type(4)));
-
 template <int W>
 struct BlockWaveShape {
     static constexpr int LPR = 64 / W;     // lanes per product row
@@ -399,6 +398,106 @@ __global__ __launch_bounds__(256) void resnet_block_wave(
     }
 }
 
+// ---- one workgroup per (system, block), w = 64 or 128 ----------------------
+// The running product on fp32 MFMA: one wave per 32-row strip (the register
+// strips of the PCR kernels).  Layer j of the block multiplies the product
+// from the left by J_j = W_j diag(sigma'(z_{j-1})): the lane's strip of W_j
+// comes from global memory (L2-resident, shared by every system), first
+// serves the state update W_j sigma(z) + b_j (forward), then has its columns
+// scaled by sigma' and is multiplied with the previous product, held
+// transposed in LDS (two buffers, one per layer parity).  The last product
+// strip, plus I, is stored as the block's operator.  Same roles of BWD and
+// the arguments as resnet_block_wave.
+template <int W, bool BWD>
+__global__ __launch_bounds__(Tile2Shape<W>::NT) void resnet_block_tile(
+    const float* __restrict__ Wt, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ S, const float* __restrict__ Gv, float* __restrict__ A,
+    float* __restrict__ r, unsigned* __restrict__ red, int B, int G, int skip, int act) {
+    using SH = Tile2Shape<W>;
+    __shared__ float PT[2][W * SH::PITCH];  // the product so far, transposed
+    __shared__ float xin[W], z[W], sg[W], ds[W];
+    const int t = threadIdx.x;
+    const int lane = t & 63, i = lane & 31, h = lane >> 5;
+    const int R = 32 * (t >> 6) + i;
+    if (!BWD && blockIdx.x == 0)
+        for (int k = t; k < 2 * kRedShards; k += SH::NT) red[k] = 0u;
+    const long long item = blockIdx.x;  // b * G + g
+    const int g = (int)(item % G);
+    const int b = (int)(item / G);
+    const long long L = (long long)G * skip;
+    // S: forward, the iterate X [B, G, W]; backward, the stored states Z [B, L, W]
+    const float* Zb = S + (long long)b * L * W;
+    if (BWD) {
+        const int m = G - 1 - g;
+        if (t < W) r[((long long)b * G + m) * W + t] = (m == 0) ? Gv[(long long)b * W + t] : 0.f;
+        if (g == 0) return;  // uniform over the workgroup
+    }
+    if (t < W) {
+        const float x = BWD ? Zb[((long long)g * skip - 1) * W + t]
+                            : (g == 0 ? z0[(long long)b * W + t] : S[(item - 1) * W + t]);
+        xin[t] = x;
+        z[t] = x;
+    }
+    const bool jac = g > 0;  // the block of row 0 couples to z0 and is never read
+    StripA<W> a;             // rows R of W_j, then of W_j diag(sigma')
+    StripC<W> c;             // rows R of the product after layer j (j >= 1)
+    strip_zero<W>(c);
+    for (int tt = 0; tt < skip; ++tt) {
+        const long long j = (long long)g * skip + tt;
+        strip_load<W, false>(Wt + j * W * W, a, R, h);
+        __syncthreads();  // z of the previous layer is in place
+        if (t < W) {
+            const float zin = BWD ? (tt == 0 ? xin[t] : Zb[(j - 1) * W + t]) : z[t];
+            float d;
+            sg[t] = act_fn(act, zin, &d);
+            ds[t] = d;
+        }
+        __syncthreads();  // sg and ds are in place; every read of z is done
+        if (!BWD) {
+            const float zr = strip_matvec<W>(a, sg, h) + bias[j * W + R];
+            if (h == 0) z[R] = zr;
+        }
+        if (jac) {
+#pragma unroll
+            for (int q = 0; q < SH::NQ; ++q) {
+                const v4f d4 = *reinterpret_cast<const v4f*>(ds + 8 * q + 4 * h);
+                a[q] *= d4;
+            }
+            const bool last = tt + 1 == skip;
+            if (tt == 0) {
+                if (!last) strip_put_T<W>(PT[0], a, R, h);
+            } else {
+                strip_product<W, 0, SH::T, false>(PT[(tt + 1) & 1], a, c, i, h);
+                if (!last) strip_put_T<W>(PT[tt & 1], c, R, h);
+            }
+        }
+    }
+    __syncthreads();  // the block's output state is in place
+    if (!BWD && t < W) r[item * W + t] = (z[t] + xin[t]) - S[item * W + t];
+    if (jac) {
+        float* Ab = A + (BWD ? ((long long)b * G + (G - g)) : item) * W * W;
+        // the diagonal element R is column 8q + 4h + e with 8q + e = R - 4h
+        const int dk = R - 4 * h;
+#pragma unroll
+        for (int q = 0; q < SH::NQ; ++q) {
+            v4f x = skip == 1 ? a[q] : strip_quad<W>(c, q);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] += dk == 8 * q + e ? 1.f : 0.f;
+            *reinterpret_cast<v4f*>(Ab + R * W + 8 * q + 4 * h) = x;
+        }
+    }
+}
+
+template <int W, bool BWD>
+hipError_t launch_block_tile(const float* Wt, const float* bias, const float* z0, const float* S,
+                             const float* Gv, float* A, float* r, unsigned* red, int B, int G,
+                             int skip, int act, hipStream_t stream) {
+    hipLaunchKernelGGL((resnet_block_tile<W, BWD>), dim3((unsigned)((long long)B * G)),
+                       dim3(Tile2Shape<W>::NT), 0, stream, Wt, bias, z0, S, Gv, A, r, red, B, G,
+                       skip, act);
+    return hipGetLastError();
+}
+
 template <int W, bool BWD>
 hipError_t launch_block_wave(const float* Wt, const float* bias, const float* z0, const float* S,
                              const float* Gv, float* A, float* r, unsigned* red, int B, int G,
@@ -428,6 +527,12 @@ hipError_t launch_resnet_block_eval(const float* W, const float* bias, const flo
     if (w == 32)
         return launch_block_wave<32, false>(W, bias, z0, X, nullptr, A, r, red, B, G, skip, act,
                                             stream);
+    if (w == 64)
+        return launch_block_tile<64, false>(W, bias, z0, X, nullptr, A, r, red, B, G, skip, act,
+                                            stream);
+    if (w == 128)
+        return launch_block_tile<128, false>(W, bias, z0, X, nullptr, A, r, red, B, G, skip, act,
+                                             stream);
     const hipError_t e = allow_lds(resnet_block_eval_kernel, block_lds_bytes(w));
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(resnet_block_eval_kernel, dim3((unsigned)((long long)B * G)),
@@ -461,6 +566,12 @@ hipError_t launch_resnet_block_jac(const float* W, const float* z0, const float*
     if (w == 32)
         return launch_block_wave<32, true>(W, nullptr, z0, Z, Gv, A, rrev, nullptr, B, G, skip,
                                            act, stream);
+    if (w == 64)
+        return launch_block_tile<64, true>(W, nullptr, z0, Z, Gv, A, rrev, nullptr, B, G, skip,
+                                           act, stream);
+    if (w == 128)
+        return launch_block_tile<128, true>(W, nullptr, z0, Z, Gv, A, rrev, nullptr, B, G, skip,
+                                            act, stream);
     const hipError_t e = allow_lds(resnet_block_jac_kernel, block_lds_bytes(w));
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(resnet_block_jac_kernel, dim3((unsigned)((long long)B * G)),

@@ -1,0 +1,165 @@
+// Register strips of w x w blocks for the fp32 MFMA kernels (w = 32, 64,
+// 128): one wave per 32-row strip of a block.  A lane (i, h) of wave v holds
+// row R = 32 v + i at the columns 8q + 4h .. +3 (q = 0 .. W/8-1).  That is
+// the left operand of v_mfma_f32_32x32x2_f32 (k-step q, element e: column
+// 8q + 4h + e), read straight from memory, and also the layout in which the
+// MFMA leaves a strip of the product (tile tc, float4 qq at q = 4 tc + qq):
+// a product strip can be the left operand of the next product as it is.
+// Right operands sit in LDS transposed (XT[col][k], pitch W + 4), so that a
+// k-step of a 32-column tile is one 16-byte read per lane.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace deeppcr {
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+template <int W>
+struct Tile2Shape {
+    static constexpr int NWV = W / 32;  // waves, one 32-row strip each
+    static constexpr int NT = 64 * NWV;
+    static constexpr int PITCH = W + 4;
+    static constexpr int NQ = W / 8;  // k-steps of 8 (4 per lane half)
+    static constexpr int T = W / 32;  // 32-column tiles of a strip
+};
+
+template <int W>
+using StripA = v4f[Tile2Shape<W>::NQ];
+template <int W>
+using StripC = v16f[Tile2Shape<W>::T];
+
+template <int W, bool TRANS>
+__device__ __forceinline__ void strip_load(const float* blk, StripA<W>& a, int R, int h) {
+#pragma unroll
+    for (int q = 0; q < Tile2Shape<W>::NQ; ++q) {
+        if constexpr (!TRANS) {
+            a[q] = *reinterpret_cast<const v4f*>(blk + R * W + 8 * q + 4 * h);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) a[q][e] = blk[(8 * q + 4 * h + e) * W + R];
+        }
+    }
+}
+
+template <int W>
+__device__ __forceinline__ v4f strip_quad(const StripA<W>& a, int q) {
+    return a[q];
+}
+template <int W>
+__device__ __forceinline__ v4f strip_quad(const StripC<W>& c, int q) {
+    const v16f& x = c[q / 4];
+    const int o = 4 * (q % 4);
+    return v4f{x[o], x[o + 1], x[o + 2], x[o + 3]};
+}
+
+template <int W>
+__device__ __forceinline__ void strip_zero(StripC<W>& c) {
+#pragma unroll
+    for (int tc = 0; tc < Tile2Shape<W>::T; ++tc) c[tc] = v16f{};
+}
+
+// (strip of M) x for x in LDS; every lane of the row gets the sum.
+template <int W, class M>
+__device__ __forceinline__ float strip_matvec(const M& a, const float* x, int h) {
+    float part = 0.f;
+#pragma unroll
+    for (int q = 0; q < Tile2Shape<W>::NQ; ++q) {
+        const v4f xv = *reinterpret_cast<const v4f*>(x + 8 * q + 4 * h);
+        const v4f av = strip_quad<W>(a, q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) part = fmaf(av[e], xv[e], part);
+    }
+    return part + __shfl_xor(part, 32, 64);
+}
+
+// acc[0 .. NTC-1] = column tiles TC0 .. TC0+NTC-1 of (strip of M) X, X in
+// LDS transposed (XT[col][k], pitch PITCH): the right operand of k-step q for
+// one column tile is one 16-byte read, and all offsets fit the immediate
+// field of one base address.  With MV also returns (strip of M) x for the
+// vector x in LDS (every lane of the row gets the sum), from the left
+// operands as they pass (for accumulator strips this avoids copying the
+// whole strip out of the accumulation registers at once).
+template <int W, int TC0, int NTC, bool MV, class M>
+__device__ __forceinline__ float strip_product(const float* XT, const M& a, v16f (&acc)[NTC],
+                                               int i, int h, const float* x = nullptr) {
+    using S = Tile2Shape<W>;
+#pragma unroll
+    for (int tc = 0; tc < NTC; ++tc) acc[tc] = v16f{};
+    const float* xb = XT + (32 * TC0 + i) * S::PITCH + 4 * h;
+    v4f pv[2][NTC], xv[2];
+    float part = 0.f;
+#pragma unroll
+    for (int q = 0; q <= S::NQ; ++q) {
+        if (q < S::NQ) {
+#pragma unroll
+            for (int tc = 0; tc < NTC; ++tc)
+                pv[q & 1][tc] = *reinterpret_cast<const v4f*>(xb + 32 * tc * S::PITCH + 8 * q);
+            if constexpr (MV) xv[q & 1] = *reinterpret_cast<const v4f*>(x + 8 * q + 4 * h);
+        }
+        // keeps the operand reads of step q beside the MFMAs of step q-1
+        __builtin_amdgcn_sched_barrier(0);
+        if (q > 0) {
+            const int qb = (q - 1) & 1;
+            const v4f av = strip_quad<W>(a, q - 1);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int tc = 0; tc < NTC; ++tc)
+                    acc[tc] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[qb][tc][e], av[e], acc[tc],
+                                                                   0, 0, 0);
+            if constexpr (MV) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) part = fmaf(av[e], xv[qb][e], part);
+            }
+        }
+    }
+    if constexpr (MV) return part + __shfl_xor(part, 32, 64);
+    return 0.f;
+}
+
+// Stores column tiles TC0 .. TC0+NTC-1 of a product strip (row-major block
+// in global memory).
+template <int W, int TC0, int NTC>
+__device__ __forceinline__ void tiles_store(float* dst, const v16f (&acc)[NTC], int R, int h) {
+#pragma unroll
+    for (int tc = 0; tc < NTC; ++tc)
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+            const v16f& x = acc[tc];
+            *reinterpret_cast<v4f*>(dst + R * W + 32 * (TC0 + tc) + 8 * qq + 4 * h) =
+                v4f{x[4 * qq], x[4 * qq + 1], x[4 * qq + 2], x[4 * qq + 3]};
+        }
+}
+
+// A strip to a row-major block in global memory.
+template <int W, class M>
+__device__ __forceinline__ void strip_store(float* dst, const M& a, int R, int h) {
+#pragma unroll
+    for (int q = 0; q < Tile2Shape<W>::NQ; ++q)
+        *reinterpret_cast<v4f*>(dst + R * W + 8 * q + 4 * h) = strip_quad<W>(a, q);
+}
+
+// A strip to a transposed block in LDS (XT[col][row], pitch PITCH).  The
+// empty asm statements keep the writes single (not paired into two-offset
+// writes, whose short offsets would need a base register per pair of rows):
+// every offset then fits the immediate field of one base address.
+template <int W, class M>
+__device__ __forceinline__ void strip_put_T(float* XT, const M& a, int R, int h) {
+    using S = Tile2Shape<W>;
+    float* xb = XT + 4 * h * S::PITCH + R;
+#pragma unroll
+    for (int q = 0; q < S::NQ; ++q) {
+        const v4f x = strip_quad<W>(a, q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            xb[(8 * q + e) * S::PITCH] = x[e];
+            asm volatile("" ::: "memory");
+        }
+    }
+}
+
+}  // namespace
+}  // namespace deeppcr

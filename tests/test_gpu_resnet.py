@@ -46,7 +46,9 @@ RELU, TANH, SIG = R.ACT_RELU, R.ACT_TANH, R.ACT_SIGMOID
 FWD_CASES = [(16, 256, 4, 4, RELU), (16, 1024, 8, 4, RELU), (4, 64, 3, 4, TANH),
              (8, 40, 2, 2, SIG), (32, 96, 2, 3, TANH), (64, 32, 2, 4, RELU),
              (128, 16, 2, 4, TANH), (17, 30, 2, 5, RELU), (16, 4, 2, 4, RELU),
-             (16, 8, 2, 4, SIG), (3, 9, 2, 1, TANH), (100, 12, 2, 3, RELU), (1, 20, 3, 4, RELU)]
+             (16, 8, 2, 4, SIG), (3, 9, 2, 1, TANH), (100, 12, 2, 3, RELU), (1, 20, 3, 4, RELU),
+             (64, 96, 3, 3, SIG), (64, 40, 2, 1, TANH), (64, 256, 4, 4, RELU),
+             (128, 48, 2, 2, SIG), (128, 12, 3, 1, RELU)]
 
 
 @pytest.mark.parametrize("w,L,B,skip,act", FWD_CASES)
@@ -63,7 +65,7 @@ def test_resnet_forward(dev, w, L, B, skip, act):
     assert ok and abs(res.iters - k_ref) <= 1
 
 
-@pytest.mark.parametrize("w", [4, 16, 64])
+@pytest.mark.parametrize("w", [4, 16, 64, 128])
 def test_resnet_fixed_count_and_prefix_exactness(dev, w):
     """tol = 0 runs exactly max_iter solves; from a zero start, k solves make
     the first k blocks (and the rows computed from them) exact."""
