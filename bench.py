@@ -49,7 +49,14 @@ def make_step(wl, dev):
     d = synth.workload_inputs(wl)
     t = {k: torch.from_numpy(v).to(dev) for k, v in d.items()}
     B, L, w = wl.B, wl.L, wl.w
-    info = {"iters": None}
+    # marks: per step, events on the launch stream before the forward, between
+    # the passes and after the backward (the split of a forward + backward step)
+    info = {"iters": None, "marks": []}
+
+    def mark():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
     if wl.kind == "pcr":
         ws = torch.empty(deeppcr.workspace_bytes(deeppcr.OP_PCR, B, L, w), dtype=torch.uint8,
                          device=dev)
@@ -88,14 +95,17 @@ def make_step(wl, dev):
                     db=torch.empty((L, w), dtype=torch.float32, device=dev))
 
         def step():
+            e0 = mark()
             res = deeppcr.deeppcr_resnet_forward(t["W"], t["bias"], t["z0"], wl.skip, wl.act, Z,
                                                  tol=wl.tol, max_iter=wl.max_iter,
                                                  workspace=wsf)
             if res.status != deeppcr.OK:
                 raise RuntimeError(f"forward status {res.status}")
             info["iters"] = res.iters
+            e1 = mark()
             deeppcr.deeppcr_resnet_backward(t["W"], t["z0"], Z, t["G"], wl.skip, wl.act,
                                             workspace=wsb, **outs)
+            info["marks"].append((e0, e1, mark()))
         return step, info
 
     op_ws = {}
@@ -118,6 +128,7 @@ def make_step(wl, dev):
                 raise RuntimeError(f"forward status {res.status}")
 
     def step():
+        e0 = mark()
         if "fwd" in wl.passes:
             res = deeppcr.deeppcr_mlp_forward(t["W"], t["bias"], t["z0"], Z, layer=wl.layer,
                                               alpha=wl.alpha, tol=wl.tol, max_iter=wl.max_iter,
@@ -125,9 +136,11 @@ def make_step(wl, dev):
             if res.status != deeppcr.OK:
                 raise RuntimeError(f"forward status {res.status}")
             info["iters"] = res.iters
+        e1 = mark()
         if "bwd" in wl.passes:
             deeppcr.deeppcr_mlp_backward(t["W"], t["bias"], t["z0"], Z, t["G"], layer=wl.layer,
                                          alpha=wl.alpha, workspace=op_ws["bwd"], **outs)
+        info["marks"].append((e0, e1, mark()))
     return step, info
 
 
@@ -222,6 +235,7 @@ def main():
     deeppcr.profile_reset()
     deeppcr.profile_enable(True)
     torch.cuda.synchronize()
+    info["marks"].clear()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
@@ -273,6 +287,12 @@ def main():
         "config": cfg, "roofline": roof,
         "kernel_ms_per_step": {k: round(v["ms"] / args.steps, 4) for k, v in prof.items()},
     }
+    if "fwd" in wl.passes and "bwd" in wl.passes and info["marks"]:
+        # device time between the marks on the launch stream, per step
+        n = len(info["marks"])
+        out["pass_ms_per_step"] = {
+            "fwd": round(sum(a.elapsed_time(b) for a, b, _ in info["marks"]) / n, 4),
+            "bwd": round(sum(b.elapsed_time(c) for _, b, c in info["marks"]) / n, 4)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)
