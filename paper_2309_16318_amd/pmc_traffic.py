@@ -23,7 +23,9 @@ import hashlib
 import json
 import os
 
-KERNEL_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "pcr_level.hip")
+# the PCR level kernels and the register-strip helpers they are built from
+KERNEL_SOURCES = [os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", f)
+                  for f in ("pcr_level.hip", "strip.h")]
 
 
 def code_digest(text: str) -> str:
@@ -37,8 +39,11 @@ def code_digest(text: str) -> str:
 
 
 def kernel_source_sha256() -> str:
-    with open(KERNEL_SOURCE, encoding="utf-8") as f:
-        return code_digest(f.read())
+    text = ""
+    for fn in KERNEL_SOURCES:
+        with open(fn, encoding="utf-8") as f:
+            text += f.read() + "\n"
+    return code_digest(text)
 
 
 def _rows(d: str):
