@@ -329,12 +329,14 @@ Ws carve(void* workspace, const Layout& lo) {
     return ws;
 }
 
-// Pinned host copy of the reduction area for the per-iteration read-back.
+// Pinned host copy of the reduction area for the per-iteration read-back
+// (mapped, so that a kernel can also write it directly).
 unsigned* host_words() {
     thread_local unsigned* words = nullptr;
     if (!words) {
         void* p = nullptr;
-        if (hipHostMalloc(&p, kRedWords * sizeof(unsigned), hipHostMallocDefault) != hipSuccess)
+        if (hipHostMalloc(&p, kRedWords * sizeof(unsigned),
+                          hipHostMallocMapped | hipHostMallocPortable) != hipSuccess)
             return nullptr;
         words = (unsigned*)p;
     }
@@ -497,13 +499,15 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
 
     if (tiny_eligible(B, L, w)) {
         // one launch for the whole solve; reads W, bias, z0 (and Z_init), writes Z
+        // and its status record straight into the mapped host words
+        void* hwd = nullptr;
+        DEEPPCR_HIP(hipHostGetDevicePointer(&hwd, hw, 0));
         const double io = 4.0 * ((double)L * w * (w + 1) + B * w + 2.0 * B * L * w);
         hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, io, 0.0, st, [&] {
-            return launch_newton_tiny(W, bias, z0, Z, Z_init, B, L, w, layer, alpha, rule, ws.red,
-                                      st);
+            return launch_newton_tiny(W, bias, z0, Z, Z_init, B, L, w, layer, alpha, rule,
+                                      (unsigned*)hwd, st);
         });
         if (e != hipSuccess) return hip_fail(e, "newton_tiny");
-        DEEPPCR_HIP(copy_async(hw, ws.red, 3 * sizeof(unsigned), hipMemcpyDeviceToHost, st));
         DEEPPCR_HIP(host_wait(st));
         if (iters_out) *iters_out = (int)hw[1];
         if (measure_out) *measure_out = bits_to_float(hw[2]);
