@@ -258,6 +258,119 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
     if (t < w) db[(long long)l * w + t] = dbacc;
 }
 
+// The same sums for w = 16, 32, 64, 128, one workgroup per layer: thread
+// (ti, tj) of a 16 x 16 grid owns the (w/16) x (w/16) tile of dW_l at rows
+// ti w/16.. and columns tj w/16..; per staged batch row it reads its rows of
+// g and columns of the layer input from LDS once and forms their outer
+// product in registers (the index arithmetic is done once, outside the
+// batch loop).
+template <int W, bool PRE>
+__global__ __launch_bounds__(kThreads) void wgrad_tile_kernel(
+    const float* __restrict__ z0, const float* __restrict__ Z, const float* __restrict__ dscale,
+    const float* __restrict__ Lambda, float* __restrict__ dW, float* __restrict__ db, int B, int L,
+    int act) {
+    constexpr int RT = W / 16;  // rows and columns of the tile of a thread
+    const int l = blockIdx.x;
+    const int t = threadIdx.x;
+    const int i0 = (t >> 4) * RT, j0 = (t & 15) * RT;
+    __shared__ float g[kWgradBC][W];
+    __shared__ float zp[kWgradBC][W];
+    float acc[RT][RT];
+#pragma unroll
+    for (int a = 0; a < RT; ++a)
+#pragma unroll
+        for (int c = 0; c < RT; ++c) acc[a][c] = 0.f;
+    float dbacc = 0.f;
+    for (int b0 = 0; b0 < B; b0 += kWgradBC) {
+        const int nb = min(kWgradBC, B - b0);
+        for (int idx = t; idx < nb * W; idx += kThreads) {
+            const int bb = idx / W, i = idx % W;
+            const long long rowi = ((long long)(b0 + bb) * L + l) * W + i;
+            const float zin = (l == 0) ? z0[(long long)(b0 + bb) * W + i] : Z[rowi - W];
+            if constexpr (PRE) {
+                float d;
+                g[bb][i] = Lambda[rowi];
+                zp[bb][i] = activate(2 * act, zin, &d);
+            } else {
+                g[bb][i] = dscale[rowi] * Lambda[rowi];
+                zp[bb][i] = zin;
+            }
+        }
+        __syncthreads();
+        for (int bb = 0; bb < nb; ++bb) {
+            float gi[RT], zj[RT];
+#pragma unroll
+            for (int a = 0; a < RT; ++a) {
+                gi[a] = g[bb][i0 + a];
+                zj[a] = zp[bb][j0 + a];
+            }
+#pragma unroll
+            for (int a = 0; a < RT; ++a)
+#pragma unroll
+                for (int c = 0; c < RT; ++c) acc[a][c] = fmaf(gi[a], zj[c], acc[a][c]);
+        }
+        if (t < W)
+            for (int bb = 0; bb < nb; ++bb) dbacc += g[bb][t];
+        __syncthreads();
+    }
+    float* dWl = dW + (long long)l * W * W;
+#pragma unroll
+    for (int a = 0; a < RT; ++a)
+#pragma unroll
+        for (int c = 0; c < RT; ++c) dWl[(i0 + a) * W + j0 + c] = acc[a][c];
+    if (t < W) db[(long long)l * W + t] = dbacc;
+}
+
+// Backward assembly without the blocks (the first PCR pass forms them from
+// the weights): per (b, l) the scale c d_l (d = sigma'(W_l Z_{l-1} + b_l))
+// and the reversed right-hand side, as layer_eval_vec<W, true> writes them.
+// One workgroup per layer, so that W_l is read once for all systems: lane
+// group i (256/w lanes) holds row i of W_l, w^2/256 columns per lane, and
+// forms the row's sums for every staged batch row.
+template <int W>
+__global__ __launch_bounds__(kThreads) void bwd_scale_kernel(
+    const float* __restrict__ W_, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ Z, const float* __restrict__ G, float* __restrict__ r,
+    float* __restrict__ dscale, int B, int L, int layer, float alpha) {
+    constexpr int LPR = kThreads / W;  // lanes per row of W_l
+    constexpr int CPL = W / LPR;       // columns per lane
+    const int l = blockIdx.x;
+    const int t = threadIdx.x;
+    const int i = t / LPR, c0 = (t % LPR) * CPL;
+    __shared__ float zs[kWgradBC][W];
+    float wr[CPL];
+    const float* Wrow = W_ + ((long long)l * W + i) * W + c0;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) wr[c] = Wrow[c];
+    const float bi = bias[(long long)l * W + i];
+    const bool res = layer_residual(layer);
+    const int mr = L - 1 - l;  // reversed row of layer l
+    for (int b0 = 0; b0 < B; b0 += kWgradBC) {
+        const int nb = min(kWgradBC, B - b0);
+        for (int idx = t; idx < nb * W; idx += kThreads) {
+            const int bb = idx / W, k = idx % W;
+            const long long b = b0 + bb;
+            zs[bb][k] = (l == 0) ? z0[b * W + k] : Z[(b * L + l - 1) * W + k];
+        }
+        __syncthreads();
+        for (int bb = 0; bb < nb; ++bb) {
+            float part = 0.f;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) part = fmaf(wr[c], zs[bb][c0 + c], part);
+#pragma unroll
+            for (int off = 1; off < LPR; off <<= 1) part += __shfl_xor(part, off, 64);
+            if (t % LPR == 0) {
+                float d;
+                activate(layer, part + bi, &d);
+                const long long b = b0 + bb;
+                dscale[(b * L + l) * W + i] = res ? alpha * d : d;
+                r[(b * L + mr) * W + i] = (mr == 0) ? G[b * W + i] : 0.f;
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // r = F - Z over n floats, max |r| bits into the kRedF slots of red.
 __global__ __launch_bounds__(kThreads) void residual_kernel(const float* __restrict__ F,
                                                            const float* __restrict__ Z,
@@ -438,6 +551,15 @@ hipError_t launch_backward_assemble(const float* W, const float* bias, const flo
     if (small_width(w))
         return launch_eval_small(true, W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, w,
                                  layer, alpha, stream);
+    if (A == nullptr && (w == 32 || w == 64 || w == 128)) {
+        // no blocks to write: one workgroup per layer
+        switch (w) {
+            case 32: hipLaunchKernelGGL((bwd_scale_kernel<32>), dim3((unsigned)L), dim3(kThreads), 0, stream, W, bias, z0, Z, G, rrev, dscale, B, L, layer, alpha); break;
+            case 64: hipLaunchKernelGGL((bwd_scale_kernel<64>), dim3((unsigned)L), dim3(kThreads), 0, stream, W, bias, z0, Z, G, rrev, dscale, B, L, layer, alpha); break;
+            default: hipLaunchKernelGGL((bwd_scale_kernel<128>), dim3((unsigned)L), dim3(kThreads), 0, stream, W, bias, z0, Z, G, rrev, dscale, B, L, layer, alpha); break;
+        }
+        return hipGetLastError();
+    }
     switch (w) {
         case 16: return launch_eval_vec<16, true>(W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, layer, alpha, stream);
         case 32: return launch_eval_vec<32, true>(W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, layer, alpha, stream);
@@ -458,19 +580,30 @@ hipError_t launch_dz0(const float* W, const float* dscale, const float* Lambda, 
     return hipGetLastError();
 }
 
+template <bool PRE>
+hipError_t launch_wgrad_any(const float* z0, const float* Z, const float* dscale,
+                            const float* Lambda, float* dW, float* db, int B, int L, int w,
+                            int act, hipStream_t stream) {
+    const dim3 grid((unsigned)L), blk(kThreads);
+    switch (w) {
+        case 16: hipLaunchKernelGGL((wgrad_tile_kernel<16, PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, act); break;
+        case 32: hipLaunchKernelGGL((wgrad_tile_kernel<32, PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, act); break;
+        case 64: hipLaunchKernelGGL((wgrad_tile_kernel<64, PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, act); break;
+        case 128: hipLaunchKernelGGL((wgrad_tile_kernel<128, PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, act); break;
+        default: hipLaunchKernelGGL((wgrad_kernel<PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, w, act); break;
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
                         const float* Lambda, float* dW, float* db, int B, int L, int w,
                         hipStream_t stream) {
-    hipLaunchKernelGGL(wgrad_kernel<false>, dim3((unsigned)L), dim3(kThreads), 0, stream, z0, Z,
-                       dscale, Lambda, dW, db, B, L, w, 0);
-    return hipGetLastError();
+    return launch_wgrad_any<false>(z0, Z, dscale, Lambda, dW, db, B, L, w, 0, stream);
 }
 
 hipError_t launch_wgrad_pre(const float* z0, const float* Z, const float* Lambda, float* dW,
                             float* db, int B, int L, int w, int act, hipStream_t stream) {
-    hipLaunchKernelGGL(wgrad_kernel<true>, dim3((unsigned)L), dim3(kThreads), 0, stream, z0, Z,
-                       nullptr, Lambda, dW, db, B, L, w, act);
-    return hipGetLastError();
+    return launch_wgrad_any<true>(z0, Z, nullptr, Lambda, dW, db, B, L, w, act, stream);
 }
 
 hipError_t launch_residual(const float* F, const float* Z, float* r, long long n, unsigned* red,
