@@ -435,15 +435,16 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
         k += pair ? 2 : 1;
     }
     if (kt > 0) {
-        // the last kt levels in one pass: the solution to ws r buffer p % 2
+        // the last kt levels in one pass, which also applies the update
+        // Z += x and reduces the convergence maxima (the iterate is read and
+        // written instead of the solution being written)
         double bytes, flops;
         tail_work(B, L, w, kt, &bytes, &flops);
-        const VecDst xo{ws.r[p & 1], ld, (long long)w};
-        hipError_t e = timed(DEEPPCR_KCLASS_PCR_TAIL, bytes, flops, st, [&] {
-            return launch_pcr_level_tail(Ain, rin, xo, B, L, w, kt, st);
+        bytes += 4.0 * B * L * w;
+        const VecDst zo{na.Z, ld, (long long)w};
+        return timed(DEEPPCR_KCLASS_PCR_TAIL, bytes, flops, st, [&] {
+            return launch_pcr_level_tail(Ain, rin, zo, B, L, w, kt, st, na.red);
         });
-        if (e != hipSuccess) return e;
-        rin = VecSrc{xo.base, xo.bstride, xo.rstride};
     }
     if (!upd) {
         // the last pass wrote the solution to the ws r buffer rin reads

@@ -163,8 +163,11 @@ int tail_levels(int B, int L, int w, int first);
 // The last kt = tail_levels(...) levels of a solve in one pass that
 // writes no operator: the solution goes to rout.  Ain holds the operators of
 // the level before (rows l >= s, s = 2^(levels - kt)), not transposed.
+// With red, rout is the Newton iterate instead: the solution is added to it
+// and max |x|, max |Z + x| are reduced into the kRedDZ, kRedZ slots of red.
 hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
-                                 int B, int L, int w, int kt, hipStream_t stream);
+                                 int B, int L, int w, int kt, hipStream_t stream,
+                                 unsigned* red = nullptr);
 
 // The last two levels of a solve (strides s, 2s with 4s >= L) in one pass
 // without operator products (mat-vecs only), for the widths last_pair_width

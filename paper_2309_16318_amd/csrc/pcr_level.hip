@@ -1356,10 +1356,13 @@ __device__ __forceinline__ void tail_product(const float* const (&col)[NTC], con
 // What the r chain reads (update terms of V_m) is next overwritten by
 // element m+2, after the barrier of element m+1, which every wave reaches
 // after its r chain of element m.
-template <int W, int KT>
+// UPD (the last pass of a Newton iteration): rout is the iterate, which each
+// solution row is added to, and max |x| and max |Z + x| are reduced into the
+// kRedDZ and kRedZ slots of red (the update kernel's work, done in place).
+template <int W, int KT, bool UPD>
 __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSrc Ain, VecSrc rin,
-                                                                       VecDst rout, int L,
-                                                                       int s) {
+                                                                       VecDst rout, int L, int s,
+                                                                       unsigned* red) {
     using S = Tile2Shape<W>;
     using T = TailShape<W, KT>;
     constexpr int NB = T::NB, D = T::D;
@@ -1376,6 +1379,7 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
     const float* ab = Ain.base + b * Ain.bstride;
     const float* rb = rin.base + b * rin.bstride;
     float* ob = rout.base + b * rout.bstride;
+    unsigned mx = 0u, mz = 0u;  // UPD: max |x|, max |Z + x| (bit patterns)
     // lane i's column of tile 0 is r column lv_i (or no r column: -1)
     const int lv_i = ((i + 1) & i) == 0 && i + 1 < (1 << KT) ? 31 - __builtin_clz(i + 1) : -1;
 
@@ -1387,16 +1391,21 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
     // would merge.
     StripA<W> a[NB];
     float rq[NB][RPL];
+    float zq[UPD ? NB : 1][RPL];  // UPD: the iterate's rows, in the same ring
     v16f acc[T::TPW];
-    auto load_r = [&](float (&dst)[RPL], long long row) {
+    auto load_r = [&](int u, long long row) {
 #pragma unroll
-        for (int rr = 0; rr < RPL; ++rr) dst[rr] = rb[row * rin.rstride + ((lane + 64 * rr) & (W - 1))];
+        for (int rr = 0; rr < RPL; ++rr) {
+            const int k = (lane + 64 * rr) & (W - 1);
+            rq[u][rr] = rb[row * rin.rstride + k];
+            if constexpr (UPD) zq[u][rr] = ob[row * rout.rstride + k];
+        }
     };
 #pragma unroll
     for (int j = 0; j < D; ++j) {
         const long long lj = c + (long long)min(j, count) * s;
         if (j >= 1) strip_load<W, false>(ab + lj * Ain.rstride, a[j], R, h);
-        load_r(rq[j], lj);
+        load_r(j, lj);
     }
     auto element = [&](int m, auto U) {
         constexpr int u = decltype(U)::value;  // m % NB
@@ -1407,7 +1416,7 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
         {
             const long long ln = c + (long long)min(m + D, count) * s;
             strip_load<W, false>(ab + ln * Ain.rstride, a[un], R, h);
-            load_r(rq[un], ln);
+            load_r(un, ln);
         }
         if (m >= 1) {
             const float* col[T::TPW];
@@ -1455,7 +1464,17 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
                         RC[wv][lv][k] = r;  // r^lv_m
                         r += m >= (1 << lv) ? up[lv] : 0.f;
                     }
-                    if (wv == 0) ob[l * rout.rstride + k] = r;
+                    if (wv == 0) {
+                        float* o = ob + l * rout.rstride + k;
+                        if constexpr (UPD) {
+                            const float z = zq[u][rr] + r;
+                            *o = z;
+                            mx = max(mx, __float_as_uint(fabsf(r)));
+                            mz = max(mz, __float_as_uint(fabsf(z)));
+                        } else {
+                            *o = r;
+                        }
+                    }
                 }
             }
         }
@@ -1467,6 +1486,19 @@ __global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSr
             if (m <= count) element(m, U);
         };
         unroll_each<0, NB>(trip);
+    }
+    if constexpr (UPD) {
+        if (wv == 0) {
+            for (int off = 32; off > 0; off >>= 1) {
+                mx = max(mx, (unsigned)__shfl_xor((int)mx, off, 64));
+                mz = max(mz, (unsigned)__shfl_xor((int)mz, off, 64));
+            }
+            if (lane == 0) {
+                const int slot = blockIdx.x % kRedShards;
+                atomicMax(red + kRedDZ + slot, mx);
+                atomicMax(red + kRedZ + slot, mz);
+            }
+        }
     }
 }
 
@@ -1954,15 +1986,24 @@ int tail_levels(int B, int L, int w, int first) {
 }
 
 hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
-                                 int B, int L, int w, int kt, hipStream_t stream) {
+                                 int B, int L, int w, int kt, hipStream_t stream,
+                                 unsigned* red) {
     // KT = 5 serves 3 to 5 levels (one 32-column tile; the levels above
     // the chain length never update, since m < 2^lv there)
     const int s = 1 << (num_levels_of(L) - kt);
     const dim3 grid((unsigned)((long long)B * s));
     if (Ain.trans) return hipErrorInvalidValue;
-#define DEEPPCR_TAIL(WW, KK)                                                             \
-    hipLaunchKernelGGL((pcr_level_tail<WW, KK>), grid, dim3((TailShape<WW, KK>::NT)), 0, \
-                       stream, Ain, rin, rout, L, s)
+#define DEEPPCR_TAIL(WW, KK)                                                                      \
+    do {                                                                                          \
+        if (red)                                                                                  \
+            hipLaunchKernelGGL((pcr_level_tail<WW, KK, true>), grid,                              \
+                               dim3((TailShape<WW, KK>::NT)), 0, stream, Ain, rin, rout, L, s,    \
+                               red);                                                              \
+        else                                                                                      \
+            hipLaunchKernelGGL((pcr_level_tail<WW, KK, false>), grid,                             \
+                               dim3((TailShape<WW, KK>::NT)), 0, stream, Ain, rin, rout, L, s,    \
+                               red);                                                              \
+    } while (0)
     if (w == 32) {
         switch (kt) {
             case 3: DEEPPCR_TAIL(32, 5); break;
