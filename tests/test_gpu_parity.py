@@ -254,6 +254,22 @@ def test_forward_reports_non_finite(dev):
     assert res.status == deeppcr.ENONFINITE and res.iters == 1
 
 
+# The same reports from the multi-kernel paths: the fused last level (w = 16),
+# the update kernel (w = 64, one workgroup row per level) and the tail pass
+# that applies the update itself (w = 32, 64, 128 with enough chains).
+@pytest.mark.parametrize("w,L,B", [(16, 100, 3), (64, 40, 2), (32, 130, 64), (64, 300, 8),
+                                   (128, 203, 16)])
+def test_forward_status_reports_every_path(dev, w, L, B):
+    _say(f"forward status reports w={w} L={L} B={B}")
+    d = dict(synth.mlp_inputs(B, L, w, seed=1700 + w + L))
+    res = _forward(d, dev, 0, 1.0, tol=1e-5, max_iter=1)
+    assert res.status == deeppcr.ENOCONV and res.iters == 1
+    d["bias"] = d["bias"].copy()
+    d["bias"][L // 2, 1] = np.nan
+    res = _forward(d, dev, 0, 1.0)
+    assert res.status == deeppcr.ENONFINITE and res.iters == 1
+
+
 def test_forward_deterministic(dev):
     d = synth.mlp_inputs(8, 64, 32, seed=12)
     a = h(_forward(d, dev, 1, 0.1).Z)
