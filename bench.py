@@ -63,8 +63,11 @@ def make_step(wl, dev):
         x = torch.empty_like(t["r"])
 
         def step():
+            e0 = mark()
             deeppcr.pcr_solve_block_bidiag(t["J"], t["r"], x, transpose=wl.transpose,
                                            workspace=ws)
+            e1 = mark()
+            info["marks"].append((e0, e1, e1))
         return step, info
 
     if wl.kind == "diffusion":
@@ -76,11 +79,14 @@ def make_step(wl, dev):
                          device=dev)
 
         def step():
+            e0 = mark()
             res = generic.newton_generic(step_fn, jac_fn, t["zT"], L, tol=wl.tol,
                                          max_iter=wl.max_iter, workspace=ws)
             if res.status != deeppcr.OK:
                 raise RuntimeError(f"sampler status {res.status}")
             info["iters"] = res.iters
+            e1 = mark()
+            info["marks"].append((e0, e1, e1))
         return step, info
 
     if wl.kind == "resnet":
@@ -287,6 +293,11 @@ def main():
         "config": cfg, "roofline": roof,
         "kernel_ms_per_step": {k: round(v["ms"] / args.steps, 4) for k, v in prof.items()},
     }
+    if info["marks"]:
+        # device time of each step (first to last mark on the launch stream)
+        per = sorted(a.elapsed_time(c) for a, _, c in info["marks"])
+        out["step_ms_min"] = round(per[0], 4)
+        out["step_ms_median"] = round(per[len(per) // 2], 4)
     if "fwd" in wl.passes and "bwd" in wl.passes and info["marks"]:
         # device time between the marks on the launch stream, per step
         n = len(info["marks"])

@@ -498,6 +498,96 @@ hipError_t launch_block_tile(const float* Wt, const float* bias, const float* z0
     return hipGetLastError();
 }
 
+// ---- one wave per (system, block) for the state expansion and the in-block
+// adjoints, w = 16, 32, 64: lane t < w owns element t, four blocks per
+// workgroup, wave-level barriers only.  Same work as resnet_expand_kernel
+// and resnet_intra_adjoint_kernel.
+template <int W>
+__global__ __launch_bounds__(256) void resnet_expand_wave(
+    const float* __restrict__ Wt, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ X, float* __restrict__ Z, int B, int G, int skip, int act) {
+    __shared__ float z_all[4][W], sg_all[4][W];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const long long item = (long long)blockIdx.x * 4 + wv;  // b * G + g
+    if (item >= (long long)B * G) return;                   // whole wave
+    const int g = (int)(item % G);
+    const int b = (int)(item / G);
+    float* z = z_all[wv];
+    float* sg = sg_all[wv];
+    const long long L = (long long)G * skip;
+    float* Zb = Z + (long long)b * L * W;
+    const float* xp = (g == 0) ? z0 + (long long)b * W : X + (item - 1) * W;
+    if (lane < W) z[lane] = xp[lane];
+    for (int tt = 0; tt + 1 < skip; ++tt) {
+        const long long j = (long long)g * skip + tt;
+        wave_sync();
+        if (lane < W) {
+            float d;
+            sg[lane] = act_fn(act, z[lane], &d);
+        }
+        wave_sync();
+        if (lane < W) {
+            const float* wr = Wt + (j * W + lane) * W;
+            float a = 0.f;
+#pragma unroll
+            for (int k = 0; k < W; ++k) a = fmaf(wr[k], sg[k], a);
+            a += bias[j * W + lane];
+            z[lane] = a;  // only lane t reads z[t] before the next barrier
+            Zb[j * W + lane] = a;
+        }
+    }
+    if (lane < W) Zb[((long long)g * skip + skip - 1) * W + lane] = X[item * W + lane];
+}
+
+template <int W>
+__global__ __launch_bounds__(256) void resnet_intra_adjoint_wave(
+    const float* __restrict__ Wt, const float* __restrict__ z0, const float* __restrict__ Z,
+    const float* __restrict__ mu, float* __restrict__ Lambda, float* __restrict__ dz0, int B,
+    int G, int skip, int act) {
+    __shared__ float lam_all[4][W];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const long long item = (long long)blockIdx.x * 4 + wv;  // b * G + g
+    if (item >= (long long)B * G) return;                   // whole wave
+    const int g = (int)(item % G);
+    const int b = (int)(item / G);
+    float* lam = lam_all[wv];
+    const long long L = (long long)G * skip;
+    const float* Zb = Z + (long long)b * L * W;
+    float* Lb = Lambda + (long long)b * L * W;
+    const long long jl = (long long)g * skip + skip - 1;
+    float mu_t = 0.f;
+    if (lane < W) {
+        mu_t = mu[item * W + lane];
+        lam[lane] = mu_t;
+        Lb[jl * W + lane] = mu_t;
+    }
+    const int lo = (g == 0) ? 0 : 1;  // block 0 also goes through layer 0 into z0
+    for (int tt = skip - 1; tt >= lo; --tt) {
+        const long long j = (long long)g * skip + tt;
+        const float* Wj = Wt + j * W * W;
+        wave_sync();
+        float v = 0.f;
+        if (lane < W) {
+            const float zin = (j == 0) ? z0[(long long)b * W + lane] : Zb[(j - 1) * W + lane];
+            float d;
+            act_fn(act, zin, &d);
+            float sum = 0.f;
+#pragma unroll
+            for (int k = 0; k < W; ++k) sum = fmaf(Wj[k * W + lane], lam[k], sum);
+            v = d * sum;
+        }
+        wave_sync();
+        if (lane < W) {
+            if (j >= 1) {
+                lam[lane] = v;
+                Lb[(j - 1) * W + lane] = v;
+            } else {
+                dz0[(long long)b * W + lane] = v + mu_t;
+            }
+        }
+    }
+}
+
 template <int W, bool BWD>
 hipError_t launch_block_wave(const float* Wt, const float* bias, const float* z0, const float* S,
                              const float* Gv, float* A, float* r, unsigned* red, int B, int G,
@@ -552,6 +642,13 @@ hipError_t launch_resnet_initial_guess(const float* W, const float* bias, const 
 hipError_t launch_resnet_expand(const float* W, const float* bias, const float* z0,
                                 const float* X, float* Z, int B, int G, int w, int skip, int act,
                                 hipStream_t stream) {
+    const dim3 g4((unsigned)(((long long)B * G + 3) / 4)), b4(256);
+    switch (w) {
+        case 16: hipLaunchKernelGGL((resnet_expand_wave<16>), g4, b4, 0, stream, W, bias, z0, X, Z, B, G, skip, act); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((resnet_expand_wave<32>), g4, b4, 0, stream, W, bias, z0, X, Z, B, G, skip, act); return hipGetLastError();
+        case 64: hipLaunchKernelGGL((resnet_expand_wave<64>), g4, b4, 0, stream, W, bias, z0, X, Z, B, G, skip, act); return hipGetLastError();
+        default: break;
+    }
     hipLaunchKernelGGL(resnet_expand_kernel, dim3((unsigned)((long long)B * G)), dim3(kThreads),
                        0, stream, W, bias, z0, X, Z, G, w, skip, act);
     return hipGetLastError();
@@ -583,6 +680,13 @@ hipError_t launch_resnet_block_jac(const float* W, const float* z0, const float*
 hipError_t launch_resnet_intra_adjoint(const float* W, const float* z0, const float* Z,
                                        const float* mu, float* Lambda, float* dz0, int B, int G,
                                        int w, int skip, int act, hipStream_t stream) {
+    const dim3 g4((unsigned)(((long long)B * G + 3) / 4)), b4(256);
+    switch (w) {
+        case 16: hipLaunchKernelGGL((resnet_intra_adjoint_wave<16>), g4, b4, 0, stream, W, z0, Z, mu, Lambda, dz0, B, G, skip, act); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((resnet_intra_adjoint_wave<32>), g4, b4, 0, stream, W, z0, Z, mu, Lambda, dz0, B, G, skip, act); return hipGetLastError();
+        case 64: hipLaunchKernelGGL((resnet_intra_adjoint_wave<64>), g4, b4, 0, stream, W, z0, Z, mu, Lambda, dz0, B, G, skip, act); return hipGetLastError();
+        default: break;
+    }
     hipLaunchKernelGGL(resnet_intra_adjoint_kernel, dim3((unsigned)((long long)B * G)),
                        dim3(kThreads), 0, stream, W, z0, Z, mu, Lambda, dz0, G, w, skip, act);
     return hipGetLastError();
