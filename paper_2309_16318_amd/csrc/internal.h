@@ -114,9 +114,9 @@ struct NewtonArgs {
 bool fused_newton_levels(int w);
 bool layer_first_level(int w);
 
-// Number of PCR levels launch_first_level_fwd runs (1, or 2 for w = 32, 64,
-// 128 when the solve has two levels or more and two_level accepts the
-// shape).
+// Number of PCR levels launch_first_level_fwd runs (1, or 2 for w = 64, 128
+// when the solve has two levels or more and two_level accepts the shape, and
+// for w = 32 from B L >= 2048 chain elements).
 int first_level_count(int B, int L, int w);
 
 // First level (s = 1) of the Newton linear solve with the layers, Jacobian

@@ -2037,8 +2037,15 @@ hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const V
 
 bool fused_newton_levels(int w) { return w == 16 || w == 32; }
 
+// The first two levels in one tile pass with the layers: w = 64, 128 where
+// two_level pairs them; w = 32 from B L >= 2048 chain elements (below, the
+// one-row segments of the wave kernel's first level keep more CUs busy: the
+// batch-1 sweep measured the pair 4-20% slower up to L = 1024 and 10-15%
+// faster from L = 2048).
 int first_level_count(int B, int L, int w) {
-    return (w == 32 || w == 64 || w == 128) && L > 2 && two_level(B, L, w) ? 2 : 1;
+    if (L <= 2 || !two_level(B, L, w)) return 1;
+    if (w == 64 || w == 128) return 2;
+    return w == 32 && (long long)B * L >= 2048 ? 2 : 1;
 }
 bool layer_first_level(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
 
