@@ -7,6 +7,8 @@
 // per layer (the shape of an eager framework's layer loop).
 #include "internal.h"
 
+#include <type_traits>
+
 namespace deeppcr {
 namespace {
 
@@ -209,11 +211,371 @@ __global__ __launch_bounds__(kThreads) void resnet_seq_backward_kernel(
     }
 }
 
+// ---- w = 16, 32, 64, 128: the weights streamed ahead of the walk -----------
+// The layers' weights do not depend on the state, so each w x w block is
+// requested NB - 1 layers before its layer into a ring of register slots
+// (every thread a w^2/256 share, slot k % NB for the walk's k-th layer) and
+// moved into one of two LDS buffers at the end of the layer before its own;
+// a layer's mat-vecs then read LDS only.  The state rows a layer reads
+// (backward: Z_{l-1}) come through the same ring.  Requests past the walk's
+// end are clamped to its last layer and never used, so that every thread
+// issues the same loads on every layer.
+
+template <int I, int N, class F>
+__device__ __forceinline__ void each_slot(F& f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        each_slot<I + 1, N>(f);
+    }
+}
+
+template <int W>
+struct Stream {
+    static constexpr int PER = W * W / kThreads;  // floats of a block per thread
+    static constexpr int NB = W <= 32 ? 8 : W == 64 ? 4 : 2;
+};
+
+// step(k, U) for k = 0 .. count-1, U = integral_constant<k % NB>.  Whole
+// trips of NB steps run unguarded, so that the compiler sees every step's
+// loads issued and can wait for just the one it needs; only the last partial
+// trip is guarded.
+template <int NB, class F>
+__device__ __forceinline__ void walk(int count, F& step) {
+    int k0 = 0;
+    for (; k0 + NB <= count; k0 += NB) {
+        auto trip = [&](auto U) { step(k0 + decltype(U)::value, U); };
+        each_slot<0, NB>(trip);
+    }
+    auto rest = [&](auto U) {
+        const int k = k0 + decltype(U)::value;
+        if (k < count) step(k, U);
+    };
+    each_slot<0, NB>(rest);
+}
+
+template <int W>
+__device__ __forceinline__ void block_to_regs(const float* __restrict__ blk,
+                                              float (&r)[Stream<W>::PER]) {
+#pragma unroll
+    for (int p = 0; p < Stream<W>::PER; ++p) r[p] = blk[threadIdx.x + kThreads * p];
+}
+
+// The LDS copy has rows of pitch w + 1, so that the lanes of a row-wise dot
+// product (rows i, i + 1, ... at the same column) fall into different banks.
+template <int W>
+__device__ __forceinline__ void regs_to_lds(const float (&r)[Stream<W>::PER], float* lds) {
+#pragma unroll
+    for (int p = 0; p < Stream<W>::PER; ++p) {
+        const int idx = threadIdx.x + kThreads * p;
+        lds[(idx / W) * (W + 1) + idx % W] = r[p];
+    }
+}
+
+// rows_dot / cols_dot on the padded LDS copy, four partial sums per lane.
+template <int W>
+__device__ __forceinline__ void rows_dot_p(const float* M, const float* v, float* out) {
+    const RowMap m = row_map(W);
+    const int t = threadIdx.x;
+    const int sub = t % m.tpr;
+    for (int i0 = 0; i0 < W; i0 += m.rows_per_pass) {
+        const int i = i0 + t / m.tpr;
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        if (i < W)
+            for (int c = 0; c < m.cols; ++c) {
+                const int j = sub + c * m.tpr;
+                if (j < W) acc[c & 3] = fmaf(M[i * (W + 1) + j], v[j], acc[c & 3]);
+            }
+        float sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+        for (int off = 1; off < m.tpr; off <<= 1) sum += __shfl_xor(sum, off, 64);
+        if (i < W && sub == 0) out[i] = sum;
+    }
+}
+
+template <int W>
+__device__ __forceinline__ void cols_dot_p(const float* M, const float* g, float* out) {
+    const RowMap m = row_map(W);
+    const int t = threadIdx.x;
+    const int sub = t % m.tpr;
+    for (int j0 = 0; j0 < W; j0 += m.rows_per_pass) {
+        const int j = j0 + t / m.tpr;
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        if (j < W)
+            for (int c = 0; c < m.cols; ++c) {
+                const int i = sub + c * m.tpr;
+                if (i < W) acc[c & 3] = fmaf(M[i * (W + 1) + j], g[i], acc[c & 3]);
+            }
+        float sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+        for (int off = 1; off < m.tpr; off <<= 1) sum += __shfl_xor(sum, off, 64);
+        if (j < W && sub == 0) out[j] = sum;
+    }
+}
+
+// As seq_forward_kernel (MLP layers), layers l0 .. l1-1.
+template <int W>
+__global__ __launch_bounds__(kThreads) void seq_forward_stream(
+    const float* __restrict__ Wt, const float* __restrict__ bias, const float* __restrict__ z0,
+    float* __restrict__ Z, int L, int layer, float alpha, int l0, int l1) {
+    using SS = Stream<W>;
+    constexpr int NB = SS::NB;
+    __shared__ float Ws[2][W * (W + 1)];
+    __shared__ float z[W], a[W];
+    const int b = blockIdx.x, t = threadIdx.x;
+    const bool res = layer_residual(layer);
+    const int count = l1 - l0;
+    if (count <= 0) return;  // uniform over the workgroup
+    const int tw = t & (W - 1);
+    float rg[NB][SS::PER], bq[NB];  // blocks and bias rows, slot k % NB
+    auto lay = [&](int k) { return l0 + min(k, count - 1); };
+    auto blk = [&](int k) { return Wt + (long long)lay(k) * W * W; };
+    auto bia = [&](int k) { return bias[(long long)lay(k) * W + tw]; };
+    block_to_regs<W>(blk(0), rg[0]);
+    regs_to_lds<W>(rg[0], Ws[0]);
+    auto pro = [&](auto J) {
+        constexpr int j = decltype(J)::value;
+        if constexpr (j >= 1) block_to_regs<W>(blk(j), rg[j]);
+        bq[j] = bia(j);
+    };
+    each_slot<0, NB>(pro);
+    for (int i = t; i < W; i += kThreads)
+        z[i] = (l0 == 0) ? z0[(long long)b * W + i] : Z[((long long)b * L + l0 - 1) * W + i];
+    __syncthreads();
+    auto step = [&](int k, auto U) {
+        constexpr int u = decltype(U)::value;
+        const int l = l0 + k;
+        const float bl = bq[u];
+        block_to_regs<W>(blk(k + NB), rg[u]);
+        bq[u] = bia(k + NB);
+        rows_dot_p<W>(Ws[k & 1], z, a);
+        __syncthreads();
+        if (t < W) {
+            float d;
+            const float y = activate(layer, a[t] + bl, &d);
+            const float f = res ? fmaf(alpha, y, z[t]) : y;
+            z[t] = f;
+            Z[((long long)b * L + l) * W + t] = f;
+        }
+        regs_to_lds<W>(rg[(u + 1) % NB], Ws[(k + 1) & 1]);
+        __syncthreads();
+    };
+    walk<NB>(count, step);
+}
+
+// As seq_backward_kernel, layers l1-1 down to l0.
+template <int W>
+__global__ __launch_bounds__(kThreads) void seq_backward_stream(
+    const float* __restrict__ Wt, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ Z, const float* __restrict__ G, float* __restrict__ Lambda,
+    float* __restrict__ dz0, int L, int layer, float alpha, int l0, int l1) {
+    using SS = Stream<W>;
+    constexpr int NB = SS::NB;
+    __shared__ float Ws[2][W * (W + 1)];
+    __shared__ float lam[W], zp[W], a[W], g[W], nl[W];
+    const int b = blockIdx.x, t = threadIdx.x;
+    const bool res = layer_residual(layer);
+    const int count = l1 - l0;
+    if (count <= 0) return;  // uniform over the workgroup
+    const int tw = t & (W - 1);
+    float rg[NB][SS::PER], zq[NB], bq[NB];
+    // the k-th layer of the walk is l1-1-k; its block, bias and input row Z_{l-1}
+    auto lay = [&](int k) { return l1 - 1 - min(k, count - 1); };
+    auto blk = [&](int k) { return Wt + (long long)lay(k) * W * W; };
+    auto bia = [&](int k) { return bias[(long long)lay(k) * W + tw]; };
+    auto zin = [&](int k) {
+        const int l = lay(k);
+        return (l == 0) ? z0[(long long)b * W + tw] : Z[((long long)b * L + l - 1) * W + tw];
+    };
+    block_to_regs<W>(blk(0), rg[0]);
+    regs_to_lds<W>(rg[0], Ws[0]);
+    auto pro = [&](auto J) {
+        constexpr int j = decltype(J)::value;
+        if constexpr (j >= 1) block_to_regs<W>(blk(j), rg[j]);
+        zq[j] = zin(j);
+        bq[j] = bia(j);
+    };
+    each_slot<0, NB>(pro);
+    for (int i = t; i < W; i += kThreads) {
+        const float v = (l1 == L) ? G[(long long)b * W + i] : Lambda[((long long)b * L + l1 - 1) * W + i];
+        lam[i] = v;
+        if (l1 == L) Lambda[((long long)b * L + L - 1) * W + i] = v;
+    }
+    auto step = [&](int k, auto U) {
+        constexpr int u = decltype(U)::value;
+        const int l = l1 - 1 - k;
+        if (t < W) zp[t] = zq[u];
+        const float bl = bq[u];
+        block_to_regs<W>(blk(k + NB), rg[u]);
+        zq[u] = zin(k + NB);
+        bq[u] = bia(k + NB);
+        __syncthreads();
+        const float* Wl = Ws[k & 1];
+        rows_dot_p<W>(Wl, zp, a);
+        __syncthreads();
+        if (t < W) {
+            float d;
+            activate(layer, a[t] + bl, &d);
+            g[t] = (res ? alpha * d : d) * lam[t];
+        }
+        __syncthreads();
+        cols_dot_p<W>(Wl, g, nl);
+        __syncthreads();
+        if (t < W) {
+            const float v = res ? lam[t] + nl[t] : nl[t];
+            lam[t] = v;
+            if (l >= 1)
+                Lambda[((long long)b * L + l - 1) * W + t] = v;
+            else
+                dz0[(long long)b * W + t] = v;
+        }
+        regs_to_lds<W>(rg[(u + 1) % NB], Ws[(k + 1) & 1]);
+        __syncthreads();
+    };
+    walk<NB>(count, step);
+}
+
+// As resnet_seq_forward_kernel, layers l0 .. l1-1.
+template <int W>
+__global__ __launch_bounds__(kThreads) void resnet_seq_forward_stream(
+    const float* __restrict__ Wt, const float* __restrict__ bias, const float* __restrict__ z0,
+    float* __restrict__ Z, int L, int skip, int act, int l0, int l1) {
+    using SS = Stream<W>;
+    constexpr int NB = SS::NB;
+    __shared__ float Ws[2][W * (W + 1)];
+    __shared__ float z[W], xs[W], sg[W], a[W];
+    const int b = blockIdx.x, t = threadIdx.x;
+    const int count = l1 - l0;
+    if (count <= 0) return;  // uniform over the workgroup
+    const int src = (l0 / skip) * skip - 1;  // the current block's input row
+    const int tw = t & (W - 1);
+    float rg[NB][SS::PER], bq[NB];
+    auto lay = [&](int k) { return l0 + min(k, count - 1); };
+    auto blk = [&](int k) { return Wt + (long long)lay(k) * W * W; };
+    auto bia = [&](int k) { return bias[(long long)lay(k) * W + tw]; };
+    block_to_regs<W>(blk(0), rg[0]);
+    regs_to_lds<W>(rg[0], Ws[0]);
+    auto pro = [&](auto J) {
+        constexpr int j = decltype(J)::value;
+        if constexpr (j >= 1) block_to_regs<W>(blk(j), rg[j]);
+        bq[j] = bia(j);
+    };
+    each_slot<0, NB>(pro);
+    for (int i = t; i < W; i += kThreads) {
+        z[i] = (l0 == 0) ? z0[(long long)b * W + i] : Z[((long long)b * L + l0 - 1) * W + i];
+        xs[i] = (src < 0) ? z0[(long long)b * W + i] : Z[((long long)b * L + src) * W + i];
+    }
+    auto step = [&](int k, auto U) {
+        constexpr int u = decltype(U)::value;
+        const int l = l0 + k;
+        const float bl = bq[u];
+        block_to_regs<W>(blk(k + NB), rg[u]);
+        bq[u] = bia(k + NB);
+        __syncthreads();
+        if (t < W) {
+            float d;
+            sg[t] = activate(2 * act, z[t], &d);
+        }
+        __syncthreads();
+        rows_dot_p<W>(Ws[k & 1], sg, a);
+        __syncthreads();
+        const bool sk = (l + 1) % skip == 0;
+        if (t < W) {
+            const float v = a[t] + bl + (sk ? xs[t] : 0.f);
+            z[t] = v;
+            Z[((long long)b * L + l) * W + t] = v;
+            if (sk) xs[t] = v;
+        }
+        regs_to_lds<W>(rg[(u + 1) % NB], Ws[(k + 1) & 1]);
+    };
+    walk<NB>(count, step);
+}
+
+// As resnet_seq_backward_kernel, layers l1-1 down to l0.
+template <int W>
+__global__ __launch_bounds__(kThreads) void resnet_seq_backward_stream(
+    const float* __restrict__ Wt, const float* __restrict__ z0, const float* __restrict__ Z,
+    const float* __restrict__ G, float* __restrict__ Lambda, float* __restrict__ dz0, int L,
+    int skip, int act, int l0, int l1) {
+    using SS = Stream<W>;
+    constexpr int NB = SS::NB;
+    __shared__ float Ws[2][W * (W + 1)];
+    __shared__ float lam[W], ds[W], nl[W];
+    const int b = blockIdx.x, t = threadIdx.x;
+    const int count = l1 - l0;
+    if (count <= 0) return;  // uniform over the workgroup
+    const int tw = t & (W - 1);
+    float* Lb = Lambda + (long long)b * L * W;
+    float rg[NB][SS::PER], zq[NB];
+    auto lay = [&](int k) { return l1 - 1 - min(k, count - 1); };
+    auto blk = [&](int k) { return Wt + (long long)lay(k) * W * W; };
+    auto zin = [&](int k) {
+        const int l = lay(k);
+        return (l == 0) ? z0[(long long)b * W + tw] : Z[((long long)b * L + l - 1) * W + tw];
+    };
+    block_to_regs<W>(blk(0), rg[0]);
+    regs_to_lds<W>(rg[0], Ws[0]);
+    zq[0] = zin(0);
+    auto pro = [&](auto J) {
+        constexpr int j = decltype(J)::value;
+        if constexpr (j >= 1) {
+            block_to_regs<W>(blk(j), rg[j]);
+            zq[j] = zin(j);
+        }
+    };
+    each_slot<0, NB>(pro);
+    // xsk: the adjoint of the current block's last row (its skip source),
+    // which the block's first layer adds; kept from when it was written
+    float xsk = 0.f;
+    if (t < W) {
+        const float v = (l1 == L) ? G[(long long)b * W + t] : Lb[(long long)(l1 - 1) * W + t];
+        lam[t] = v;
+        xsk = v;
+        if (l1 == L) Lb[(long long)(L - 1) * W + t] = v;
+    }
+    auto step = [&](int k, auto U) {
+        constexpr int u = decltype(U)::value;
+        const int l = l1 - 1 - k;
+        const float zv = zq[u];
+        block_to_regs<W>(blk(k + NB), rg[u]);
+        zq[u] = zin(k + NB);
+        __syncthreads();
+        if (t < W) {
+            float d;
+            activate(2 * act, zv, &d);
+            ds[t] = d;
+        }
+        __syncthreads();
+        cols_dot_p<W>(Ws[k & 1], lam, nl);
+        __syncthreads();
+        const bool first = l % skip == 0;  // first layer of a block: its input took the skip
+        if (t < W) {
+            // row l + skip - 1 was written by this thread in this launch (then
+            // xsk holds it), or, in a launch that starts below it, earlier
+            const float sa = l + skip - 1 <= l1 - 1 ? xsk : Lb[(long long)(l + skip - 1) * W + t];
+            const float v = nl[t] * ds[t] + (first ? sa : 0.f);
+            if (l >= 1) {
+                lam[t] = v;
+                Lb[(long long)(l - 1) * W + t] = v;
+                if (l % skip == 0) xsk = v;  // row l - 1 ends the block below
+            } else {
+                dz0[(long long)b * W + t] = v;
+            }
+        }
+        regs_to_lds<W>(rg[(u + 1) % NB], Ws[(k + 1) & 1]);
+    };
+    walk<NB>(count, step);
+}
+
 }  // namespace
 
 hipError_t launch_resnet_seq_forward(const float* W, const float* bias, const float* z0, float* Z,
                                      int B, int L, int w, int skip, int act, int l0, int l1,
                                      hipStream_t stream) {
+    switch (w) {
+        case 16: hipLaunchKernelGGL((resnet_seq_forward_stream<16>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, skip, act, l0, l1); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((resnet_seq_forward_stream<32>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, skip, act, l0, l1); return hipGetLastError();
+        case 64: hipLaunchKernelGGL((resnet_seq_forward_stream<64>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, skip, act, l0, l1); return hipGetLastError();
+        case 128: hipLaunchKernelGGL((resnet_seq_forward_stream<128>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, skip, act, l0, l1); return hipGetLastError();
+        default: break;
+    }
     hipLaunchKernelGGL(resnet_seq_forward_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, W,
                        bias, z0, Z, L, w, skip, act, l0, l1);
     return hipGetLastError();
@@ -223,6 +585,13 @@ hipError_t launch_resnet_seq_backward(const float* W, const float* z0, const flo
                                       const float* G, float* Lambda, float* dz0, int B, int L,
                                       int w, int skip, int act, int l0, int l1,
                                       hipStream_t stream) {
+    switch (w) {
+        case 16: hipLaunchKernelGGL((resnet_seq_backward_stream<16>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, z0, Z, G, Lambda, dz0, L, skip, act, l0, l1); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((resnet_seq_backward_stream<32>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, z0, Z, G, Lambda, dz0, L, skip, act, l0, l1); return hipGetLastError();
+        case 64: hipLaunchKernelGGL((resnet_seq_backward_stream<64>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, z0, Z, G, Lambda, dz0, L, skip, act, l0, l1); return hipGetLastError();
+        case 128: hipLaunchKernelGGL((resnet_seq_backward_stream<128>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, z0, Z, G, Lambda, dz0, L, skip, act, l0, l1); return hipGetLastError();
+        default: break;
+    }
     hipLaunchKernelGGL(resnet_seq_backward_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream,
                        W, z0, Z, G, Lambda, dz0, L, w, skip, act, l0, l1);
     return hipGetLastError();
@@ -231,6 +600,13 @@ hipError_t launch_resnet_seq_backward(const float* W, const float* z0, const flo
 hipError_t launch_seq_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
                               int L, int w, int layer, float alpha, int l0, int l1,
                               hipStream_t stream) {
+    switch (w) {
+        case 16: hipLaunchKernelGGL((seq_forward_stream<16>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((seq_forward_stream<32>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 64: hipLaunchKernelGGL((seq_forward_stream<64>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 128: hipLaunchKernelGGL((seq_forward_stream<128>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
+        default: break;
+    }
     hipLaunchKernelGGL(seq_forward_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias,
                        z0, Z, L, w, layer, alpha, l0, l1);
     return hipGetLastError();
@@ -239,6 +615,13 @@ hipError_t launch_seq_forward(const float* W, const float* bias, const float* z0
 hipError_t launch_seq_backward(const float* W, const float* bias, const float* z0, const float* Z,
                                const float* G, float* Lambda, float* dz0, int B, int L, int w,
                                int layer, float alpha, int l0, int l1, hipStream_t stream) {
+    switch (w) {
+        case 16: hipLaunchKernelGGL((seq_backward_stream<16>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((seq_backward_stream<32>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 64: hipLaunchKernelGGL((seq_backward_stream<64>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 128: hipLaunchKernelGGL((seq_backward_stream<128>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
+        default: break;
+    }
     hipLaunchKernelGGL(seq_backward_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias,
                        z0, Z, G, Lambda, dz0, L, w, layer, alpha, l0, l1);
     return hipGetLastError();
