@@ -564,11 +564,291 @@ __global__ __launch_bounds__(kThreads) void resnet_seq_backward_stream(
     walk<NB>(count, step);
 }
 
+// ---- w = 16, 32, 64: one wave per system ----------------------------------
+// (forward at w = 16, 32, 64, backward at w = 16, 32: at w = 64 the
+// backward's transposed product, one column per lane over all rows, made the
+// one-wave version slower than the workgroup one, 29 against 22 ms at
+// L = 16384)
+// Lane group i (64/w lanes) holds row i of each layer's block, w^2/64
+// columns per lane, in a ring of register slots requested NB - 1 layers
+// ahead (with the bias); the state lives in the wave's LDS, so a layer costs
+// one wave-level barrier.  The backward also puts each block into LDS for the
+// transposed product.
+template <int W>
+struct WaveSeq {
+    static constexpr int LPR = 64 / W;   // lanes per row
+    static constexpr int CPL = W / LPR;  // columns per lane
+    static constexpr int NB = W == 16 ? 16 : W == 32 ? 8 : 4;
+};
+
+
+template <int W>
+__device__ __forceinline__ void row_to_regs(const float* __restrict__ blk, int i, int c0,
+                                            float (&r)[WaveSeq<W>::CPL]) {
+    const float* src = blk + i * W + c0;
+#pragma unroll
+    for (int c = 0; c < WaveSeq<W>::CPL; c += 4) {
+        const float4 x = *reinterpret_cast<const float4*>(src + c);
+        r[c] = x.x;
+        r[c + 1] = x.y;
+        r[c + 2] = x.z;
+        r[c + 3] = x.w;
+    }
+}
+
+// sum over the row of (registers) x (vector in LDS); every lane of the row
+// group receives it
+template <int W>
+__device__ __forceinline__ float wave_row_dot(const float (&r)[WaveSeq<W>::CPL], const float* v,
+                                              int c0) {
+    constexpr int CPL = WaveSeq<W>::CPL;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) acc[c & 3] = fmaf(r[c], v[c0 + c], acc[c & 3]);
+    float sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+#pragma unroll
+    for (int off = 1; off < WaveSeq<W>::LPR; off <<= 1) sum += __shfl_xor(sum, off, 64);
+    return sum;
+}
+
+// As seq_forward_kernel, one wave per system.
+template <int W>
+__global__ __launch_bounds__(64) void seq_forward_wave(
+    const float* __restrict__ Wt, const float* __restrict__ bias, const float* __restrict__ z0,
+    float* __restrict__ Z, int L, int layer, float alpha, int l0, int l1) {
+    using SQ = WaveSeq<W>;
+    constexpr int NB = SQ::NB;
+    __shared__ float z[2][W];
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int i = lane / SQ::LPR, c0 = (lane % SQ::LPR) * SQ::CPL;
+    const bool lead = lane % SQ::LPR == 0;
+    const bool res = layer_residual(layer);
+    const int count = l1 - l0;
+    if (count <= 0) return;
+    float wr[NB][SQ::CPL], bq[NB];
+    auto lay = [&](int k) { return l0 + min(k, count - 1); };
+    auto load = [&](int k, float (&r)[SQ::CPL], float& bb) {
+        const int l = lay(k);
+        row_to_regs<W>(Wt + (long long)l * W * W, i, c0, r);
+        bb = bias[(long long)l * W + i];
+    };
+    auto pro = [&](auto J) {
+        constexpr int j = decltype(J)::value;
+        load(j, wr[j], bq[j]);
+    };
+    each_slot<0, NB>(pro);
+    if (lane < W)
+        z[0][lane] = (l0 == 0) ? z0[(long long)b * W + lane] : Z[((long long)b * L + l0 - 1) * W + lane];
+    auto step = [&](int k, auto U) {
+        constexpr int u = decltype(U)::value;
+        const int l = l0 + k;
+        const float* zc = z[k & 1];
+        wave_sync();
+        const float a = wave_row_dot<W>(wr[u], zc, c0) + bq[u];
+        load(k + NB, wr[u], bq[u]);
+        float d;
+        const float y = activate(layer, a, &d);
+        const float f = res ? fmaf(alpha, y, zc[i]) : y;
+        if (lead) {
+            z[(k + 1) & 1][i] = f;
+            Z[((long long)b * L + l) * W + i] = f;
+        }
+    };
+    walk<NB>(count, step);
+}
+
+// As seq_backward_kernel, one wave per system.
+template <int W>
+__global__ __launch_bounds__(64) void seq_backward_wave(
+    const float* __restrict__ Wt, const float* __restrict__ bias, const float* __restrict__ z0,
+    const float* __restrict__ Z, const float* __restrict__ G, float* __restrict__ Lambda,
+    float* __restrict__ dz0, int L, int layer, float alpha, int l0, int l1) {
+    using SQ = WaveSeq<W>;
+    constexpr int NB = SQ::NB;
+    __shared__ float Wl[W * (W + 1)];  // the current block, rows of pitch w + 1
+    __shared__ float zp[W], g[W], lam[W];
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int i = lane / SQ::LPR, c0 = (lane % SQ::LPR) * SQ::CPL;
+    const bool lead = lane % SQ::LPR == 0;
+    const bool res = layer_residual(layer);
+    const int count = l1 - l0;
+    if (count <= 0) return;
+    const int tw = lane & (W - 1);
+    float wr[NB][SQ::CPL], bq[NB], zq[NB];
+    auto lay = [&](int k) { return l1 - 1 - min(k, count - 1); };
+    auto load = [&](int k, float (&r)[SQ::CPL], float& bb, float& zz) {
+        const int l = lay(k);
+        row_to_regs<W>(Wt + (long long)l * W * W, i, c0, r);
+        bb = bias[(long long)l * W + i];
+        zz = (l == 0) ? z0[(long long)b * W + tw] : Z[((long long)b * L + l - 1) * W + tw];
+    };
+    auto pro = [&](auto J) {
+        constexpr int j = decltype(J)::value;
+        load(j, wr[j], bq[j], zq[j]);
+    };
+    each_slot<0, NB>(pro);
+    if (lane < W) {
+        const float v = (l1 == L) ? G[(long long)b * W + lane] : Lambda[((long long)b * L + l1 - 1) * W + lane];
+        lam[lane] = v;
+        if (l1 == L) Lambda[((long long)b * L + L - 1) * W + lane] = v;
+    }
+    auto step = [&](int k, auto U) {
+        constexpr int u = decltype(U)::value;
+        const int l = l1 - 1 - k;
+        wave_sync();  // the previous layer's reads of Wl, zp, g and lam are done
+        if (lane < W) zp[lane] = zq[u];
+#pragma unroll
+        for (int c = 0; c < SQ::CPL; ++c) Wl[i * (W + 1) + c0 + c] = wr[u][c];
+        wave_sync();
+        const float a = wave_row_dot<W>(wr[u], zp, c0) + bq[u];
+        load(k + NB, wr[u], bq[u], zq[u]);
+        float d;
+        activate(layer, a, &d);
+        if (lead) g[i] = (res ? alpha * d : d) * lam[i];
+        wave_sync();
+        // column j = lane (w <= 64 lanes): sum over the rows of Wl[r][j] g[r]
+        if (lane < W) {
+            float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int r = 0; r < W; ++r) acc[r & 3] = fmaf(Wl[r * (W + 1) + lane], g[r], acc[r & 3]);
+            const float nl = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+            const float v = res ? lam[lane] + nl : nl;
+            if (l >= 1)
+                Lambda[((long long)b * L + l - 1) * W + lane] = v;
+            else
+                dz0[(long long)b * W + lane] = v;
+            lam[lane] = v;  // this lane alone read lam[lane] above
+        }
+    };
+    walk<NB>(count, step);
+}
+
+// As resnet_seq_forward_kernel, one wave per system (w = 16, 32).
+template <int W>
+__global__ __launch_bounds__(64) void resnet_seq_forward_wave(
+    const float* __restrict__ Wt, const float* __restrict__ bias, const float* __restrict__ z0,
+    float* __restrict__ Z, int L, int skip, int act, int l0, int l1) {
+    using SQ = WaveSeq<W>;
+    constexpr int NB = SQ::NB;
+    __shared__ float sg[W];
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int i = lane / SQ::LPR, c0 = (lane % SQ::LPR) * SQ::CPL;
+    const int count = l1 - l0;
+    if (count <= 0) return;
+    const int tw = lane & (W - 1);
+    const int src = (l0 / skip) * skip - 1;  // the current block's input row
+    float wr[NB][SQ::CPL], bq[NB];
+    auto lay = [&](int k) { return l0 + min(k, count - 1); };
+    auto load = [&](int k, float (&r)[SQ::CPL], float& bb) {
+        const int l = lay(k);
+        row_to_regs<W>(Wt + (long long)l * W * W, i, c0, r);
+        bb = bias[(long long)l * W + i];
+    };
+    auto pro = [&](auto J) {
+        constexpr int j = decltype(J)::value;
+        load(j, wr[j], bq[j]);
+    };
+    each_slot<0, NB>(pro);
+    // every lane holds element tw of the state and of the skip source
+    float z = (l0 == 0) ? z0[(long long)b * W + tw] : Z[((long long)b * L + l0 - 1) * W + tw];
+    float xs = (src < 0) ? z0[(long long)b * W + tw] : Z[((long long)b * L + src) * W + tw];
+    auto step = [&](int k, auto U) {
+        constexpr int u = decltype(U)::value;
+        const int l = l0 + k;
+        wave_sync();  // the previous layer's reads of sg are done
+        if (lane < W) {
+            float d;
+            sg[lane] = activate(2 * act, z, &d);
+        }
+        wave_sync();
+        const float a = wave_row_dot<W>(wr[u], sg, c0) + bq[u];
+        load(k + NB, wr[u], bq[u]);
+        const bool sk = (l + 1) % skip == 0;
+        // row i's value to every lane holding element i (lane tw == i)
+        const float v = __shfl(a, (tw) * SQ::LPR, 64) + (sk ? xs : 0.f);
+        z = v;
+        if (sk) xs = v;
+        if (lane < W) Z[((long long)b * L + l) * W + lane] = v;
+    };
+    walk<NB>(count, step);
+}
+
+// As resnet_seq_backward_kernel, one wave per system (w = 16, 32).
+template <int W>
+__global__ __launch_bounds__(64) void resnet_seq_backward_wave(
+    const float* __restrict__ Wt, const float* __restrict__ z0, const float* __restrict__ Z,
+    const float* __restrict__ G, float* __restrict__ Lambda, float* __restrict__ dz0, int L,
+    int skip, int act, int l0, int l1) {
+    using SQ = WaveSeq<W>;
+    constexpr int NB = SQ::NB;
+    __shared__ float Wl[W * (W + 1)];  // the current block, rows of pitch w + 1
+    __shared__ float lam[W];
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int i = lane / SQ::LPR, c0 = (lane % SQ::LPR) * SQ::CPL;
+    const int count = l1 - l0;
+    if (count <= 0) return;
+    const int tw = lane & (W - 1);
+    float* Lb = Lambda + (long long)b * L * W;
+    float wr[NB][SQ::CPL], zq[NB];
+    auto lay = [&](int k) { return l1 - 1 - min(k, count - 1); };
+    auto load = [&](int k, float (&r)[SQ::CPL], float& zz) {
+        const int l = lay(k);
+        row_to_regs<W>(Wt + (long long)l * W * W, i, c0, r);
+        zz = (l == 0) ? z0[(long long)b * W + tw] : Z[((long long)b * L + l - 1) * W + tw];
+    };
+    auto pro = [&](auto J) {
+        constexpr int j = decltype(J)::value;
+        load(j, wr[j], zq[j]);
+    };
+    each_slot<0, NB>(pro);
+    // xsk: the adjoint of the current block's last row (its skip source)
+    float xsk = (l1 == L) ? G[(long long)b * W + tw] : Lb[(long long)(l1 - 1) * W + tw];
+    if (lane < W) {
+        lam[lane] = xsk;
+        if (l1 == L) Lb[(long long)(L - 1) * W + lane] = xsk;
+    }
+    auto step = [&](int k, auto U) {
+        constexpr int u = decltype(U)::value;
+        const int l = l1 - 1 - k;
+        wave_sync();  // the previous layer's reads of Wl and lam are done
+#pragma unroll
+        for (int c = 0; c < SQ::CPL; ++c) Wl[i * (W + 1) + c0 + c] = wr[u][c];
+        float d;
+        activate(2 * act, zq[u], &d);
+        load(k + NB, wr[u], zq[u]);
+        wave_sync();
+        // element tw: sum over the rows of Wl[r][tw] lam[r]
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int r = 0; r < W; ++r) acc[r & 3] = fmaf(Wl[r * (W + 1) + tw], lam[r], acc[r & 3]);
+        const float nl = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+        const bool first = l % skip == 0;  // first layer of a block: its input took the skip
+        const float sa = l + skip - 1 <= l1 - 1 ? xsk : Lb[(long long)(l + skip - 1) * W + tw];
+        const float v = nl * d + (first ? sa : 0.f);
+        wave_sync();  // every lane's reads of lam are done
+        if (l >= 1) {
+            if (lane < W) {
+                lam[lane] = v;
+                Lb[(long long)(l - 1) * W + lane] = v;
+            }
+            if (l % skip == 0) xsk = v;  // row l - 1 ends the block below
+        } else if (lane < W) {
+            dz0[(long long)b * W + lane] = v;
+        }
+    };
+    walk<NB>(count, step);
+}
+
 }  // namespace
 
 hipError_t launch_resnet_seq_forward(const float* W, const float* bias, const float* z0, float* Z,
                                      int B, int L, int w, int skip, int act, int l0, int l1,
                                      hipStream_t stream) {
+    switch (w) {
+        case 16: hipLaunchKernelGGL((resnet_seq_forward_wave<16>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, skip, act, l0, l1); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((resnet_seq_forward_wave<32>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, skip, act, l0, l1); return hipGetLastError();
+        default: break;
+    }
     switch (w) {
         case 16: hipLaunchKernelGGL((resnet_seq_forward_stream<16>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, skip, act, l0, l1); return hipGetLastError();
         case 32: hipLaunchKernelGGL((resnet_seq_forward_stream<32>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, skip, act, l0, l1); return hipGetLastError();
@@ -586,6 +866,11 @@ hipError_t launch_resnet_seq_backward(const float* W, const float* z0, const flo
                                       int w, int skip, int act, int l0, int l1,
                                       hipStream_t stream) {
     switch (w) {
+        case 16: hipLaunchKernelGGL((resnet_seq_backward_wave<16>), dim3((unsigned)B), dim3(64), 0, stream, W, z0, Z, G, Lambda, dz0, L, skip, act, l0, l1); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((resnet_seq_backward_wave<32>), dim3((unsigned)B), dim3(64), 0, stream, W, z0, Z, G, Lambda, dz0, L, skip, act, l0, l1); return hipGetLastError();
+        default: break;
+    }
+    switch (w) {
         case 16: hipLaunchKernelGGL((resnet_seq_backward_stream<16>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, z0, Z, G, Lambda, dz0, L, skip, act, l0, l1); return hipGetLastError();
         case 32: hipLaunchKernelGGL((resnet_seq_backward_stream<32>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, z0, Z, G, Lambda, dz0, L, skip, act, l0, l1); return hipGetLastError();
         case 64: hipLaunchKernelGGL((resnet_seq_backward_stream<64>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, z0, Z, G, Lambda, dz0, L, skip, act, l0, l1); return hipGetLastError();
@@ -601,6 +886,12 @@ hipError_t launch_seq_forward(const float* W, const float* bias, const float* z0
                               int L, int w, int layer, float alpha, int l0, int l1,
                               hipStream_t stream) {
     switch (w) {
+        case 16: hipLaunchKernelGGL((seq_forward_wave<16>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((seq_forward_wave<32>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 64: hipLaunchKernelGGL((seq_forward_wave<64>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
+        default: break;
+    }
+    switch (w) {
         case 16: hipLaunchKernelGGL((seq_forward_stream<16>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
         case 32: hipLaunchKernelGGL((seq_forward_stream<32>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
         case 64: hipLaunchKernelGGL((seq_forward_stream<64>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
@@ -615,6 +906,11 @@ hipError_t launch_seq_forward(const float* W, const float* bias, const float* z0
 hipError_t launch_seq_backward(const float* W, const float* bias, const float* z0, const float* Z,
                                const float* G, float* Lambda, float* dz0, int B, int L, int w,
                                int layer, float alpha, int l0, int l1, hipStream_t stream) {
+    switch (w) {
+        case 16: hipLaunchKernelGGL((seq_backward_wave<16>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 32: hipLaunchKernelGGL((seq_backward_wave<32>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
+        default: break;
+    }
     switch (w) {
         case 16: hipLaunchKernelGGL((seq_backward_stream<16>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
         case 32: hipLaunchKernelGGL((seq_backward_stream<32>), dim3((unsigned)B), dim3(kThreads), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();

@@ -159,7 +159,9 @@ def test_resnet_deterministic(dev):
 
 
 @pytest.mark.parametrize("w,L,B,skip,act", [(16, 256, 4, 4, RELU), (3, 9, 2, 1, TANH),
-                                            (33, 60, 2, 3, SIG), (128, 16, 2, 4, RELU)])
+                                            (33, 60, 2, 3, SIG), (128, 16, 2, 4, RELU),
+                                            (32, 96, 2, 3, TANH), (16, 20, 3, 1, SIG),
+                                            (64, 40, 2, 4, RELU), (16, 6, 2, 2, TANH)])
 @pytest.mark.parametrize("per_layer", [False, True])
 def test_resnet_sequential_passes(dev, w, L, B, skip, act, per_layer):
     d = synth.resnet_inputs(B, L, w, seed=1600 + w + L)
