@@ -547,10 +547,14 @@ __global__ __launch_bounds__(kThreads) void resnet_seq_backward_stream(
         __syncthreads();
         const bool first = l % skip == 0;  // first layer of a block: its input took the skip
         if (t < W) {
-            // row l + skip - 1 was written by this thread in this launch (then
-            // xsk holds it), or, in a launch that starts below it, earlier
-            const float sa = l + skip - 1 <= l1 - 1 ? xsk : Lb[(long long)(l + skip - 1) * W + t];
-            const float v = nl[t] * ds[t] + (first ? sa : 0.f);
+            // the first layer of a block adds the adjoint of the block's last
+            // row l + skip - 1 (<= L - 1 only for a first layer): written by
+            // this thread in this launch (then xsk holds it), or, in a launch
+            // that starts below it, earlier
+            float sa = 0.f;
+            if (first)
+                sa = l + skip - 1 <= l1 - 1 ? xsk : Lb[(long long)min(l + skip - 1, L - 1) * W + t];
+            const float v = nl[t] * ds[t] + sa;
             if (l >= 1) {
                 lam[t] = v;
                 Lb[(long long)(l - 1) * W + t] = v;
@@ -823,8 +827,11 @@ __global__ __launch_bounds__(64) void resnet_seq_backward_wave(
         for (int r = 0; r < W; ++r) acc[r & 3] = fmaf(Wl[r * (W + 1) + tw], lam[r], acc[r & 3]);
         const float nl = (acc[0] + acc[1]) + (acc[2] + acc[3]);
         const bool first = l % skip == 0;  // first layer of a block: its input took the skip
-        const float sa = l + skip - 1 <= l1 - 1 ? xsk : Lb[(long long)(l + skip - 1) * W + tw];
-        const float v = nl * d + (first ? sa : 0.f);
+        // the block's last row l + skip - 1 is <= L - 1 only for a first layer
+        float sa = 0.f;
+        if (first)
+            sa = l + skip - 1 <= l1 - 1 ? xsk : Lb[(long long)min(l + skip - 1, L - 1) * W + tw];
+        const float v = nl * d + sa;
         wave_sync();  // every lane's reads of lam are done
         if (l >= 1) {
             if (lane < W) {
