@@ -568,8 +568,8 @@ __global__ __launch_bounds__(kThreads) void resnet_seq_backward_stream(
     walk<NB>(count, step);
 }
 
-// ---- w = 16, 32, 64: one wave per system ----------------------------------
-// (forward at w = 16, 32, 64, backward at w = 16, 32: at w = 64 the
+// ---- w = 2 .. 64: one wave per system -------------------------------------
+// (forward at w = 2 .. 64, backward at w = 2 .. 32: at w = 64 the
 // backward's transposed product, one column per lane over all rows, made the
 // one-wave version slower than the workgroup one, 29 against 22 ms at
 // L = 16384)
@@ -580,9 +580,10 @@ __global__ __launch_bounds__(kThreads) void resnet_seq_backward_stream(
 // transposed product.
 template <int W>
 struct WaveSeq {
-    static constexpr int LPR = 64 / W;   // lanes per row
-    static constexpr int CPL = W / LPR;  // columns per lane
-    static constexpr int NB = W == 16 ? 16 : W == 32 ? 8 : 4;
+    static constexpr int LPR = W >= 16 ? 64 / W : W;  // lanes per row
+    static constexpr int CPL = W / LPR;               // columns per lane
+    static constexpr int RL = W * LPR;                // lanes that hold a row (64 from w = 8)
+    static constexpr int NB = W <= 16 ? 16 : W == 32 ? 8 : 4;
 };
 
 
@@ -590,13 +591,18 @@ template <int W>
 __device__ __forceinline__ void row_to_regs(const float* __restrict__ blk, int i, int c0,
                                             float (&r)[WaveSeq<W>::CPL]) {
     const float* src = blk + i * W + c0;
+    if constexpr (WaveSeq<W>::CPL % 4 == 0) {
 #pragma unroll
-    for (int c = 0; c < WaveSeq<W>::CPL; c += 4) {
-        const float4 x = *reinterpret_cast<const float4*>(src + c);
-        r[c] = x.x;
-        r[c + 1] = x.y;
-        r[c + 2] = x.z;
-        r[c + 3] = x.w;
+        for (int c = 0; c < WaveSeq<W>::CPL; c += 4) {
+            const float4 x = *reinterpret_cast<const float4*>(src + c);
+            r[c] = x.x;
+            r[c + 1] = x.y;
+            r[c + 2] = x.z;
+            r[c + 3] = x.w;
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < WaveSeq<W>::CPL; ++c) r[c] = src[c];
     }
 }
 
@@ -624,8 +630,9 @@ __global__ __launch_bounds__(64) void seq_forward_wave(
     constexpr int NB = SQ::NB;
     __shared__ float z[2][W];
     const int b = blockIdx.x, lane = threadIdx.x;
-    const int i = lane / SQ::LPR, c0 = (lane % SQ::LPR) * SQ::CPL;
-    const bool lead = lane % SQ::LPR == 0;
+    // lanes past the rows (w < 8) read the last row again and write nothing
+    const int i = min(lane / SQ::LPR, W - 1), c0 = (lane % SQ::LPR) * SQ::CPL;
+    const bool lead = lane % SQ::LPR == 0 && lane < SQ::RL;
     const bool res = layer_residual(layer);
     const int count = l1 - l0;
     if (count <= 0) return;
@@ -672,8 +679,9 @@ __global__ __launch_bounds__(64) void seq_backward_wave(
     __shared__ float Wl[W * (W + 1)];  // the current block, rows of pitch w + 1
     __shared__ float zp[W], g[W], lam[W];
     const int b = blockIdx.x, lane = threadIdx.x;
-    const int i = lane / SQ::LPR, c0 = (lane % SQ::LPR) * SQ::CPL;
-    const bool lead = lane % SQ::LPR == 0;
+    // lanes past the rows (w < 8) read the last row again and write nothing
+    const int i = min(lane / SQ::LPR, W - 1), c0 = (lane % SQ::LPR) * SQ::CPL;
+    const bool lead = lane % SQ::LPR == 0 && lane < SQ::RL;
     const bool res = layer_residual(layer);
     const int count = l1 - l0;
     if (count <= 0) return;
@@ -701,8 +709,10 @@ __global__ __launch_bounds__(64) void seq_backward_wave(
         const int l = l1 - 1 - k;
         wave_sync();  // the previous layer's reads of Wl, zp, g and lam are done
         if (lane < W) zp[lane] = zq[u];
+        if (lane < SQ::RL) {
 #pragma unroll
-        for (int c = 0; c < SQ::CPL; ++c) Wl[i * (W + 1) + c0 + c] = wr[u][c];
+            for (int c = 0; c < SQ::CPL; ++c) Wl[i * (W + 1) + c0 + c] = wr[u][c];
+        }
         wave_sync();
         const float a = wave_row_dot<W>(wr[u], zp, c0) + bq[u];
         load(k + NB, wr[u], bq[u], zq[u]);
@@ -736,7 +746,7 @@ __global__ __launch_bounds__(64) void resnet_seq_forward_wave(
     constexpr int NB = SQ::NB;
     __shared__ float sg[W];
     const int b = blockIdx.x, lane = threadIdx.x;
-    const int i = lane / SQ::LPR, c0 = (lane % SQ::LPR) * SQ::CPL;
+    const int i = min(lane / SQ::LPR, W - 1), c0 = (lane % SQ::LPR) * SQ::CPL;
     const int count = l1 - l0;
     if (count <= 0) return;
     const int tw = lane & (W - 1);
@@ -788,7 +798,7 @@ __global__ __launch_bounds__(64) void resnet_seq_backward_wave(
     __shared__ float Wl[W * (W + 1)];  // the current block, rows of pitch w + 1
     __shared__ float lam[W];
     const int b = blockIdx.x, lane = threadIdx.x;
-    const int i = lane / SQ::LPR, c0 = (lane % SQ::LPR) * SQ::CPL;
+    const int i = min(lane / SQ::LPR, W - 1), c0 = (lane % SQ::LPR) * SQ::CPL;
     const int count = l1 - l0;
     if (count <= 0) return;
     const int tw = lane & (W - 1);
@@ -893,6 +903,9 @@ hipError_t launch_seq_forward(const float* W, const float* bias, const float* z0
                               int L, int w, int layer, float alpha, int l0, int l1,
                               hipStream_t stream) {
     switch (w) {
+        case 2: hipLaunchKernelGGL((seq_forward_wave<2>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 4: hipLaunchKernelGGL((seq_forward_wave<4>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 8: hipLaunchKernelGGL((seq_forward_wave<8>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
         case 16: hipLaunchKernelGGL((seq_forward_wave<16>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
         case 32: hipLaunchKernelGGL((seq_forward_wave<32>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
         case 64: hipLaunchKernelGGL((seq_forward_wave<64>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, L, layer, alpha, l0, l1); return hipGetLastError();
@@ -914,6 +927,9 @@ hipError_t launch_seq_backward(const float* W, const float* bias, const float* z
                                const float* G, float* Lambda, float* dz0, int B, int L, int w,
                                int layer, float alpha, int l0, int l1, hipStream_t stream) {
     switch (w) {
+        case 2: hipLaunchKernelGGL((seq_backward_wave<2>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 4: hipLaunchKernelGGL((seq_backward_wave<4>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
+        case 8: hipLaunchKernelGGL((seq_backward_wave<8>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
         case 16: hipLaunchKernelGGL((seq_backward_wave<16>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
         case 32: hipLaunchKernelGGL((seq_backward_wave<32>), dim3((unsigned)B), dim3(64), 0, stream, W, bias, z0, Z, G, Lambda, dz0, L, layer, alpha, l0, l1); return hipGetLastError();
         default: break;

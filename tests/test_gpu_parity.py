@@ -468,11 +468,12 @@ def test_workspace_too_small_is_rejected(dev):
 
 
 # ------------------------------------------------------- sequential baseline
-# one wave per system (w = 16, 32; forward also 64), the streamed workgroup
+# one wave per system (w = 2 .. 32; forward also 64), the streamed workgroup
 # kernels (w = 64 backward, 128) and the generic one (33); walks shorter than
 # the weight ring and walks ending in a partial trip of it
 @pytest.mark.parametrize("w,L,B", [(4, 50, 3), (16, 300, 2), (33, 40, 2), (128, 20, 2),
-                                   (32, 70, 2), (64, 33, 3), (32, 3, 2), (128, 3, 1)])
+                                   (32, 70, 2), (64, 33, 3), (32, 3, 2), (128, 3, 1),
+                                   (2, 37, 2), (8, 65, 3), (8, 2, 1)])
 @pytest.mark.parametrize("layer,alpha", [(0, 1.0), (3, 0.1), (4, 1.0)])
 @pytest.mark.parametrize("per_layer", [False, True])
 def test_sequential_passes(dev, w, L, B, layer, alpha, per_layer):
