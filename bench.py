@@ -185,14 +185,24 @@ def cpu_baseline(wl, budget_s):
         if "bwd" in wl.passes:
             oracle.seq_backward(wl.layer, wl.alpha, d["W"], d["bias"], d["z0"], Z, d["G"])
 
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        once()
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s:
-            break
+    def rate(budget):
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            once()
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget:
+                return reps, el
+
+    reps, el = rate(budget_s)
+    # the same with one BLAS thread, on half the budget
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            reps1, el1 = rate(budget_s / 2)
+        one = B * L * reps1 / el1
+    except Exception:  # pragma: no cover
+        one = None
     parts = "+".join(("seq_solve",) if wl.kind == "pcr" else
                      ("resnet_seq_forward", "resnet_seq_backward") if wl.kind == "resnet" else
                      ("diffusion seq_sample",) if wl.kind == "diffusion" else
@@ -201,7 +211,8 @@ def cpu_baseline(wl, budget_s):
     return {"value": B * L * reps / el, "unit": "layer-steps/s", "cores": int(cores),
             "kind": "oracle",
             "sample": f"full workload ({parts}, numpy float64) x {reps} repetitions, "
-                      f"{el:.1f} s wall"}
+                      f"{el:.1f} s wall",
+            "value_1_thread": one}
 
 
 def measured_traffic(workload):
