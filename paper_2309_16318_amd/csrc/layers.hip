@@ -321,6 +321,37 @@ __global__ __launch_bounds__(kThreads) void wgrad_tile_kernel(
     if (t < W) db[(long long)l * W + t] = dbacc;
 }
 
+// The same sums for w <= 8: one thread per element (l, i, j) of dW (and of db
+// for j = 0), the batch summed in the same order, so the results equal
+// wgrad_kernel's.
+template <bool PRE>
+__global__ __launch_bounds__(kThreads) void wgrad_small_kernel(
+    const float* __restrict__ z0, const float* __restrict__ Z, const float* __restrict__ dscale,
+    const float* __restrict__ Lambda, float* __restrict__ dW, float* __restrict__ db, int B, int L,
+    int w, int act) {
+    const long long o = (long long)blockIdx.x * kThreads + threadIdx.x;  // (l w + i) w + j
+    if (o >= (long long)L * w * w) return;
+    const int j = (int)(o % w);
+    const long long li = o / w;
+    const int i = (int)(li % w);
+    const long long l = li / w;
+    float acc = 0.f, dbacc = 0.f;
+    for (int b = 0; b < B; ++b) {
+        const long long row = ((long long)b * L + l) * w;
+        const float gi = PRE ? Lambda[row + i] : dscale[row + i] * Lambda[row + i];
+        const float zin = (l == 0) ? z0[(long long)b * w + j] : Z[row - w + j];
+        float zpj = zin;
+        if constexpr (PRE) {
+            float d;
+            zpj = activate(2 * act, zin, &d);
+        }
+        acc = fmaf(gi, zpj, acc);
+        dbacc += gi;
+    }
+    dW[o] = acc;
+    if (j == 0) db[l * w + i] = dbacc;
+}
+
 // Backward assembly without the blocks (the first PCR pass forms them from
 // the weights): per (b, l) the scale c d_l (d = sigma'(W_l Z_{l-1} + b_l))
 // and the reversed right-hand side, as layer_eval_vec<W, true> writes them.
@@ -590,7 +621,14 @@ hipError_t launch_wgrad_any(const float* z0, const float* Z, const float* dscale
         case 32: hipLaunchKernelGGL((wgrad_tile_kernel<32, PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, act); break;
         case 64: hipLaunchKernelGGL((wgrad_tile_kernel<64, PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, act); break;
         case 128: hipLaunchKernelGGL((wgrad_tile_kernel<128, PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, act); break;
-        default: hipLaunchKernelGGL((wgrad_kernel<PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, w, act); break;
+        default:
+            if (w <= 8) {
+                const long long n = (long long)L * w * w;
+                hipLaunchKernelGGL((wgrad_small_kernel<PRE>), dim3((unsigned)((n + kThreads - 1) / kThreads)), blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, w, act);
+            } else {
+                hipLaunchKernelGGL((wgrad_kernel<PRE>), grid, blk, 0, stream, z0, Z, dscale, Lambda, dW, db, B, L, w, act);
+            }
+            break;
     }
     return hipGetLastError();
 }
