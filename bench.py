@@ -232,6 +232,20 @@ def measured_traffic(workload):
     return round(t["traffic_bytes_per_launch"])
 
 
+def roofline(cls, w):
+    """Roofline position of one kernel class from the library's counts:
+    algorithmic flops and bytes of its launches over their summed event
+    time; MFMA-bound at an intensity above the ridge (or at w >= 64)."""
+    intensity = cls["flops"] / max(cls["bytes"], 1.0)
+    if intensity >= RIDGE or w >= 64:
+        achieved = cls["flops"] / (cls["ms"] * 1e-3) / 1e12
+        return {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4)}
+    achieved = cls["bytes"] / (cls["ms"] * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -263,21 +277,14 @@ def main():
 
     ms_step = el * 1e3 / args.steps
     value = wl.B * wl.L / (el / args.steps)
-    lvl = prof["pcr_level"]
-    intensity = lvl["flops"] / max(lvl["bytes"], 1.0)
-    if intensity >= RIDGE or wl.w >= 64:
-        achieved = lvl["flops"] / (lvl["ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4)}
-    else:
-        achieved = lvl["bytes"] / (lvl["ms"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof = roofline(prof["pcr_level"], wl.w)
     roof["traffic"] = measured_traffic(wl.name)
-    roof["alg_bytes_per_launch"] = round(lvl["bytes"] / max(lvl["launches"], 1))
+    roof["alg_bytes_per_launch"] = round(prof["pcr_level"]["bytes"] /
+                                         max(prof["pcr_level"]["launches"], 1))
     roof["kernel"] = "pcr_level"
-    roof["avg_launch_us"] = round(lvl["ms"] * 1e3 / max(lvl["launches"], 1), 3)
-    roof["launches"] = lvl["launches"]
+    roof["avg_launch_us"] = round(prof["pcr_level"]["ms"] * 1e3 /
+                                  max(prof["pcr_level"]["launches"], 1), 3)
+    roof["launches"] = prof["pcr_level"]["launches"]
 
     layer_names = ["tanh_mlp", "tanh_residual", "sigmoid_mlp", "sigmoid_residual", "relu_mlp",
                    "relu_residual"]
@@ -304,6 +311,12 @@ def main():
         "config": cfg, "roofline": roof,
         "kernel_ms_per_step": {k: round(v["ms"] / args.steps, 4) for k, v in prof.items()},
     }
+    tail = prof["pcr_tail"]
+    if tail["launches"] > 0:
+        # the last levels' pass, timed as a class of its own
+        out["roofline_tail"] = {"kernel": "pcr_level_tail", **roofline(tail, wl.w),
+                                "avg_launch_us": round(tail["ms"] * 1e3 / tail["launches"], 3),
+                                "launches": tail["launches"]}
     if info["marks"]:
         # device time of each step (first to last mark on the launch stream)
         per = sorted(a.elapsed_time(c) for a, _, c in info["marks"])
