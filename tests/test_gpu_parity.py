@@ -190,10 +190,12 @@ def test_forward_all_layer_kinds(dev, w, L, B, layer, alpha):
 # (w = 64, B = 40 and w = 128, B = 16), even and odd level counts (L = 130
 # and 203: 8 levels, L = 300: 9), and the one-pass tail of the last levels
 # at w = 32 (L = 130, B = 64: 6 tail levels right after the first pair with
-# the layers; L = 300, B = 40: that pair, one more pair and 5 tail levels),
-# 64 and 128.
+# the layers; L = 300, B = 40: that pair, one more pair and 5 tail levels;
+# L = 17, B = 128 and L = 33, B = 64: 3 and 4 tail levels on chains of 4-5
+# and 8-9 elements, shorter than and just past the tail's ring of blocks in
+# flight), 64 and 128.
 @pytest.mark.parametrize("w,L,B", [(64, 130, 40), (64, 300, 8), (128, 203, 16), (32, 130, 64),
-                                   (32, 300, 40)])
+                                   (32, 300, 40), (32, 17, 128), (32, 33, 64)])
 @pytest.mark.parametrize("layer,alpha", ALL_KINDS)
 def test_forward_tile_segments(dev, w, L, B, layer, alpha):
     _say(f"forward tile segments w={w} L={L} B={B} layer={layer}")
@@ -410,9 +412,10 @@ def test_backward_shapes(dev, w, L, B, layer, alpha):
 # Tile widths with several elements per workgroup segment in every pass of
 # the transposed sweep (the first pass forms its blocks from the weights),
 # odd and even level counts (L = 130: 8 levels; L = 203 and 300: 8 and 9),
-# and the tail of the last levels at w = 32, 64, 128.
+# and the tail of the last levels at w = 32, 64, 128 (at w = 32 also on
+# chains shorter than its ring of blocks in flight: L = 17 and 33).
 @pytest.mark.parametrize("w,L,B", [(64, 130, 40), (64, 300, 8), (128, 203, 16), (32, 130, 64),
-                                   (32, 300, 40)])
+                                   (32, 300, 40), (32, 17, 128), (32, 33, 64)])
 @pytest.mark.parametrize("layer,alpha", ALL_KINDS)
 def test_backward_tile_segments(dev, w, L, B, layer, alpha):
     _say(f"backward tile segments w={w} L={L} B={B} layer={layer}")
