@@ -10,6 +10,8 @@
 namespace deeppcr {
 namespace {
 
+typedef float v4f __attribute__((ext_vector_type(4)));
+
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 
@@ -355,24 +357,29 @@ __global__ __launch_bounds__(kThreads) void wgrad_small_kernel(
 // Backward assembly without the blocks (the first PCR pass forms them from
 // the weights): per (b, l) the scale c d_l (d = sigma'(W_l Z_{l-1} + b_l))
 // and the reversed right-hand side, as layer_eval_vec<W, true> writes them.
-// One workgroup per layer, so that W_l is read once for all systems: lane
-// group i (256/w lanes) holds row i of W_l, w^2/256 columns per lane, and
-// forms the row's sums for every staged batch row.
+// One workgroup per layer, so that W_l is read once for all systems: thread
+// t holds row i = t % w of W_l in registers and forms that row's sum for
+// batch rows t / w, t / w + 256 / w, ... of each staged chunk (the chunk's
+// state rows are read from LDS as broadcasts, and each wave's results are
+// consecutive rows, so the stores are contiguous).
 template <int W>
 __global__ __launch_bounds__(kThreads) void bwd_scale_kernel(
     const float* __restrict__ W_, const float* __restrict__ bias, const float* __restrict__ z0,
     const float* __restrict__ Z, const float* __restrict__ G, float* __restrict__ r,
     float* __restrict__ dscale, int B, int L, int layer, float alpha) {
-    constexpr int LPR = kThreads / W;  // lanes per row of W_l
-    constexpr int CPL = W / LPR;       // columns per lane
+    constexpr int NG = kThreads / W;  // batch rows formed at once
     const int l = blockIdx.x;
     const int t = threadIdx.x;
-    const int i = t / LPR, c0 = (t % LPR) * CPL;
-    __shared__ float zs[kWgradBC][W];
-    float wr[CPL];
-    const float* Wrow = W_ + ((long long)l * W + i) * W + c0;
+    const int i = t % W, grp = t / W;
+    __shared__ __align__(16) float zs[kWgradBC][W];
+    float wr[W];
+    const float* Wrow = W_ + ((long long)l * W + i) * W;
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) wr[c] = Wrow[c];
+    for (int q = 0; q < W / 4; ++q) {
+        const v4f x = *reinterpret_cast<const v4f*>(Wrow + 4 * q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) wr[4 * q + e] = x[e];
+    }
     const float bi = bias[(long long)l * W + i];
     const bool res = layer_residual(layer);
     const int mr = L - 1 - l;  // reversed row of layer l
@@ -384,19 +391,20 @@ __global__ __launch_bounds__(kThreads) void bwd_scale_kernel(
             zs[bb][k] = (l == 0) ? z0[b * W + k] : Z[(b * L + l - 1) * W + k];
         }
         __syncthreads();
-        for (int bb = 0; bb < nb; ++bb) {
-            float part = 0.f;
+        for (int bb = grp; bb < nb; bb += NG) {
+            // four partial sums (columns k = 4q + e), added pairwise
+            float p[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) part = fmaf(wr[c], zs[bb][c0 + c], part);
+            for (int q = 0; q < W / 4; ++q) {
+                const v4f z4 = *reinterpret_cast<const v4f*>(&zs[bb][4 * q]);
 #pragma unroll
-            for (int off = 1; off < LPR; off <<= 1) part += __shfl_xor(part, off, 64);
-            if (t % LPR == 0) {
-                float d;
-                activate(layer, part + bi, &d);
-                const long long b = b0 + bb;
-                dscale[(b * L + l) * W + i] = res ? alpha * d : d;
-                r[(b * L + mr) * W + i] = (mr == 0) ? G[b * W + i] : 0.f;
+                for (int e = 0; e < 4; ++e) p[e] = fmaf(wr[4 * q + e], z4[e], p[e]);
             }
+            float d;
+            activate(layer, ((p[0] + p[1]) + (p[2] + p[3])) + bi, &d);
+            const long long b = b0 + bb;
+            dscale[(b * L + l) * W + i] = res ? alpha * d : d;
+            r[(b * L + mr) * W + i] = (mr == 0) ? G[b * W + i] : 0.f;
         }
         __syncthreads();
     }
@@ -441,7 +449,6 @@ __global__ __launch_bounds__(kThreads) void copy_rows_kernel(VecSrc src, VecDst 
 // float4 stores.  Mode FWD writes J_l at row l and the residual; mode BWD
 // writes J_l (not transposed) at reversed row L - l (unless A is null),
 // c * d_l and the reversed right-hand side (G at reversed row 0).
-typedef float v4f __attribute__((ext_vector_type(4)));
 
 template <int W>
 struct EvalShape {
