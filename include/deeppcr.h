@@ -296,7 +296,8 @@ int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, con
  * launches of one class on one stream (no host wait or other class between
  * them, e.g. the levels of one PCR sweep) share one event pair, so the time
  * of such a run includes the gaps between its kernels but no event overhead
- * per kernel.  Not thread-safe.
+ * per kernel; where a run of one class follows a run of another, one event
+ * ends the first and starts the second.  Not thread-safe.
  */
 enum {
     DEEPPCR_KCLASS_PCR_LEVEL = 0,  /* one PCR level (Alg. 1 inner parfor)      */
@@ -309,6 +310,10 @@ enum {
     DEEPPCR_KCLASS_COUNT = 7
 };
 int deeppcr_profile_enable(int on);
+/* Times only the classes whose bit (1 << class) is set in `class_mask` (all
+ * by default); a launch of another class ends the open span without events
+ * of its own.  Fewer classes mean fewer events between kernels. */
+int deeppcr_profile_select(unsigned class_mask);
 void deeppcr_profile_reset(void);
 /* Waits for the recorded events, then reports class `kclass`. */
 int deeppcr_profile_read(int kclass, long long* launches, double* total_ms,

@@ -42,10 +42,12 @@ struct ProfRec {
     hipEvent_t e0, e1;
     long long n;
     double bytes, flops;
+    bool share0;  // e0 is the end event of the record before (owned there)
 };
 
 struct Prof {
     bool on = false;
+    unsigned mask = ~0u;  // classes that are timed
     bool open = false;  // the last record may be extended; its end event is not recorded yet
     std::vector<ProfRec> pending;
     std::vector<hipEvent_t> pool;
@@ -87,9 +89,18 @@ struct SpanGuard {
 
 // Runs `launch` (which enqueues one kernel on `st` and returns its
 // hipGetLastError), bracketed by events when instrumentation is on.
+// A launch of a class that is not timed ends the open span first.  Where a
+// span of another class on the same stream is open, one event ends it and
+// starts the new one (each event is a marker between two kernels, which
+// costs the stream a few microseconds).
 template <class F>
 hipError_t timed(int kclass, double bytes, double flops, hipStream_t st, F&& launch) {
     if (!g_prof.on) return launch();
+    if (!((g_prof.mask >> kclass) & 1u)) {
+        hipError_t e = prof_break();
+        if (e != hipSuccess) return e;
+        return launch();
+    }
     if (g_prof.open) {
         ProfRec& r = g_prof.pending.back();
         if (r.kclass == kclass && r.st == st) {
@@ -100,6 +111,20 @@ hipError_t timed(int kclass, double bytes, double flops, hipStream_t st, F&& lau
             r.flops += flops;
             return hipSuccess;
         }
+        if (r.st == st) {
+            hipEvent_t e1 = take_event();
+            if (e1) {
+                const hipEvent_t e0 = r.e1;
+                g_prof.open = false;
+                hipError_t e = hipEventRecord(e0, st);
+                if (e != hipSuccess) return e;
+                e = launch();
+                if (e != hipSuccess) return e;
+                g_prof.pending.push_back({kclass, st, e0, e1, 1, bytes, flops, true});
+                g_prof.open = true;
+                return hipSuccess;
+            }
+        }
         hipError_t e = prof_break();
         if (e != hipSuccess) return e;
     }
@@ -109,7 +134,7 @@ hipError_t timed(int kclass, double bytes, double flops, hipStream_t st, F&& lau
     if (e != hipSuccess) return e;
     e = launch();
     if (e != hipSuccess) return e;
-    g_prof.pending.push_back({kclass, st, e0, e1, 1, bytes, flops});
+    g_prof.pending.push_back({kclass, st, e0, e1, 1, bytes, flops, false});
     g_prof.open = true;
     return hipSuccess;
 }
@@ -1048,11 +1073,17 @@ int deeppcr_profile_enable(int on) {
     return DEEPPCR_OK;
 }
 
+int deeppcr_profile_select(unsigned class_mask) {
+    (void)prof_break();
+    g_prof.mask = class_mask;
+    return DEEPPCR_OK;
+}
+
 void deeppcr_profile_reset(void) {
     (void)prof_break();
     for (auto& p : g_prof.pending) {
         (void)hipEventSynchronize(p.e1);
-        g_prof.pool.push_back(p.e0);
+        if (!p.share0) g_prof.pool.push_back(p.e0);
         g_prof.pool.push_back(p.e1);
     }
     g_prof.pending.clear();
@@ -1079,7 +1110,7 @@ int deeppcr_profile_read(int kclass, long long* launches, double* total_ms, doub
         g_prof.ms[p.kclass] += ms;
         g_prof.bytes[p.kclass] += p.bytes;
         g_prof.flops[p.kclass] += p.flops;
-        g_prof.pool.push_back(p.e0);
+        if (!p.share0) g_prof.pool.push_back(p.e0);
         g_prof.pool.push_back(p.e1);
     }
     g_prof.pending.clear();

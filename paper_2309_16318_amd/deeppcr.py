@@ -62,6 +62,7 @@ SIGNATURES = {
     "deeppcr_seq_backward": (_c.c_int, [_c.c_void_p] * 7 + [_c.c_int] * 4 + [_c.c_float, _c.c_int,
                                                                            _c.c_void_p]),
     "deeppcr_profile_enable": (_c.c_int, [_c.c_int]),
+    "deeppcr_profile_select": (_c.c_int, [_c.c_uint]),
     "deeppcr_profile_reset": (None, []),
     "deeppcr_profile_read": (_c.c_int, [_c.c_int, _c.POINTER(_c.c_longlong),
                                         _c.POINTER(_c.c_double), _c.POINTER(_c.c_double),
@@ -420,6 +421,14 @@ def deeppcr_seq_backward(W, bias, z0, Z, G, layer: int = TANH_MLP, alpha: float 
 # ---------------------------------------------------------- instrumentation
 def profile_enable(on: bool = True) -> None:
     lib().deeppcr_profile_enable(1 if on else 0)
+
+
+def profile_select(kclasses) -> None:
+    """Times only the given kernel classes (KCLASS_* values) while enabled."""
+    mask = 0
+    for c in kclasses:
+        mask |= 1 << int(c)
+    lib().deeppcr_profile_select(mask)
 
 
 def profile_reset() -> None:

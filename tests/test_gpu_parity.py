@@ -272,6 +272,34 @@ def test_forward_status_reports_every_path(dev, w, L, B):
     assert res.status == deeppcr.ENONFINITE and res.iters == 1
 
 
+def test_profiling_times_selected_classes_and_changes_nothing(dev):
+    """Instrumentation on (only the PCR level and tail classes timed, with
+    events shared at span boundaries) leaves the result bitwise unchanged."""
+    _say("profiling on a w=32 forward")
+    d = synth.mlp_inputs(64, 130, 32, seed=31)
+    ref = _forward(d, dev, 0, 1.0)
+    timed = (deeppcr.KCLASS_PCR_LEVEL, deeppcr.KCLASS_PCR_TAIL)
+    deeppcr.profile_reset()
+    deeppcr.profile_select(timed)
+    deeppcr.profile_enable(True)
+    try:
+        res = _forward(d, dev, 0, 1.0)
+        res2 = _forward(d, dev, 0, 1.0)
+    finally:
+        deeppcr.profile_enable(False)
+        deeppcr.profile_select(range(len(deeppcr.KCLASS_NAMES)))
+    reads = {c: deeppcr.profile_read(c) for c in range(len(deeppcr.KCLASS_NAMES))}
+    deeppcr.profile_reset()
+    assert res.status == deeppcr.OK and res2.status == deeppcr.OK
+    assert torch.equal(res.Z, ref.Z) and torch.equal(res2.Z, ref.Z)
+    for c, rd in reads.items():
+        if c in timed:
+            assert rd["launches"] >= 2 * res.iters and rd["ms"] > 0.0 and rd["flops"] > 0.0
+        else:
+            assert rd["launches"] == 0 and rd["ms"] == 0.0
+    assert all(deeppcr.profile_read(c)["launches"] == 0 for c in range(len(deeppcr.KCLASS_NAMES)))
+
+
 def test_forward_deterministic(dev):
     d = synth.mlp_inputs(8, 64, 32, seed=12)
     a = h(_forward(d, dev, 1, 0.1).Z)
