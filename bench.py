@@ -150,9 +150,23 @@ def make_step(wl, dev):
     return step, info
 
 
+def cpu_model():
+    """The host CPU's model name (as lscpu reports it), from /proc/cpuinfo."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return None
+
+
 def cpu_baseline(wl, budget_s):
     """The oracle (numpy float64, sequential substitution) on the same
-    workload, repeated until about `budget_s` seconds of CPU work."""
+    workload: one warm-up run, then the minimum of 5 timed runs (fewer if
+    one run takes more than a fifth of `budget_s`), with all BLAS threads
+    and again with one."""
     import oracle
     from paper_2309_16318_amd import synth
 
@@ -185,22 +199,25 @@ def cpu_baseline(wl, budget_s):
         if "bwd" in wl.passes:
             oracle.seq_backward(wl.layer, wl.alpha, d["W"], d["bias"], d["z0"], Z, d["G"])
 
-    def rate(budget):
-        reps, t0 = 0, time.perf_counter()
-        while True:
+    def best(budget):
+        t0 = time.perf_counter()
+        once()
+        warm = time.perf_counter() - t0
+        runs = 5 if warm * 5 <= budget else max(1, int(budget / warm))
+        times = []
+        for _ in range(runs):
+            t0 = time.perf_counter()
             once()
-            reps += 1
-            el = time.perf_counter() - t0
-            if el >= budget:
-                return reps, el
+            times.append(time.perf_counter() - t0)
+        return min(times), runs
 
-    reps, el = rate(budget_s)
-    # the same with one BLAS thread, on half the budget
+    t_all, runs = best(budget_s)
+    # the same with one BLAS thread
     try:
         from threadpoolctl import threadpool_limits
         with threadpool_limits(limits=1):
-            reps1, el1 = rate(budget_s / 2)
-        one = B * L * reps1 / el1
+            t_one, _ = best(budget_s)
+        one = B * L / t_one
     except Exception:  # pragma: no cover
         one = None
     parts = "+".join(("seq_solve",) if wl.kind == "pcr" else
@@ -208,11 +225,11 @@ def cpu_baseline(wl, budget_s):
                      ("diffusion seq_sample",) if wl.kind == "diffusion" else
                      tuple(p for p, on in (("seq_forward", "fwd" in wl.passes),
                                            ("seq_backward", "bwd" in wl.passes)) if on))
-    return {"value": B * L * reps / el, "unit": "layer-steps/s", "cores": int(cores),
+    return {"value": B * L / t_all, "unit": "layer-steps/s", "cores": int(cores),
             "kind": "oracle",
-            "sample": f"full workload ({parts}, numpy float64) x {reps} repetitions, "
-                      f"{el:.1f} s wall",
-            "value_1_thread": one}
+            "sample": f"full workload ({parts}, numpy float64): 1 warm-up, then the minimum "
+                      f"of {runs} runs ({t_all * 1e3:.1f} ms per run)",
+            "value_1_thread": one, "host_cpu_count": os.cpu_count(), "host_cpu_model": cpu_model()}
 
 
 def measured_traffic(workload):
@@ -232,18 +249,40 @@ def measured_traffic(workload):
     return round(t["traffic_bytes_per_launch"])
 
 
+def measured_mfma_util(workload):
+    """Mean MfmaUtil (percent of cycles the MFMA units are busy) of the PCR
+    level launches and of the tail pass, from the committed rocprofv3
+    summary of this workload, or None if there is none or the kernel source
+    changed since it was taken."""
+    from paper_2309_16318_amd import pmc_traffic
+
+    fn = os.path.join(ROOT, "profiles", f"pcr_level_mfma_util_{workload}.json")
+    if not os.path.exists(fn):
+        return None
+    with open(fn) as f:
+        t = json.load(f)
+    if t.get("kernel_source_sha256") != pmc_traffic.kernel_source_sha256():
+        return None
+    return {"pcr_level_pct": t.get("pcr_level_mfma_util_pct"),
+            "pcr_tail_pct": t.get("pcr_tail_mfma_util_pct")}
+
+
 def roofline(cls, w):
     """Roofline position of one kernel class from the library's counts:
     algorithmic flops and bytes of its launches over their summed event
     time; MFMA-bound at an intensity above the ridge (or at w >= 64)."""
     intensity = cls["flops"] / max(cls["bytes"], 1.0)
+    tflops = cls["flops"] / (cls["ms"] * 1e-3) / 1e12
+    gbs = cls["bytes"] / (cls["ms"] * 1e-3) / 1e9
+    # both positions, so that a w <= 32 class placed on the MFMA side still
+    # shows its fraction of the HBM peak (and the other way round)
+    both = {"frac_of_mfma_peak": round(tflops / PEAK_FP32_TFLOPS, 4),
+            "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
     if intensity >= RIDGE or w >= 64:
-        achieved = cls["flops"] / (cls["ms"] * 1e-3) / 1e12
-        return {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4)}
-    achieved = cls["bytes"] / (cls["ms"] * 1e-3) / 1e9
-    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-            "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+        return {"bound": "mfma", "achieved": round(tflops, 3), "peak": PEAK_FP32_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(tflops / PEAK_FP32_TFLOPS, 4), **both}
+    return {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), **both}
 
 
 def main():
@@ -283,6 +322,7 @@ def main():
     value = wl.B * wl.L / (el / args.steps)
     roof = roofline(prof["pcr_level"], wl.w)
     roof["traffic"] = measured_traffic(wl.name)
+    roof["mfma_util"] = measured_mfma_util(wl.name)
     roof["alg_bytes_per_launch"] = round(prof["pcr_level"]["bytes"] /
                                          max(prof["pcr_level"]["launches"], 1))
     roof["kernel"] = "pcr_level"

@@ -13,10 +13,21 @@
  *   - Indices are 0-based.  Layer l = 0..L-1 maps Z[:, l-1] to Z[:, l] with
  *     Z[:, -1] := z0 (an input).  J_l = dZ[:, l] / dZ[:, l-1].
  *   - Every array pointer is a DEVICE pointer to contiguous, row-major float32
- *     memory owned by the caller.  The library never allocates device memory;
- *     all scratch lives in the caller's `workspace` (size from
- *     deeppcr_workspace_bytes), which must not overlap any other argument.
- *     One workspace must not be used by two calls that run concurrently.
+ *     memory owned by the caller, starting on a 16-byte boundary (the kernels
+ *     load rows as 16-byte vectors; a misaligned pointer returns
+ *     DEEPPCR_EINVAL).  The library never allocates device memory; all
+ *     scratch lives in the caller's `workspace` (size from
+ *     deeppcr_workspace_bytes, also 16-byte aligned), which must not overlap
+ *     any other argument.  One workspace must not be used by two calls that
+ *     run concurrently.
+ *   - Host-side state.  The first Newton call (the forward entry points and
+ *     deeppcr_newton_step) of a host thread allocates one pinned, mapped host
+ *     buffer of 3 KiB for that thread's per-iteration read-back of the
+ *     convergence measures; it is reused by the thread's later calls and
+ *     freed by deeppcr_release_thread_state().  The text of the last error
+ *     and the instrumentation state are also per host thread.  Nothing else
+ *     persists between calls, so calls from different host threads on
+ *     different workspaces are independent.
  *   - All GPU work is enqueued on `stream` (a hipStream_t passed as void*;
  *     NULL is the default stream).  pcr_solve_block_bidiag and
  *     deeppcr_mlp_backward return without waiting for the GPU;
@@ -81,6 +92,12 @@ const char* deeppcr_status_string(int status);
 /* Text of the last DEEPPCR_EHIP error raised on the calling thread. */
 const char* deeppcr_last_error(void);
 
+/* Frees what the library holds for the calling host thread: its pinned
+ * read-back buffer and its instrumentation events (after waiting for the
+ * recorded ones).  Call it before a thread that used the library ends, or
+ * before the process unloads the library; later calls allocate again. */
+void deeppcr_release_thread_state(void);
+
 /*
  * Standalone block-bidiagonal solve by Parallel Cyclic Reduction
  * (Sec. 3, Alg. 1 and Eqs. 4-6; the transposed form is the system of
@@ -106,16 +123,21 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x,
  * current iterate Z the caller supplies, for every step in parallel, the step
  * values F[b, l] = f_l(Z[b, l-1]) (Z[b, -1] being the fixed start) and the
  * Jacobians J[b, l] = df_l/dz at Z[b, l-1]; the library forms the residual
- * r = F - Z, solves the block-bidiagonal system of Eq. 3 for dZ by PCR and
- * applies Z += dZ.  J[b, 0] is never read.
+ * r = F - Z, solves the block-bidiagonal system of Eq. 3 for dZ by PCR,
+ * applies Z += dZ and tests the update with the rule of
+ * deeppcr_mlp_forward: max|dZ| < tol * max(1, max|Z|).  J[b, 0] is never read.
  *   J [B, L, w, w], F [B, L, w]  inputs;  Z [B, L, w] input and output
+ *   tol            >= 0 and finite; 0 never reports convergence (a caller
+ *                  running a fixed number of iterations ignores ENOCONV)
  *   residual_out   (host, may be NULL) max |F - Z| before the update
  *   max_update_out (host, may be NULL) max |dZ|;  max_abs_out: max |Z| after it
- * Returns DEEPPCR_ENONFINITE if any of the three is NaN/Inf.  Waits for the GPU
- * once.  workspace_bytes >= deeppcr_workspace_bytes(DEEPPCR_OP_PCR, B, L, w).
+ * Returns DEEPPCR_OK when the update met the tolerance (the iteration has
+ * converged), DEEPPCR_ENOCONV when it did not (the caller iterates again),
+ * DEEPPCR_ENONFINITE if any of the three measures is NaN/Inf.  Waits for the
+ * GPU once.  workspace_bytes >= deeppcr_workspace_bytes(DEEPPCR_OP_PCR, B, L, w).
  */
 int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, int w,
-                        void* workspace, size_t workspace_bytes, float* residual_out,
+                        float tol, void* workspace, size_t workspace_bytes, float* residual_out,
                         float* max_update_out, float* max_abs_out, void* stream);
 
 /*
@@ -297,7 +319,8 @@ int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, con
  * them, e.g. the levels of one PCR sweep) share one event pair, so the time
  * of such a run includes the gaps between its kernels but no event overhead
  * per kernel; where a run of one class follows a run of another, one event
- * ends the first and starts the second.  Not thread-safe.
+ * ends the first and starts the second.  The state is per host thread: a
+ * thread's enable, select, reset and read see only that thread's launches.
  */
 enum {
     DEEPPCR_KCLASS_PCR_LEVEL = 0,  /* one PCR level (Alg. 1 inner parfor)      */

@@ -84,6 +84,15 @@ def seq_sample(p: dict, zT, eps):
     return Z
 
 
+def initial_guess(p: dict, zT, eps):
+    """Start of Newton on the denoising chain (App. F.2): every row holds the
+    first step's output f_0(z_T).  Returns [B, L, w]."""
+    eps = _f64(eps)
+    L = eps.shape[1]
+    f0 = step(p, 0, _f64(zT), eps[:, 0])
+    return np.repeat(f0[:, None, :], L, axis=1)
+
+
 def newton_sample(p: dict, zT, eps, tol: float, max_iter: int, Z_init=None, solve=seq_solve):
     """Newton on the denoising chain (Sec. 2, Eqs. 2-3) with the update rule
     max|dZ| < tol * max(1, max|Z|); start Z_init or f_0(zT) in every row
@@ -92,7 +101,7 @@ def newton_sample(p: dict, zT, eps, tol: float, max_iter: int, Z_init=None, solv
     B, L, w = eps.shape
     zT = _f64(zT)
     if Z_init is None:
-        Z = np.repeat(step(p, 0, zT, eps[:, 0])[:, None, :], L, axis=1)
+        Z = initial_guess(p, zT, eps)
     else:
         Z = _f64(Z_init).copy()
     hist = []

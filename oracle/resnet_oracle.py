@@ -124,6 +124,16 @@ def expand_blocks(act: int, skip: int, W, bias, z0, X):
     return Z
 
 
+def resnet_initial_guess(act: int, skip: int, W, bias, z0):
+    """Start of Newton on the block chain: App. F.2 copies the output of the
+    first step into every unknown; the first step of the collapsed chain is
+    the first block F_0, so every X_g starts at F_0(z0).  Returns X [B, L/s, w]."""
+    W, bias, z0 = _f64(W), _f64(bias), _f64(z0)
+    G = W.shape[0] // skip
+    f0 = group_step(act, skip, W, bias, 0, z0)
+    return np.repeat(f0[:, None, :], G, axis=1)
+
+
 def resnet_newton_forward(act: int, skip: int, W, bias, z0, tol: float, max_iter: int,
                           Z_init=None, solve=seq_solve):
     """Newton on the collapsed system (App. A.3 with Sec. 2, Eqs. 2-3).
@@ -137,11 +147,9 @@ def resnet_newton_forward(act: int, skip: int, W, bias, z0, tol: float, max_iter
     Returns (Z [B, L, w], solves, converged, [max|dX| per iteration]).
     """
     W, bias, z0 = _f64(W), _f64(bias), _f64(z0)
-    L = W.shape[0]
-    G = L // skip
+    G = W.shape[0] // skip
     if Z_init is None:
-        f0 = group_step(act, skip, W, bias, 0, z0)
-        X = np.repeat(f0[:, None, :], G, axis=1)
+        X = resnet_initial_guess(act, skip, W, bias, z0)
     else:
         X = _f64(Z_init)[:, skip - 1::skip].copy()
     history = []

@@ -6,6 +6,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <vector>
 
 #include "../../include/deeppcr.h"
@@ -45,6 +46,9 @@ struct ProfRec {
     bool share0;  // e0 is the end event of the record before (owned there)
 };
 
+// Per host thread: the instrumentation of a thread sees only the launches
+// that thread makes (enable, select, reset and read act on the calling
+// thread's state).
 struct Prof {
     bool on = false;
     unsigned mask = ~0u;  // classes that are timed
@@ -56,7 +60,7 @@ struct Prof {
     double bytes[DEEPPCR_KCLASS_COUNT] = {};
     double flops[DEEPPCR_KCLASS_COUNT] = {};
 };
-Prof g_prof;
+thread_local Prof g_prof;
 
 hipEvent_t take_event() {
     if (!g_prof.pool.empty()) {
@@ -129,7 +133,12 @@ hipError_t timed(int kclass, double bytes, double flops, hipStream_t st, F&& lau
         if (e != hipSuccess) return e;
     }
     hipEvent_t e0 = take_event(), e1 = take_event();
-    if (!e0 || !e1) return launch();
+    if (!e0 || !e1) {
+        // no event pair: run untimed and keep whichever event was obtained
+        if (e0) g_prof.pool.push_back(e0);
+        if (e1) g_prof.pool.push_back(e1);
+        return launch();
+    }
     hipError_t e = hipEventRecord(e0, st);
     if (e != hipSuccess) return e;
     e = launch();
@@ -216,6 +225,15 @@ int num_passes(int B, int L, int w) {
     const int kt = tail_levels(B, L, w, 0);
     const int K1 = num_levels(L) - kt;
     return (two_level(B, L, w) ? (K1 + 1) / 2 : K1) + (kt > 0 ? 1 : 0);
+}
+
+// Every array argument must start on a 16-byte boundary (the kernels load
+// rows of blocks, states and weights as 16-byte vectors); NULL passes (the
+// null checks are separate).
+bool aligned(std::initializer_list<const void*> ps) {
+    for (const void* p : ps)
+        if (((uintptr_t)p & 15u) != 0) return false;
+    return true;
 }
 
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
@@ -355,17 +373,19 @@ Ws carve(void* workspace, const Layout& lo) {
 }
 
 // Pinned host copy of the reduction area for the per-iteration read-back
-// (mapped, so that a kernel can also write it directly).
+// (mapped, so that a kernel can also write it directly).  Allocated on the
+// first Newton call of a host thread; deeppcr_release_thread_state frees it.
+thread_local unsigned* g_host_words = nullptr;
+
 unsigned* host_words() {
-    thread_local unsigned* words = nullptr;
-    if (!words) {
+    if (!g_host_words) {
         void* p = nullptr;
         if (hipHostMalloc(&p, kRedWords * sizeof(unsigned),
                           hipHostMallocMapped | hipHostMallocPortable) != hipSuccess)
             return nullptr;
-        words = (unsigned*)p;
+        g_host_words = (unsigned*)p;
     }
-    return words;
+    return g_host_words;
 }
 
 // Max over kRedShards slots.
@@ -492,6 +512,7 @@ int check_forward_args(const float* W, const float* bias, const float* z0, float
                        int L, int w, int layer, float alpha) {
     if (!W || !bias || !z0 || !Z || !workspace || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
     if (layer < 0 || layer >= kNumLayerKinds || !std::isfinite(alpha)) return DEEPPCR_EINVAL;
+    if (!aligned({W, bias, z0, Z, Z_init, workspace})) return DEEPPCR_EINVAL;
     const Layout lo = layout(DEEPPCR_OP_FWD, B, L, w);
     if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
     const size_t nv = (size_t)B * L * w * 4;
@@ -620,6 +641,9 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
     return rule.tol > 0.f ? DEEPPCR_ENOCONV : DEEPPCR_OK;
 }
 
+int pcr_solve_run(const float* J, const float* r, float* x, int B, int L, int w, int transpose,
+                  void* workspace, hipStream_t st);
+
 }  // namespace
 
 extern "C" {
@@ -649,6 +673,7 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x, int B, int 
     const SpanGuard span_guard;
     if (!J || !r || !x || !workspace || !sizes_ok(B, L, w) || (transpose != 0 && transpose != 1))
         return DEEPPCR_EINVAL;
+    if (!aligned({J, r, x, workspace})) return DEEPPCR_EINVAL;
     const Layout lo = layout(DEEPPCR_OP_PCR, B, L, w);
     if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
     const size_t nJ = (size_t)B * L * w * w * 4, nv = (size_t)B * L * w * 4;
@@ -656,8 +681,17 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x, int B, int 
         overlaps(workspace, lo.total, r, nv) || overlaps(workspace, lo.total, x, nv))
         return DEEPPCR_EINVAL;
     if ((x != r) && overlaps(x, nv, r, nv)) return DEEPPCR_EINVAL;
+    return pcr_solve_run(J, r, x, B, L, w, transpose, workspace, (hipStream_t)stream);
+}
 
-    hipStream_t st = (hipStream_t)stream;
+}  // extern "C"
+
+namespace {
+
+// The solve behind pcr_solve_block_bidiag, after validation.
+int pcr_solve_run(const float* J, const float* r, float* x, int B, int L, int w, int transpose,
+                  void* workspace, hipStream_t st) {
+    const Layout lo = layout(DEEPPCR_OP_PCR, B, L, w);
     Ws ws = carve(workspace, lo);
     const long long bw2 = (long long)L * w * w, w2 = (long long)w * w;
     BlockSrc A0;
@@ -679,11 +713,17 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x, int B, int 
     return DEEPPCR_OK;
 }
 
-int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, int w,
+}  // namespace
+
+extern "C" {
+
+int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, int w, float tol,
                         void* workspace, size_t workspace_bytes, float* residual_out,
                         float* max_update_out, float* max_abs_out, void* stream) {
     const SpanGuard span_guard;
     if (!J || !F || !Z || !workspace || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
+    if (!(tol >= 0.f) || !std::isfinite(tol)) return DEEPPCR_EINVAL;
+    if (!aligned({J, F, Z, workspace})) return DEEPPCR_EINVAL;
     const Layout lo = layout(DEEPPCR_OP_PCR, B, L, w);
     if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
     const size_t nJ = (size_t)B * L * w * w * 4, nv = (size_t)B * L * w * 4;
@@ -720,7 +760,10 @@ int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, 
     if (max_update_out) *max_update_out = bits_to_float(mx);
     if (max_abs_out) *max_abs_out = bits_to_float(mz);
     if (mr >= 0x7f800000u || mx >= 0x7f800000u || mz >= 0x7f800000u) return DEEPPCR_ENONFINITE;
-    return DEEPPCR_OK;
+    // the stopping test of the forward entry point, on this step's update
+    const float m = bits_to_float(mx), zmax = bits_to_float(mz);
+    if (tol > 0.f && m < tol * (zmax > 1.f ? zmax : 1.f)) return DEEPPCR_OK;
+    return DEEPPCR_ENOCONV;
 }
 
 int deeppcr_mlp_forward(const float* W, const float* bias, const float* z0, float* Z, int B,
@@ -764,6 +807,7 @@ int deeppcr_mlp_backward(const float* W, const float* bias, const float* z0, con
         return DEEPPCR_EINVAL;
     if (layer < 0 || layer >= kNumLayerKinds) return DEEPPCR_EINVAL;
     if (!std::isfinite(alpha)) return DEEPPCR_EINVAL;
+    if (!aligned({W, bias, z0, Z, G, Lambda, dz0, dW, db, workspace})) return DEEPPCR_EINVAL;
     const Layout lo = layout(DEEPPCR_OP_BWD, B, L, w);
     if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
     const size_t nv = (size_t)B * L * w * 4, nW = (size_t)L * w * w * 4;
@@ -826,6 +870,7 @@ int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, f
     if (!W || !bias || !z0 || !Z || !workspace || !resnet_shape_ok(B, L, w, skip, act))
         return DEEPPCR_EINVAL;
     if (!(tol >= 0.f) || !std::isfinite(tol) || max_iter < 1) return DEEPPCR_EINVAL;
+    if (!aligned({W, bias, z0, Z, Z_init, workspace})) return DEEPPCR_EINVAL;
     const int G = L / skip;
     const Layout lo = resnet_layout(DEEPPCR_OP_FWD, B, G, w);
     if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
@@ -913,6 +958,7 @@ int deeppcr_resnet_backward(const float* W, const float* z0, const float* Z, con
     if (!W || !z0 || !Z || !G_ || !Lambda || !dz0 || !dW || !db || !workspace ||
         !resnet_shape_ok(B, L, w, skip, act))
         return DEEPPCR_EINVAL;
+    if (!aligned({W, z0, Z, G_, Lambda, dz0, dW, db, workspace})) return DEEPPCR_EINVAL;
     const int G = L / skip;
     const Layout lo = resnet_layout(DEEPPCR_OP_BWD, B, G, w);
     if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
@@ -966,6 +1012,7 @@ int deeppcr_resnet_seq_forward(const float* W, const float* bias, const float* z
     if (!W || !bias || !z0 || !Z || !resnet_shape_ok(B, L, w, skip, act) ||
         (launch_per_layer != 0 && launch_per_layer != 1))
         return DEEPPCR_EINVAL;
+    if (!aligned({W, bias, z0, Z})) return DEEPPCR_EINVAL;
     const size_t nv = (size_t)B * L * w * 4;
     if (overlaps(Z, nv, W, (size_t)L * w * w * 4) || overlaps(Z, nv, bias, (size_t)L * w * 4) ||
         overlaps(Z, nv, z0, (size_t)B * w * 4))
@@ -992,6 +1039,7 @@ int deeppcr_resnet_seq_backward(const float* W, const float* z0, const float* Z,
     if (!W || !z0 || !Z || !G || !Lambda || !dz0 || !resnet_shape_ok(B, L, w, skip, act) ||
         (launch_per_layer != 0 && launch_per_layer != 1))
         return DEEPPCR_EINVAL;
+    if (!aligned({W, z0, Z, G, Lambda, dz0})) return DEEPPCR_EINVAL;
     const size_t nv = (size_t)B * L * w * 4, nb = (size_t)B * w * 4;
     const void* ins[] = {W, z0, Z, G};
     const size_t nins[] = {(size_t)L * w * w * 4, nb, nv, nb};
@@ -1020,6 +1068,7 @@ int deeppcr_seq_forward(const float* W, const float* bias, const float* z0, floa
     if (!W || !bias || !z0 || !Z || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
     if (layer < 0 || layer >= kNumLayerKinds || !std::isfinite(alpha)) return DEEPPCR_EINVAL;
     if (launch_per_layer != 0 && launch_per_layer != 1) return DEEPPCR_EINVAL;
+    if (!aligned({W, bias, z0, Z})) return DEEPPCR_EINVAL;
     const size_t nv = (size_t)B * L * w * 4;
     if (overlaps(Z, nv, W, (size_t)L * w * w * 4) || overlaps(Z, nv, bias, (size_t)L * w * 4) ||
         overlaps(Z, nv, z0, (size_t)B * w * 4))
@@ -1045,6 +1094,7 @@ int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, con
     if (!W || !bias || !z0 || !Z || !G || !Lambda || !dz0 || !sizes_ok(B, L, w)) return DEEPPCR_EINVAL;
     if (layer < 0 || layer >= kNumLayerKinds || !std::isfinite(alpha)) return DEEPPCR_EINVAL;
     if (launch_per_layer != 0 && launch_per_layer != 1) return DEEPPCR_EINVAL;
+    if (!aligned({W, bias, z0, Z, G, Lambda, dz0})) return DEEPPCR_EINVAL;
     const size_t nv = (size_t)B * L * w * 4, nb = (size_t)B * w * 4;
     const void* ins[] = {W, bias, z0, Z, G};
     const size_t nins[] = {(size_t)L * w * w * 4, (size_t)L * w * 4, nb, nv, nb};
@@ -1065,6 +1115,22 @@ int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, con
         if (e != hipSuccess) return hip_fail(e, "seq_backward");
     }
     return DEEPPCR_OK;
+}
+
+void deeppcr_release_thread_state(void) {
+    (void)prof_break();
+    for (auto& p : g_prof.pending) {
+        (void)hipEventSynchronize(p.e1);
+        if (!p.share0) (void)hipEventDestroy(p.e0);
+        (void)hipEventDestroy(p.e1);
+    }
+    g_prof.pending.clear();
+    for (hipEvent_t e : g_prof.pool) (void)hipEventDestroy(e);
+    g_prof.pool.clear();
+    if (g_host_words) {
+        (void)hipHostFree(g_host_words);
+        g_host_words = nullptr;
+    }
 }
 
 int deeppcr_profile_enable(int on) {

@@ -37,8 +37,9 @@ SIGNATURES = {
                                        _c.c_size_t, _c.POINTER(_c.c_int),
                                        _c.POINTER(_c.c_float), _c.c_void_p]),
     "deeppcr_newton_step": (_c.c_int, [_c.c_void_p] * 3 + [_c.c_int] * 3 +
-                            [_c.c_void_p, _c.c_size_t] + [_c.POINTER(_c.c_float)] * 3 +
-                            [_c.c_void_p]),
+                            [_c.c_float, _c.c_void_p, _c.c_size_t] +
+                            [_c.POINTER(_c.c_float)] * 3 + [_c.c_void_p]),
+    "deeppcr_release_thread_state": (None, []),
     "deeppcr_mlp_forward_residual": (_c.c_int, [_c.c_void_p, _c.c_void_p, _c.c_void_p,
                                                 _c.c_void_p, _c.c_int, _c.c_int, _c.c_int,
                                                 _c.c_int, _c.c_float, _c.c_float, _c.c_float,
@@ -199,19 +200,21 @@ class NewtonStepResult:
     status: int
 
 
-def deeppcr_newton_step(J, F, Z, workspace=None, stream=None) -> NewtonStepResult:
+def deeppcr_newton_step(J, F, Z, tol: float = 1e-5, workspace=None,
+                        stream=None) -> NewtonStepResult:
     """One Newton + PCR iteration for caller-evaluated step values F and
-    Jacobians J at the iterate Z (updated in place)."""
+    Jacobians J at the iterate Z (updated in place); ``status`` is OK once
+    the update meets ``tol``, ENOCONV before, ENONFINITE on a NaN/Inf."""
     B, L, w = Z.shape
     _check(J, (B, L, w, w), "J")
     _check(F, (B, L, w), "F")
     _check(Z, (B, L, w), "Z")
     ws, nbytes = _workspace(OP_PCR, B, L, w, workspace, Z.device)
     res, mx, mz = ctypes.c_float(0.0), ctypes.c_float(0.0), ctypes.c_float(0.0)
-    st = lib().deeppcr_newton_step(_ptr(J), _ptr(F), _ptr(Z), B, L, w, _ptr(ws), nbytes,
-                                   ctypes.byref(res), ctypes.byref(mx), ctypes.byref(mz),
+    st = lib().deeppcr_newton_step(_ptr(J), _ptr(F), _ptr(Z), B, L, w, float(tol), _ptr(ws),
+                                   nbytes, ctypes.byref(res), ctypes.byref(mx), ctypes.byref(mz),
                                    _stream(stream))
-    if st not in (OK, ENONFINITE):
+    if st not in (OK, ENOCONV, ENONFINITE):
         raise DeepPCRError(st, "deeppcr_newton_step")
     return NewtonStepResult(res.value, mx.value, mz.value, st)
 
@@ -416,6 +419,11 @@ def deeppcr_seq_backward(W, bias, z0, Z, G, layer: int = TANH_MLP, alpha: float 
     if st != OK:
         raise DeepPCRError(st, "deeppcr_seq_backward")
     return Lambda, dz0
+
+
+def release_thread_state() -> None:
+    """Frees the calling thread's pinned read-back buffer and profiler events."""
+    lib().deeppcr_release_thread_state()
 
 
 # ---------------------------------------------------------- instrumentation

@@ -39,12 +39,12 @@ def newton_generic(step_fn, jac_fn, z_start, L: int, tol: float = 1e-5, max_iter
         Zprev = torch.cat([z_start[:, None, :], Z[:, :-1, :]], dim=1)
         F = step_fn(Zprev).contiguous()
         J = jac_fn(Zprev).contiguous()
-        r = deeppcr.deeppcr_newton_step(J, F, Z, workspace=workspace, stream=stream)
+        r = deeppcr.deeppcr_newton_step(J, F, Z, tol=tol, workspace=workspace, stream=stream)
         last = r.max_update
-        if r.status != deeppcr.OK:
+        # the library's test: OK once converged, ENOCONV to go on
+        if r.status != deeppcr.ENOCONV:
             return deeppcr.ForwardResult(Z, k, last, r.status)
-        if tol > 0 and r.max_update < tol * max(1.0, r.max_abs):
-            return deeppcr.ForwardResult(Z, k, last, deeppcr.OK)
+    # tol = 0 asks for exactly max_iter iterations, which is not a failure
     return deeppcr.ForwardResult(Z, max_iter, last, deeppcr.ENOCONV if tol > 0 else deeppcr.OK)
 
 

@@ -77,7 +77,7 @@ def test_pcr_solve_rejects_invalid_arguments():
     assert _pcr(x=ctypes.c_void_p(P[0].value + 64)) == E
     assert _pcr(ws=ctypes.c_void_p(P[1].value - 16)) == E
     # x partially overlapping r (exact aliasing is allowed)
-    assert _pcr(x=ctypes.c_void_p(P[1].value + 4)) == E
+    assert _pcr(x=ctypes.c_void_p(P[1].value + 16)) == E
     assert _pcr(nws=deeppcr.workspace_bytes(deeppcr.OP_PCR, 2, 8, 4) - 1) == deeppcr.EWORKSPACE
 
 
@@ -102,7 +102,7 @@ def test_forward_rejects_invalid_arguments():
     assert _fwd(tol=float("inf")) == E
     assert _fwd(alpha=float("nan")) == E
     assert _fwd(w=200) == E
-    assert _fwd(Zi=ctypes.c_void_p(P[3].value + 4)) == E     # partial overlap with Z
+    assert _fwd(Zi=ctypes.c_void_p(P[3].value + 16)) == E     # partial overlap with Z
     assert _fwd(ws=ctypes.c_void_p(P[3].value)) == E          # workspace over Z
     assert _fwd(nws=100) == deeppcr.EWORKSPACE
 
@@ -131,7 +131,7 @@ def test_forward_residual_rejects_invalid_arguments():
     assert _fwd_res(alpha=float("nan")) == E
     assert _fwd_res(B=0) == E
     assert _fwd_res(w=129) == E
-    assert _fwd_res(Zi=ctypes.c_void_p(P[3].value + 4)) == E
+    assert _fwd_res(Zi=ctypes.c_void_p(P[3].value + 16)) == E
     assert _fwd_res(ws=ctypes.c_void_p(P[0].value)) == E      # workspace over W
     assert _fwd_res(nws=100) == deeppcr.EWORKSPACE
 
@@ -179,7 +179,7 @@ def test_sequential_passes_reject_invalid_arguments():
     assert f(P[0], P[1], P[2], P[3], 2, 8, 0, 0, 1.0, 0, None) == E
     assert f(P[0], P[1], P[2], P[3], 2, 8, 4, 6, 1.0, 0, None) == E
     assert f(P[0], P[1], P[2], P[3], 2, 8, 4, 0, 1.0, 2, None) == E
-    assert f(P[0], P[1], P[2], ctypes.c_void_p(P[0].value + 4), 2, 8, 4, 0, 1.0, 0, None) == E
+    assert f(P[0], P[1], P[2], ctypes.c_void_p(P[0].value + 16), 2, 8, 4, 0, 1.0, 0, None) == E
     g = deeppcr.lib().deeppcr_seq_backward
     assert g(*P[:6], None, 2, 8, 4, 0, 1.0, 0, None) == E
     assert g(*P[:7], 2, 8, 4, -1, 1.0, 0, None) == E
@@ -221,7 +221,7 @@ def test_resnet_forward_rejects_invalid_arguments():
     assert _rfwd(tol=float("nan")) == E
     assert _rfwd(max_iter=0) == E
     assert _rfwd(w=129) == E
-    assert _rfwd(Zi=ctypes.c_void_p(P[3].value + 4)) == E
+    assert _rfwd(Zi=ctypes.c_void_p(P[3].value + 16)) == E
     assert _rfwd(ws=ctypes.c_void_p(P[1].value)) == E
     assert _rfwd(nws=100) == deeppcr.EWORKSPACE
 
@@ -268,8 +268,8 @@ def test_newton_step_rejects_invalid_arguments():
     E = deeppcr.EINVAL
     f = deeppcr.lib().deeppcr_newton_step
 
-    def call(J=P[0], F=P[1], Z=P[2], B=2, L=8, w=4, ws=P[3], nws=BIG):
-        return f(J, F, Z, B, L, w, ws, nws, None, None, None, None)
+    def call(J=P[0], F=P[1], Z=P[2], B=2, L=8, w=4, tol=1e-5, ws=P[3], nws=BIG):
+        return f(J, F, Z, B, L, w, tol, ws, nws, None, None, None, None)
 
     assert call(J=None) == E
     assert call(F=None) == E
@@ -280,3 +280,61 @@ def test_newton_step_rejects_invalid_arguments():
     assert call(Z=P[1]) == E                                # Z over F
     assert call(ws=ctypes.c_void_p(P[2].value - 16)) == E   # workspace runs into Z
     assert call(nws=deeppcr.workspace_bytes(deeppcr.OP_PCR, 2, 8, 4) - 1) == deeppcr.EWORKSPACE
+    for bad in (-1e-5, float("nan"), float("inf")):
+        assert call(tol=bad) == E
+    for k in ("J", "F", "Z", "ws"):
+        assert call(**{k: ctypes.c_void_p(dict(J=P[0], F=P[1], Z=P[2], ws=P[3])[k].value + 4)}) == E
+
+
+def _misaligned(p, off=4):
+    return ctypes.c_void_p(p.value + off)
+
+
+def test_every_entry_point_rejects_misaligned_pointers():
+    """Every float array and the workspace must start on a 16-byte boundary;
+    offsets of 4 and 8 bytes are rejected before any HIP call."""
+    E = deeppcr.EINVAL
+    for off in (4, 8):
+        for i in range(4):
+            args = dict(J=P[0], r=P[1], x=P[2], ws=P[3])
+            k = list(args)[i]
+            args[k] = _misaligned(args[k], off)
+            assert _pcr(**args) == E, k
+        for k, base in (("W", P[0]), ("b", P[1]), ("z0", P[2]), ("Z", P[3]), ("ws", P[5])):
+            assert _fwd(**{k: _misaligned(base, off)}) == E, k
+            assert _fwd_res(**{k: _misaligned(base, off)}) == E, k
+            assert _rfwd(**{k: _misaligned(base, off)}) == E, k
+        assert _fwd(Zi=_misaligned(P[6], off)) == E
+        for i in range(9):
+            p = list(P[:9])
+            p[i] = _misaligned(p[i], off)
+            assert _bwd(p) == E, i
+        assert _bwd(ws=_misaligned(P[10], off)) == E
+        for i in range(8):
+            p = list(P[:8])
+            p[i] = _misaligned(p[i], off)
+            assert _rbwd(p) == E, i
+        sf = deeppcr.lib().deeppcr_seq_forward
+        sb = deeppcr.lib().deeppcr_seq_backward
+        rf = deeppcr.lib().deeppcr_resnet_seq_forward
+        rb = deeppcr.lib().deeppcr_resnet_seq_backward
+        for i in range(4):
+            p = list(P[:4])
+            p[i] = _misaligned(p[i], off)
+            assert sf(*p, 2, 8, 4, 0, 1.0, 0, None) == E, i
+            assert rf(*p, 2, 8, 4, 4, 2, 0, None) == E, i
+        for i in range(7):
+            p = list(P[:7])
+            p[i] = _misaligned(p[i], off)
+            assert sb(*p, 2, 8, 4, 0, 1.0, 0, None) == E, i
+        for i in range(6):
+            p = list(P[:6])
+            p[i] = _misaligned(p[i], off)
+            assert rb(*p, 2, 8, 4, 4, 2, 0, None) == E, i
+
+
+def test_release_thread_state_without_a_gpu():
+    """Nothing was allocated on this thread (no Newton call ran): releasing
+    is a no-op and can be repeated."""
+    deeppcr.release_thread_state()
+    deeppcr.release_thread_state()

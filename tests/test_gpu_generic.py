@@ -47,14 +47,29 @@ def test_newton_step_is_one_oracle_iteration(dev, w, L, B):
     F = rng.standard_normal((B, L, w)).astype(np.float32)
     Z = rng.standard_normal((B, L, w)).astype(np.float32)
     Zg = g(Z, dev)
-    res = deeppcr.deeppcr_newton_step(g(d["J"], dev), g(F, dev), Zg)
-    assert res.status == deeppcr.OK
+    res = deeppcr.deeppcr_newton_step(g(d["J"], dev), g(F, dev), Zg, tol=0.0)
+    assert res.status == deeppcr.ENOCONV      # tol = 0 never reports convergence
     dZ = oracle.seq_solve(d["J"], F.astype(np.float64) - Z)
     want = Z + dZ
     assert normwise_rel_err(h(Zg), want) <= TOL
     assert res.residual == pytest.approx(float(np.max(np.abs(F.astype(np.float64) - Z))), rel=1e-6)
     assert res.max_update == pytest.approx(float(np.max(np.abs(dZ))), rel=1e-4)
     assert res.max_abs == pytest.approx(float(np.max(np.abs(want))), rel=1e-4)
+
+
+def test_newton_step_applies_the_stopping_test(dev):
+    """The library's test max|dZ| < tol * max(1, max|Z|): a tolerance above
+    the measured ratio reports convergence, one below it does not."""
+    B, L, w = 2, 40, 16
+    d = synth.random_system(B, L, w, seed=2400, scale=0.9)
+    rng = np.random.default_rng(7)
+    F = rng.standard_normal((B, L, w)).astype(np.float32)
+    Z = rng.standard_normal((B, L, w)).astype(np.float32)
+    dZ = oracle.seq_solve(d["J"], F.astype(np.float64) - Z)
+    ratio = float(np.max(np.abs(dZ))) / max(1.0, float(np.max(np.abs(Z + dZ))))
+    for tol, want in ((ratio * 1.01, deeppcr.OK), (ratio * 0.99, deeppcr.ENOCONV)):
+        res = deeppcr.deeppcr_newton_step(g(d["J"], dev), g(F, dev), g(Z, dev), tol=tol)
+        assert res.status == want, (tol, ratio)
 
 
 DIFF_CASES = [(64, 16, 32, 4), (1024, 16, 64, 2), (256, 64, 128, 2), (100, 17, 20, 3),

@@ -2,7 +2,9 @@
 the same seeded float32 inputs.  Tolerance: normwise relative error
 max_b ||got_b - ref_b||_inf / ||ref_b||_inf <= 1e-4 for solves, forward states
 and adjoints; ||.||_inf over the whole tensor for dW, db."""
+import json
 import math
+import os
 import sys
 
 import numpy as np
@@ -10,12 +12,18 @@ import pytest
 
 import oracle
 from paper_2309_16318_amd import deeppcr, synth
-from tests._util import normwise_rel_err
+from tests._util import normwise_rel_err, per_layer_rel_err
 
 pytestmark = pytest.mark.gpu
 TOL = 1e-4
 
 torch = pytest.importorskip("torch")
+
+# Newton solve counts of the oracle on the full-size forward workloads,
+# written by tests/golden/make_newton_counts.py (oracle only).
+with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                       "newton_counts.json")) as _f:
+    NEWTON_COUNTS = json.load(_f)
 
 
 def _say(msg):
@@ -144,9 +152,10 @@ def test_forward_residual_workload(dev):
     assert res.status == deeppcr.OK
     ref = oracle.seq_forward(wl.layer, wl.alpha, d["W"], d["bias"], d["z0"])
     err = normwise_rel_err(h(res.Z), ref)
-    _say(f"  err {err:.3e}; gpu iters {res.iters}")
+    k_ref = NEWTON_COUNTS[wl.name]["solves"]
+    _say(f"  err {err:.3e}; gpu iters {res.iters}, oracle {k_ref}")
     assert err <= TOL
-    assert res.iters <= 12
+    assert NEWTON_COUNTS[wl.name]["converged"] and abs(res.iters - k_ref) <= 1
 
 
 @pytest.mark.parametrize("w,L,B", [(1, 5, 2), (3, 40, 3), (16, 100, 2), (17, 33, 2),
@@ -414,6 +423,20 @@ def _backward_check(d, Z32, dev, layer, alpha, tol=TOL):
             normwise_rel_err(h(dW), rW, axes="all"), normwise_rel_err(h(db), rb, axes="all"))
     _say(f"  backward errs adjoints {errs[0]:.2e} dW {errs[1]:.2e} db {errs[2]:.2e}")
     assert max(errs) <= tol
+    _per_layer_check(h(lam), h(dW), h(db), rl, rW, rb, tol)
+
+
+def _per_layer_check(lam, dW, db, rl, rW, rb, tol=TOL):
+    """The same bound layer by layer, on every layer whose reference norm is
+    at least 1e-6 of the largest (adjoints per system and layer; dW and db
+    per layer), so that an error confined to early layers, whose adjoints
+    are orders of magnitude below the last ones, does not pass unseen."""
+    el, il = per_layer_rel_err(lam, rl, layer_axis=1)
+    eW, iW = per_layer_rel_err(dW, rW, layer_axis=0)
+    eb, ib = per_layer_rel_err(db, rb, layer_axis=0)
+    _say(f"  worst layer: adjoints {el:.2e} at (b, l) {il}, dW {eW:.2e} at l {iW[0]}, "
+         f"db {eb:.2e} at l {ib[0]}")
+    assert max(el, eW, eb) <= tol
 
 
 def adjoint_err(lam, dz0, rl, rz):
@@ -479,6 +502,51 @@ def test_residual_forward_then_backward_workload(dev):
             normwise_rel_err(h(db), rb, axes="all"))
     _say("  errs Z %.2e adjoints %.2e dz0 %.2e dW %.2e db %.2e" % errs)
     assert max(errs) <= TOL
+    _per_layer_check(h(lam), h(dW), h(db), rl, rW, rb)
+    k_ref = NEWTON_COUNTS[wl.name]["solves"]
+    _say(f"  gpu iters {res.iters}, oracle {k_ref}")
+    assert abs(res.iters - k_ref) <= 1
+
+
+# w = 64 with B >= 16 and 513 <= L <= 1024: the last six levels run as one
+# tail pass (strides 16 .. 512), forward (with the Newton update) and
+# backward; residual layers keep the adjoints of early layers in range, so
+# every layer is compared.
+@pytest.mark.parametrize("L,B", [(1000, 16), (600, 20)])
+def test_w64_six_level_tail_forward(dev, L, B):
+    w, layer, alpha = 64, 1, 0.1
+    _say(f"w=64 six-level tail forward L={L} B={B}")
+    d = synth.mlp_inputs(B, L, w, seed=3100 + L)
+    res = _forward(d, dev, layer, alpha)
+    assert res.status == deeppcr.OK
+    ref = oracle.seq_forward(layer, alpha, d["W"], d["bias"], d["z0"])
+    err = normwise_rel_err(h(res.Z), ref)
+    e1, i1 = per_layer_rel_err(h(res.Z), ref, layer_axis=1)
+    _say(f"  err {err:.2e}, worst layer {e1:.2e} at {i1}; gpu iters {res.iters}")
+    assert err <= TOL and e1 <= TOL
+
+
+@pytest.mark.parametrize("L,B,layer,alpha", [(1000, 16, 1, 0.1), (600, 20, 3, 0.2),
+                                             (1024, 16, 0, 1.0)])
+def test_w64_six_level_tail_backward(dev, L, B, layer, alpha):
+    w = 64
+    _say(f"w=64 six-level tail backward L={L} B={B} layer={layer}")
+    d = synth.mlp_inputs(B, L, w, seed=3200 + L + layer)
+    Z32 = oracle.seq_forward(layer, alpha, d["W"], d["bias"], d["z0"]).astype(np.float32)
+    _backward_check(d, Z32, dev, layer, alpha)
+
+
+@pytest.mark.parametrize("transpose", [1, 0])
+def test_pcr_solve_w64_six_level_tail(dev, transpose):
+    B, L, w = 16, 1024, 64
+    _say(f"pcr solve w=64 B={B} L={L} transpose={transpose}")
+    d = synth.random_system(B, L, w, seed=3300 + transpose, scale=0.9)
+    x = h(deeppcr.pcr_solve_block_bidiag(g(d["J"], dev), g(d["r"], dev), transpose=transpose))
+    ref = oracle.seq_solve(d["J"], d["r"], bool(transpose))
+    err = normwise_rel_err(x, ref)
+    e1, i1 = per_layer_rel_err(x, ref, layer_axis=1)
+    _say(f"  err {err:.2e}, worst row {e1:.2e} at {i1}")
+    assert err <= TOL and e1 <= TOL
 
 
 def test_backward_deterministic(dev):

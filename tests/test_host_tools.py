@@ -122,3 +122,39 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert p.returncode == 2
     assert "one GPU" in p.stderr
+
+
+def test_calibration_scales_by_the_copy_and_checks_the_add(tmp_path):
+    # 1 MiB probe: the copy reads 1 MiB in 512 FETCH units (2048 B per unit)
+    # and writes it in 1024 WRITE units; the add reads 0.5 MiB and writes
+    # 0.25 MiB, here measured 1% high on reads
+    cp = "__amd_rocclr_copyBuffer"
+    add = "void at::native::vectorized_elementwise_kernel<4, at::native::AddFunctor<float>>"
+    f = _counter_dir(tmp_path, "f", [(1, cp, "FETCH_SIZE", 512.0),
+                                     (2, add + "(x)", "FETCH_SIZE", 256.0 * 1.01)])
+    w = _counter_dir(tmp_path, "w", [(1, cp, "WRITE_SIZE", 1024.0),
+                                     (2, add + "(x)", "WRITE_SIZE", 256.0)])
+    out = pmc_traffic.calibrate(["--fetch", f, "--write", w, "--mib", "1",
+                                 "--out", str(tmp_path / "c.json")])
+    assert out["fetch_bytes_per_counter_unit"] == pytest.approx(2048.0)
+    assert out["write_bytes_per_counter_unit"] == pytest.approx(1024.0)
+    assert out["add_read_ratio"] == pytest.approx(1.01)
+    assert out["add_write_ratio"] == pytest.approx(1.0)
+    assert json.loads((tmp_path / "c.json").read_text())["add_kernel"].startswith("at::native")
+
+
+def test_mfma_summary_weights_by_dispatch_and_splits_the_tail(tmp_path):
+    pair, tail = "pcr_level2_tile<128, false, false>", "pcr_level_tail<128, 6, true>"
+    rows = [(1, pair, "MfmaUtil", 70.0), (1, pair, "SQ_BUSY_CYCLES", 10.0),
+            (2, pair, "MfmaUtil", 74.0), (2, pair, "SQ_BUSY_CYCLES", 30.0),
+            (3, "pcr_level2_tile_layer<128>", "MfmaUtil", 60.0),
+            (4, tail, "MfmaUtil", 50.0), (5, "other", "MfmaUtil", 1.0)]
+    d = _counter_dir(tmp_path, "m", rows)
+    out = pmc_traffic.mfma(["--workload", "x", "--dir", d, "--out", str(tmp_path / "m.json")])
+    assert out["by_kernel"][pair]["launches"] == 2
+    assert out["by_kernel"][pair]["MfmaUtil"] == pytest.approx(72.0)
+    assert out["by_kernel"][pair]["SQ_BUSY_CYCLES"] == pytest.approx(20.0)
+    assert out["pcr_level_mfma_util_pct"] == pytest.approx((70 + 74 + 60) / 3)
+    assert out["pcr_tail_mfma_util_pct"] == pytest.approx(50.0)
+    assert "other" not in out["by_kernel"]
+    assert out["kernel_source_sha256"] == pmc_traffic.kernel_source_sha256()
