@@ -117,6 +117,32 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x,
                            void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * pcr_solve_block_bidiag without a workspace argument and without any
+ * allocation, for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * The solve, its kernels and its results are those of
+ * pcr_solve_block_bidiag (bit for bit); its scratch is a fixed device array
+ * of DEEPPCR_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, held
+ * from the library's first use on that GPU until the process ends.  The
+ * call allocates nothing (no hipMalloc, no host allocation, no new events, even
+ * with instrumentation enabled) and enqueues only kernels on `stream`.
+ *   J, r, x, B, L, w, transpose as for pcr_solve_block_bidiag.
+ * Returns DEEPPCR_EWORKSPACE when the problem needs more scratch than that
+ * (deeppcr_workspace_bytes(DEEPPCR_OP_PCR, B, L, w) >
+ * DEEPPCR_NOALLOC_SCRATCH_BYTES; e.g. B L w (w + 1) <= about 8.3 million at
+ * 64 MiB), before any HIP call.
+ * All calls on one GPU share its scratch array: two calls that overlap in
+ * time on one GPU (on different streams, or from different host threads)
+ * race and give wrong results; serialise them.  The solve needs no part of
+ * the scratch to start at zero.
+ */
+#define DEEPPCR_NOALLOC_SCRATCH_BYTES (64u << 20)
+int pcr_solve_block_bidiag_noalloc(const float* J, const float* r, float* x,
+                                   int B, int L, int w, int transpose, void* stream);
+/* The size of that scratch array, DEEPPCR_NOALLOC_SCRATCH_BYTES. */
+size_t deeppcr_noalloc_scratch_bytes(void);
+
+/*
  * One Newton iteration for a step function the caller evaluates (Sec. 2,
  * Eqs. 1-3; the paper's general setting of z_l = f_l(z_{l-1}), e.g. the
  * denoising steps of App. A.4 whose Jacobians come from autograd).  At the

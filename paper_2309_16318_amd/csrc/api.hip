@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstring>
 #include <initializer_list>
+#include <mutex>
 #include <vector>
 
 #include "../../include/deeppcr.h"
@@ -688,7 +689,9 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x, int B, int 
 
 namespace {
 
-// The solve behind pcr_solve_block_bidiag, after validation.
+// The solve behind pcr_solve_block_bidiag and its no-allocation variant,
+// after validation: the workspace (or the library's scratch) is carved by
+// the same layout.
 int pcr_solve_run(const float* J, const float* r, float* x, int B, int L, int w, int transpose,
                   void* workspace, hipStream_t st) {
     const Layout lo = layout(DEEPPCR_OP_PCR, B, L, w);
@@ -715,7 +718,69 @@ int pcr_solve_run(const float* J, const float* r, float* x, int B, int L, int w,
 
 }  // namespace
 
+// ------------------------------------------------- no-allocation variant
+// The scratch of pcr_solve_block_bidiag_noalloc: a fixed device array in
+// place of the caller's workspace.  Each GPU holds its own copy (allocated
+// when the library's code object is loaded on that GPU, kept until the
+// process ends).  In host code `scratch` names a host-side stand-in, not
+// the device array: host code uses only the address from
+// hipGetSymbolAddress, kept per device.
+static __device__ __align__(256) unsigned char scratch[DEEPPCR_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr size_t kScratchBytes = (size_t)DEEPPCR_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of the current device's scratch, looked up once per
+// device (with that device current) and cached.
+hipError_t scratch_address(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
 extern "C" {
+
+int pcr_solve_block_bidiag_noalloc(const float* J, const float* r, float* x, int B, int L,
+                                   int w, int transpose, void* stream) {
+    const SpanGuard span_guard;
+    if (!J || !r || !x || !sizes_ok(B, L, w) || (transpose != 0 && transpose != 1))
+        return DEEPPCR_EINVAL;
+    if (!aligned({J, r, x})) return DEEPPCR_EINVAL;
+    const size_t nJ = (size_t)B * L * w * w * 4, nv = (size_t)B * L * w * 4;
+    if (overlaps(x, nv, J, nJ)) return DEEPPCR_EINVAL;
+    if ((x != r) && overlaps(x, nv, r, nv)) return DEEPPCR_EINVAL;
+    if (layout(DEEPPCR_OP_PCR, B, L, w).total > kScratchBytes) return DEEPPCR_EWORKSPACE;
+    // no event is created or recorded during this call, whatever the
+    // instrumentation setting
+    const bool prof_on = g_prof.on;
+    g_prof.on = false;
+    void* ws = nullptr;
+    hipError_t e = scratch_address(&ws);
+    int status = e != hipSuccess ? hip_fail(e, "hipGetSymbolAddress(scratch)")
+                                 : pcr_solve_run(J, r, x, B, L, w, transpose, ws,
+                                                 (hipStream_t)stream);
+    g_prof.on = prof_on;
+    return status;
+}
+
+size_t deeppcr_noalloc_scratch_bytes(void) { return kScratchBytes; }
 
 int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, int w, float tol,
                         void* workspace, size_t workspace_bytes, float* residual_out,

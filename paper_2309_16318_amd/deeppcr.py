@@ -31,6 +31,10 @@ SIGNATURES = {
     "pcr_solve_block_bidiag": (_c.c_int, [_c.c_void_p, _c.c_void_p, _c.c_void_p, _c.c_int,
                                           _c.c_int, _c.c_int, _c.c_int, _c.c_void_p,
                                           _c.c_size_t, _c.c_void_p]),
+    "pcr_solve_block_bidiag_noalloc": (_c.c_int, [_c.c_void_p, _c.c_void_p, _c.c_void_p,
+                                                  _c.c_int, _c.c_int, _c.c_int, _c.c_int,
+                                                  _c.c_void_p]),
+    "deeppcr_noalloc_scratch_bytes": (_c.c_size_t, []),
     "deeppcr_mlp_forward": (_c.c_int, [_c.c_void_p, _c.c_void_p, _c.c_void_p, _c.c_void_p,
                                        _c.c_int, _c.c_int, _c.c_int, _c.c_int, _c.c_float,
                                        _c.c_float, _c.c_int, _c.c_void_p, _c.c_void_p,
@@ -153,6 +157,20 @@ def pcr_solve_block_bidiag(J, r, x=None, transpose: int = 0, workspace=None, str
                                       _ptr(ws), nbytes, _stream(stream))
     if st != OK:
         raise DeepPCRError(st, "pcr_solve_block_bidiag")
+    return x
+
+
+def pcr_solve_block_bidiag_noalloc(J, r, x, transpose: int = 0, stream=None):
+    """The same solve into the caller's x without a workspace: the library
+    uses its own fixed scratch array and allocates nothing."""
+    B, L, w = r.shape
+    _check(J, (B, L, w, w), "J")
+    _check(r, (B, L, w), "r")
+    _check(x, (B, L, w), "x")
+    st = lib().pcr_solve_block_bidiag_noalloc(_ptr(J), _ptr(r), _ptr(x), B, L, w, int(transpose),
+                                              _stream(stream))
+    if st != OK:
+        raise DeepPCRError(st, "pcr_solve_block_bidiag_noalloc")
     return x
 
 

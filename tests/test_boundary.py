@@ -81,6 +81,28 @@ def test_pcr_solve_rejects_invalid_arguments():
     assert _pcr(nws=deeppcr.workspace_bytes(deeppcr.OP_PCR, 2, 8, 4) - 1) == deeppcr.EWORKSPACE
 
 
+def test_noalloc_solve_rejects_invalid_arguments_and_oversized_problems():
+    E = deeppcr.EINVAL
+    f = deeppcr.lib().pcr_solve_block_bidiag_noalloc
+
+    def call(J=P[0], r=P[1], x=P[2], B=2, L=8, w=4, tr=0):
+        return f(J, r, x, B, L, w, tr, None)
+
+    assert deeppcr.lib().deeppcr_noalloc_scratch_bytes() == 64 << 20
+    for k in ("J", "r", "x"):
+        assert call(**{k: None}) == E
+        assert call(**{k: ctypes.c_void_p(dict(J=P[0], r=P[1], x=P[2])[k].value + 4)}) == E
+    assert call(w=129) == E
+    assert call(tr=2) == E
+    assert call(x=ctypes.c_void_p(P[0].value + 64)) == E       # x over J
+    assert call(x=ctypes.c_void_p(P[1].value + 16)) == E       # x partly over r
+    # past the fixed scratch: the workspace the solve would need exceeds it
+    cap = 64 << 20
+    assert deeppcr.workspace_bytes(deeppcr.OP_PCR, 1, 512, 128) > cap
+    assert call(B=1, L=512, w=128) == deeppcr.EWORKSPACE
+    assert call(B=64, L=1024, w=16) == deeppcr.EWORKSPACE
+
+
 def _fwd(W=P[0], b=P[1], z0=P[2], Z=P[3], B=2, L=8, w=4, layer=0, alpha=1.0, tol=1e-5,
          max_iter=20, Zi=None, ws=P[5], nws=BIG):
     it = ctypes.c_int(-1)
