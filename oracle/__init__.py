@@ -13,3 +13,4 @@ from .deeppcr_oracle import (  # noqa: F401
 )
 from . import resnet_oracle  # noqa: F401
 from . import diffusion_oracle  # noqa: F401
+from . import sharded_oracle  # noqa: F401
