@@ -117,6 +117,36 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x,
                            void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The standalone solve of pcr_solve_block_bidiag computed the way a solve
+ * whose rows are spread over G devices would compute it (the memory and
+ * communication setting of Sec. 3.1), all on this one GPU: the rows of each
+ * system are cut into consecutive chunks of Lc = ceil(L / G) rows (natural
+ * row order; the last chunk may be shorter, so there are ceil(L / Lc) <= G
+ * chunks).
+ *   1. Chunk-local PCR (Alg. 1 inside every chunk, all chunks at once) that
+ *      keeps each chunk's coupling to the one unknown outside it, x_in (row
+ *      a-1 of chunk [a, e) for transpose = 0, row e for transpose = 1), so
+ *      that every row ends as x_l = P_l x_in + q_l.
+ *   2. A pass over the chunk ends in solve order: the carry-in of the next
+ *      chunk is P x_in + q at the current chunk's last row (the first
+ *      chunk's carry-in is zero).
+ *   3. x_l = q_l + P_l x_in for every row.
+ * On G devices step 1 runs on each device's rows, step 2 needs the G
+ * chunk-end maps (P, q) of one row each from every device, and step 3 is
+ * local again.  The result is the solution of pcr_solve_block_bidiag (the
+ * summation order differs).
+ *   J, r, x, B, L, w, transpose  as for pcr_solve_block_bidiag (x may alias r)
+ *   G  >= 1: the number of chunks asked for (G >= L gives one row per chunk)
+ * workspace_bytes >= deeppcr_chunked_workspace_bytes(B, L, w, G): two copies
+ * of the operators [B, L, w, w], two of the vectors [B, L, w] and the
+ * carry-ins [B, chunks, w].  Returns without waiting for the GPU.
+ */
+size_t deeppcr_chunked_workspace_bytes(int B, int L, int w, int G);
+int pcr_solve_block_bidiag_chunked(const float* J, const float* r, float* x,
+                                   int B, int L, int w, int transpose, int G,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * pcr_solve_block_bidiag without a workspace argument and without any
  * allocation, for callers that cannot allocate device memory (code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).

@@ -718,6 +718,107 @@ int pcr_solve_run(const float* J, const float* r, float* x, int B, int L, int w,
 
 }  // namespace
 
+// ------------------------------------------------------ row-chunked solve
+namespace {
+
+struct ChunkLayout {
+    size_t A[2], r[2], xin, total;
+};
+
+ChunkLayout chunk_layout(int B, int L, int w, int G) {
+    const size_t nA = (size_t)B * L * w * w * sizeof(float);
+    const size_t nr = (size_t)B * L * w * sizeof(float);
+    const int Lc = (L + G - 1) / G;
+    const size_t nx = (size_t)B * chunk_count(L, Lc) * w * sizeof(float);
+    ChunkLayout lo{};
+    size_t off = 0;
+    lo.A[0] = off; off += align_up(nA);
+    lo.A[1] = off; off += align_up(nA);
+    lo.r[0] = off; off += align_up(nr);
+    lo.r[1] = off; off += align_up(nr);
+    lo.xin = off; off += align_up(nx);
+    lo.total = off;
+    return lo;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t deeppcr_chunked_workspace_bytes(int B, int L, int w, int G) {
+    if (!sizes_ok(B, L, w) || G < 1) return 0;
+    return chunk_layout(B, L, w, G).total;
+}
+
+int pcr_solve_block_bidiag_chunked(const float* J, const float* r, float* x, int B, int L, int w,
+                                   int transpose, int G, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+    const SpanGuard span_guard;
+    if (!J || !r || !x || !workspace || !sizes_ok(B, L, w) || G < 1 ||
+        (transpose != 0 && transpose != 1))
+        return DEEPPCR_EINVAL;
+    if (!aligned({J, r, x, workspace})) return DEEPPCR_EINVAL;
+    const ChunkLayout lo = chunk_layout(B, L, w, G);
+    if (workspace_bytes < lo.total) return DEEPPCR_EWORKSPACE;
+    const size_t nJ = (size_t)B * L * w * w * 4, nv = (size_t)B * L * w * 4;
+    if (overlaps(x, nv, J, nJ) || overlaps(workspace, lo.total, J, nJ) ||
+        overlaps(workspace, lo.total, r, nv) || overlaps(workspace, lo.total, x, nv))
+        return DEEPPCR_EINVAL;
+    if ((x != r) && overlaps(x, nv, r, nv)) return DEEPPCR_EINVAL;
+
+    hipStream_t st = (hipStream_t)stream;
+    char* base = (char*)workspace;
+    float* wsA[2] = {(float*)(base + lo.A[0]), (float*)(base + lo.A[1])};
+    float* wsr[2] = {(float*)(base + lo.r[0]), (float*)(base + lo.r[1])};
+    float* xin = (float*)(base + lo.xin);
+    const long long bw2 = (long long)L * w * w, w2 = (long long)w * w;
+    const int rev = transpose;
+    BlockSrc Ain;
+    VecSrc rin;
+    VecDst xd;
+    if (!transpose) {
+        Ain = BlockSrc{J, bw2, w2, 0};
+        rin = VecSrc{r, (long long)L * w, w};
+        xd = VecDst{x, (long long)L * w, w};
+    } else {
+        // reversed row order: internal row m = L-1-l has operator J_{L-m}^T
+        Ain = BlockSrc{J + (long long)L * w2, bw2, -w2, 1};
+        rin = VecSrc{r + (long long)(L - 1) * w, (long long)L * w, -(long long)w};
+        xd = VecDst{x + (long long)(L - 1) * w, (long long)L * w, -(long long)w};
+    }
+    const int Lc = (L + G - 1) / G;
+    // levels s = 1, 2, ... while s < Lc; a chunk of one row still takes one
+    // (copying) level, which moves its block into the operator buffer
+    int k = 0;
+    for (int s = 1; k == 0 || s < Lc; s *= 2, ++k) {
+        double bytes, flops;
+        chunk_level_work(B, L, w, Lc, rev, s, &bytes, &flops);
+        float* Aout = wsA[k & 1];
+        float* rout = wsr[k & 1];
+        hipError_t e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
+            return launch_chunk_level(Ain, rin, Aout, rout, B, L, w, Lc, rev, s, st);
+        });
+        if (e != hipSuccess) return hip_fail(e, "pcr_solve_block_bidiag_chunked");
+        Ain = BlockSrc{Aout, bw2, w2, 0};
+        rin = VecSrc{rout, (long long)L * w, w};
+    }
+    const float* P = wsA[(k - 1) & 1];
+    const float* q = wsr[(k - 1) & 1];
+    const int nch = chunk_count(L, Lc);
+    hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * B * nch * (w2 + 2.0 * w),
+                         2.0 * B * nch * w2, st,
+                         [&] { return launch_chunk_carry(P, q, xin, B, L, w, Lc, rev, st); });
+    if (e != hipSuccess) return hip_fail(e, "pcr_solve_block_bidiag_chunked");
+    const double apply_rows = (double)B * (L - (transpose ? L - (nch - 1) * Lc : Lc));
+    e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * (apply_rows * w2 + 2.0 * B * L * w),
+              2.0 * apply_rows * w2, st,
+              [&] { return launch_chunk_apply(P, q, xin, xd, B, L, w, Lc, rev, st); });
+    if (e != hipSuccess) return hip_fail(e, "pcr_solve_block_bidiag_chunked");
+    return DEEPPCR_OK;
+}
+
+}  // extern "C"
+
 // ------------------------------------------------- no-allocation variant
 // The scratch of pcr_solve_block_bidiag_noalloc: a fixed device array in
 // place of the caller's workspace.  Each GPU holds its own copy (allocated

@@ -300,6 +300,25 @@ hipError_t launch_resnet_seq_backward(const float* W, const float* z0, const flo
                                       int w, int skip, int act, int l0, int l1,
                                       hipStream_t stream);
 
+// ----------------------------------------------------- row-chunked solve
+// The rows of each system cut into chunks of Lc rows (natural order; the
+// last chunk may be shorter); rev = 1 runs the transposed system in reversed
+// internal row order.  Chunk-local PCR level with stride s keeping every
+// chunk's coupling to the row outside it (except the chunk holding internal
+// row 0): Aout [B, L, w, w] and rout [B, L, w] contiguous, internal order.
+int chunk_count(int L, int Lc);
+void chunk_level_work(int B, int L, int w, int Lc, int rev, int s, double* bytes,
+                      double* flops);
+hipError_t launch_chunk_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout, float* rout,
+                              int B, int L, int w, int Lc, int rev, int s, hipStream_t stream);
+// xin [B, chunk_count, w]: the carry-in of every chunk (internal chunk order)
+// from the chunk-end rows of P (the final operators) and q (final vectors).
+hipError_t launch_chunk_carry(const float* P, const float* q, float* xin, int B, int L, int w,
+                              int Lc, int rev, hipStream_t stream);
+// x (natural-order destination) = q + P xin of each row's chunk.
+hipError_t launch_chunk_apply(const float* P, const float* q, const float* xin, const VecDst& x,
+                              int B, int L, int w, int Lc, int rev, hipStream_t stream);
+
 // ------------------------------------------------------------- tiny path
 // Whole Newton + PCR forward solve in one workgroup with everything in LDS,
 // for batches that fit in 64 KiB.  result[0] = status (0 ok, 2 no

@@ -35,6 +35,9 @@ SIGNATURES = {
                                                   _c.c_int, _c.c_int, _c.c_int, _c.c_int,
                                                   _c.c_void_p]),
     "deeppcr_noalloc_scratch_bytes": (_c.c_size_t, []),
+    "deeppcr_chunked_workspace_bytes": (_c.c_size_t, [_c.c_int] * 4),
+    "pcr_solve_block_bidiag_chunked": (_c.c_int, [_c.c_void_p] * 3 + [_c.c_int] * 5 +
+                                       [_c.c_void_p, _c.c_size_t, _c.c_void_p]),
     "deeppcr_mlp_forward": (_c.c_int, [_c.c_void_p, _c.c_void_p, _c.c_void_p, _c.c_void_p,
                                        _c.c_int, _c.c_int, _c.c_int, _c.c_int, _c.c_float,
                                        _c.c_float, _c.c_int, _c.c_void_p, _c.c_void_p,
@@ -171,6 +174,28 @@ def pcr_solve_block_bidiag_noalloc(J, r, x, transpose: int = 0, stream=None):
                                               _stream(stream))
     if st != OK:
         raise DeepPCRError(st, "pcr_solve_block_bidiag_noalloc")
+    return x
+
+
+def pcr_solve_block_bidiag_chunked(J, r, G: int, x=None, transpose: int = 0, workspace=None,
+                                   stream=None):
+    """The same solve computed over G row chunks (chunk-local PCR keeping each
+    chunk's coupling, a pass over the chunk ends, then the apply)."""
+    torch = _torch()
+    B, L, w = r.shape
+    _check(J, (B, L, w, w), "J")
+    _check(r, (B, L, w), "r")
+    if x is None:
+        x = torch.empty_like(r)
+    _check(x, (B, L, w), "x")
+    n = int(lib().deeppcr_chunked_workspace_bytes(B, L, w, int(G)))
+    if workspace is None:
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=r.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    st = lib().pcr_solve_block_bidiag_chunked(_ptr(J), _ptr(r), _ptr(x), B, L, w, int(transpose),
+                                              int(G), _ptr(workspace), nbytes, _stream(stream))
+    if st != OK:
+        raise DeepPCRError(st, "pcr_solve_block_bidiag_chunked")
     return x
 
 

@@ -360,3 +360,38 @@ def test_release_thread_state_without_a_gpu():
     is a no-op and can be repeated."""
     deeppcr.release_thread_state()
     deeppcr.release_thread_state()
+
+
+def test_chunked_workspace_sizes():
+    f = deeppcr.lib().deeppcr_chunked_workspace_bytes
+    up = lambda x: (x + 255) // 256 * 256
+    B, L, w = 3, 10, 5
+    nA, nr = B * L * w * w * 4, B * L * w * 4
+    # G = 4 over 10 rows: chunks of 3, so 4 chunks; G = 6: chunks of 2, 5 chunks
+    assert f(B, L, w, 4) == 2 * up(nA) + 2 * up(nr) + up(B * 4 * w * 4)
+    assert f(B, L, w, 6) == 2 * up(nA) + 2 * up(nr) + up(B * 5 * w * 4)
+    assert f(B, L, w, 1) == 2 * up(nA) + 2 * up(nr) + up(B * w * 4)
+    for bad in ((0, 4, 4, 2), (1, 0, 4, 2), (1, 4, 129, 2), (1, 4, 4, 0), (1, 4, 4, -3)):
+        assert f(*bad) == 0
+
+
+def test_chunked_solve_rejects_invalid_arguments():
+    E = deeppcr.EINVAL
+    fn = deeppcr.lib().pcr_solve_block_bidiag_chunked
+
+    def call(J=P[0], r=P[1], x=P[2], B=2, L=8, w=4, tr=0, G=2, ws=P[3], nws=BIG):
+        return fn(J, r, x, B, L, w, tr, G, ws, nws, None)
+
+    for k in ("J", "r", "x", "ws"):
+        assert call(**{k: None}) == E
+        assert call(**{k: _misaligned(dict(J=P[0], r=P[1], x=P[2], ws=P[3])[k], 4)}) == E
+    assert call(G=0) == E
+    assert call(G=-1) == E
+    assert call(tr=2) == E
+    assert call(w=129) == E
+    assert call(B=0) == E
+    assert call(x=ctypes.c_void_p(P[0].value + 64)) == E       # x over J
+    assert call(x=ctypes.c_void_p(P[1].value + 16)) == E       # x partly over r
+    assert call(ws=ctypes.c_void_p(P[1].value - 16)) == E      # workspace over r
+    need = deeppcr.lib().deeppcr_chunked_workspace_bytes(2, 8, 4, 2)
+    assert call(nws=need - 1) == deeppcr.EWORKSPACE
