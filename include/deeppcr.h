@@ -77,7 +77,10 @@ enum {
 enum { DEEPPCR_OP_PCR = 0, DEEPPCR_OP_FWD = 1, DEEPPCR_OP_BWD = 2 };
 
 /* Largest supported state width w. */
-#define DEEPPCR_MAX_WIDTH 128
+#define DEEPPCR_MAX_WIDTH 1024
+/* Largest width of the collapsed-skip ResNet entry points and of
+ * pcr_solve_block_bidiag_chunked. */
+#define DEEPPCR_MAX_BLOCK_WIDTH 128
 
 /* Bytes of device workspace that operation `op` (DEEPPCR_OP_*) needs for a
  * batch of B systems of L rows of width w: two ping-pong copies of the

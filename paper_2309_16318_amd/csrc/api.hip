@@ -210,8 +210,12 @@ Layout resnet_layout(int op, int B, int G, int w) {
     return lo;
 }
 
+// The ResNet block kernels and the chunked solve hold a whole block per
+// workgroup: widths up to DEEPPCR_MAX_BLOCK_WIDTH.
+bool block_sizes_ok(int B, int L, int w) { return sizes_ok(B, L, w) && w <= DEEPPCR_MAX_BLOCK_WIDTH; }
+
 bool resnet_shape_ok(int B, int L, int w, int skip, int act) {
-    return sizes_ok(B, L, w) && skip >= 1 && L % skip == 0 && act >= 0 && act <= 2;
+    return block_sizes_ok(B, L, w) && skip >= 1 && L % skip == 0 && act >= 0 && act <= 2;
 }
 
 int num_levels(int L) {
@@ -746,7 +750,7 @@ ChunkLayout chunk_layout(int B, int L, int w, int G) {
 extern "C" {
 
 size_t deeppcr_chunked_workspace_bytes(int B, int L, int w, int G) {
-    if (!sizes_ok(B, L, w) || G < 1) return 0;
+    if (!block_sizes_ok(B, L, w) || G < 1) return 0;
     return chunk_layout(B, L, w, G).total;
 }
 
@@ -754,7 +758,7 @@ int pcr_solve_block_bidiag_chunked(const float* J, const float* r, float* x, int
                                    int transpose, int G, void* workspace,
                                    size_t workspace_bytes, void* stream) {
     const SpanGuard span_guard;
-    if (!J || !r || !x || !workspace || !sizes_ok(B, L, w) || G < 1 ||
+    if (!J || !r || !x || !workspace || !block_sizes_ok(B, L, w) || G < 1 ||
         (transpose != 0 && transpose != 1))
         return DEEPPCR_EINVAL;
     if (!aligned({J, r, x, workspace})) return DEEPPCR_EINVAL;
@@ -1240,6 +1244,19 @@ int deeppcr_seq_forward(const float* W, const float* bias, const float* z0, floa
         overlaps(Z, nv, z0, (size_t)B * w * 4))
         return DEEPPCR_EINVAL;
     hipStream_t st = (hipStream_t)stream;
+    if (wide_width(w)) {
+        // one launch per layer whatever launch_per_layer says: a layer's
+        // matrix is spread over the chip (one workgroup per system cannot
+        // stream a block this size at speed)
+        for (int l = 0; l < L; ++l) {
+            hipError_t e = timed(DEEPPCR_KCLASS_SEQUENTIAL, 4.0 * ((double)w * w + 2.0 * B * w),
+                                 2.0 * B * w * w, st, [&] {
+                return launch_seq_forward_wide(W, bias, z0, Z, B, L, w, layer, alpha, l, st);
+            });
+            if (e != hipSuccess) return hip_fail(e, "seq_forward");
+        }
+        return DEEPPCR_OK;
+    }
     const int step = launch_per_layer ? 1 : L;
     for (int l0 = 0; l0 < L; l0 += step) {
         const int l1 = l0 + step < L ? l0 + step : L;
@@ -1269,6 +1286,19 @@ int deeppcr_seq_backward(const float* W, const float* bias, const float* z0, con
             return DEEPPCR_EINVAL;
     if (overlaps(Lambda, nv, dz0, nb)) return DEEPPCR_EINVAL;
     hipStream_t st = (hipStream_t)stream;
+    if (wide_width(w)) {
+        // per layer (see deeppcr_seq_forward): the scaled adjoint, then its
+        // product with W_l^T
+        for (int l = L - 1; l >= 0; --l) {
+            hipError_t e = timed(DEEPPCR_KCLASS_SEQUENTIAL, 4.0 * (2.0 * w * w + 4.0 * B * w),
+                                 4.0 * B * w * w, st, [&] {
+                return launch_seq_backward_wide(W, bias, z0, Z, G, Lambda, dz0, B, L, w, layer,
+                                                alpha, l, st);
+            });
+            if (e != hipSuccess) return hip_fail(e, "seq_backward");
+        }
+        return DEEPPCR_OK;
+    }
     const int step = launch_per_layer ? 1 : L;
     for (int l1 = L; l1 > 0; l1 -= step) {
         const int l0 = l1 - step > 0 ? l1 - step : 0;

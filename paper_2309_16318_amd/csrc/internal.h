@@ -9,7 +9,11 @@
 
 namespace deeppcr {
 
+// Widths up to kMaxWidth use the per-width kernels (one workgroup or wave
+// holds a whole block); kMaxWidth < w <= kMaxWideWidth use the tiled kernels
+// of wide.hip.
 constexpr int kMaxWidth = 128;
+constexpr int kMaxWideWidth = 1024;
 
 // The Newton convergence maxima are reduced into kRedShards slots each
 // (slot = workgroup index mod kRedShards) to keep atomic contention low; the
@@ -318,6 +322,39 @@ hipError_t launch_chunk_carry(const float* P, const float* q, float* xin, int B,
 // x (natural-order destination) = q + P xin of each row's chunk.
 hipError_t launch_chunk_apply(const float* P, const float* q, const float* xin, const VecDst& x,
                               int B, int L, int w, int Lc, int rev, hipStream_t stream);
+
+// ------------------------------------------------------------ wide widths
+// kMaxWidth < w <= kMaxWideWidth: the same operations as launch_pcr_level,
+// launch_forward_eval, launch_initial_guess, launch_backward_assemble (blocks
+// stored as J_l, read transposed), launch_dz0 and launch_wgrad, and one
+// layer l of the sequential passes (the backward uses dz0 as its scratch for
+// the scaled adjoint until the last step).
+bool wide_width(int w);
+hipError_t launch_pcr_level_wide(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
+                                 const VecDst& rout, int B, int L, int w, int s,
+                                 hipStream_t stream);
+hipError_t launch_forward_eval_wide(const float* W, const float* bias, const float* z0,
+                                    const float* Z, float* A, float* r, unsigned* red, int B,
+                                    int L, int w, int layer, float alpha, hipStream_t stream);
+hipError_t launch_initial_guess_wide(const float* W, const float* bias, const float* z0, float* Z,
+                                     int B, int L, int w, int layer, float alpha,
+                                     hipStream_t stream);
+hipError_t launch_backward_assemble_wide(const float* W, const float* bias, const float* z0,
+                                         const float* Z, const float* G, float* A, float* rrev,
+                                         float* dscale, int B, int L, int w, int layer,
+                                         float alpha, hipStream_t stream);
+hipError_t launch_dz0_wide(const float* W, const float* dscale, const float* Lambda, float* dz0,
+                           int B, int L, int w, int layer, hipStream_t stream);
+hipError_t launch_wgrad_wide(const float* z0, const float* Z, const float* dscale,
+                             const float* Lambda, float* dW, float* db, int B, int L, int w,
+                             hipStream_t stream);
+hipError_t launch_seq_forward_wide(const float* W, const float* bias, const float* z0, float* Z,
+                                   int B, int L, int w, int layer, float alpha, int l,
+                                   hipStream_t stream);
+hipError_t launch_seq_backward_wide(const float* W, const float* bias, const float* z0,
+                                    const float* Z, const float* G, float* Lambda, float* dz0,
+                                    int B, int L, int w, int layer, float alpha, int l,
+                                    hipStream_t stream);
 
 // ------------------------------------------------------------- tiny path
 // Whole Newton + PCR forward solve in one workgroup with everything in LDS,

@@ -545,6 +545,8 @@ hipError_t launch_forward_eval(const float* W, const float* bias, const float* z
     if (small_width(w))
         return launch_eval_small(false, W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, w,
                                  layer, alpha, stream);
+    if (wide_width(w))
+        return launch_forward_eval_wide(W, bias, z0, Z, A, r, red, B, L, w, layer, alpha, stream);
     switch (w) {
         case 16: return launch_eval_vec<16, false>(W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, layer, alpha, stream);
         case 32: return launch_eval_vec<32, false>(W, bias, z0, Z, nullptr, A, r, nullptr, red, B, L, layer, alpha, stream);
@@ -558,12 +560,14 @@ hipError_t launch_forward_eval(const float* W, const float* bias, const float* z
 }
 
 bool backward_blocks_transposed(int w) {
-    return small_width(w) || w == 16 || w == 32 || w == 64 || w == 128;
+    return small_width(w) || w == 16 || w == 32 || w == 64 || w == 128 || wide_width(w);
 }
 
 hipError_t launch_initial_guess(const float* W, const float* bias, const float* z0, float* Z,
                                 int B, int L, int w, int layer, float alpha,
                                 hipStream_t stream) {
+    if (wide_width(w))
+        return launch_initial_guess_wide(W, bias, z0, Z, B, L, w, layer, alpha, stream);
     const int rows_per_block = 64;
     const int chunks = (L + rows_per_block - 1) / rows_per_block;
     hipLaunchKernelGGL(initial_guess_kernel, dim3((unsigned)((long long)B * chunks)),
@@ -589,6 +593,9 @@ hipError_t launch_backward_assemble(const float* W, const float* bias, const flo
     if (small_width(w))
         return launch_eval_small(true, W, bias, z0, Z, G, A, rrev, dscale, nullptr, B, L, w,
                                  layer, alpha, stream);
+    if (wide_width(w))
+        return launch_backward_assemble_wide(W, bias, z0, Z, G, A, rrev, dscale, B, L, w, layer,
+                                             alpha, stream);
     if (A == nullptr && (w == 32 || w == 64 || w == 128)) {
         // no blocks to write: one workgroup per layer
         switch (w) {
@@ -613,6 +620,7 @@ hipError_t launch_backward_assemble(const float* W, const float* bias, const flo
 
 hipError_t launch_dz0(const float* W, const float* dscale, const float* Lambda, float* dz0,
                       int B, int L, int w, int layer, hipStream_t stream) {
+    if (wide_width(w)) return launch_dz0_wide(W, dscale, Lambda, dz0, B, L, w, layer, stream);
     hipLaunchKernelGGL(dz0_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, W, dscale,
                        Lambda, dz0, L, w, layer);
     return hipGetLastError();
@@ -643,6 +651,7 @@ hipError_t launch_wgrad_any(const float* z0, const float* Z, const float* dscale
 hipError_t launch_wgrad(const float* z0, const float* Z, const float* dscale,
                         const float* Lambda, float* dW, float* db, int B, int L, int w,
                         hipStream_t stream) {
+    if (wide_width(w)) return launch_wgrad_wide(z0, Z, dscale, Lambda, dW, db, B, L, w, stream);
     return launch_wgrad_any<false>(z0, Z, dscale, Lambda, dW, db, B, L, w, 0, stream);
 }
 

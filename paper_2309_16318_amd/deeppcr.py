@@ -18,7 +18,8 @@ ACT_TANH, ACT_SIGMOID, ACT_RELU = 0, 1, 2
 (KCLASS_PCR_LEVEL, KCLASS_LAYER, KCLASS_UPDATE, KCLASS_WGRAD, KCLASS_OTHER, KCLASS_SEQUENTIAL,
  KCLASS_PCR_TAIL) = range(7)
 KCLASS_NAMES = ("pcr_level", "layer", "update", "wgrad", "other", "sequential", "pcr_tail")
-MAX_WIDTH = 128
+MAX_WIDTH = 1024
+MAX_BLOCK_WIDTH = 128  # collapsed-skip ResNet and the chunked solve
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdeeppcr.so")
 

@@ -42,7 +42,7 @@ def test_workspace_sizes():
     assert f(deeppcr.OP_PCR, B, L, w) == 2 * up(nA) + 2 * up(nr) + red
     assert f(deeppcr.OP_FWD, B, L, w) == 2 * up(nA) + 2 * up(nr) + red
     assert f(deeppcr.OP_BWD, B, L, w) == 2 * up(nA) + 3 * up(nr) + red
-    for bad in ((0, 1, 1), (1, 0, 1), (1, 1, 0), (1, 1, 129), (-1, 4, 4)):
+    for bad in ((0, 1, 1), (1, 0, 1), (1, 1, 0), (1, 1, 1025), (-1, 4, 4)):
         assert f(deeppcr.OP_PCR, *bad) == 0
     assert f(7, 1, 1, 1) == 0
 
@@ -71,7 +71,7 @@ def test_pcr_solve_rejects_invalid_arguments():
     assert _pcr(B=0) == E
     assert _pcr(L=0) == E
     assert _pcr(w=0) == E
-    assert _pcr(w=129) == E
+    assert _pcr(w=1025) == E
     assert _pcr(tr=2) == E
     # x overlapping J, workspace overlapping r
     assert _pcr(x=ctypes.c_void_p(P[0].value + 64)) == E
@@ -92,7 +92,7 @@ def test_noalloc_solve_rejects_invalid_arguments_and_oversized_problems():
     for k in ("J", "r", "x"):
         assert call(**{k: None}) == E
         assert call(**{k: ctypes.c_void_p(dict(J=P[0], r=P[1], x=P[2])[k].value + 4)}) == E
-    assert call(w=129) == E
+    assert call(w=1025) == E
     assert call(tr=2) == E
     assert call(x=ctypes.c_void_p(P[0].value + 64)) == E       # x over J
     assert call(x=ctypes.c_void_p(P[1].value + 16)) == E       # x partly over r
@@ -123,7 +123,7 @@ def test_forward_rejects_invalid_arguments():
     assert _fwd(tol=float("nan")) == E
     assert _fwd(tol=float("inf")) == E
     assert _fwd(alpha=float("nan")) == E
-    assert _fwd(w=200) == E
+    assert _fwd(w=1025) == E
     assert _fwd(Zi=ctypes.c_void_p(P[3].value + 16)) == E     # partial overlap with Z
     assert _fwd(ws=ctypes.c_void_p(P[3].value)) == E          # workspace over Z
     assert _fwd(nws=100) == deeppcr.EWORKSPACE
@@ -152,7 +152,7 @@ def test_forward_residual_rejects_invalid_arguments():
         assert _fwd_res(rtol=bad) == E
     assert _fwd_res(alpha=float("nan")) == E
     assert _fwd_res(B=0) == E
-    assert _fwd_res(w=129) == E
+    assert _fwd_res(w=1025) == E
     assert _fwd_res(Zi=ctypes.c_void_p(P[3].value + 16)) == E
     assert _fwd_res(ws=ctypes.c_void_p(P[0].value)) == E      # workspace over W
     assert _fwd_res(nws=100) == deeppcr.EWORKSPACE
@@ -206,6 +206,17 @@ def test_sequential_passes_reject_invalid_arguments():
     assert g(*P[:6], None, 2, 8, 4, 0, 1.0, 0, None) == E
     assert g(*P[:7], 2, 8, 4, -1, 1.0, 0, None) == E
     assert g(*P[:5], P[3], P[6], 2, 8, 4, 0, 1.0, 0, None) == E   # Lambda over Z
+
+
+def test_wide_widths_accepted_up_to_1024():
+    """The plain entry points take 1 <= w <= 1024; the ResNet and chunked
+    entry points stop at 128."""
+    assert deeppcr.MAX_WIDTH == 1024 and deeppcr.MAX_BLOCK_WIDTH == 128
+    for w in (129, 130, 256, 1000, 1024):
+        assert deeppcr.workspace_bytes(deeppcr.OP_FWD, 1, 4, w) > 0
+        assert _pcr(w=w, nws=10) == deeppcr.EWORKSPACE   # valid shape, short workspace
+    assert deeppcr.lib().deeppcr_resnet_workspace_bytes(deeppcr.OP_FWD, 1, 8, 129, 4) == 0
+    assert deeppcr.lib().deeppcr_chunked_workspace_bytes(1, 8, 129, 2) == 0
 
 
 def test_resnet_workspace_sizes():
@@ -297,7 +308,7 @@ def test_newton_step_rejects_invalid_arguments():
     assert call(F=None) == E
     assert call(Z=None) == E
     assert call(ws=None) == E
-    assert call(w=129) == E
+    assert call(w=1025) == E
     assert call(Z=ctypes.c_void_p(P[0].value + 64)) == E   # Z over J
     assert call(Z=P[1]) == E                                # Z over F
     assert call(ws=ctypes.c_void_p(P[2].value - 16)) == E   # workspace runs into Z
