@@ -407,19 +407,23 @@ __global__ __launch_bounds__(kThreads) void backward_assemble_wide(
 }
 
 // out[b][k] = sum_i W[i][k] g_b[i] (+ add[b][k]) with g_b = g1_b (* g2_b).
-// Grid (chunks of 64 k, B); thread (k = k0 + t % 64, group t / 64) sums
-// over i = group, group + 4, ...; the four groups meet in LDS.
+// Grid (chunks of 64 k, B), 1024 threads: thread (k = k0 + t % 64, group
+// t / 64) sums over i = group, group + 16, ... (eight loads in flight per
+// thread); the sixteen groups meet in LDS in a fixed order.
 // single = 1: one workgroup per system covers every chunk after g_b is in
 // LDS (out may then be the memory g1 points to).
-__global__ __launch_bounds__(kThreads) void matvec_t_wide(
+constexpr int kMvtThreads = 1024;
+constexpr int kMvtGroups = kMvtThreads / 64;
+
+__global__ __launch_bounds__(kMvtThreads) void matvec_t_wide(
     const float* __restrict__ W, const float* g1, long long g1_bstride, const float* g2,
     long long g2_bstride, const float* add, long long add_bstride, float* out,
     long long out_bstride, int w, int single) {
     __shared__ float g[kWide];
-    __shared__ float part[kWaves][64];
+    __shared__ float part[kMvtGroups][64];
     const int b = blockIdx.y;
     const int t = threadIdx.x, kk = t & 63, grp = t >> 6;
-    for (int i = t; i < w; i += kThreads) {
+    for (int i = t; i < w; i += kMvtThreads) {
         float x = g1[b * g1_bstride + i];
         if (g2) x *= g2[b * g2_bstride + i];
         g[i] = x;
@@ -430,12 +434,23 @@ __global__ __launch_bounds__(kThreads) void matvec_t_wide(
     for (int c = c0; c < c1; ++c) {
         const int k = 64 * c + kk;
         float acc = 0.f;
-        if (k < w)
-            for (int i = grp; i < w; i += kWaves) acc = fmaf(W[(long long)i * w + k], g[i], acc);
+        if (k < w) {
+            const float* col = W + k;
+            int i = grp;
+            for (; i + 7 * kMvtGroups < w; i += 8 * kMvtGroups) {
+                float v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) v[u] = col[(long long)(i + u * kMvtGroups) * w];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) acc = fmaf(v[u], g[i + u * kMvtGroups], acc);
+            }
+            for (; i < w; i += kMvtGroups) acc = fmaf(col[(long long)i * w], g[i], acc);
+        }
         part[grp][kk] = acc;
         __syncthreads();
         if (grp == 0 && k < w) {
-            float sum = ((part[0][kk] + part[1][kk]) + part[2][kk]) + part[3][kk];
+            float sum = part[0][kk];
+            for (int q = 1; q < kMvtGroups; ++q) sum += part[q][kk];
             if (add) sum += add[b * add_bstride + k];
             out[b * out_bstride + k] = sum;
         }
@@ -639,7 +654,7 @@ hipError_t launch_dz0_wide(const float* W, const float* dscale, const float* Lam
     // dz0[b] = W_0^T (dscale_0 * Lambda_0) (+ Lambda_0 for residual layers)
     const long long ld = (long long)L * w;
     const dim3 grid((unsigned)((w + 63) / 64), (unsigned)B);
-    hipLaunchKernelGGL(matvec_t_wide, grid, dim3(kThreads), 0, stream, W, dscale, ld, Lambda, ld,
+    hipLaunchKernelGGL(matvec_t_wide, grid, dim3(kMvtThreads), 0, stream, W, dscale, ld, Lambda, ld,
                        layer_residual(layer) ? Lambda : nullptr, ld, dz0, (long long)w, w, 0);
     return hipGetLastError();
 }
@@ -686,10 +701,10 @@ hipError_t launch_seq_backward_wide(const float* W, const float* bias, const flo
     const float* add = layer_residual(layer) ? Lambda + (long long)l * w : nullptr;
     if (l >= 1) {
         const dim3 g2((unsigned)((w + 63) / 64), (unsigned)B);
-        hipLaunchKernelGGL(matvec_t_wide, g2, dim3(kThreads), 0, stream, Wl, dz0, (long long)w,
+        hipLaunchKernelGGL(matvec_t_wide, g2, dim3(kMvtThreads), 0, stream, Wl, dz0, (long long)w,
                            nullptr, 0LL, add, ld, Lambda + (long long)(l - 1) * w, ld, w, 0);
     } else {
-        hipLaunchKernelGGL(matvec_t_wide, dim3(1u, (unsigned)B), dim3(kThreads), 0, stream, Wl, dz0,
+        hipLaunchKernelGGL(matvec_t_wide, dim3(1u, (unsigned)B), dim3(kMvtThreads), 0, stream, Wl, dz0,
                            (long long)w, nullptr, 0LL, add, ld, dz0, (long long)w, w, 1);
     }
     return hipGetLastError();

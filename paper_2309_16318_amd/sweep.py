@@ -227,6 +227,9 @@ def main():
     p.add_argument("--widths", default="2,4,8,16,32,64,128")
     p.add_argument("--depths", default=",".join(str(2 ** k) for k in range(1, 15)))
     p.add_argument("--reps", type=int, default=3)
+    p.add_argument("--max-w2l", type=float, default=0.0,
+                   help="> 0: skip the points with w^2 L above this (the operator storage and "
+                        "the PCR work grow as w^2 L and w^3 L log L)")
     p.add_argument("--resnet-skip", type=int, default=0,
                    help="> 0: the collapsed-skip ResNet with this skip length (activation "
                         "--act), depths that are multiples of it")
@@ -270,6 +273,8 @@ def main():
         return
     for w in [int(x) for x in a.widths.split(",")]:
         for L in [int(x) for x in a.depths.split(",")]:
+            if a.max_w2l > 0 and float(w) * w * L > a.max_w2l:
+                continue
             r = run_point(w, L, a.batch, a.layer, a.alpha, a.reps, dev)
             rows.append(r)
             print(json.dumps(r), flush=True)
