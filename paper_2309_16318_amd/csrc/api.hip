@@ -342,7 +342,8 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
         } else {
             level_work(B, L, w, s, &bytes, &flops);
             e = timed(DEEPPCR_KCLASS_PCR_LEVEL, bytes, flops, st, [&] {
-                return launch_pcr_level(Ain, rin, Aout, rout, B, L, w, s, st);
+                return wide_width(w) ? launch_pcr_level_wide(Ain, rin, Aout, rout, B, L, w, s, st)
+                                     : launch_pcr_level(Ain, rin, Aout, rout, B, L, w, s, st);
             });
         }
         if (e != hipSuccess) return e;

@@ -1816,7 +1816,6 @@ hipError_t launch_pcr_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout,
         return hipGetLastError();
     }
     if (small_width(w)) return launch_pcr_level_small(Ain, rin, Aout, rout, B, L, w, s, stream);
-    if (wide_width(w)) return launch_pcr_level_wide(Ain, rin, Aout, rout, B, L, w, s, stream);
     const long long rows = (long long)B * L;
     hipLaunchKernelGGL(pcr_level_generic, dim3((unsigned)rows), dim3(kThreads), 0, stream,
                        Ain, rin, Aout, rout, L, w, s);

@@ -266,36 +266,50 @@ pcr_wide_prod(BlockSrc Ain, VecSrc rin, float* __restrict__ Aout, VecDst rout, i
 }
 
 // Rows l < min(2s, L) of a level: copy (l < s) or r_l + A_l r_{l-s}
-// (s <= l < 2s).  One workgroup per (system, row); wave per output row, or
-// (TRANS, A_l(i, k) = blk[k w + i]) a thread per output element.
+// (s <= l < 2s).  Workgroup (system and row, 32 output rows): a wave per
+// output row (four waves, eight rows each), or (TRANS, A_l(i, k) =
+// blk[k w + i]) eight groups of 32 threads over k, one output row per
+// thread, meeting in LDS.
+constexpr int kRowsPerWg = 32;
+
 template <bool VEC, bool TRANS>
 __global__ __launch_bounds__(kThreads) void pcr_wide_rows(BlockSrc Ain, VecSrc rin, VecDst rout,
                                                           int L, int w, int s, int nrows) {
     __shared__ float rp[kWide];
+    __shared__ float part[kThreads / kRowsPerWg][kRowsPerWg];
     const int b = blockIdx.x / nrows;
     const int l = blockIdx.x - b * nrows;
+    const int i0 = kRowsPerWg * blockIdx.y;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const float* rl = rin.base + b * rin.bstride + (long long)l * rin.rstride;
     float* xo = rout.base + b * rout.bstride + (long long)l * rout.rstride;
     if (l < s) {
-        for (int i = t; i < w; i += kThreads) xo[i] = rl[i];
+        if (t < kRowsPerWg && i0 + t < w) xo[i0 + t] = rl[i0 + t];
         return;
     }
     stage_vec(rp, rin.base + b * rin.bstride + (long long)(l - s) * rin.rstride, w);
     __syncthreads();
     const float* Al = Ain.base + b * Ain.bstride + (long long)l * Ain.rstride;
     if constexpr (!TRANS) {
-        for (int i = wave; i < w; i += kWaves) {
+        for (int i = i0 + wave; i < min(w, i0 + kRowsPerWg); i += kWaves) {
             float v[16];
             row_load<VEC>(Al + (long long)i * w, w, v, lane);
             const float d = row_dot<VEC>(v, rp, lane);
             if (lane == 0) xo[i] = rl[i] + d;
         }
     } else {
-        for (int i = t; i < w; i += kThreads) {
-            float acc = 0.f;
-            for (int k = 0; k < w; ++k) acc = fmaf(Al[(long long)k * w + i], rp[k], acc);
-            xo[i] = rl[i] + acc;
+        const int ii = t % kRowsPerWg, kg = t / kRowsPerWg;
+        const int i = i0 + ii;
+        float acc = 0.f;
+        if (i < w)
+            for (int k = kg; k < w; k += kThreads / kRowsPerWg)
+                acc = fmaf(Al[(long long)k * w + i], rp[k], acc);
+        part[kg][ii] = acc;
+        __syncthreads();
+        if (kg == 0 && i < w) {
+            float sum = part[0][ii];
+            for (int q = 1; q < kThreads / kRowsPerWg; ++q) sum += part[q][ii];
+            xo[i] = rl[i] + sum;
         }
     }
 }
@@ -337,27 +351,6 @@ __global__ __launch_bounds__(kThreads) void forward_eval_wide(
                                   res ? i : -1, lane);
     }
     if (lane == 0) atomicMax(red + kRedF + (int)(row % kRedShards), mr);
-}
-
-// Z[b, 0] = f_0(z0[b]), one workgroup per system (the other rows follow by
-// the broadcast kernel).
-template <bool VEC>
-__global__ __launch_bounds__(kThreads) void first_layer_wide(
-    const float* __restrict__ W, const float* __restrict__ bias, const float* __restrict__ z0,
-    float* __restrict__ Z, int L, int w, int layer, float alpha) {
-    __shared__ float zp[kWide];
-    const int b = blockIdx.x;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    stage_vec(zp, z0 + (long long)b * w, w);
-    __syncthreads();
-    for (int i = wave; i < w; i += kWaves) {
-        float v[16];
-        row_load<VEC>(W + (long long)i * w, w, v, lane);
-        const float a = row_dot<VEC>(v, zp, lane) + bias[i];
-        float d;
-        const float y = activate(layer, a, &d);
-        if (lane == 0) Z[(long long)b * L * w + i] = layer_residual(layer) ? fmaf(alpha, y, zp[i]) : y;
-    }
 }
 
 // Z[b, l] = Z[b, 0] for l >= 1.
@@ -579,7 +572,7 @@ hipError_t launch_pcr_level_wide(const BlockSrc& Ain, const VecSrc& rin, float* 
     const bool vec = (w % 4) == 0;
     const bool tr = Ain.trans != 0;
     const int nrows = L < 2 * s ? L : 2 * s;
-    const dim3 g1((unsigned)((long long)B * nrows));
+    const dim3 g1((unsigned)((long long)B * nrows), (unsigned)((w + kRowsPerWg - 1) / kRowsPerWg));
 #define DEEPPCR_WIDE_ROWS(V, T) \
     hipLaunchKernelGGL((pcr_wide_rows<V, T>), g1, dim3(kThreads), 0, stream, Ain, rin, rout, L, w, s, nrows)
     if (vec && tr) DEEPPCR_WIDE_ROWS(true, true);
@@ -620,13 +613,8 @@ hipError_t launch_forward_eval_wide(const float* W, const float* bias, const flo
 hipError_t launch_initial_guess_wide(const float* W, const float* bias, const float* z0, float* Z,
                                      int B, int L, int w, int layer, float alpha,
                                      hipStream_t stream) {
-    if (w % 4 == 0)
-        hipLaunchKernelGGL((first_layer_wide<true>), dim3((unsigned)B), dim3(kThreads), 0, stream,
-                           W, bias, z0, Z, L, w, layer, alpha);
-    else
-        hipLaunchKernelGGL((first_layer_wide<false>), dim3((unsigned)B), dim3(kThreads), 0,
-                           stream, W, bias, z0, Z, L, w, layer, alpha);
-    hipError_t e = hipGetLastError();
+    // Z[:, 0] = f_0(z0) (the sequential kernel's layer 0), then the broadcast
+    hipError_t e = launch_seq_forward_wide(W, bias, z0, Z, B, L, w, layer, alpha, 0, stream);
     if (e != hipSuccess || L == 1) return e;
     const int rows_per_block = 16;
     const int chunks = (L + rows_per_block - 1) / rows_per_block;

@@ -58,6 +58,9 @@ WORKLOADS = {
     # depth 1024, Newton + PCR forward and the transposed backward
     "resnet_skip4_fwd_bwd": Workload("resnet_skip4_fwd_bwd", "resnet", B=64, L=1024, w=16,
                                      passes=("fwd", "bwd"), skip=4, act=2),
+    # the paper's widest MLP width (Sec. 4.1): tiled block products
+    "mlp_wide_fwd_bwd": Workload("mlp_wide_fwd_bwd", "mlp", B=1, L=256, w=1024,
+                                 passes=("fwd", "bwd")),
     # a diffusion-style sampler (App. A.4): 1024 denoising steps of a 64-wide
     # latent with a synthetic 128-wide denoiser, steps evaluated by the caller
     "diffusion_generic": Workload("diffusion_generic", "diffusion", B=16, L=1024, w=64,
