@@ -267,10 +267,11 @@ def measured_mfma_util(workload):
             "pcr_tail_pct": t.get("pcr_tail_mfma_util_pct")}
 
 
-def roofline(cls, w):
+def roofline(cls, w, by_intensity=False):
     """Roofline position of one kernel class from the library's counts:
     algorithmic flops and bytes of its launches over their summed event
-    time; MFMA-bound at an intensity above the ridge (or at w >= 64)."""
+    time; MFMA-bound at an intensity above the ridge (or, for the PCR level
+    class, at w >= 64, the widths the workload targets rate against MFMA)."""
     intensity = cls["flops"] / max(cls["bytes"], 1.0)
     tflops = cls["flops"] / (cls["ms"] * 1e-3) / 1e12
     gbs = cls["bytes"] / (cls["ms"] * 1e-3) / 1e9
@@ -278,7 +279,7 @@ def roofline(cls, w):
     # shows its fraction of the HBM peak (and the other way round)
     both = {"frac_of_mfma_peak": round(tflops / PEAK_FP32_TFLOPS, 4),
             "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
-    if intensity >= RIDGE or w >= 64:
+    if intensity >= RIDGE or (w >= 64 and not by_intensity):
         return {"bound": "mfma", "achieved": round(tflops, 3), "peak": PEAK_FP32_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(tflops / PEAK_FP32_TFLOPS, 4), **both}
     return {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
@@ -357,8 +358,10 @@ def main():
     }
     tail = prof["pcr_tail"]
     if tail["launches"] > 0:
-        # the last levels' pass, timed as a class of its own
-        out["roofline_tail"] = {"kernel": "pcr_level_tail", **roofline(tail, wl.w),
+        # the last levels' pass (substitution along the chains), timed as a
+        # class of its own
+        out["roofline_tail"] = {"kernel": "pcr_chain_subst",
+                                **roofline(tail, wl.w, by_intensity=True),
                                 "avg_launch_us": round(tail["ms"] * 1e3 / tail["launches"], 3),
                                 "launches": tail["launches"]}
     if info["marks"]:

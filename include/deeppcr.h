@@ -388,7 +388,7 @@ enum {
     DEEPPCR_KCLASS_WGRAD = 3,      /* parameter gradients                      */
     DEEPPCR_KCLASS_OTHER = 4,      /* initial guess, copies, dz0               */
     DEEPPCR_KCLASS_SEQUENTIAL = 5, /* sequential baseline passes               */
-    DEEPPCR_KCLASS_PCR_TAIL = 6,   /* last PCR levels as products with vectors */
+    DEEPPCR_KCLASS_PCR_TAIL = 6,   /* last levels: substitution along the chains */
     DEEPPCR_KCLASS_COUNT = 7
 };
 int deeppcr_profile_enable(int on);

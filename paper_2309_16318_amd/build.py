@@ -16,7 +16,7 @@ OBJ = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdeeppcr.so")
 
 SOURCES = ["api.hip", "pcr_level.hip", "layers.hip", "tiny.hip", "sequential.hip", "small.hip",
-           "resnet.hip", "chunked.hip", "wide.hip"]
+           "resnet.hip", "chunked.hip", "wide.hip", "chain.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",

@@ -280,15 +280,18 @@ void last2_work(int B, int L, int w, int s, double* bytes, double* flops) {
     *flops = (double)B * 2.0 * w2 * (2.0 * n1 + n2);
 }
 
-// Algorithmic work of the last kt levels as products with vectors: A_l read
-// once for l >= s; per row 2^kt - 1 mat-vecs (the composite operators of the
-// kt levels applied to their vectors); r read and the solution written.
+// Algorithmic work of the last kt levels solved by substitution along the
+// chains (s = 2^(levels - kt)): A_l read once and one mat-vec for every row
+// l >= s; r read and the solution written.
 void tail_work(int B, int L, int w, int kt, double* bytes, double* flops) {
     const int s = 1 << (num_levels(L) - kt);
     const double w2 = (double)w * w;
     *bytes = 4.0 * B * ((double)(L - s) * w2 + 2.0 * L * w);
-    *flops = (double)B * (L - s) * ((1 << kt) - 1) * 2.0 * w2;
+    *flops = (double)B * (L - s) * 2.0 * w2;
 }
+
+// Stride of the rows the last kt levels start from.
+int tail_stride(int L, int kt) { return 1 << (num_levels(L) - kt); }
 
 // Runs all PCR levels.  Level 0 reads (A0, r0); level k writes operators to
 // ws A buffer (k + a_first) % 2 and vectors to ws r buffer (k + r_first) % 2,
@@ -356,7 +359,9 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
     double bytes, flops;
     tail_work(B, L, w, kt, &bytes, &flops);
     return timed(DEEPPCR_KCLASS_PCR_TAIL, bytes, flops, st,
-                 [&] { return launch_pcr_level_tail(Ain, rin, x, B, L, w, kt, st); });
+                 [&] {
+                     return launch_pcr_chain_subst(Ain, rin, x, B, L, w, tail_stride(L, kt), st);
+                 });
 }
 
 struct Ws {
@@ -486,15 +491,17 @@ hipError_t fused_rest_levels(const NewtonArgs& na, int B, int L, int w, const Ws
         k += pair ? 2 : 1;
     }
     if (kt > 0) {
-        // the last kt levels in one pass, which also applies the update
-        // Z += x and reduces the convergence maxima (the iterate is read and
-        // written instead of the solution being written)
+        // the chains left for the last kt levels solved by substitution in
+        // one pass, which also applies the update Z += x and reduces the
+        // convergence maxima (the iterate is read and written instead of
+        // the solution being written)
         double bytes, flops;
         tail_work(B, L, w, kt, &bytes, &flops);
         bytes += 4.0 * B * L * w;
         const VecDst zo{na.Z, ld, (long long)w};
         return timed(DEEPPCR_KCLASS_PCR_TAIL, bytes, flops, st, [&] {
-            return launch_pcr_level_tail(Ain, rin, zo, B, L, w, kt, st, na.red);
+            return launch_pcr_chain_subst(Ain, rin, zo, B, L, w, tail_stride(L, kt), st,
+                                          na.red);
         });
     }
     if (!upd) {

@@ -160,18 +160,21 @@ bool two_level(int B, int L, int w);
 hipError_t launch_pcr_level2_bwd(const BwdArgs& bw, const VecSrc& rin, float* Aout,
                                  const VecDst& rout, int B, int L, int w, hipStream_t stream);
 
-// The number of last levels that one tail pass does (0: none), for the
-// problem shape and the number of levels `first` the solve's first pass
-// does (then pairs up to the tail): 3 to 6 levels at w = 32, 64, 128.
+// The number of last levels (0: none) solved instead by substitution along
+// the chains they act on (launch_pcr_chain_subst), for the problem shape and
+// the number of levels `first` the solve's first pass does (then pairs up to
+// them): 3 to 6 levels at w = 32, 64, 128.
 int tail_levels(int B, int L, int w, int first);
-// The last kt = tail_levels(...) levels of a solve in one pass that
-// writes no operator: the solution goes to rout.  Ain holds the operators of
-// the level before (rows l >= s, s = 2^(levels - kt)), not transposed.
-// With red, rout is the Newton iterate instead: the solution is added to it
-// and max |x|, max |Z + x| are reduced into the kRedDZ, kRedZ slots of red.
-hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
-                                 int B, int L, int w, int kt, hipStream_t stream,
-                                 unsigned* red = nullptr);
+// After the levels with strides below s = 2^(levels - kt) every row l >= s
+// satisfies x_l = A_l x_{l-s} + r_l: B s independent chains
+// (l = c, c + s, ...), each solved by substitution, one mat-vec per row.
+// Ain holds the operators of the level before (rows l >= s), not
+// transposed; the solution goes to rout.  With red, rout is the Newton
+// iterate instead: the solution is added to it and max |x|, max |Z + x| are
+// reduced into the kRedDZ, kRedZ slots of red.
+hipError_t launch_pcr_chain_subst(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
+                                  int B, int L, int w, int s, hipStream_t stream,
+                                  unsigned* red = nullptr);
 
 // The last two levels of a solve (strides s, 2s with 4s >= L) in one pass
 // without operator products (mat-vecs only), for the widths last_pair_width

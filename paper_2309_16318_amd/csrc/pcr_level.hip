@@ -18,9 +18,9 @@
 //                registers, right operands in LDS), two levels per pass; the
 //                strip kernels also serve w = 32 for the first two levels of
 //                a Newton iteration or backward solve.
-//   tail         the last 3-6 levels of a solve at w = 32, 64, 128 in one
-//                pass, one workgroup per independent chain, the level
-//                products applied to vectors.
+//   last levels  at w = 32, 64, 128 the last 3-6 levels are not run here:
+//                the chains they act on are solved by substitution
+//                (chain.hip; tail_levels below says how many).
 //   w <= 8       lane groups of a wave per row (small.hip).
 //   other w      generic path: one workgroup per (system, row), float32 FMA on
 //                the vector ALUs, operands staged through LDS in k-chunks.
@@ -30,7 +30,6 @@
 #include "internal.h"
 #include "strip.h"
 
-#include <type_traits>
 
 namespace deeppcr {
 namespace {
@@ -1270,239 +1269,6 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
     }
 }
 
-// ---- the last KT levels of a solve, w = 32, 64, 128 -----------------------
-// After the levels below stride s the system is s independent chains per
-// system, and the last KT levels (strides s .. s 2^{KT-1}, s 2^KT >= L) write
-// no operator: their products only ever meet vectors.  Level i updates
-//   r^{i+1}_m = r^i_m + A_m A_{m-1} ... A_{m-2^i+1} r^i_{m-2^i}   (m >= 2^i)
-// along a chain of stride s (A the blocks this pass reads).  Walking the
-// chain, element m keeps, per level i, the vectors g^i_{j,m} =
-// A_m g^i_{j-1,m-1} (g^i_{0,m} = r^i_m), j = 1 .. 2^i, so that g^i_{2^i,m}
-// is the term of the update.  All of them are A_m times vectors of element
-// m-1, so one product per element, A_m V_{m-1} with V the W x (2^KT - 1)
-// matrix of the carried vectors, does every level's work on MFMA.  Column
-// 2^i - 1 + j of V holds g^i_{j} (j = 0 .. 2^i - 1, j = 0 being r^i); the
-// same column of the product is then g^i_{j+1}.  One workgroup walks one
-// whole chain (at most 2^KT elements), so no segment warm-up is needed; the
-// r chain of an element (r^{i+1} = r^i + g^i_{2^i}) takes KT adds per row.
-template <int W, int KT>
-struct TailShape {
-    static constexpr int NP = 1 << KT;   // columns of V, padded (2^KT - 1 used)
-    static constexpr int NTC = NP / 32;  // 32-column tiles of the product
-    // tiles per wave: as many waves as SIMDs where the tiles allow (more
-    // waves would not add MFMA throughput, only strip reloads); at w = 64
-    // one wave per row strip with all its column tiles, whose independent
-    // accumulators interleave (measured 15% faster than a wave per tile,
-    // which at w = 32 is the faster choice)
-    static constexpr int TPW = W == 64                 ? NTC
-                               : (W / 32) * NTC >= 8 ? (W / 32) * NTC / 4
-                                                     : 1;
-    static constexpr int NWV = (W / 32) * NTC / TPW;
-    static constexpr int NT = 64 * NWV;
-    // elements whose block and right-hand side are in flight: an element's
-    // product is short at small w, so the loads are issued D elements ahead
-    // (a ring of D + 1 strips in registers; at w = 32, D = 7 measured 17%
-    // faster than D = 3, and D = 11 or more as slow as D = 3)
-    static constexpr int D = W == 32 ? 7 : W == 64 ? 2 : 1;
-    static constexpr int NB = D + 1;
-    static_assert(NP % 32 == 0 && NTC % TPW == 0, "whole tiles");
-};
-
-// f(integral_constant<0>), ..., f(integral_constant<N-1>): ring slots as
-// compile-time indices, so that the ring stays in registers.
-template <int I, int N, class F>
-__device__ __forceinline__ void unroll_each(F& f) {
-    if constexpr (I < N) {
-        f(std::integral_constant<int, I>{});
-        unroll_each<I + 1, N>(f);
-    }
-}
-
-// acc[tt] = (strip of A) x (column tile tc0 + tt of V): lane i supplies
-// column i of each tile from col[tt] (its k = 4h .. rows, contiguous).
-template <int W, int NTC>
-__device__ __forceinline__ void tail_product(const float* const (&col)[NTC], const StripA<W>& a,
-                                             v16f (&acc)[NTC]) {
-    constexpr int NQ = Tile2Shape<W>::NQ;
-#pragma unroll
-    for (int tc = 0; tc < NTC; ++tc) acc[tc] = v16f{};
-    v4f pv[2][NTC];
-#pragma unroll
-    for (int q = 0; q <= NQ; ++q) {
-        if (q < NQ) {
-#pragma unroll
-            for (int tc = 0; tc < NTC; ++tc)
-                pv[q & 1][tc] = *reinterpret_cast<const v4f*>(col[tc] + 8 * q);
-        }
-        // keeps the operand reads of step q beside the MFMAs of step q-1
-        __builtin_amdgcn_sched_barrier(0);
-        if (q > 0) {
-            const int qb = (q - 1) & 1;
-            const v4f av = a[q - 1];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-#pragma unroll
-                for (int tc = 0; tc < NTC; ++tc)
-                    acc[tc] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[qb][tc][e], av[e], acc[tc],
-                                                                   0, 0, 0);
-        }
-    }
-}
-
-// One barrier per element.  The r columns of V (n = 2^lv - 1, all in column
-// tile 0) are the only part of V that depends on the r chain, so every wave
-// that computes tile 0 forms the r chain of all W rows itself and keeps
-// those columns in its own LDS rows (RC), which its product reads in place
-// of V's; V's r-column slots hold the update terms of the element instead.
-// What the r chain reads (update terms of V_m) is next overwritten by
-// element m+2, after the barrier of element m+1, which every wave reaches
-// after its r chain of element m.
-// UPD (the last pass of a Newton iteration): rout is the iterate, which each
-// solution row is added to, and max |x| and max |Z + x| are reduced into the
-// kRedDZ and kRedZ slots of red (the update kernel's work, done in place).
-template <int W, int KT, bool UPD>
-__global__ __launch_bounds__((TailShape<W, KT>::NT)) void pcr_level_tail(BlockSrc Ain, VecSrc rin,
-                                                                       VecDst rout, int L, int s,
-                                                                       unsigned* red) {
-    using S = Tile2Shape<W>;
-    using T = TailShape<W, KT>;
-    constexpr int NB = T::NB, D = T::D;
-    constexpr int RPL = W > 64 ? W / 64 : 1;  // rows of the r chain per lane
-    __shared__ float VT[2][T::NP * S::PITCH];  // V_{m-1} / V_m, transposed (VT[n][k])
-    __shared__ float RC[T::NWV][KT][S::PITCH];  // per wave: r^lv_m, lv = 0 .. KT-1
-    const int t = threadIdx.x;
-    const int lane = t & 63, i = lane & 31, h = lane >> 5, wv = t >> 6;
-    const int tc0 = T::TPW * (wv / (W / 32));  // the wave's first column tile
-    const int R = 32 * (wv % (W / 32)) + i;    // the lane's row
-    const int b = (int)(blockIdx.x / s);
-    const int c = (int)(blockIdx.x - (long long)b * s);
-    const int count = (L - 1 - c) / s;  // elements m = 0 .. count
-    const float* ab = Ain.base + b * Ain.bstride;
-    const float* rb = rin.base + b * rin.bstride;
-    float* ob = rout.base + b * rout.bstride;
-    unsigned mx = 0u, mz = 0u;  // UPD: max |x|, max |Z + x| (bit patterns)
-    // lane i's column of tile 0 is r column lv_i (or no r column: -1)
-    const int lv_i = ((i + 1) & i) == 0 && i + 1 < (1 << KT) ? 31 - __builtin_clz(i + 1) : -1;
-
-    // Ring slot m % NB holds A_m (A_0 is never read) and, per r-chain row of
-    // the lane, r_m; element m requests A_{m+D} and r_{m+D}.  Every thread
-    // issues the same loads on every element (rows past the chain's end are
-    // clamped to its last row and never used), so the compiler can count the
-    // requests in flight instead of waiting for all of them where a branch
-    // would merge.
-    StripA<W> a[NB];
-    float rq[NB][RPL];
-    float zq[UPD ? NB : 1][RPL];  // UPD: the iterate's rows, in the same ring
-    v16f acc[T::TPW];
-    auto load_r = [&](int u, long long row) {
-#pragma unroll
-        for (int rr = 0; rr < RPL; ++rr) {
-            const int k = (lane + 64 * rr) & (W - 1);
-            rq[u][rr] = rb[row * rin.rstride + k];
-            if constexpr (UPD) zq[u][rr] = ob[row * rout.rstride + k];
-        }
-    };
-#pragma unroll
-    for (int j = 0; j < D; ++j) {
-        const long long lj = c + (long long)min(j, count) * s;
-        if (j >= 1) strip_load<W, false>(ab + lj * Ain.rstride, a[j], R, h);
-        load_r(j, lj);
-    }
-    auto element = [&](int m, auto U) {
-        constexpr int u = decltype(U)::value;  // m % NB
-        constexpr int un = (u + D) % NB;
-        const float* Vp = VT[(m + 1) & 1];
-        float* Vn = VT[m & 1];
-        const long long l = c + (long long)m * s;
-        {
-            const long long ln = c + (long long)min(m + D, count) * s;
-            strip_load<W, false>(ab + ln * Ain.rstride, a[un], R, h);
-            load_r(un, ln);
-        }
-        if (m >= 1) {
-            const float* col[T::TPW];
-#pragma unroll
-            for (int tt = 0; tt < T::TPW; ++tt)
-                col[tt] = (tc0 + tt == 0 && lv_i >= 0 ? RC[wv][lv_i]
-                                                      : Vp + (32 * (tc0 + tt) + i) * S::PITCH) +
-                          4 * h;
-            tail_product<W, T::TPW>(col, a[u], acc);
-        }
-        // Column n of the product (level lv, n = 2^lv - 1 + j) is g^lv_{j+1};
-        // it goes to column n + 1 of V_m, or, for j + 1 = 2^lv (n + 2 a power
-        // of two), to the update term of level lv, kept in V_m's r-column slot
-        // 2^lv - 1; the padding column goes to the padding column.  The
-        // destination is computed, not branched on.  Element 0 has no block:
-        // its g columns are 0.
-#pragma unroll
-        for (int tt = 0; tt < T::TPW; ++tt)
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
-                const int n0 = 32 * (tc0 + tt) + 8 * qq + 4 * h;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int n = n0 + e;
-                    const int lv = 30 - __builtin_clz(n + 2);
-                    const int col = n == T::NP - 1         ? n
-                                    : ((n + 2) & (n + 1)) ? n + 1
-                                                          : (1 << lv) - 1;
-                    Vn[col * S::PITCH + R] = m >= 1 ? acc[tt][4 * qq + e] : 0.f;
-                }
-            }
-        __syncthreads();  // the g columns of V_m and the update terms are written
-        if (tc0 == 0) {
-#pragma unroll
-            for (int rr = 0; rr < RPL; ++rr) {
-                const int k = lane + 64 * rr;
-                if (k < W) {
-                    // all update terms are read before the sums that need them
-                    float up[KT];
-#pragma unroll
-                    for (int lv = 0; lv < KT; ++lv) up[lv] = Vn[((1 << lv) - 1) * S::PITCH + k];
-                    float r = rq[u][rr];
-#pragma unroll
-                    for (int lv = 0; lv < KT; ++lv) {
-                        RC[wv][lv][k] = r;  // r^lv_m
-                        r += m >= (1 << lv) ? up[lv] : 0.f;
-                    }
-                    if (wv == 0) {
-                        float* o = ob + l * rout.rstride + k;
-                        if constexpr (UPD) {
-                            const float z = zq[u][rr] + r;
-                            *o = z;
-                            mx = max(mx, __float_as_uint(fabsf(r)));
-                            mz = max(mz, __float_as_uint(fabsf(z)));
-                        } else {
-                            *o = r;
-                        }
-                    }
-                }
-            }
-        }
-    };
-    // NB elements per trip, so that every ring index is a constant
-    for (int mb = 0; mb <= count; mb += NB) {
-        auto trip = [&](auto U) {
-            const int m = mb + decltype(U)::value;
-            if (m <= count) element(m, U);
-        };
-        unroll_each<0, NB>(trip);
-    }
-    if constexpr (UPD) {
-        if (wv == 0) {
-            for (int off = 32; off > 0; off >>= 1) {
-                mx = max(mx, (unsigned)__shfl_xor((int)mx, off, 64));
-                mz = max(mz, (unsigned)__shfl_xor((int)mz, off, 64));
-            }
-            if (lane == 0) {
-                const int slot = blockIdx.x % kRedShards;
-                atomicMax(red + kRedDZ + slot, mx);
-                atomicMax(red + kRedZ + slot, mz);
-            }
-        }
-    }
-}
-
 // The last two levels of a solve (strides s and 2s, 4s >= L): no operator
 // is written, and the one product the walk would form, A'_m = A_m A_{m-1},
 // only ever meets the vector r'_{m-2}, so A'_m r'_{m-2} is taken as
@@ -1984,56 +1750,6 @@ int tail_levels(int B, int L, int w, int first) {
         return kt;
     }
     return 0;
-}
-
-hipError_t launch_pcr_level_tail(const BlockSrc& Ain, const VecSrc& rin, const VecDst& rout,
-                                 int B, int L, int w, int kt, hipStream_t stream,
-                                 unsigned* red) {
-    // KT = 5 serves 3 to 5 levels (one 32-column tile; the levels above
-    // the chain length never update, since m < 2^lv there)
-    const int s = 1 << (num_levels_of(L) - kt);
-    const dim3 grid((unsigned)((long long)B * s));
-    if (Ain.trans) return hipErrorInvalidValue;
-#define DEEPPCR_TAIL(WW, KK)                                                                      \
-    do {                                                                                          \
-        if (red)                                                                                  \
-            hipLaunchKernelGGL((pcr_level_tail<WW, KK, true>), grid,                              \
-                               dim3((TailShape<WW, KK>::NT)), 0, stream, Ain, rin, rout, L, s,    \
-                               red);                                                              \
-        else                                                                                      \
-            hipLaunchKernelGGL((pcr_level_tail<WW, KK, false>), grid,                             \
-                               dim3((TailShape<WW, KK>::NT)), 0, stream, Ain, rin, rout, L, s,    \
-                               red);                                                              \
-    } while (0)
-    if (w == 32) {
-        switch (kt) {
-            case 3: DEEPPCR_TAIL(32, 5); break;
-            case 4: DEEPPCR_TAIL(32, 5); break;
-            case 5: DEEPPCR_TAIL(32, 5); break;
-            case 6: DEEPPCR_TAIL(32, 6); break;
-            default: return hipErrorInvalidValue;
-        }
-    } else if (w == 64) {
-        switch (kt) {
-            case 3: DEEPPCR_TAIL(64, 5); break;
-            case 4: DEEPPCR_TAIL(64, 5); break;
-            case 5: DEEPPCR_TAIL(64, 5); break;
-            case 6: DEEPPCR_TAIL(64, 6); break;
-            default: return hipErrorInvalidValue;
-        }
-    } else if (w == 128) {
-        switch (kt) {
-            case 3: DEEPPCR_TAIL(128, 5); break;
-            case 4: DEEPPCR_TAIL(128, 5); break;
-            case 5: DEEPPCR_TAIL(128, 5); break;
-            case 6: DEEPPCR_TAIL(128, 6); break;
-            default: return hipErrorInvalidValue;
-        }
-    } else {
-        return hipErrorInvalidValue;
-    }
-#undef DEEPPCR_TAIL
-    return hipGetLastError();
 }
 
 bool fused_newton_levels(int w) { return w == 16 || w == 32; }

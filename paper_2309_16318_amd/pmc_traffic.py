@@ -28,9 +28,22 @@ import hashlib
 import json
 import os
 
-# the PCR level kernels and the register-strip helpers they are built from
+# the PCR level kernels, the register-strip helpers they are built from and
+# the substitution pass of the last levels
 KERNEL_SOURCES = [os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", f)
-                  for f in ("pcr_level.hip", "strip.h")]
+                  for f in ("pcr_level.hip", "strip.h", "chain.hip")]
+
+# kernels of the last levels' pass (timed as a class of their own)
+TAIL_PREFIXES = ("pcr_chain_subst", "pcr_level_tail")
+
+
+def is_tail(name: str) -> bool:
+    return name.startswith(TAIL_PREFIXES)
+
+
+def is_pcr(name: str) -> bool:
+    """A kernel of the PCR sweep: a level pass or the last levels' pass."""
+    return "pcr_level" in name or is_tail(name)
 
 
 def code_digest(text: str) -> str:
@@ -186,7 +199,7 @@ def mfma(argv=None) -> dict:
     allk = per_kernel_all(a.dir)
     kernels = {}
     for name, cs in allk.items():
-        if "pcr_level" not in name or "MfmaUtil" not in cs:
+        if not is_pcr(name) or "MfmaUtil" not in cs:
             continue
         kernels[name] = {"launches": cs["MfmaUtil"][0],
                          **{c: v[1] / v[0] for c, v in cs.items()}}
@@ -196,8 +209,8 @@ def mfma(argv=None) -> dict:
         n = sum(v["launches"] for v in ks)
         return (sum(v["MfmaUtil"] * v["launches"] for v in ks) / n) if n else None
     out = {"workload": a.workload, "kernel_source_sha256": kernel_source_sha256(),
-           "pcr_level_mfma_util_pct": weighted(lambda n: not n.startswith("pcr_level_tail")),
-           "pcr_tail_mfma_util_pct": weighted(lambda n: n.startswith("pcr_level_tail")),
+           "pcr_level_mfma_util_pct": weighted(lambda n: not is_tail(n)),
+           "pcr_tail_mfma_util_pct": weighted(is_tail),
            "by_kernel": kernels}
     os.makedirs(os.path.dirname(os.path.abspath(a.out)), exist_ok=True)
     with open(a.out, "w") as f:
@@ -232,7 +245,7 @@ def traffic():
     write = per_kernel(a.write, "WRITE_SIZE")
     kernels = {}
     for name in fetch:
-        if "pcr_level" not in name or name not in write:
+        if not is_pcr(name) or name not in write:
             continue
         n = fetch[name][0]
         kernels[name] = {"launches": n,
@@ -240,7 +253,7 @@ def traffic():
                          "write_bytes_per_launch": write[name][1] * wf / write[name][0]}
     # The tail pass is timed as a class of its own, so the per-launch average
     # that goes with the PCR-level roofline leaves it out.
-    level = {k: v for k, v in kernels.items() if not k.startswith("pcr_level_tail")}
+    level = {k: v for k, v in kernels.items() if not is_tail(k)}
     n_all = sum(v["launches"] for v in level.values())
     rd = sum(v["read_bytes_per_launch"] * v["launches"] for v in level.values()) / n_all
     wr = sum(v["write_bytes_per_launch"] * v["launches"] for v in level.values()) / n_all
