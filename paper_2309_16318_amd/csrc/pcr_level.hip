@@ -1133,21 +1133,37 @@ __global__ __launch_bounds__(256) void pcr_level2_wave(BlockSrc Ain, VecSrc rin,
 // Level-2s product of an element, A''_m = A'_m A'_{m-2} (A'_{m-2} in YT),
 // two column tiles at a time, each pair stored as soon as it is done (so no
 // whole product strip is held); returns A'_m r'_{m-2} (r'_{m-2} in LDS).
-template <int W>
+// side(q) runs at k-step q of the first pair of column tiles (see
+// strip_product).
+template <int W, class F = NoSide>
 __device__ __forceinline__ float second_product(const float* YT, const StripC<W>& pC,
                                                 const float* rpp, float* dst, int i, int h,
-                                                int R) {
+                                                int R, F side = F{}) {
     constexpr int T = Tile2Shape<W>::T;
     constexpr int N0 = T < 2 ? T : 2;
     v16f acc[N0];
     const float part = strip_matvec<W>(pC, rpp, h);
-    strip_product<W, 0, N0, false>(YT, pC, acc, i, h);
+    strip_product<W, 0, N0, false>(YT, pC, acc, i, h, nullptr, side);
     tiles_store<W, 0, N0>(dst, acc, R, h);
     if constexpr (T == 4) {
         strip_product<W, 2, 2, false>(YT, pC, acc, i, h);
         tiles_store<W, 2, 2>(dst, acc, R, h);
     }
     return part;
+}
+
+// Quad q of the strip of strip_load_bwd below.
+template <int W>
+__device__ __forceinline__ void strip_load_bwd_quad(const BwdArgs& bw, int b, int L, int m,
+                                                    StripA<W>& a, int R, int h, int q) {
+    const int lay = L - max(m, 1);
+    const float* Wl = bw.W + (long long)lay * W * W;
+    const float* dl = bw.dscale + ((long long)b * L + lay) * W;
+    const int dk = bw.residual ? R - 4 * h : -1;
+    const v4f d4 = *reinterpret_cast<const v4f*>(dl + 8 * q + 4 * h);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        a[q][e] = fmaf(d4[e], Wl[(8 * q + 4 * h + e) * W + R], dk == 8 * q + e ? 1.f : 0.f);
 }
 
 // The strip of row m of the backward's reversed transposed system, formed
@@ -1217,6 +1233,12 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
         else
             strip_load<W, TRANS>(ab + (long long)row * Ain.rstride, a, R, h);
     };
+    auto load_quad = [&](int row, int q) {
+        if constexpr (SRCB)
+            strip_load_bwd_quad<W>(bw, b, L, row, a, R, h, q);
+        else
+            strip_load_quad<W, TRANS>(ab + (long long)row * Ain.rstride, a, R, h, q);
+    };
     int l = c + s * mw;
     if (t < W) rv[mw & 1][t] = rb[(long long)l * rin.rstride + t];
     if (mw >= 1) load(l);
@@ -1244,17 +1266,40 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
             strip_zero<W>(pC);
         }
         __syncthreads();  // B0: X and rv are read
-        if (more && m >= 1) strip_put_T<W>(X, a, R, h);  // A_m
         if (more && t < W) rv[(m + 1) & 1][t] = rnext;
-        // without a next element this rereads the current block (unused)
-        load(more ? l + s : l);
+        // A_m to X and the strip of the next element into a (without a next
+        // element the load rereads the current block, unused).  At w = 128
+        // from memory: quad by quad beside the level-2s product, which reads
+        // neither (the matrix cores are otherwise idle while a lone
+        // workgroup per CU writes and loads); else before it (w = 64 measured
+        // no faster, and the quad form of the backward's strips spills).
+        constexpr bool SIDE = W == 128 && !SRCB;
+        const bool putx = more && m >= 1;
+        const int nrow = more ? l + s : l;
+        auto side = [&](int q) {
+            if (putx) strip_put_T_quad<W>(X, a, R, h, q);
+            load_quad(nrow, q);
+        };
+        if constexpr (!SIDE) {
+            if (putx) strip_put_T<W>(X, a, R, h);
+            load(nrow);
+        }
         // level 2s: r''_m and A''_m
         float r2 = r1;
         const bool prod2 = m >= 4 && out_row;
-        if (prod2)
-            r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)l * W * W, i, h, R);
-        else if (m >= 2 && out_row)
-            r2 += strip_matvec<W>(pC, rp[m & 1], h);
+        if (prod2) {
+            if constexpr (SIDE)
+                r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)l * W * W, i, h, R,
+                                        side);
+            else
+                r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)l * W * W, i, h, R);
+        } else {
+            if constexpr (SIDE) {
+#pragma unroll
+                for (int q = 0; q < S::NQ; ++q) side(q);
+            }
+            if (m >= 2 && out_row) r2 += strip_matvec<W>(pC, rp[m & 1], h);
+        }
         if (out_row && h == 0) ob[(long long)l * rout.rstride + R] = r2;
         __syncthreads();  // B1: Y and rp are read
         if (h == 0) rp[m & 1][R] = r1;
@@ -1480,22 +1525,42 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
                 strip_zero<W>(pC);
             }
             __syncthreads();  // B0: X, rv and zv are read
-            if (more && m >= 1) strip_put_T<W>(X, aC, R, h);  // J_m
             if (h == 0) rv[m & 1][R] = rm;
+            // J_m to X and (without PF) the weight strip of the next element
+            // into aC (without a next element this rereads the current one,
+            // unused): at w = 128 quad by quad beside the level-2 product,
+            // which reads neither, else before it
+            constexpr bool SIDE = W == 128 && !PF;
+            const bool putx = more && m >= 1;
+            const float* wn = na.W + (long long)(more ? m + 1 : m) * W * W;
+            auto side = [&](int q) {
+                if (putx) strip_put_T_quad<W>(X, aC, R, h, q);
+                strip_load_quad<W, false>(wn, aC, R, h, q);
+            };
+            if constexpr (!SIDE)
+                if (putx) strip_put_T<W>(X, aC, R, h);  // J_m
             if constexpr (PF) {
                 if (more && t < W) zv[(m + 1) & 1][t] = zO;
             } else {
                 if (more && t < W) zv[(m + 1) & 1][t] = znext;
-                // without a next element this rereads the current block (unused)
-                strip_load<W, false>(na.W + (long long)(more ? m + 1 : m) * W * W, aC, R, h);
+                if constexpr (!SIDE) strip_load<W, false>(wn, aC, R, h);
             }
             // level 2: r''_m and A''_m
             float r2 = r1;
             const bool prod2 = m >= 4 && out_row;
-            if (prod2)
-                r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)m * W * W, i, h, R);
-            else if (m >= 2 && out_row)
-                r2 += strip_matvec<W>(pC, rp[m & 1], h);
+            if (prod2) {
+                if constexpr (SIDE)
+                    r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)m * W * W, i, h, R,
+                                            side);
+                else
+                    r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)m * W * W, i, h, R);
+            } else {
+                if constexpr (SIDE) {
+#pragma unroll
+                    for (int q = 0; q < S::NQ; ++q) side(q);
+                }
+                if (m >= 2 && out_row) r2 += strip_matvec<W>(pC, rp[m & 1], h);
+            }
             if (out_row && h == 0) ob[(long long)m * rout.rstride + R] = r2;
             __syncthreads();  // B1: Y and rp are read
             if (h == 0) rp[m & 1][R] = r1;

@@ -75,16 +75,24 @@ __device__ __forceinline__ float strip_matvec(const M& a, const float* x, int h)
     return part + __shfl_xor(part, 32, 64);
 }
 
+// No side work in a product's k-loop.
+struct NoSide {
+    __device__ __forceinline__ void operator()(int) const {}
+};
+
 // acc[0 .. NTC-1] = column tiles TC0 .. TC0+NTC-1 of (strip of M) X, X in
 // LDS transposed (XT[col][k], pitch PITCH): the right operand of k-step q for
 // one column tile is one 16-byte read, and all offsets fit the immediate
 // field of one base address.  With MV also returns (strip of M) x for the
 // vector x in LDS (every lane of the row gets the sum), from the left
 // operands as they pass (for accumulator strips this avoids copying the
-// whole strip out of the accumulation registers at once).
-template <int W, int TC0, int NTC, bool MV, class M>
+// whole strip out of the accumulation registers at once).  side(q) runs at
+// k-step q beside the MFMAs of step q-1: work that touches neither XT, a,
+// acc nor x (a block going to another LDS buffer, the next strip's loads).
+template <int W, int TC0, int NTC, bool MV, class M, class F = NoSide>
 __device__ __forceinline__ float strip_product(const float* XT, const M& a, v16f (&acc)[NTC],
-                                               int i, int h, const float* x = nullptr) {
+                                               int i, int h, const float* x = nullptr,
+                                               F side = F{}) {
     using S = Tile2Shape<W>;
 #pragma unroll
     for (int tc = 0; tc < NTC; ++tc) acc[tc] = v16f{};
@@ -98,6 +106,7 @@ __device__ __forceinline__ float strip_product(const float* XT, const M& a, v16f
             for (int tc = 0; tc < NTC; ++tc)
                 pv[q & 1][tc] = *reinterpret_cast<const v4f*>(xb + 32 * tc * S::PITCH + 8 * q);
             if constexpr (MV) xv[q & 1] = *reinterpret_cast<const v4f*>(x + 8 * q + 4 * h);
+            side(q);
         }
         // keeps the operand reads of step q beside the MFMAs of step q-1
         __builtin_amdgcn_sched_barrier(0);
@@ -140,6 +149,31 @@ __device__ __forceinline__ void strip_store(float* dst, const M& a, int R, int h
 #pragma unroll
     for (int q = 0; q < Tile2Shape<W>::NQ; ++q)
         *reinterpret_cast<v4f*>(dst + R * W + 8 * q + 4 * h) = strip_quad<W>(a, q);
+}
+
+// Quad q (columns 8q + 4h .. +3) of a strip from a block in global memory.
+template <int W, bool TRANS>
+__device__ __forceinline__ void strip_load_quad(const float* blk, StripA<W>& a, int R, int h,
+                                                int q) {
+    if constexpr (!TRANS) {
+        a[q] = *reinterpret_cast<const v4f*>(blk + R * W + 8 * q + 4 * h);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a[q][e] = blk[(8 * q + 4 * h + e) * W + R];
+    }
+}
+
+// Quad q of a strip to a transposed block in LDS (see strip_put_T).
+template <int W, class M>
+__device__ __forceinline__ void strip_put_T_quad(float* XT, const M& a, int R, int h, int q) {
+    using S = Tile2Shape<W>;
+    float* xb = XT + 4 * h * S::PITCH + R;
+    const v4f x = strip_quad<W>(a, q);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        xb[(8 * q + e) * S::PITCH] = x[e];
+        asm volatile("" ::: "memory");
+    }
 }
 
 // A strip to a transposed block in LDS (XT[col][row], pitch PITCH).  The
