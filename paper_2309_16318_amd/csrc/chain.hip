@@ -27,14 +27,20 @@ namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
+// Measured (bench.py, one MI355X, same box): at w = 128, 1024 threads and
+// one row ahead 206 us per pass against 217 with 512 threads and 246 with
+// two rows ahead (more rows in flight make the pass slower, not faster: its
+// limit is the per-row chain of mat-vec, shuffles and barrier, not the bytes
+// in flight); w = 32: 4 rows ahead 49 us, 8 rows 59 us; w = 64: 1-3 rows
+// ahead 224-227 us, 4 rows 235 us.
 template <int W>
 struct ChainShape {
-    static constexpr int NT = W == 128 ? 512 : 256;  // threads per workgroup
-    static constexpr int TPR = NT / W;               // threads per block row
-    static constexpr int CPT = W / TPR;              // columns per thread
-    static constexpr int NV = CPT / 4;               // float4 per thread per block
-    static constexpr int D = W == 32 ? 8 : W == 64 ? 4 : 2;  // rows requested ahead
-    static constexpr int NB = D + 1;                 // ring slots
+    static constexpr int NT = W == 128 ? 1024 : 256;  // threads per workgroup
+    static constexpr int TPR = NT / W;                // threads per block row
+    static constexpr int CPT = W / TPR;               // columns per thread
+    static constexpr int NV = CPT / 4;                // float4 per thread per block
+    static constexpr int D = W == 32 ? 4 : W == 64 ? 2 : 1;  // rows requested ahead
+    static constexpr int NB = D + 1;                  // ring slots
     static_assert(CPT % 4 == 0 && TPR <= 64 && (TPR & (TPR - 1)) == 0, "row split");
 };
 
