@@ -62,10 +62,18 @@ def make_step(wl, dev):
                          device=dev)
         x = torch.empty_like(t["r"])
 
+        if wl.chunks > 1:
+            ws = torch.empty(deeppcr.lib().deeppcr_chunked_workspace_bytes(B, L, w, wl.chunks),
+                             dtype=torch.uint8, device=dev)
+
         def step():
             e0 = mark()
-            deeppcr.pcr_solve_block_bidiag(t["J"], t["r"], x, transpose=wl.transpose,
-                                           workspace=ws)
+            if wl.chunks > 1:
+                deeppcr.pcr_solve_block_bidiag_chunked(t["J"], t["r"], wl.chunks, x,
+                                                       transpose=wl.transpose, workspace=ws)
+            else:
+                deeppcr.pcr_solve_block_bidiag(t["J"], t["r"], x, transpose=wl.transpose,
+                                               workspace=ws)
             e1 = mark()
             info["marks"].append((e0, e1, e1))
         return step, info
@@ -346,6 +354,7 @@ def main():
            "passes": list(wl.passes), "newton_iters": info["iters"],
            **({"skip": wl.skip, "unknowns_per_system": wl.L // wl.skip}
               if wl.kind == "resnet" else {}),
+           **({"row_chunks": wl.chunks} if wl.chunks > 1 else {}),
            "newton_tol": wl.tol if "fwd" in wl.passes else None,
            "parallelism": "single-gpu"}
     out = {

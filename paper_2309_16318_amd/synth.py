@@ -40,6 +40,7 @@ class Workload:
     skip: int = 1        # collapsed-skip ResNet: layers per block
     act: int = 2         # collapsed-skip ResNet activation: 0 tanh, 1 sigmoid, 2 ReLU
     hidden: int = 0      # diffusion-style sampler: denoiser width
+    chunks: int = 1      # row-chunked solve: chunks of the depth split
 
 
 # The workloads the build is measured on (tanh MLPs / residual nets with
@@ -58,6 +59,10 @@ WORKLOADS = {
     # depth 1024, Newton + PCR forward and the transposed backward
     "resnet_skip4_fwd_bwd": Workload("resnet_skip4_fwd_bwd", "resnet", B=64, L=1024, w=16,
                                      passes=("fwd", "bwd"), skip=4, act=2),
+    # the standalone solve's system computed over 8 row chunks (the
+    # single-GPU part of a depth split over 8 devices)
+    "pcr_solve_chunked": Workload("pcr_solve_chunked", "pcr", B=64, L=1024, w=16, transpose=1,
+                                  passes=("pcr",), chunks=8),
     # the paper's widest MLP width (Sec. 4.1): tiled block products
     "mlp_wide_fwd_bwd": Workload("mlp_wide_fwd_bwd", "mlp", B=1, L=256, w=1024,
                                  passes=("fwd", "bwd")),
