@@ -13,7 +13,7 @@
 // TPR-th of its columns; the blocks and right-hand sides of the next D rows
 // are requested into a register ring before the current row's mat-vec (the
 // loads do not depend on the chain's solution), the partial dot products
-// meet through lane shuffles, and the new x goes to LDS for the next row
+// meet through DPP lane permutations, and the new x goes to LDS for the next row
 // (double-buffered, one barrier per row).
 // UPD (the last pass of a Newton iteration): rout is the iterate; each
 // solution row is added to it and max |x|, max |Z + x| are reduced into the
@@ -30,19 +30,41 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // Measured (bench.py, one MI355X, same box): at w = 128, 1024 threads and
 // one row ahead 206 us per pass against 217 with 512 threads and 246 with
 // two rows ahead (more rows in flight make the pass slower, not faster: its
-// limit is the per-row chain of mat-vec, shuffles and barrier, not the bytes
-// in flight); w = 32: 4 rows ahead 49 us, 8 rows 59 us; w = 64: 1-3 rows
-// ahead 224-227 us, 4 rows 235 us.
+// limit is the per-row chain of mat-vec, reduction and barrier, not the
+// bytes in flight); w = 32: 4 rows ahead 49 us, 8 rows 59 us; w = 64: 1-3
+// rows ahead 224-227 us, 4 rows 235 us.  w = 16: one wave per chain (a
+// 1 KiB block is one float4 per lane), 8 rows ahead.
 template <int W>
 struct ChainShape {
-    static constexpr int NT = W == 128 ? 1024 : 256;  // threads per workgroup
-    static constexpr int TPR = NT / W;                // threads per block row
-    static constexpr int CPT = W / TPR;               // columns per thread
-    static constexpr int NV = CPT / 4;                // float4 per thread per block
-    static constexpr int D = W == 32 ? 4 : W == 64 ? 2 : 1;  // rows requested ahead
-    static constexpr int NB = D + 1;                  // ring slots
-    static_assert(CPT % 4 == 0 && TPR <= 64 && (TPR & (TPR - 1)) == 0, "row split");
+    // threads per workgroup
+    static constexpr int NT = W == 128 ? 1024 : W == 16 ? 64 : 256;
+    static constexpr int TPR = NT / W;   // threads per block row
+    static constexpr int CPT = W / TPR;  // columns per thread
+    static constexpr int NV = CPT / 4;   // float4 per thread per block
+    // rows requested ahead
+    static constexpr int D = W == 16 ? 8 : W == 32 ? 4 : W == 64 ? 2 : 1;
+    static constexpr int NB = D + 1;  // ring slots
+    static_assert(CPT % 4 == 0 && TPR >= 2 && TPR <= 16 && (TPR & (TPR - 1)) == 0, "row split");
 };
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the TPR consecutive lanes of a block row (TPR = 2 .. 16, inside
+// one 16-lane DPP row), in every lane of the row: butterfly steps whose
+// partner lanes come from DPP permutations (quad_perm [1,0,3,2] and
+// [2,3,0,1], then the half-row and row mirrors, which pair each lane with one
+// of the other group of 4 or 8 lanes), VALU operations with no LDS round trip.
+template <int TPR>
+__device__ __forceinline__ float row_sum(float v) {
+    v += dpp<0xB1>(v);
+    if constexpr (TPR >= 4) v += dpp<0x4E>(v);
+    if constexpr (TPR >= 8) v += dpp<0x141>(v);
+    if constexpr (TPR >= 16) v += dpp<0x140>(v);
+    return v;
+}
 
 template <int I, int N, class F>
 __device__ __forceinline__ void each_slot(F& f) {
@@ -124,9 +146,7 @@ __global__ __launch_bounds__(ChainShape<W>::NT) void pcr_chain_subst(BlockSrc Ai
 #pragma unroll
                 for (int e = 0; e < 4; ++e) acc = fmaf(blk[j][v][e], xv[e], acc);
             }
-#pragma unroll
-            for (int off = 1; off < S::TPR; off <<= 1) acc += __shfl_xor(acc, off, 64);
-            const float x = rr[j] + acc;
+            const float x = rr[j] + row_sum<S::TPR>(acc);
             if (p == 0) {
                 float* o = ob + (long long)(c + (long long)s * m) * rout.rstride + i;
                 if constexpr (UPD) {
@@ -182,6 +202,7 @@ hipError_t launch_pcr_chain_subst(const BlockSrc& Ain, const VecSrc& rin, const 
                                stream, Ain, rin, rout, red, L, s);                             \
     } while (0)
     switch (w) {
+        case 16: DEEPPCR_CHAIN(16); break;
         case 32: DEEPPCR_CHAIN(32); break;
         case 64: DEEPPCR_CHAIN(64); break;
         case 128: DEEPPCR_CHAIN(128); break;

@@ -1506,15 +1506,22 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
             const float f = layer_out<W>(na, strip_matvec<W>(aC, zp, h) + bm, zp[R], &dsc);
             const float rm = f - zv[m & 1][R];
             mr = max(mr, __float_as_uint(fabsf(rm)));
-            // the diagonal is column k = R, at 8q + e = R - 4h (the empty asm
-            // keeps the compiler from holding 64 precomputed selects)
-            int dk = res ? R - 4 * h : -1;
-            asm volatile("" : "+v"(dk));
+            if (res) {
+                // the diagonal is column k = R, at 8q + e = R - 4h (the empty
+                // asm keeps the compiler from holding 64 precomputed selects)
+                int dk = R - 4 * h;
+                asm volatile("" : "+v"(dk));
 #pragma unroll
-            for (int q = 0; q < S::NQ; ++q)
+                for (int q = 0; q < S::NQ; ++q)
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    aC[q][e] = fmaf(dsc, aC[q][e], dk == 8 * q + e ? 1.f : 0.f);
+                    for (int e = 0; e < 4; ++e)
+                        aC[q][e] = fmaf(dsc, aC[q][e], dk == 8 * q + e ? 1.f : 0.f);
+            } else {
+#pragma unroll
+                for (int q = 0; q < S::NQ; ++q)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) aC[q][e] *= dsc;
+            }
             // level 1: r'_m and A'_m
             float r1 = rm;
             const bool prod1 = m >= 2 && have_prev;
@@ -1804,7 +1811,7 @@ int num_levels_of(int L) {
 }  // namespace
 
 int tail_levels(int B, int L, int w, int first) {
-    if (!(w == 32 || w == 64 || w == 128) || !two_level(B, L, w)) return 0;
+    if (!(w == 16 || w == 32 || w == 64 || w == 128) || !two_level(B, L, w)) return 0;
     const int K = num_levels_of(L);
     // the most levels (6 down to 3) such that the levels before the tail are
     // the first pass plus pairs, the tail reads operators written by this

@@ -61,6 +61,15 @@ __device__ __forceinline__ void strip_zero(StripC<W>& c) {
     for (int tc = 0; tc < Tile2Shape<W>::T; ++tc) c[tc] = v16f{};
 }
 
+// x + (x of lane l ^ 32): one v_permlane32_swap exchanges the two halves of
+// the wave (no LDS round trip); its two results hold, in every lane, the
+// lane's own value and its partner's.
+__device__ __forceinline__ float half_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // (strip of M) x for x in LDS; every lane of the row gets the sum.
 template <int W, class M>
 __device__ __forceinline__ float strip_matvec(const M& a, const float* x, int h) {
@@ -72,7 +81,7 @@ __device__ __forceinline__ float strip_matvec(const M& a, const float* x, int h)
 #pragma unroll
         for (int e = 0; e < 4; ++e) part = fmaf(av[e], xv[e], part);
     }
-    return part + __shfl_xor(part, 32, 64);
+    return half_sum(part);
 }
 
 // No side work in a product's k-loop.
@@ -125,7 +134,7 @@ __device__ __forceinline__ float strip_product(const float* XT, const M& a, v16f
             }
         }
     }
-    if constexpr (MV) return part + __shfl_xor(part, 32, 64);
+    if constexpr (MV) return half_sum(part);
     return 0.f;
 }
 

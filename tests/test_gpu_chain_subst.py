@@ -41,8 +41,10 @@ def h(t):
     return t.detach().cpu().numpy()
 
 
-# (w, B, L): 3, 4, 5 and 6 substituted levels at w = 32, 64, 128, odd L
-SHAPES = [(32, 64, 33), (32, 64, 65), (32, 64, 127), (32, 64, 129), (32, 64, 300),
+# (w, B, L): 3, 4, 5 and 6 substituted levels at w = 16, 32, 64, 128, odd L
+SHAPES = [(16, 64, 1024), (16, 64, 17), (16, 64, 33), (16, 32, 65), (16, 16, 129),
+          (16, 8, 300), (16, 4, 1000), (16, 256, 64),
+          (32, 64, 33), (32, 64, 65), (32, 64, 127), (32, 64, 129), (32, 64, 300),
           (32, 16, 65), (32, 16, 257), (32, 16, 1000),
           (64, 32, 65), (64, 32, 129), (64, 32, 300), (64, 8, 257), (64, 8, 1000),
           (128, 16, 129), (128, 16, 200), (128, 4, 513)]
