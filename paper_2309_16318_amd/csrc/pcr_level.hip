@@ -1306,11 +1306,12 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
         if (more && m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
         l += s;
     };
-    for (int m = mw; m <= m1; ++m) {
-        if (m & 1)
-            element(m, pO, pE);
-        else
-            element(m, pE, pO);
+    // an even and an odd element per loop step, so that every register set
+    // keeps its role through the loop (no parity branch to merge); an odd
+    // first element starts the loop with its even slot skipped
+    for (int m = mw & ~1; m <= m1; m += 2) {
+        if (m >= mw) element(m, pE, pO);
+        if (m + 1 <= m1) element(m + 1, pO, pE);
     }
 }
 
@@ -1573,17 +1574,21 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
             if (h == 0) rp[m & 1][R] = r1;
             if (more && m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
         };
-        for (int m = mw; m <= m1; ++m) {
-            if constexpr (PF) {
-                if (m & 1)
-                    element(m, pO, pE, aO, aE, zq1, zq0, bq1, bq0);
-                else
+        // an even and an odd element per loop step, so that every register
+        // set keeps its role through the loop (no parity branch to merge);
+        // an odd first element starts the loop with its even slot skipped
+        for (int m = mw & ~1; m <= m1; m += 2) {
+            if (m >= mw) {
+                if constexpr (PF)
                     element(m, pE, pO, aE, aO, zq0, zq1, bq0, bq1);
-            } else {
-                if (m & 1)
-                    element(m, pO, pE, aE, aE, zq1, zq0, bq1, bq0);
                 else
                     element(m, pE, pO, aE, aE, zq0, zq1, bq0, bq1);
+            }
+            if (m + 1 <= m1) {
+                if constexpr (PF)
+                    element(m + 1, pO, pE, aO, aE, zq1, zq0, bq1, bq0);
+                else
+                    element(m + 1, pO, pE, aE, aE, zq1, zq0, bq1, bq0);
             }
         }
     }
