@@ -155,7 +155,45 @@ def make_step(wl, dev):
             deeppcr.deeppcr_mlp_backward(t["W"], t["bias"], t["z0"], Z, t["G"], layer=wl.layer,
                                          alpha=wl.alpha, workspace=op_ws["bwd"], **outs)
         info["marks"].append((e0, e1, mark()))
+
+    if wl.passes == ("fwd",):
+        def c_call():
+            # the C entry point alone: the same call with its arguments
+            # marshalled once (no Python-side checks, stream lookup or result
+            # object), timed on the host; it returns after the solve's
+            # host wait, as every forward call does
+            import ctypes
+
+            f = deeppcr.lib().deeppcr_mlp_forward
+            it, last = ctypes.c_int(0), ctypes.c_float(0.0)
+            a = (ctypes.c_void_p(t["W"].data_ptr()), ctypes.c_void_p(t["bias"].data_ptr()),
+                 ctypes.c_void_p(t["z0"].data_ptr()), ctypes.c_void_p(Z.data_ptr()), B, L, w,
+                 int(wl.layer), float(wl.alpha), float(wl.tol), int(wl.max_iter), None,
+                 ctypes.c_void_p(op_ws["fwd"].data_ptr()), op_ws["fwd"].numel(),
+                 ctypes.byref(it), ctypes.byref(last),
+                 ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+            return lambda: f(*a)
+
+        def py_call():
+            deeppcr.deeppcr_mlp_forward(t["W"], t["bias"], t["z0"], Z, layer=wl.layer,
+                                        alpha=wl.alpha, tol=wl.tol, max_iter=wl.max_iter,
+                                        workspace=op_ws["fwd"])
+        info["c_call"] = c_call
+        info["py_call"] = py_call
     return step, info
+
+
+def call_latency_us(fn, n, reps=5):
+    """Minimum over reps of the mean host time of n back-to-back calls."""
+    for _ in range(min(n, 50)):
+        fn()
+    best = float("inf")
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        for _ in range(n):
+            fn()
+        best = min(best, (time.perf_counter() - t0) / n)
+    return best * 1e6
 
 
 def cpu_model():
@@ -384,6 +422,15 @@ def main():
         out["pass_ms_per_step"] = {
             "fwd": round(sum(a.elapsed_time(b) for a, b, _ in info["marks"]) / n, 4),
             "bwd": round(sum(b.elapsed_time(c) for _, b, c in info["marks"]) / n, 4)}
+    if "c_call" in info and ms_step < 1.0:
+        # latency-bound forward: per-call host time through the Python
+        # binding and through the C entry point directly, beside the
+        # solve's own device time (event-timed launches above)
+        n = max(10, int(200.0 / max(ms_step, 1e-3)))
+        out["call_latency_us"] = {
+            "python_binding": round(call_latency_us(info["py_call"], n), 2),
+            "c_entry": round(call_latency_us(info["c_call"](), n), 2),
+            "pcr_level_event": roof["avg_launch_us"]}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)

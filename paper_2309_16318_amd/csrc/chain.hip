@@ -93,17 +93,31 @@ __global__ __launch_bounds__(ChainShape<W>::NT) void pcr_chain_subst(BlockSrc Ai
 
     v4f blk[S::NB][S::NV];
     float rr[S::NB], zz[S::NB];
-    // element m >= 1 of the chain into ring slot m % NB (rows past the end
-    // of the chain re-read its last row; their results are never used);
-    // with UPD also the iterate's row, which the solution row is added to
-    auto request = [&](auto slot, int m) {
-        const int mm = m < count ? m : count;
-        const long long l = c + (long long)s * (mm > 0 ? mm : 1);
-        const float* a = ab + l * Ain.rstride + (long long)i * W + col0;
+    // Rows are requested in chain order, m = 1, 2, ...: the row bases (the
+    // same in every lane) advance by one chain step per request and stop at
+    // the chain's last row, which rows past the end re-read (their results
+    // are never used); the lane's offsets are added at the access.
+    const long long sa = (long long)s * Ain.rstride, sr = (long long)s * rin.rstride,
+                    so = (long long)s * rout.rstride;
+    const float* qa = ab + (long long)(c + s) * Ain.rstride;
+    const float* qr = rb + (long long)(c + s) * rin.rstride;
+    const float* qz = ob + (long long)(c + s) * rout.rstride;
+    int mq = 1;
+    const int offa = i * W + col0;
+    // element mq into ring slot mq % NB; with UPD also the iterate's row,
+    // which the solution row is added to
+    auto request = [&](auto slot) {
 #pragma unroll
-        for (int v = 0; v < S::NV; ++v) blk[slot][v] = *reinterpret_cast<const v4f*>(a + 4 * v);
-        rr[slot] = rb[l * rin.rstride + i];
-        if constexpr (UPD) zz[slot] = ob[l * rout.rstride + i];
+        for (int v = 0; v < S::NV; ++v)
+            blk[slot][v] = *reinterpret_cast<const v4f*>(qa + offa + 4 * v);
+        rr[slot] = qr[i];
+        if constexpr (UPD) zz[slot] = qz[i];
+        if (mq < count) {
+            qa += sa;
+            qr += sr;
+            qz += so;
+        }
+        ++mq;
     };
     // element 0: row c is final.  Maxima as bit patterns of non-negative
     // floats, which order like the floats (NaN above Inf).
@@ -125,11 +139,13 @@ __global__ __launch_bounds__(ChainShape<W>::NT) void pcr_chain_subst(BlockSrc Ai
     }
     auto prefetch = [&](auto slot) {
         if constexpr (decltype(slot)::value >= 1)
-            if (decltype(slot)::value <= S::D) request(slot, decltype(slot)::value);
+            if (decltype(slot)::value <= S::D) request(slot);
     };
     each_slot<0, S::NB>(prefetch);
     __syncthreads();
-    // elements 1 .. count, NB per round so that ring slots are compile-time
+    // elements 1 .. count, NB per round so that ring slots are compile-time;
+    // po: the row base of element m
+    float* po = ob + (long long)(c + s) * rout.rstride;
     for (int m0 = 0; m0 <= count; m0 += S::NB) {
         auto element = [&](auto jc) {
             constexpr int j = decltype(jc)::value;
@@ -137,7 +153,7 @@ __global__ __launch_bounds__(ChainShape<W>::NT) void pcr_chain_subst(BlockSrc Ai
             if (m < 1 || m > count) return;  // uniform over the workgroup
             // the block D rows ahead into the slot freed by row m - 1
             constexpr int ahead = (j + S::D) % S::NB;
-            request(std::integral_constant<int, ahead>{}, m + S::D);
+            request(std::integral_constant<int, ahead>{});
             const float* xp = xs[(m - 1) & 1] + col0;
             float acc = 0.f;
 #pragma unroll
@@ -148,7 +164,7 @@ __global__ __launch_bounds__(ChainShape<W>::NT) void pcr_chain_subst(BlockSrc Ai
             }
             const float x = rr[j] + row_sum<S::TPR>(acc);
             if (p == 0) {
-                float* o = ob + (long long)(c + (long long)s * m) * rout.rstride + i;
+                float* o = po + i;
                 if constexpr (UPD) {
                     const float z = zz[j] + x;
                     *o = z;
@@ -159,7 +175,13 @@ __global__ __launch_bounds__(ChainShape<W>::NT) void pcr_chain_subst(BlockSrc Ai
                 mx = max(mx, __float_as_uint(fabsf(x)));
                 xs[m & 1][i] = x;
             }
-            __syncthreads();
+            // one wave (w = 16): its LDS operations complete in issue order,
+            // so the next row's reads see this write without a barrier
+            if constexpr (S::NT > 64)
+                __syncthreads();
+            else
+                __builtin_amdgcn_wave_barrier();
+            po += so;
         };
         each_slot<0, S::NB>(element);
     }
