@@ -37,6 +37,9 @@ def parse():
     p.add_argument("--workload", default="resnet_fwd_bwd")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
+    # forward-only workloads: also time single calls on the host, through
+    # the Python binding and through the C entry point
+    p.add_argument("--call-latency", action="store_true")
     return p.parse_args()
 
 
@@ -422,7 +425,7 @@ def main():
         out["pass_ms_per_step"] = {
             "fwd": round(sum(a.elapsed_time(b) for a, b, _ in info["marks"]) / n, 4),
             "bwd": round(sum(b.elapsed_time(c) for _, b, c in info["marks"]) / n, 4)}
-    if "c_call" in info and ms_step < 1.0:
+    if args.call_latency and "c_call" in info:
         # latency-bound forward: per-call host time through the Python
         # binding and through the C entry point directly, beside the
         # solve's own device time (event-timed launches above)
