@@ -226,6 +226,180 @@ __global__ __launch_bounds__(kThreads) void newton_tiny_kernel(
         result[0] = status;
         result[1] = iters;
         result[2] = meas;
+        // then the completion word the host may watch instead of waiting for
+        // the stream: visible only after the record
+        __threadfence_system();
+        __hip_atomic_store(result + 3, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+}
+
+template <int CTRL>
+__device__ __forceinline__ unsigned dpp_u(unsigned v) {
+    return (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+// Max over the wave in every lane, from register-to-register exchanges:
+// DPP quad permutations and row mirrors within each 16-lane row, then the
+// row swaps of v_permlane16_swap and v_permlane32_swap (each returns, in
+// every lane, its own value and its partner row's).
+__device__ __forceinline__ unsigned wave_umax_dpp(unsigned v) {
+    v = max(v, dpp_u<0xB1>(v));   // quad_perm [1,0,3,2]
+    v = max(v, dpp_u<0x4E>(v));   // quad_perm [2,3,0,1]
+    v = max(v, dpp_u<0x141>(v));  // row_half_mirror
+    v = max(v, dpp_u<0x140>(v));  // row_mirror
+    const auto a = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    v = max(a[0], a[1]);
+    const auto c = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return max(c[0], c[1]);
+}
+
+// The same solve held in one wave's registers, for problems whose iterate has
+// at most 64 entries and w in {1, 2, 4, 8}: lane t owns entry t of Z
+// (system b, layer l, row i), the row i of W_l, A_l and r_l that goes with it,
+// and every value from another row (the previous layer's state, row l - s of
+// a PCR level) arrives by a lane shuffle; no LDS and no barriers.  Each PCR
+// level computes the new values from the old ones of all lanes before any
+// lane keeps them, as the two buffers of a level do in the workgroup form;
+// rows l < 2s keep their operator (never read again).  Same steps, stopping
+// rules and status record as newton_tiny_kernel.
+template <int W>
+__global__ __launch_bounds__(64) void newton_wave_kernel(
+    const float* __restrict__ Wg, const float* __restrict__ bg, const float* __restrict__ z0,
+    float* __restrict__ Zout, const float* __restrict__ Z_init, int B, int L, int layer,
+    float alpha, StopRule rule, unsigned* __restrict__ result) {
+    const int t = threadIdx.x;
+    const int n = B * L * W;
+    const bool on = t < n;
+    const int i = t % W, bl = t / W;
+    const int l = on ? bl % L : -1, b = bl / L;
+    const bool res = layer_residual(layer);
+    // lane of entry (b, l, 0): rows of the same system are W lanes apart
+    const int row0 = t - i;
+    float Wr[W], W0[W], zin[W];
+    float bias = 0.f, bias0 = 0.f, zini = 0.f;  // zini: z0[b][i]
+#pragma unroll
+    for (int j = 0; j < W; ++j) Wr[j] = W0[j] = zin[j] = 0.f;
+    if (on) {
+#pragma unroll
+        for (int j = 0; j < W; ++j) {
+            Wr[j] = Wg[((long long)l * W + i) * W + j];
+            W0[j] = Wg[i * W + j];
+            zin[j] = z0[b * W + j];
+        }
+        bias = bg[l * W + i];
+        bias0 = bg[i];
+        zini = z0[b * W + i];
+    }
+    // initial guess: Z_init, or f_0(z0) in every row (App. F.2)
+    float Z = 0.f;
+    if (on) {
+        if (Z_init) {
+            Z = Z_init[t];
+        } else {
+            float a = 0.f;
+#pragma unroll
+            for (int j = 0; j < W; ++j) a = fmaf(W0[j], zin[j], a);
+            float d;
+            const float y = activate(layer, a + bias0, &d);
+            Z = res ? fmaf(alpha, y, zini) : y;
+        }
+    }
+    unsigned status = 2u;
+    unsigned meas = 0u, iters = 0u;
+    float res0 = 0.f;
+    for (int k = 0; k <= rule.max_iter; ++k) {
+        if (!rule.residual && k == rule.max_iter) break;
+        // layer l at Z_{l-1} (z0 for l = 0): r and row i of J_l
+        float zp[W];
+#pragma unroll
+        for (int j = 0; j < W; ++j) {
+            const float zj = __shfl(Z, l >= 1 ? row0 - W + j : t, 64);
+            zp[j] = l >= 1 ? zj : zin[j];
+        }
+        float a = 0.f;
+#pragma unroll
+        for (int j = 0; j < W; ++j) a = fmaf(Wr[j], zp[j], a);
+        a += bias;
+        float d;
+        const float y = activate(layer, a, &d);
+        // the lane's own entry of the previous state
+        const float zpi = __shfl(Z, l >= 1 ? t - W : t, 64);
+        const float f = res ? fmaf(alpha, y, l >= 1 ? zpi : zini) : y;
+        float r = on ? f - Z : 0.f;
+        const float dsc = res ? alpha * d : d;
+        float A[W];
+#pragma unroll
+        for (int j = 0; j < W; ++j) {
+            float v = dsc * Wr[j];
+            if (res && i == j) v += 1.f;
+            A[j] = v;
+        }
+        if (rule.residual) {
+            const unsigned lr = wave_umax_dpp(__float_as_uint(fabsf(r)));
+            iters = (unsigned)k;
+            meas = lr;
+            if (lr >= 0x7f800000u) {
+                status = 3u;
+                break;
+            }
+            const float rv = __uint_as_float(lr);
+            if (k == 0) res0 = rv;
+            if (rv <= rule.atol || rv <= rule.rtol * res0) {
+                status = 0u;
+                break;
+            }
+            if (k == rule.max_iter) break;
+        }
+        // PCR levels (Alg. 1): every lane reads the old values of row l - s
+        // before it replaces its own
+        for (int st = 1; st < L; st *= 2) {
+            const bool has = l >= st;
+            const int src = has ? row0 - st * W : t;
+            float acc = 0.f;
+#pragma unroll
+            for (int j = 0; j < W; ++j) acc = fmaf(A[j], __shfl(r, src + (has ? j : 0), 64), acc);
+            float An[W];
+#pragma unroll
+            for (int j = 0; j < W; ++j) An[j] = 0.f;
+#pragma unroll
+            for (int q = 0; q < W; ++q)
+#pragma unroll
+                for (int j = 0; j < W; ++j)
+                    An[j] = fmaf(A[q], __shfl(A[j], src + (has ? q : 0), 64), An[j]);
+            if (has) r += acc;
+            if (l >= 2 * st) {
+#pragma unroll
+                for (int j = 0; j < W; ++j) A[j] = An[j];
+            }
+        }
+        // update and convergence measures
+        const float z = Z + r;
+        if (on) Z = z;
+        const unsigned lmx = wave_umax_dpp(on ? __float_as_uint(fabsf(r)) : 0u);
+        const unsigned lmz = wave_umax_dpp(on ? __float_as_uint(fabsf(z)) : 0u);
+        if (rule.residual) continue;
+        meas = lmx;
+        iters = (unsigned)(k + 1);
+        if (lmx >= 0x7f800000u || lmz >= 0x7f800000u) {
+            status = 3u;
+            break;
+        }
+        const float m = __uint_as_float(lmx), zmax = __uint_as_float(lmz);
+        if (rule.tol > 0.f && m < rule.tol * fmaxf(1.f, zmax)) {
+            status = 0u;
+            break;
+        }
+    }
+    if (!rule.residual && rule.tol == 0.f && status == 2u) status = 0u;
+    if (on) Zout[t] = Z;
+    if (t == 0) {
+        result[0] = status;
+        result[1] = iters;
+        result[2] = meas;
+        // then the completion word the host may watch instead of waiting for
+        // the stream: visible only after the record
+        __threadfence_system();
+        __hip_atomic_store(result + 3, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
 }
 
@@ -244,6 +418,19 @@ bool tiny_eligible(int B, int L, int w) {
 hipError_t launch_newton_tiny(const float* W, const float* bias, const float* z0, float* Z,
                               const float* Z_init, int B, int L, int w, int layer, float alpha,
                               const StopRule& rule, unsigned* result, hipStream_t stream) {
+    if ((long long)B * L * w <= 64 && (w == 1 || w == 2 || w == 4 || w == 8)) {
+#define DEEPPCR_WAVE(WT)                                                                    \
+    hipLaunchKernelGGL((newton_wave_kernel<WT>), dim3(1), dim3(64), 0, stream, W, bias, z0, Z, \
+                       Z_init, B, L, layer, alpha, rule, result)
+        switch (w) {
+            case 1: DEEPPCR_WAVE(1); break;
+            case 2: DEEPPCR_WAVE(2); break;
+            case 4: DEEPPCR_WAVE(4); break;
+            default: DEEPPCR_WAVE(8); break;
+        }
+#undef DEEPPCR_WAVE
+        return hipGetLastError();
+    }
     const size_t lds = tiny_lds_bytes(B, L, w);
 #define DEEPPCR_TINY(WT)                                                                     \
     hipLaunchKernelGGL((newton_tiny_kernel<WT>), dim3(1), dim3(kThreads), lds, stream, W, bias, \
