@@ -32,7 +32,12 @@
  *     NULL is the default stream).  pcr_solve_block_bidiag and
  *     deeppcr_mlp_backward return without waiting for the GPU;
  *     the two forward entry points wait once per Newton iteration to read their
- *     convergence measure.
+ *     convergence measure (a problem small enough for the one-launch solver
+ *     waits once: the kernel writes its status record and then a completion
+ *     word into the thread's mapped host buffer, and the call watches that
+ *     word, falling back to a stream wait after 5 ms; the launch may still be
+ *     retiring when the call returns, and later work on `stream` is ordered
+ *     after it).
  *   - Host out-parameters are plain host pointers.
  *   - Arguments are validated before any HIP call: an invalid argument returns
  *     DEEPPCR_EINVAL (or DEEPPCR_EWORKSPACE for a short workspace) and
