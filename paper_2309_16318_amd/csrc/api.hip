@@ -302,7 +302,7 @@ int tail_stride(int L, int kt) { return 1 << (num_levels(L) - kt); }
 // the weights instead of reading A0 (w = 32, 64, 128 and L > 2 only).
 hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int B, int L, int w,
                      float* wsA[2], float* wsr[2], int a_first, int r_first, hipStream_t st,
-                     const BwdArgs* bwd = nullptr) {
+                     const BwdArgs* bwd = nullptr, unsigned* upd_red = nullptr) {
     const int K = num_levels(L);
     if (K == 0) {
         const double bytes = 8.0 * B * L * w;
@@ -360,10 +360,10 @@ hipError_t pcr_sweep(const BlockSrc& A0, const VecSrc& r0, const VecDst& x, int 
     if (kt == 0) return hipSuccess;
     double bytes, flops;
     tail_work(B, L, w, kt, &bytes, &flops);
-    return timed(DEEPPCR_KCLASS_PCR_TAIL, bytes, flops, st,
-                 [&] {
-                     return launch_pcr_chain_subst(Ain, rin, x, B, L, w, tail_stride(L, kt), st);
-                 });
+    if (upd_red) bytes += 4.0 * B * L * w;  // the iterate is read as well
+    return timed(DEEPPCR_KCLASS_PCR_TAIL, bytes, flops, st, [&] {
+        return launch_pcr_chain_subst(Ain, rin, x, B, L, w, tail_stride(L, kt), st, upd_red);
+    });
 }
 
 struct Ws {
@@ -1103,19 +1103,31 @@ int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, f
     const double eval_bytes = 4.0 * ((double)L * w2 + (double)B * G * (w2 + 3.0 * w));
     const double eval_flops = (double)B * G * ((skip - 1) * 2.0 * w2 * w + skip * 2.0 * w2);
     int status = tol > 0.f ? DEEPPCR_ENOCONV : DEEPPCR_OK;
+    const bool upd_in_tail = tail_levels(B, G, w, 0) > 0;
     for (int k = 1; k <= max_iter; ++k) {
         hipError_t e = timed(DEEPPCR_KCLASS_LAYER, eval_bytes, eval_flops, st, [&] {
             return launch_resnet_block_eval(W, bias, z0, X, ws.A[1], ws.r[1], ws.red, B, G, w,
                                             skip, act, st);
         });
         if (e != hipSuccess) return hip_fail(e, "resnet_block_eval");
-        e = pcr_sweep(BlockSrc{ws.A[1], (long long)G * w * w, (long long)w * w, 0},
-                      VecSrc{ws.r[1], (long long)G * w, (long long)w}, xd, B, G, w, ws.A, ws.r,
-                      0, 0, st);
-        if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
-        e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
-                  [&] { return launch_update_reduce(X, xd.base, n, ws.red, st); });
-        if (e != hipSuccess) return hip_fail(e, "update_reduce");
+        if (upd_in_tail) {
+            // the substitution pass of the last levels adds the solution to
+            // the iterate and reduces the convergence maxima itself (the
+            // block evaluation cleared their slots)
+            e = pcr_sweep(BlockSrc{ws.A[1], (long long)G * w * w, (long long)w * w, 0},
+                          VecSrc{ws.r[1], (long long)G * w, (long long)w},
+                          VecDst{X, (long long)G * w, (long long)w}, B, G, w, ws.A, ws.r, 0, 0,
+                          st, nullptr, ws.red);
+            if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+        } else {
+            e = pcr_sweep(BlockSrc{ws.A[1], (long long)G * w * w, (long long)w * w, 0},
+                          VecSrc{ws.r[1], (long long)G * w, (long long)w}, xd, B, G, w, ws.A,
+                          ws.r, 0, 0, st);
+            if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+            e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
+                      [&] { return launch_update_reduce(X, xd.base, n, ws.red, st); });
+            if (e != hipSuccess) return hip_fail(e, "update_reduce");
+        }
         DEEPPCR_HIP(copy_async(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
                                    hipMemcpyDeviceToHost, st));
         DEEPPCR_HIP(host_wait(st));
