@@ -1443,6 +1443,16 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
         const int m1 = min(count, m0 + plan.n - 1);
         const int mw = max(0, m0 - 3);
         const bool res = layer_residual(na.layer);
+        // w = 128 (registers to spare): the residual layers' identity as a
+        // per-lane pattern held through the walk, one FMA per strip element
+        float dg[S::NQ][4];
+        if constexpr (W == 128) {
+            const int dk = res ? R0 - 4 * h0 : -1;
+#pragma unroll
+            for (int q = 0; q < S::NQ; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) dg[q][e] = dk == 8 * q + e ? 1.f : 0.f;
+        }
         const float* Zb = na.Z + (long long)b * L * W;
         float* ob = rout.base + b * rout.bstride;
         float* Ob = Aout + (long long)b * L * W * W;
@@ -1507,7 +1517,12 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
             const float f = layer_out<W>(na, strip_matvec<W>(aC, zp, h) + bm, zp[R], &dsc);
             const float rm = f - zv[m & 1][R];
             mr = max(mr, __float_as_uint(fabsf(rm)));
-            if (res) {
+            if (W == 128 && res) {
+#pragma unroll
+                for (int q = 0; q < S::NQ; ++q)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) aC[q][e] = fmaf(dsc, aC[q][e], dg[q][e]);
+            } else if (res) {
                 // the diagonal is column k = R, at 8q + e = R - 4h (the empty
                 // asm keeps the compiler from holding 64 precomputed selects)
                 int dk = R - 4 * h;
