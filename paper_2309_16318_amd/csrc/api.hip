@@ -934,15 +934,23 @@ int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, 
     e = timed(DEEPPCR_KCLASS_LAYER, 12.0 * n, (double)n, st,
               [&] { return launch_residual(F, Z, ws.r[1], n, ws.red, st); });
     if (e != hipSuccess) return hip_fail(e, "residual");
-    // Eq. 3 with the caller's blocks (J[:, 0] unused) by PCR, then Z += dZ
-    const VecDst xd{ws.r[(num_passes(B, L, w) + 1) & 1], (long long)L * w, (long long)w};
-    e = pcr_sweep(BlockSrc{J, (long long)L * w * w, (long long)w * w, 0},
-                  VecSrc{ws.r[1], (long long)L * w, (long long)w}, xd, B, L, w, ws.A, ws.r, 0, 0,
-                  st);
-    if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
-    e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
-              [&] { return launch_update_reduce(Z, xd.base, n, ws.red, st); });
-    if (e != hipSuccess) return hip_fail(e, "update_reduce");
+    // Eq. 3 with the caller's blocks (J[:, 0] unused) by PCR, then Z += dZ:
+    // applied by the substitution pass of the last levels where the sweep
+    // ends in one, else by the update kernel
+    const BlockSrc J0{J, (long long)L * w * w, (long long)w * w, 0};
+    const VecSrc r0{ws.r[1], (long long)L * w, (long long)w};
+    if (tail_levels(B, L, w, 0) > 0) {
+        e = pcr_sweep(J0, r0, VecDst{Z, (long long)L * w, (long long)w}, B, L, w, ws.A, ws.r, 0,
+                      0, st, nullptr, ws.red);
+        if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+    } else {
+        const VecDst xd{ws.r[(num_passes(B, L, w) + 1) & 1], (long long)L * w, (long long)w};
+        e = pcr_sweep(J0, r0, xd, B, L, w, ws.A, ws.r, 0, 0, st);
+        if (e != hipSuccess) return hip_fail(e, "pcr_sweep");
+        e = timed(DEEPPCR_KCLASS_UPDATE, 12.0 * n, 2.0 * n, st,
+                  [&] { return launch_update_reduce(Z, xd.base, n, ws.red, st); });
+        if (e != hipSuccess) return hip_fail(e, "update_reduce");
+    }
     DEEPPCR_HIP(copy_async(hw, ws.red, kRedWords * sizeof(unsigned), hipMemcpyDeviceToHost,
                                st));
     DEEPPCR_HIP(host_wait(st));
