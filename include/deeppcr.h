@@ -134,7 +134,11 @@ int pcr_solve_block_bidiag(const float* J, const float* r, float* x,
  *   1. Chunk-local PCR (Alg. 1 inside every chunk, all chunks at once) that
  *      keeps each chunk's coupling to the one unknown outside it, x_in (row
  *      a-1 of chunk [a, e) for transpose = 0, row e for transpose = 1), so
- *      that every row ends as x_l = P_l x_in + q_l.
+ *      that every row ends as x_l = P_l x_in + q_l.  For w <= 16 and
+ *      w = 32, 64, 128 the chunk's last levels (all but the first
+ *      max(1, ceil(log2 Lc) - 6)) are replaced by substitution along the
+ *      chains of at most 64 rows they act on: P_j = A_j P_{j-s},
+ *      q_j = A_j q_{j-s} + r_j, the way the full solve ends.
  *   2. A pass over the chunk ends in solve order: the carry-in of the next
  *      chunk is P x_in + q at the current chunk's last row (the first
  *      chunk's carry-in is zero).

@@ -813,10 +813,17 @@ int pcr_solve_block_bidiag_chunked(const float* J, const float* r, float* x, int
         xd = VecDst{x + (long long)(L - 1) * w, (long long)L * w, -(long long)w};
     }
     const int Lc = (L + G - 1) / G;
-    // levels s = 1, 2, ... while s < Lc; a chunk of one row still takes one
-    // (copying) level, which moves its block into the operator buffer
+    // levels s = 1, 2, ... while s < Lc (a chunk of one row still takes one,
+    // copying, level, which moves its block into the operator buffer); where
+    // the width allows, only the first Kc - 6 of the Kc levels (at least one),
+    // and the chains of at most 64 rows they leave by substitution
+    int Kc = 0;
+    for (long long t = 1; t < Lc; t *= 2) ++Kc;
+    const int k0 = Kc - 6 > 1 ? Kc - 6 : 1;
+    const bool chains = chunk_chain_width(w) && k0 < Kc;
+    const int klev = chains ? k0 : (Kc > 1 ? Kc : 1);
     int k = 0;
-    for (int s = 1; k == 0 || s < Lc; s *= 2, ++k) {
+    for (int s = 1; k < klev; s *= 2, ++k) {
         double bytes, flops;
         chunk_level_work(B, L, w, Lc, rev, s, &bytes, &flops);
         float* Aout = wsA[k & 1];
@@ -830,6 +837,16 @@ int pcr_solve_block_bidiag_chunked(const float* J, const float* r, float* x, int
     }
     const float* P = wsA[(k - 1) & 1];
     const float* q = wsr[(k - 1) & 1];
+    if (chains) {
+        double bytes, flops;
+        chunk_chain_work(B, L, w, Lc, rev, 1 << k, &bytes, &flops);
+        hipError_t e = timed(DEEPPCR_KCLASS_PCR_TAIL, bytes, flops, st, [&] {
+            return launch_chunk_chain(P, q, wsA[k & 1], wsr[k & 1], B, L, w, Lc, rev, 1 << k, st);
+        });
+        if (e != hipSuccess) return hip_fail(e, "pcr_solve_block_bidiag_chunked");
+        P = wsA[k & 1];
+        q = wsr[k & 1];
+    }
     const int nch = chunk_count(L, Lc);
     hipError_t e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * B * nch * (w2 + 2.0 * w),
                          2.0 * B * nch * w2, st,

@@ -19,13 +19,12 @@
 // solution row is added to it and max |x|, max |Z + x| are reduced into the
 // kRedDZ, kRedZ slots of red.
 #include "internal.h"
+#include "strip.h"
 
 #include <type_traits>
 
 namespace deeppcr {
 namespace {
-
-typedef float v4f __attribute__((ext_vector_type(4)));
 
 // Measured (bench.py, one MI355X, same box): at w = 128, 1024 threads and
 // one row ahead 206 us per pass against 217 with 512 threads and 246 with
@@ -46,25 +45,6 @@ struct ChainShape {
     static constexpr int NB = D + 1;  // ring slots
     static_assert(CPT % 4 == 0 && TPR >= 2 && TPR <= 16 && (TPR & (TPR - 1)) == 0, "row split");
 };
-
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over the TPR consecutive lanes of a block row (TPR = 2 .. 16, inside
-// one 16-lane DPP row), in every lane of the row: butterfly steps whose
-// partner lanes come from DPP permutations (quad_perm [1,0,3,2] and
-// [2,3,0,1], then the half-row and row mirrors, which pair each lane with one
-// of the other group of 4 or 8 lanes), VALU operations with no LDS round trip.
-template <int TPR>
-__device__ __forceinline__ float row_sum(float v) {
-    v += dpp<0xB1>(v);
-    if constexpr (TPR >= 4) v += dpp<0x4E>(v);
-    if constexpr (TPR >= 8) v += dpp<0x141>(v);
-    if constexpr (TPR >= 16) v += dpp<0x140>(v);
-    return v;
-}
 
 template <int I, int N, class F>
 __device__ __forceinline__ void each_slot(F& f) {

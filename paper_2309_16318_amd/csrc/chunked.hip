@@ -152,11 +152,15 @@ __global__ __launch_bounds__(kThreads) void chunk_level_generic(BlockSrc Ain, Ve
 constexpr int kSmallW = 16;
 constexpr int kSmallRows = kThreads / 64;
 
+// WT > 0: the width as a compile-time constant (index arithmetic in shifts,
+// inner loops unrolled); WT = 0 reads it at run time.
+template <int WT>
 __global__ __launch_bounds__(kThreads) void chunk_level_small(BlockSrc Ain, VecSrc rin,
                                                               float* __restrict__ Aout,
                                                               float* __restrict__ rout, int B,
-                                                              int L, int Lc, int rev, int w,
+                                                              int L, int Lc, int rev, int w_rt,
                                                               int s) {
+    const int w = WT > 0 ? WT : w_rt;
     __shared__ float Am_all[kSmallRows][kSmallW][kSmallW + 1];
     __shared__ float Ap_all[kSmallRows][kSmallW][kSmallW + 1];
     __shared__ float rp_all[kSmallRows][kSmallW];
@@ -177,8 +181,8 @@ __global__ __launch_bounds__(kThreads) void chunk_level_small(BlockSrc Ain, VecS
         if (lane < w) xo[lane] = rl[lane];
         if (coupled)
             for (int idx = lane; idx < n2; idx += 64) {
-                const int i = idx / w, k = idx - (idx / w) * w;
-                Ao[idx] = block_elem(Al, i, k, w, Ain.trans);
+                const int u = idx / w, v = idx - (idx / w) * w;
+                Ao[Ain.trans ? v * w + u : idx] = Al[idx];
             }
         return;
     }
@@ -187,10 +191,13 @@ __global__ __launch_bounds__(kThreads) void chunk_level_small(BlockSrc Ain, VecS
     float* rp = rp_all[wave];
     const bool prod = coupled || j >= 2 * s;
     const float* Pl = Ain.base + b * Ain.bstride + (long long)(m - s) * Ain.rstride;
+    // the blocks read in memory order (contiguous across the wave), each
+    // entry placed at its (row, column) of the stored or transposed block
     for (int idx = lane; idx < n2; idx += 64) {
-        const int i = idx / w, k = idx - (idx / w) * w;
-        Am[i][k] = block_elem(Al, i, k, w, Ain.trans);
-        if (prod) Ap[i][k] = block_elem(Pl, i, k, w, Ain.trans);
+        const int u = idx / w, v = idx - (idx / w) * w;
+        const int i = Ain.trans ? v : u, k = Ain.trans ? u : v;
+        Am[i][k] = Al[idx];
+        if (prod) Ap[i][k] = Pl[idx];
     }
     if (lane < w) rp[lane] = rin.base[b * rin.bstride + (long long)(m - s) * rin.rstride + lane];
     wave_sync();
@@ -263,9 +270,222 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void chunk_level_strip(BlockSrc 
     if (h == 0) xo[R] = rl[R] + part;
 }
 
+// ---- the chains of the last chunk-local levels, by substitution ---------
+// After the chunk-local levels with strides below s, every row j >= s of a
+// chunk satisfies x_j = A_j x_{j-s} + r_j, and rows j < s are final: maps
+// x_j = P_j x_in + q_j of the chunk's carry-in in a coupled chunk, plain
+// values in the chunk holding internal row 0.  Each chunk is then s
+// independent chains (rows c, c + s, ... of the chunk, c < s), and walking a
+// chain in order gives every row's map: P_j = A_j P_{j-s},
+// q_j = A_j q_{j-s} + r_j (q only in the first chunk, whose carry-in is
+// zero and whose P is never read).  The walk replaces the chunk's remaining
+// levels the way the full solve's substitution pass replaces its last ones.
+// (b, k, c) of a chain from its index, chunk k's first internal row ms, its
+// length n; false for an empty chain (c beyond a short chunk).
+struct ChainPos {
+    int b, k, c, ms, n;
+};
+
+__device__ inline bool chain_of(long long chain, int L, int Lc, int rev, int s, ChainPos* p) {
+    const int nch = num_chunks(L, Lc);
+    p->c = (int)(chain % s);
+    const long long bk = chain / s;
+    p->k = (int)(bk % nch);
+    p->b = (int)(bk / nch);
+    p->ms = chunk_start(p->k, L, Lc, rev);
+    p->n = (p->k + 1 < nch ? chunk_start(p->k + 1, L, Lc, rev) : L) - p->ms;
+    return p->c < p->n;
+}
+
+// w <= 16: one wave per chain; the chain's previous map and the current
+// block in the wave's LDS, the next block and right-hand side requested
+// into registers while the current row is formed.
+constexpr int kSmallPer = kSmallW * kSmallW / 64;  // block entries per lane
+constexpr int kSmallAhead = 4;                       // rows requested ahead
+
+template <int WT>
+__global__ __launch_bounds__(kThreads) void chunk_chain_small(const float* __restrict__ Ain,
+                                                              const float* __restrict__ rin,
+                                                              float* __restrict__ Pout,
+                                                              float* __restrict__ qout, int B,
+                                                              int L, int Lc, int rev, int w_rt,
+                                                              int s) {
+    const int w = WT > 0 ? WT : w_rt;
+    __shared__ float As_all[kSmallRows][kSmallW][kSmallW + 1];
+    __shared__ float Pp_all[kSmallRows][kSmallW][kSmallW + 1];
+    __shared__ float qp_all[kSmallRows][kSmallW];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const long long chain = (long long)blockIdx.x * kSmallRows + wave;
+    if (chain >= (long long)B * num_chunks(L, Lc) * s) return;  // uniform over the wave
+    ChainPos cp;
+    if (!chain_of(chain, L, Lc, rev, s, &cp)) return;
+    const bool coupled = cp.k >= 1;
+    const int n2 = w * w;
+    const int count = (cp.n - 1 - cp.c) / s;
+    float (*As)[kSmallW + 1] = As_all[wave];
+    float (*Pp)[kSmallW + 1] = Pp_all[wave];
+    float* qp = qp_all[wave];
+    long long row = (long long)cp.b * L + cp.ms + cp.c;
+    // element 0: final; its map is the chain's first
+    if (lane < w) {
+        const float v = rin[row * w + lane];
+        qout[row * w + lane] = v;
+        qp[lane] = v;
+    }
+    if (coupled)
+        for (int idx = lane; idx < n2; idx += 64) {
+            const float v = Ain[row * n2 + idx];
+            Pout[row * n2 + idx] = v;
+            Pp[idx / w][idx - (idx / w) * w] = v;
+        }
+    // a ring of kSmallAhead rows in flight: element t uses slot (t - 1) % D
+    constexpr int D = kSmallAhead;
+    float an[D][kSmallPer], rn[D];
+    auto request = [&](int slot, long long rw) {
+#pragma unroll
+        for (int p = 0; p < kSmallPer; ++p) {
+            const int idx = lane + 64 * p;
+            an[slot][p] = idx < n2 ? Ain[rw * n2 + idx] : 0.f;
+        }
+        rn[slot] = lane < w ? rin[rw * w + lane] : 0.f;
+    };
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+        if (1 + j <= count) request(j, row + (long long)(1 + j) * s);
+    for (int t0 = 1; t0 <= count; t0 += D) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+        const int t = t0 + j;
+        if (t > count) break;  // uniform over the wave
+        row += s;
+#pragma unroll
+        for (int p = 0; p < kSmallPer; ++p) {
+            const int idx = lane + 64 * p;
+            if (idx < n2) As[idx / w][idx - (idx / w) * w] = an[j][p];
+        }
+        const float rc = rn[j];
+        if (t + D <= count) request(j, row + (long long)D * s);
+        wave_sync();
+        float qn = 0.f;
+        if (lane < w) {
+            qn = rc;
+            for (int kk = 0; kk < w; ++kk) qn = fmaf(As[lane][kk], qp[kk], qn);
+        }
+        float pn[kSmallPer];
+        if (coupled) {
+#pragma unroll
+            for (int p = 0; p < kSmallPer; ++p) {
+                const int idx = lane + 64 * p;
+                float acc = 0.f;
+                if (idx < n2) {
+                    const int i = idx / w, jj = idx - (idx / w) * w;
+                    for (int kk = 0; kk < w; ++kk) acc = fmaf(As[i][kk], Pp[kk][jj], acc);
+                }
+                pn[p] = acc;
+            }
+        }
+        wave_sync();  // every lane has read As, Pp and qp
+        if (lane < w) {
+            qp[lane] = qn;
+            qout[row * w + lane] = qn;
+        }
+        if (coupled) {
+#pragma unroll
+            for (int p = 0; p < kSmallPer; ++p) {
+                const int idx = lane + 64 * p;
+                if (idx < n2) {
+                    Pp[idx / w][idx - (idx / w) * w] = pn[p];
+                    Pout[row * n2 + idx] = pn[p];
+                }
+            }
+        }
+        wave_sync();
+    }
+    }
+}
+
+// w = 32, 64, 128: one workgroup per chain, one wave per 32-row strip.  The
+// row's block is the left MFMA operand in registers (the next one requested
+// before the current product), the chain's previous map goes through LDS
+// transposed, and q_{j-s} rides on the product's operand reads.
+template <int W>
+__global__ __launch_bounds__(Tile2Shape<W>::NT) void chunk_chain_strip(
+    const float* __restrict__ Ain, const float* __restrict__ rin, float* __restrict__ Pout,
+    float* __restrict__ qout, int L, int Lc, int rev, int s) {
+    using S = Tile2Shape<W>;
+    __shared__ float XT[W * S::PITCH];  // P of the chain's previous row, transposed
+    __shared__ float qp[W];
+    const int t = threadIdx.x;
+    const int lane = t & 63, i = lane & 31, h = lane >> 5;
+    const int R = 32 * (t >> 6) + i;
+    ChainPos cp;
+    if (!chain_of(blockIdx.x, L, Lc, rev, s, &cp)) return;  // uniform over the workgroup
+    const bool coupled = cp.k >= 1;
+    const long long w2 = (long long)W * W;
+    const int count = (cp.n - 1 - cp.c) / s;
+    long long row = (long long)cp.b * L + cp.ms + cp.c;
+    // a ring of D rows in flight: element tt uses slot (tt - 1) % D
+    constexpr int D = W == 128 ? 1 : W == 64 ? 2 : 4;
+    StripA<W> a, an[D];
+    float rn[D];
+    if (t < W) {
+        const float v = rin[row * W + t];
+        qout[row * W + t] = v;
+        qp[t] = v;
+    }
+    if (coupled) {
+        strip_load<W, false>(Ain + row * w2, a, R, h);
+        strip_store<W>(Pout + row * w2, a, R, h);
+        strip_put_T<W>(XT, a, R, h);
+    }
+    auto request = [&](int slot, long long rw) {
+        strip_load<W, false>(Ain + rw * w2, an[slot], R, h);
+        rn[slot] = rin[rw * W + R];
+    };
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+        if (1 + j <= count) request(j, row + (long long)(1 + j) * s);
+    __syncthreads();
+    for (int t0 = 1; t0 <= count; t0 += D) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+        const int tt = t0 + j;
+        if (tt > count) break;  // uniform over the workgroup
+        row += s;
+#pragma unroll
+        for (int q = 0; q < S::NQ; ++q) a[q] = an[j][q];
+        const float rc = rn[j];
+        if (tt + D <= count) request(j, row + (long long)D * s);
+        StripC<W> acc;
+        float part;
+        if (coupled)
+            part = strip_product<W, 0, S::T, true>(XT, a, acc, i, h, qp);
+        else
+            part = strip_matvec<W>(a, qp, h);
+        const float qn = rc + part;
+        __syncthreads();  // XT and qp are read
+        if (h == 0) {
+            qp[R] = qn;
+            qout[row * W + R] = qn;
+        }
+        if (coupled) {
+            tiles_store<W, 0, S::T>(Pout + row * w2, acc, R, h);
+            strip_put_T<W>(XT, acc, R, h);
+        }
+        __syncthreads();
+    }
+    }
+}
+
 // Carry pass, one workgroup per system: in internal chunk order,
 // xin[b, k] = carry; carry <- P_e carry + q_e at the chunk's last row e
-// (P_e of the first chunk is not read: its carry-in is zero).
+// (P_e of the first chunk is not read: its carry-in is zero).  At w <= 16
+// the next chunk's P_e and q_e (one entry per thread) are requested into
+// registers before the current chunk's product and staged in LDS after it.
+__device__ inline int chunk_end(int k, int nch, int L, int Lc, int rev) {
+    return (k + 1 < nch ? chunk_start(k + 1, L, Lc, rev) : L) - 1;
+}
+
 __global__ __launch_bounds__(kThreads) void chunk_carry_kernel(const float* __restrict__ P,
                                                                const float* __restrict__ q,
                                                                float* __restrict__ xin, int L,
@@ -275,12 +495,38 @@ __global__ __launch_bounds__(kThreads) void chunk_carry_kernel(const float* __re
     const int nch = num_chunks(L, Lc);
     __shared__ float c[kMaxWidth], cn[kMaxWidth];
     for (int i = t; i < w; i += kThreads) c[i] = 0.f;
+    if (w <= kSmallW) {
+        __shared__ float Ps[kSmallW * kSmallW], qs[kSmallW];
+        const int n2 = w * w;
+        float pv = 0.f, qv = 0.f;
+        auto request = [&](int k) {
+            const long long e = (long long)b * L + chunk_end(k, nch, L, Lc, rev);
+            pv = (k >= 1 && t < n2) ? P[e * n2 + t] : 0.f;
+            qv = t < w ? q[e * w + t] : 0.f;
+        };
+        request(0);
+        for (int k = 0; k < nch; ++k) {
+            if (t < n2) Ps[t] = pv;
+            if (t < w) qs[t] = qv;
+            if (k + 1 < nch) request(k + 1);
+            __syncthreads();
+            if (t < w) {
+                xin[((long long)b * nch + k) * w + t] = c[t];
+                float acc = qs[t];
+                for (int j = 0; j < w; ++j) acc = fmaf(Ps[t * w + j], c[j], acc);
+                cn[t] = acc;
+            }
+            __syncthreads();
+            if (t < w) c[t] = cn[t];
+        }
+        return;
+    }
     __syncthreads();
     for (int k = 0; k < nch; ++k) {
         for (int i = t; i < w; i += kThreads) xin[((long long)b * nch + k) * w + i] = c[i];
-        const int e = (k + 1 < nch ? chunk_start(k + 1, L, Lc, rev) : L) - 1;
-        const float* Pe = P + ((long long)b * L + e) * w * w;
-        const float* qe = q + ((long long)b * L + e) * w;
+        const long long e = (long long)b * L + chunk_end(k, nch, L, Lc, rev);
+        const float* Pe = P + e * w * w;
+        const float* qe = q + e * w;
         for (int ii = wave; ii < w; ii += kThreads / 64) {
             float acc = 0.f;
             if (k >= 1)
@@ -292,6 +538,97 @@ __global__ __launch_bounds__(kThreads) void chunk_carry_kernel(const float* __re
         for (int i = t; i < w; i += kThreads) c[i] = cn[i];
         __syncthreads();
     }
+}
+
+// Carry and apply at w = 32, 64, 128: thread t takes row t / TPR of a block
+// and TPR-th of its columns (float4 reads along the row), partial dot
+// products summed over the row's TPR lanes by DPP.
+template <int W>
+struct RowSplit {
+    static constexpr int TPR = kThreads / W;  // threads per block row
+    static constexpr int CPT = W / TPR;       // columns per thread
+    static constexpr int NV = CPT / 4;        // float4 per thread
+};
+
+template <int W>
+__device__ __forceinline__ float row_dot(const float* prow, const float* v) {
+    float acc = 0.f;
+#pragma unroll
+    for (int u = 0; u < RowSplit<W>::NV; ++u) {
+        const v4f a = *reinterpret_cast<const v4f*>(prow + 4 * u);
+        const v4f c = *reinterpret_cast<const v4f*>(v + 4 * u);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc = fmaf(a[e], c[e], acc);
+    }
+    return acc;
+}
+
+// The carry at w = 32, 64, 128, one workgroup per system; the next
+// chunk's P_e entries of a thread are requested before the current product.
+template <int W>
+__global__ __launch_bounds__(kThreads) void chunk_carry_rows(const float* __restrict__ P,
+                                                             const float* __restrict__ q,
+                                                             float* __restrict__ xin, int L,
+                                                             int Lc, int rev) {
+    using S = RowSplit<W>;
+    const int b = blockIdx.x;
+    const int t = threadIdx.x, i = t / S::TPR, p = t % S::TPR;
+    const int nch = num_chunks(L, Lc);
+    __shared__ float c[2][W];
+    if (t < W) c[0][t] = 0.f;
+    v4f pe[S::NV];
+    float qe = 0.f;
+    auto request = [&](int k) {
+        const long long e = (long long)b * L + chunk_end(k, nch, L, Lc, rev);
+        const float* pr = P + (e * W + i) * W + p * S::CPT;
+#pragma unroll
+        for (int u = 0; u < S::NV; ++u)
+            pe[u] = k >= 1 ? *reinterpret_cast<const v4f*>(pr + 4 * u) : v4f{0.f, 0.f, 0.f, 0.f};
+        qe = q[e * W + i];
+    };
+    request(0);
+    __syncthreads();
+    for (int k = 0; k < nch; ++k) {
+        const float* cc = c[k & 1];
+        if (t < W) xin[((long long)b * nch + k) * W + t] = cc[t];
+        v4f pc[S::NV];
+#pragma unroll
+        for (int u = 0; u < S::NV; ++u) pc[u] = pe[u];
+        const float qc = qe;
+        if (k + 1 < nch) request(k + 1);
+        float acc = 0.f;
+#pragma unroll
+        for (int u = 0; u < S::NV; ++u) {
+            const v4f cv = *reinterpret_cast<const v4f*>(cc + p * S::CPT + 4 * u);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc = fmaf(pc[u][e], cv[e], acc);
+        }
+        acc = row_sum<S::TPR>(acc);
+        if (p == 0) c[(k + 1) & 1][i] = qc + acc;
+        __syncthreads();
+    }
+}
+
+// The apply at w = 32, 64, 128: one workgroup per row of the system.
+template <int W>
+__global__ __launch_bounds__(kThreads) void chunk_apply_rows(const float* __restrict__ P,
+                                                             const float* __restrict__ q,
+                                                             const float* __restrict__ xin,
+                                                             VecDst x, int L, int Lc, int rev) {
+    using S = RowSplit<W>;
+    const long long row = blockIdx.x;
+    const int m = (int)(row % L);
+    const int b = (int)(row / L);
+    const int t = threadIdx.x, i = t / S::TPR, p = t % S::TPR;
+    const ChunkPos cp = chunk_of(m, L, Lc, rev);
+    float* xo = x.base + b * x.bstride + (long long)m * x.rstride;
+    if (cp.k == 0) {  // uniform over the workgroup
+        if (t < W) xo[t] = q[row * W + t];
+        return;
+    }
+    const float* c = xin + ((long long)b * num_chunks(L, Lc) + cp.k) * W + p * S::CPT;
+    const float acc = row_sum<S::TPR>(row_dot<W>(P + (row * W + i) * W + p * S::CPT, c));
+    if (p == 0) xo[i] = q[row * W + i] + acc;
 }
 
 // x at internal row m: q_m + P_m xin[chunk of m] (just q_m in the first
@@ -325,25 +662,29 @@ __global__ __launch_bounds__(kThreads) void chunk_apply_kernel(const float* __re
     }
 }
 
-// The apply at w <= 16: one wave per row, lane i forms output i.
+// The apply at w <= 16: sixteen lanes per row (four rows per wave), lane i
+// forms output i from row i of P_m.
+template <int WT>
 __global__ __launch_bounds__(kThreads) void chunk_apply_small(const float* __restrict__ P,
                                                               const float* __restrict__ q,
                                                               const float* __restrict__ xin,
                                                               VecDst x, int B, int L, int Lc,
-                                                              int rev, int w) {
+                                                              int rev, int w_rt) {
+    const int w = WT > 0 ? WT : w_rt;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const long long row = (long long)blockIdx.x * kSmallRows + wave;
-    if (row >= (long long)B * L || lane >= w) return;
+    const long long row = ((long long)blockIdx.x * kSmallRows + wave) * 4 + lane / 16;
+    const int i = lane & 15;
+    if (row >= (long long)B * L || i >= w) return;
     const int m = (int)(row % L);
     const int b = (int)(row / L);
     const ChunkPos cp = chunk_of(m, L, Lc, rev);
-    float acc = q[row * w + lane];
+    float acc = q[row * w + i];
     if (cp.k >= 1) {
         const float* c = xin + ((long long)b * num_chunks(L, Lc) + cp.k) * w;
-        const float* Pm = P + row * w * w + (long long)lane * w;
+        const float* Pm = P + row * w * w + (long long)i * w;
         for (int k = 0; k < w; ++k) acc = fmaf(Pm[k], c[k], acc);
     }
-    x.base[b * x.bstride + (long long)m * x.rstride + lane] = acc;
+    x.base[b * x.bstride + (long long)m * x.rstride + i] = acc;
 }
 
 }  // namespace
@@ -386,16 +727,84 @@ hipError_t launch_chunk_level(const BlockSrc& Ain, const VecSrc& rin, float* Aou
 #undef DEEPPCR_CHUNK_STRIP
     if (w <= kSmallW) {
         const long long nwg = ((long long)B * L + kSmallRows - 1) / kSmallRows;
-        chunk_level_small<<<dim3((unsigned)nwg), kThreads, 0, stream>>>(Ain, rin, Aout, rout, B,
-                                                                       L, Lc, rev, w, s);
+#define DEEPPCR_LEVEL_SMALL(WT)                                                           \
+    chunk_level_small<WT><<<dim3((unsigned)nwg), kThreads, 0, stream>>>(Ain, rin, Aout, rout, \
+                                                                       B, L, Lc, rev, w, s)
+        switch (w) {
+            case 4: DEEPPCR_LEVEL_SMALL(4); break;
+            case 8: DEEPPCR_LEVEL_SMALL(8); break;
+            case 16: DEEPPCR_LEVEL_SMALL(16); break;
+            default: DEEPPCR_LEVEL_SMALL(0); break;
+        }
+#undef DEEPPCR_LEVEL_SMALL
         return hipGetLastError();
     }
     chunk_level_generic<<<grid, kThreads, 0, stream>>>(Ain, rin, Aout, rout, L, Lc, rev, w, s);
     return hipGetLastError();
 }
 
+bool chunk_chain_width(int w) { return w <= kSmallW || w == 32 || w == 64 || w == 128; }
+
+void chunk_chain_work(int B, int L, int w, int Lc, int rev, int s, double* bytes,
+                      double* flops) {
+    // every row's block and right-hand side read, its map written; the rows
+    // past the chains' first (rows j >= s) form one product and one mat-vec
+    double rows_c = 0, rows_u = 0, fin_c = 0;
+    const int nch = num_chunks(L, Lc);
+    for (int k = 0; k < nch; ++k) {
+        const int n = (k + 1 < nch ? chunk_start(k + 1, L, Lc, rev) : L) - chunk_start(k, L, Lc, rev);
+        const int past = n > s ? n - s : 0;
+        if (k >= 1) {
+            rows_c += past;
+            fin_c += n - past;
+        } else {
+            rows_u += past;
+        }
+    }
+    const double w2 = (double)w * w;
+    *bytes = 4.0 * B * (2.0 * (rows_c + fin_c) * w2 + rows_u * w2 + 2.0 * L * w);
+    *flops = (double)B * (rows_c * (2.0 * w2 * w + 2.0 * w2) + rows_u * 2.0 * w2);
+}
+
+hipError_t launch_chunk_chain(const float* Ain, const float* rin, float* Pout, float* qout,
+                              int B, int L, int w, int Lc, int rev, int s, hipStream_t stream) {
+    const long long chains = (long long)B * num_chunks(L, Lc) * s;
+#define DEEPPCR_CHUNK_CHAIN(WW)                                                              \
+    if (w == WW) {                                                                           \
+        chunk_chain_strip<WW><<<dim3((unsigned)chains), Tile2Shape<WW>::NT, 0, stream>>>(    \
+            Ain, rin, Pout, qout, L, Lc, rev, s);                                            \
+        return hipGetLastError();                                                            \
+    }
+    DEEPPCR_CHUNK_CHAIN(32)
+    DEEPPCR_CHUNK_CHAIN(64)
+    DEEPPCR_CHUNK_CHAIN(128)
+#undef DEEPPCR_CHUNK_CHAIN
+    if (w > kSmallW) return hipErrorInvalidValue;
+    const long long nwg = (chains + kSmallRows - 1) / kSmallRows;
+#define DEEPPCR_CHAIN_SMALL(WT)                                                             \
+    chunk_chain_small<WT><<<dim3((unsigned)nwg), kThreads, 0, stream>>>(Ain, rin, Pout, qout, B, \
+                                                                       L, Lc, rev, w, s)
+    switch (w) {
+        case 4: DEEPPCR_CHAIN_SMALL(4); break;
+        case 8: DEEPPCR_CHAIN_SMALL(8); break;
+        case 16: DEEPPCR_CHAIN_SMALL(16); break;
+        default: DEEPPCR_CHAIN_SMALL(0); break;
+    }
+#undef DEEPPCR_CHAIN_SMALL
+    return hipGetLastError();
+}
+
 hipError_t launch_chunk_carry(const float* P, const float* q, float* xin, int B, int L, int w,
                               int Lc, int rev, hipStream_t stream) {
+#define DEEPPCR_CARRY_ROWS(WW)                                                                 \
+    if (w == WW) {                                                                             \
+        chunk_carry_rows<WW><<<B, kThreads, 0, stream>>>(P, q, xin, L, Lc, rev);               \
+        return hipGetLastError();                                                              \
+    }
+    DEEPPCR_CARRY_ROWS(32)
+    DEEPPCR_CARRY_ROWS(64)
+    DEEPPCR_CARRY_ROWS(128)
+#undef DEEPPCR_CARRY_ROWS
     chunk_carry_kernel<<<B, kThreads, 0, stream>>>(P, q, xin, L, Lc, rev, w);
     return hipGetLastError();
 }
@@ -403,12 +812,26 @@ hipError_t launch_chunk_carry(const float* P, const float* q, float* xin, int B,
 hipError_t launch_chunk_apply(const float* P, const float* q, const float* xin, const VecDst& x,
                               int B, int L, int w, int Lc, int rev, hipStream_t stream) {
     if (w <= kSmallW) {
-        const long long nwg = ((long long)B * L + kSmallRows - 1) / kSmallRows;
-        chunk_apply_small<<<dim3((unsigned)nwg), kThreads, 0, stream>>>(P, q, xin, x, B, L, Lc,
-                                                                       rev, w);
+        const long long rows_per_wg = 4LL * kSmallRows;
+        const long long nwg = ((long long)B * L + rows_per_wg - 1) / rows_per_wg;
+        if (w == 16)
+            chunk_apply_small<16><<<dim3((unsigned)nwg), kThreads, 0, stream>>>(P, q, xin, x, B, L,
+                                                                               Lc, rev, w);
+        else
+            chunk_apply_small<0><<<dim3((unsigned)nwg), kThreads, 0, stream>>>(P, q, xin, x, B, L,
+                                                                              Lc, rev, w);
         return hipGetLastError();
     }
     const dim3 grid((unsigned)((long long)B * L));
+#define DEEPPCR_APPLY_ROWS(WW)                                                                 \
+    if (w == WW) {                                                                             \
+        chunk_apply_rows<WW><<<grid, kThreads, 0, stream>>>(P, q, xin, x, L, Lc, rev);         \
+        return hipGetLastError();                                                              \
+    }
+    DEEPPCR_APPLY_ROWS(32)
+    DEEPPCR_APPLY_ROWS(64)
+    DEEPPCR_APPLY_ROWS(128)
+#undef DEEPPCR_APPLY_ROWS
     chunk_apply_kernel<<<grid, kThreads, 0, stream>>>(P, q, xin, x, L, Lc, rev, w);
     return hipGetLastError();
 }

@@ -318,6 +318,16 @@ void chunk_level_work(int B, int L, int w, int Lc, int rev, int s, double* bytes
                       double* flops);
 hipError_t launch_chunk_level(const BlockSrc& Ain, const VecSrc& rin, float* Aout, float* rout,
                               int B, int L, int w, int Lc, int rev, int s, hipStream_t stream);
+// The chains left after the chunk-local levels with strides below s, solved
+// by substitution into every row's map (P_j, q_j; q only in the chunk
+// holding internal row 0), for the widths chunk_chain_width accepts; Ain and
+// rin are the level buffers (contiguous, internal order), Pout and qout the
+// same layout.
+bool chunk_chain_width(int w);
+void chunk_chain_work(int B, int L, int w, int Lc, int rev, int s, double* bytes,
+                      double* flops);
+hipError_t launch_chunk_chain(const float* Ain, const float* rin, float* Pout, float* qout,
+                              int B, int L, int w, int Lc, int rev, int s, hipStream_t stream);
 // xin [B, chunk_count, w]: the carry-in of every chunk (internal chunk order)
 // from the chunk-end rows of P (the final operators) and q (final vectors).
 hipError_t launch_chunk_carry(const float* P, const float* q, float* xin, int B, int L, int w,

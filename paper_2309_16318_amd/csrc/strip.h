@@ -84,6 +84,25 @@ __device__ __forceinline__ float strip_matvec(const M& a, const float* x, int h)
     return half_sum(part);
 }
 
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the TPR consecutive lanes of a block row (TPR = 2 .. 16, inside
+// one 16-lane DPP row), in every lane of the row: butterfly steps whose
+// partner lanes come from DPP permutations (quad_perm [1,0,3,2] and
+// [2,3,0,1], then the half-row and row mirrors, which pair each lane with one
+// of the other group of 4 or 8 lanes), VALU operations with no LDS round trip.
+template <int TPR>
+__device__ __forceinline__ float row_sum(float v) {
+    v += dpp<0xB1>(v);
+    if constexpr (TPR >= 4) v += dpp<0x4E>(v);
+    if constexpr (TPR >= 8) v += dpp<0x141>(v);
+    if constexpr (TPR >= 16) v += dpp<0x140>(v);
+    return v;
+}
+
 // No side work in a product's k-loop.
 struct NoSide {
     __device__ __forceinline__ void operator()(int) const {}
