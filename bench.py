@@ -410,7 +410,7 @@ def main():
     if tail["launches"] > 0:
         # the last levels' pass (substitution along the chains), timed as a
         # class of its own
-        out["roofline_tail"] = {"kernel": "pcr_chain_subst",
+        out["roofline_tail"] = {"kernel": "chunk_chain" if wl.chunks > 1 else "pcr_chain_subst",
                                 **roofline(tail, wl.w, by_intensity=True),
                                 "avg_launch_us": round(tail["ms"] * 1e3 / tail["launches"], 3),
                                 "launches": tail["launches"]}
