@@ -219,8 +219,7 @@ __device__ inline float eval_layer_row(const NewtonArgs& na, int l, const float*
 #pragma unroll
         for (int e = 0; e < 4; ++e) part = fmaf(w_in[4 * q + e], z4[e], part);
     }
-#pragma unroll
-    for (int off = W; off < 64; off <<= 1) part += __shfl_xor(part, off, 64);
+    part = group_sum<W>(part);
     const float a = part + na.bias[(long long)l * W + i];
     float d;
     const float y = activate(na.layer, a, &d);
@@ -377,8 +376,7 @@ __global__ __launch_bounds__(256) void pcr_level_wave(
 #pragma unroll
                 for (int e = 0; e < 4; ++e) part = fmaf(aR[4 * q + e], rp[e], part);
             }
-#pragma unroll
-            for (int off = W; off < 64; off <<= 1) part += __shfl_xor(part, off, 64);
+            part = group_sum<W>(part);
             emit(l, ri + part);
             // A_l A_{l-s}
             if (m >= 2) {
@@ -1004,8 +1002,7 @@ __device__ inline float wave_matvec(const float* aR, const float* x, int g) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) part = fmaf(aR[4 * q + e], xv[e], part);
     }
-#pragma unroll
-    for (int off = W; off < 64; off <<= 1) part += __shfl_xor(part, off, 64);
+    part = group_sum<W>(part);
     return part;
 }
 

@@ -70,6 +70,20 @@ __device__ __forceinline__ float half_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Sum over the lanes l, l ^ W, l ^ 2W, ... of the wave (W = 16 or 32) in
+// every lane: the row swap of v_permlane16_swap (16-lane rows 2r and 2r + 1)
+// and then that of v_permlane32_swap, no LDS round trip.
+template <int W>
+__device__ __forceinline__ float group_sum(float v) {
+    static_assert(W == 16 || W == 32, "lane groups of 16 or 32");
+    if constexpr (W == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
+                                                        false, false);
+        v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    }
+    return half_sum(v);
+}
+
 // (strip of M) x for x in LDS; every lane of the row gets the sum.
 template <int W, class M>
 __device__ __forceinline__ float strip_matvec(const M& a, const float* x, int h) {
