@@ -1127,24 +1127,47 @@ __global__ __launch_bounds__(256) void pcr_level2_wave(BlockSrc Ain, VecSrc rin,
 // operand of A''_m = A'_m A'_{m-2}; only the right operands A_{m-1} and
 // A'_{m-2} go through LDS (two blocks), and each element costs one block
 // read and one block write for two levels.
+// Column tiles TC0 .. TC0+NTC-1 of a product strip to global memory through
+// the wave's 4 KiB LDS buffer stg: each tile goes in in the MFMA layout and
+// comes back as 8 rows of 32 columns per store (whole 128-byte lines instead
+// of 32-byte pieces of 32 rows).  Measured at w = 128 (one box): pair kernel
+// 1177 -> 1160 us on the B 16, L 1024 solve; at w = 32 (one wave per
+// workgroup) the extra 4 KiB and registers cost occupancy and it was slower.
+template <int W, int TC0, int NTC>
+__device__ __forceinline__ void tiles_store_staged(float* dst, const v16f (&acc)[NTC], int R,
+                                                   int h, float* stg) {
+    const int i = R & 31, lane = threadIdx.x & 63;
+    float* d = dst + (R - i + lane / 8) * W + 4 * (lane % 8);
+#pragma unroll
+    for (int tc = 0; tc < NTC; ++tc) {
+        v4f cst[4];
+        stage_tile(stg, acc[tc], i, h, cst);
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+            *reinterpret_cast<v4f*>(d + 8 * p * W + 32 * (TC0 + tc)) = cst[p];
+    }
+}
+
 // Level-2s product of an element, A''_m = A'_m A'_{m-2} (A'_{m-2} in YT),
 // two column tiles at a time, each pair stored as soon as it is done (so no
-// whole product strip is held); returns A'_m r'_{m-2} (r'_{m-2} in LDS).
-// side(q) runs at k-step q of the first pair of column tiles (see
-// strip_product).
+// whole product strip is held; at w = 128 through stg); returns A'_m r'_{m-2}
+// (r'_{m-2} in LDS).  side(q) runs at k-step q of the first pair of column
+// tiles (see strip_product).
 template <int W, class F = NoSide>
 __device__ __forceinline__ float second_product(const float* YT, const StripC<W>& pC,
                                                 const float* rpp, float* dst, int i, int h,
-                                                int R, F side = F{}) {
+                                                int R, float* stg, F side = F{}) {
     constexpr int T = Tile2Shape<W>::T;
     constexpr int N0 = T < 2 ? T : 2;
     v16f acc[N0];
     const float part = strip_matvec<W>(pC, rpp, h);
     strip_product<W, 0, N0, false>(YT, pC, acc, i, h, nullptr, side);
-    tiles_store<W, 0, N0>(dst, acc, R, h);
     if constexpr (T == 4) {
+        tiles_store_staged<W, 0, N0>(dst, acc, R, h, stg);
         strip_product<W, 2, 2, false>(YT, pC, acc, i, h);
-        tiles_store<W, 2, 2>(dst, acc, R, h);
+        tiles_store_staged<W, 2, 2>(dst, acc, R, h, stg);
+    } else {
+        tiles_store<W, 0, N0>(dst, acc, R, h);
     }
     return part;
 }
@@ -1202,9 +1225,12 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
     __shared__ float Y[W * S::PITCH];  // A'_{m-2}, transposed
     __shared__ float rv[2][W];         // r_m in slot m & 1, r_{m-1} in the other
     __shared__ float rp[2][W];         // r'_{m-2} in slot m & 1, r'_{m-1} in the other
+    // w = 128: per-wave staging of the level-2s product's stores
+    __shared__ float STG[W == 128 ? S::NWV * 1024 : 1];
     const int t = threadIdx.x;
     const int lane = t & 63, i = lane & 31, h = lane >> 5;
     const int R = 32 * (t >> 6) + i;
+    float* stg = STG + (W == 128 ? (t >> 6) * 1024 : 0);
     const int s = plan.s;
     const long long item = blockIdx.x;
     const long long per_b = (long long)s * plan.segs_per_class;
@@ -1287,9 +1313,10 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
         if (prod2) {
             if constexpr (SIDE)
                 r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)l * W * W, i, h, R,
-                                        side);
+                                        stg, side);
             else
-                r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)l * W * W, i, h, R);
+                r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)l * W * W, i, h, R,
+                                        stg);
         } else {
             if constexpr (SIDE) {
 #pragma unroll
@@ -1426,7 +1453,9 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
     __shared__ float rv[2][W];         // r_{m-1} in slot (m+1) & 1
     __shared__ float rp[2][W];         // r'_{m-2} in slot m & 1
     __shared__ float zv[2][W];         // Z_m in slot m & 1, Z_{m-1} in the other
+    __shared__ float STG[W == 128 ? S::NWV * 1024 : 1];  // as in pcr_level2_tile
     const int t = threadIdx.x;
+    float* stg = STG + (W == 128 ? (t >> 6) * 1024 : 0);
     if (blockIdx.x == 0)
         for (int k = t; k < 2 * kRedShards; k += S::NT) na.red[k] = 0u;
     const int lane = t & 63, i0 = lane & 31, h0 = lane >> 5;
@@ -1542,7 +1571,10 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
                 r1 += strip_product<W, 0, S::T, true>(X, aC, pC, i, h, rv[(m + 1) & 1]);
             } else {
                 if (m >= 1 && have_prev) r1 += strip_matvec<W>(aC, rv[(m + 1) & 1], h);
-                strip_zero<W>(pC);
+                // pC is read only where a product has set it (m >= 2 after
+                // the walk's first element); at w = 32 its zeroing, which
+                // the compiler hoists onto every element, is left out
+                if constexpr (W != 32) strip_zero<W>(pC);
             }
             __syncthreads();  // B0: X, rv and zv are read
             if (h == 0) rv[m & 1][R] = rm;
@@ -1571,9 +1603,10 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer
             if (prod2) {
                 if constexpr (SIDE)
                     r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)m * W * W, i, h, R,
-                                            side);
+                                            stg, side);
                 else
-                    r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)m * W * W, i, h, R);
+                    r2 += second_product<W>(Y, pC, rp[m & 1], Ob + (long long)m * W * W, i, h, R,
+                                            stg);
             } else {
                 if constexpr (SIDE) {
 #pragma unroll
