@@ -1443,9 +1443,13 @@ __global__ __launch_bounds__(Tile2Shape<W>::NT) void pcr_level2_tile_last(BlockS
 // r_m = f_m(Z_{m-1}) - Z_m and, scaling its own row, the strip of
 // J_m = D_m W_m (+ I); the walk goes on with A_m = J_m.  Also clears the
 // max|dZ|, max|Z| slots and reduces max|r| into the kRedF slots.
+// w = 32: four one-wave workgroups per SIMD (128 registers, 9.75 KiB of LDS
+// each: the CU's 160 KiB hold all sixteen); with 4096 segments that is one
+// round over the chip (measured on one box: PCR level time of the B 256,
+// L 256 forward 0.91 -> 0.85-0.89 ms against three per SIMD and 6144).
 template <int W>
 __global__ __launch_bounds__(Tile2Shape<W>::NT)
-__attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : 1))) void pcr_level2_tile_layer(
+__attribute__((amdgpu_waves_per_eu(W == 32 ? 4 : 1))) void pcr_level2_tile_layer(
     float* __restrict__ Aout, VecDst rout, int L, LevelPlan plan, NewtonArgs na) {
     using S = Tile2Shape<W>;
     __shared__ float X[W * S::PITCH];  // J_{m-1}, transposed
@@ -1740,11 +1744,15 @@ LevelPlan plan_level2_tile(int B, int L, int s, long long target_wgs) {
 }
 
 // Workgroups per tile pass: w = 128 and 64 fill the CUs with one or two
-// workgroups of 4 or 2 waves each; a w = 32 workgroup is one wave (6144:
-// segments of 11 elements for the B 256, L 256 forward, 3% faster than 8192
-// segments of 8 and 1.4% faster than 4096 of 16, measured on one box; 512
-// workgroups at w = 128 and 2048 at w = 64 were 3% and 13% slower).
-long long pair_tile_target(int w) { return w == 32 ? 6144 : w == 64 ? 1024 : 256; }
+// workgroups of 4 or 2 waves each; a w = 32 workgroup is one wave: 4096 for
+// the first pair with the layers (four per SIMD, one round; segments of 16
+// elements for the B 256, L 256 forward), 6144 for the backward's first
+// pair (three per SIMD; with three per SIMD the forward measured 3% faster
+// at 6144 than at 8192 and 1.4% than at 4096, on one box); 512 workgroups
+// at w = 128 and 2048 at w = 64 were 3% and 13% slower.
+long long pair_tile_target(int w, bool layer = false) {
+    return w == 32 ? (layer ? 4096 : 6144) : w == 64 ? 1024 : 256;
+}
 
 LevelPlan plan_level2(int B, int L, int s, long long target_items) {
     LevelPlan p;
@@ -1894,7 +1902,7 @@ bool layer_first_level(int w) { return w == 16 || w == 32 || w == 64 || w == 128
 hipError_t launch_first_level_fwd(const NewtonArgs& na, float* Aout, const VecDst& rout, int B,
                                   int L, int w, hipStream_t stream) {
     if (first_level_count(B, L, w) == 2) {
-        const LevelPlan q = plan_level2_tile(B, L, 1, pair_tile_target(w));
+        const LevelPlan q = plan_level2_tile(B, L, 1, pair_tile_target(w, true));
         const dim3 grid((unsigned)q.total);
         if (w == 32)
             hipLaunchKernelGGL((pcr_level2_tile_layer<32>), grid, dim3(Tile2Shape<32>::NT), 0,
