@@ -22,7 +22,7 @@
  *     run concurrently.
  *   - Host-side state.  The first Newton call (the forward entry points and
  *     deeppcr_newton_step) of a host thread allocates one pinned, mapped host
- *     buffer of 3 KiB for that thread's per-iteration read-back of the
+ *     buffer of 32 bytes for that thread's per-iteration read-back of the
  *     convergence measures; it is reused by the thread's later calls and
  *     freed by deeppcr_release_thread_state().  The text of the last error
  *     and the instrumentation state are also per host thread.  Nothing else
@@ -31,13 +31,14 @@
  *   - All GPU work is enqueued on `stream` (a hipStream_t passed as void*;
  *     NULL is the default stream).  pcr_solve_block_bidiag and
  *     deeppcr_mlp_backward return without waiting for the GPU;
- *     the two forward entry points wait once per Newton iteration to read their
- *     convergence measure (a problem small enough for the one-launch solver
- *     waits once: the kernel writes its status record and then a completion
- *     word into the thread's mapped host buffer, and the call watches that
- *     word, falling back to a stream wait after 5 ms; the launch may still be
- *     retiring when the call returns, and later work on `stream` is ordered
- *     after it).
+ *     the Newton entry points wait once per Newton iteration to read their
+ *     convergence measures: a one-workgroup kernel at the end of the
+ *     iteration reduces them and writes them, then a sequence word, into the
+ *     thread's mapped host buffer, and the call watches that word, falling
+ *     back to a stream wait after 5 ms (a problem small enough for the
+ *     one-launch solver waits once, the same way, for the kernel's status
+ *     record and completion word).  The last kernel may still be retiring
+ *     when the call returns; later work on `stream` is ordered after it.
  *   - Host out-parameters are plain host pointers.
  *   - Arguments are validated before any HIP call: an invalid argument returns
  *     DEEPPCR_EINVAL (or DEEPPCR_EWORKSPACE for a short workspace) and

@@ -385,33 +385,74 @@ Ws carve(void* workspace, const Layout& lo) {
     return ws;
 }
 
-// Pinned host copy of the reduction area for the per-iteration read-back
-// (mapped, so that a kernel can also write it directly).  Allocated on the
-// first Newton call of a host thread; deeppcr_release_thread_state frees it.
+// Pinned, mapped host words that kernels write the per-call and
+// per-iteration records into: words 0-3 the one-launch solver's status
+// record and completion word, words 4-7 (kHostMeas) the Newton measures and
+// their sequence word.  Allocated on the first Newton call of a host thread;
+// deeppcr_release_thread_state frees them.
+constexpr int kHostMeas = 4, kHostWords = 8;
 thread_local unsigned* g_host_words = nullptr;
 
 unsigned* host_words() {
     if (!g_host_words) {
         void* p = nullptr;
-        if (hipHostMalloc(&p, kRedWords * sizeof(unsigned),
+        if (hipHostMalloc(&p, kHostWords * sizeof(unsigned),
                           hipHostMallocMapped | hipHostMallocPortable) != hipSuccess)
             return nullptr;
+        std::memset(p, 0, kHostWords * sizeof(unsigned));
         g_host_words = (unsigned*)p;
     }
     return g_host_words;
-}
-
-// Max over kRedShards slots.
-unsigned max_slots(const unsigned* slots) {
-    unsigned a = 0u;
-    for (int k = 0; k < kRedShards; ++k) a = slots[k] > a ? slots[k] : a;
-    return a;
 }
 
 float bits_to_float(unsigned u) {
     float f;
     std::memcpy(&f, &u, sizeof f);
     return f;
+}
+
+// Waits until the host-mapped word `word`, which a kernel writes after its
+// record, holds `value`: the host watches it for up to 5 ms (Newton
+// iterations and small solves take microseconds to a few milliseconds) and
+// then waits for the stream, which also reports a failed launch.  The
+// acquire fence orders the record's reads after the word's.
+hipError_t watch_word(const volatile unsigned* word, unsigned value, hipStream_t st) {
+    hipError_t e = prof_break();
+    if (e != hipSuccess) return e;
+    bool seen = false;
+    const auto t0 = std::chrono::steady_clock::now();
+    while (!(seen = (*word == value)) &&
+           std::chrono::steady_clock::now() - t0 < std::chrono::milliseconds(5)) {
+    }
+    if (!seen) {
+        e = host_wait(st);
+        if (e != hipSuccess) return e;
+        if (*word != value) return hipErrorUnknown;
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    return hipSuccess;
+}
+
+// The stopping measures of a Newton iteration, after its last kernel on st:
+// m[0] = max |dZ|, m[1] = max |Z|, m[2] = max |F| (float bit patterns, the
+// max over each measure's slots of red).  One small kernel reduces the slots
+// and writes them with a fresh sequence number into the host words, which
+// the host watches instead of waiting for the stream.
+hipError_t read_measures(const unsigned* red, unsigned* hw, hipStream_t st, unsigned m[3]) {
+    thread_local unsigned seq = 0u;
+    seq = seq + 1u == 0u ? 1u : seq + 1u;
+    void* hwd = nullptr;
+    hipError_t e = hipHostGetDevicePointer(&hwd, hw, 0);
+    if (e != hipSuccess) return e;
+    e = timed(DEEPPCR_KCLASS_OTHER, 4.0 * kRedWords, 0.0, st, [&] {
+        return launch_measures(red, (unsigned*)hwd + kHostMeas, seq, st);
+    });
+    if (e != hipSuccess) return e;
+    const volatile unsigned* rec = hw + kHostMeas;
+    e = watch_word(rec + 3, seq, st);
+    if (e != hipSuccess) return e;
+    for (int j = 0; j < 3; ++j) m[j] = rec[j];
+    return hipSuccess;
 }
 
 // The fused Newton linear solve (w = 16, 32, 64, 128): the layer evaluation
@@ -575,14 +616,7 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
                                       (unsigned*)hwd, st);
         });
         if (e != hipSuccess) return hip_fail(e, "newton_tiny");
-        DEEPPCR_HIP(prof_break());
-        bool seen = false;
-        const auto t0 = std::chrono::steady_clock::now();
-        while (!(seen = (*done == 1u)) &&
-               std::chrono::steady_clock::now() - t0 < std::chrono::milliseconds(5)) {
-        }
-        if (!seen) DEEPPCR_HIP(host_wait(st));
-        std::atomic_thread_fence(std::memory_order_acquire);
+        DEEPPCR_HIP(watch_word(done, 1u, st));
         if (iters_out) *iters_out = (int)hw[1];
         if (measure_out) *measure_out = bits_to_float(hw[2]);
         if (hw[0] == 3u) return DEEPPCR_ENONFINITE;
@@ -626,10 +660,9 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
         }
         if (e != hipSuccess) return hip_fail(e, "layer evaluation");
         if (rule.residual) {
-            DEEPPCR_HIP(copy_async(hw + kRedF, fslots, kRedShards * sizeof(unsigned),
-                                       hipMemcpyDeviceToHost, st));
-            DEEPPCR_HIP(host_wait(st));
-            const unsigned mf = max_slots(hw + kRedF);
+            unsigned ms[3];
+            DEEPPCR_HIP(read_measures(ws.red, hw, st, ms));
+            const unsigned mf = ms[2];
             if (iters_out) *iters_out = k;
             if (measure_out) *measure_out = bits_to_float(mf);
             if (mf >= 0x7f800000u) return DEEPPCR_ENONFINITE;
@@ -655,10 +688,9 @@ int newton_forward(const float* W, const float* bias, const float* z0, float* Z,
             if (e != hipSuccess) return hip_fail(e, "update_reduce");
         }
         if (rule.residual) continue;
-        DEEPPCR_HIP(copy_async(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
-                                   hipMemcpyDeviceToHost, st));
-        DEEPPCR_HIP(host_wait(st));
-        const unsigned mx = max_slots(hw + kRedDZ), mz = max_slots(hw + kRedZ);
+        unsigned ms[3];
+        DEEPPCR_HIP(read_measures(ws.red, hw, st, ms));
+        const unsigned mx = ms[0], mz = ms[1];
         if (iters_out) *iters_out = k + 1;
         if (measure_out) *measure_out = bits_to_float(mx);
         if (mx >= 0x7f800000u || mz >= 0x7f800000u) return DEEPPCR_ENONFINITE;
@@ -968,11 +1000,9 @@ int deeppcr_newton_step(const float* J, const float* F, float* Z, int B, int L, 
                   [&] { return launch_update_reduce(Z, xd.base, n, ws.red, st); });
         if (e != hipSuccess) return hip_fail(e, "update_reduce");
     }
-    DEEPPCR_HIP(copy_async(hw, ws.red, kRedWords * sizeof(unsigned), hipMemcpyDeviceToHost,
-                               st));
-    DEEPPCR_HIP(host_wait(st));
-    const unsigned mr = max_slots(hw + kRedF), mx = max_slots(hw + kRedDZ),
-                   mz = max_slots(hw + kRedZ);
+    unsigned ms[3];
+    DEEPPCR_HIP(read_measures(ws.red, hw, st, ms));
+    const unsigned mr = ms[2], mx = ms[0], mz = ms[1];
     if (residual_out) *residual_out = bits_to_float(mr);
     if (max_update_out) *max_update_out = bits_to_float(mx);
     if (max_abs_out) *max_abs_out = bits_to_float(mz);
@@ -1153,10 +1183,9 @@ int deeppcr_resnet_forward(const float* W, const float* bias, const float* z0, f
                       [&] { return launch_update_reduce(X, xd.base, n, ws.red, st); });
             if (e != hipSuccess) return hip_fail(e, "update_reduce");
         }
-        DEEPPCR_HIP(copy_async(hw, ws.red, 2 * kRedShards * sizeof(unsigned),
-                                   hipMemcpyDeviceToHost, st));
-        DEEPPCR_HIP(host_wait(st));
-        const unsigned mx = max_slots(hw + kRedDZ), mz = max_slots(hw + kRedZ);
+        unsigned ms[3];
+        DEEPPCR_HIP(read_measures(ws.red, hw, st, ms));
+        const unsigned mx = ms[0], mz = ms[1];
         if (iters_out) *iters_out = k;
         if (last_update_out) *last_update_out = bits_to_float(mx);
         if (mx >= 0x7f800000u || mz >= 0x7f800000u) {

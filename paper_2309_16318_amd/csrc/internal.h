@@ -234,6 +234,9 @@ hipError_t launch_residual(const float* F, const float* Z, float* r, long long n
 
 // p[0 .. n) = 0 (a kernel, so that the call can sit in a captured graph).
 hipError_t launch_zero_words(unsigned* p, int n, hipStream_t stream);
+// out (host-mapped): out[0..2] = max over the kRedDZ, kRedZ, kRedF slots of
+// red, then out[3] = seq.
+hipError_t launch_measures(const unsigned* red, unsigned* out, unsigned seq, hipStream_t stream);
 
 // dW[l] = sum_b Lambda[b,l] sigma(Zprev[b,l])^T, db[l] = sum_b Lambda[b,l]
 // (pre-activation layers W sigma(z) + b; activation act: 0 tanh, 1 sigmoid,

@@ -431,6 +431,33 @@ __global__ __launch_bounds__(kThreads) void zero_words_kernel(unsigned* __restri
     if (i < n) p[i] = 0u;
 }
 
+// The Newton stopping measures for the host: max |dZ|, max |Z| and max |F|,
+// each the max over its kRedShards slots, go to out[0..2], then seq to
+// out[3] after a system-scope fence, so that a host that reads seq in out[3]
+// (host-mapped memory) also reads the maxima.  One workgroup of kRedShards
+// threads, one slot of each measure per thread.
+__global__ __launch_bounds__(kRedShards) void measures_kernel(const unsigned* __restrict__ red,
+                                                              unsigned* out, unsigned seq) {
+    __shared__ unsigned part[3][kRedShards / 64];
+    const int t = threadIdx.x;
+    unsigned v[3] = {red[kRedDZ + t], red[kRedZ + t], red[kRedF + t]};
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+        for (int off = 32; off > 0; off >>= 1) v[j] = max(v[j], (unsigned)__shfl_xor((int)v[j], off, 64));
+    if ((t & 63) == 0)
+        for (int j = 0; j < 3; ++j) part[j][t >> 6] = v[j];
+    __syncthreads();
+    if (t == 0) {
+        for (int j = 0; j < 3; ++j) {
+            unsigned m = part[j][0];
+            for (int q = 1; q < kRedShards / 64; ++q) m = max(m, part[j][q]);
+            out[j] = m;
+        }
+        __threadfence_system();
+        __hip_atomic_store(out + 3, seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+}
+
 __global__ __launch_bounds__(kThreads) void copy_rows_kernel(VecSrc src, VecDst dst, int L, int w) {
     const long long row = blockIdx.x;
     const int l = (int)(row % L);
@@ -673,6 +700,11 @@ hipError_t launch_residual(const float* F, const float* Z, float* r, long long n
 hipError_t launch_zero_words(unsigned* p, int n, hipStream_t stream) {
     hipLaunchKernelGGL(zero_words_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
                        dim3(kThreads), 0, stream, p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_measures(const unsigned* red, unsigned* out, unsigned seq, hipStream_t stream) {
+    hipLaunchKernelGGL(measures_kernel, dim3(1), dim3(kRedShards), 0, stream, red, out, seq);
     return hipGetLastError();
 }
 
