@@ -147,3 +147,29 @@ def test_wide_newton_step_generic(dev):
     deeppcr.deeppcr_newton_step(g(d["J"], dev), g(F, dev), Z, tol=0.0)
     ref = Z0.astype(np.float64) + oracle.seq_solve(d["J"], F.astype(np.float64) - Z0, False)
     assert normwise_rel_err(h(Z), ref) <= TOL
+
+
+def test_wide_forward_iterations_past_the_watch(dev):
+    """Newton iterations long enough (w = 1024, L = 96, B = 1: about ten
+    milliseconds each) that the host's 5 ms watch of the measures word runs
+    out and the read-back falls back to waiting for the stream: the same
+    solution and iteration count as the oracle's Newton run."""
+    import time
+    B, L, w, layer = 1, 96, 1024, 1
+    d = synth.mlp_inputs(B, L, w, seed=9400)
+    t = {k: g(v, dev) for k, v in d.items()}
+    deeppcr.deeppcr_mlp_forward(t["W"], t["bias"], t["z0"], layer=layer, alpha=0.1, tol=0.0,
+                                max_iter=1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    res = deeppcr.deeppcr_mlp_forward(t["W"], t["bias"], t["z0"], layer=layer, alpha=0.1,
+                                      tol=1e-5, max_iter=20)
+    ms = (time.perf_counter() - t0) * 1e3
+    assert res.status == deeppcr.OK
+    ref = oracle.seq_forward(layer, 0.1, d["W"], d["bias"], d["z0"])
+    err = normwise_rel_err(h(res.Z), ref)
+    _, k_ref, ok, _ = oracle.newton_forward(layer, 0.1, d["W"], d["bias"], d["z0"], 1e-5, 20)
+    _say(f"  {res.iters} iterations in {ms:.1f} ms ({ms / max(res.iters, 1):.1f} ms each), "
+         f"err {err:.2e}, oracle {k_ref}")
+    assert err <= TOL
+    assert ok and abs(res.iters - k_ref) <= 1
