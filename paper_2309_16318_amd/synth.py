@@ -43,7 +43,7 @@ class Workload:
     chunks: int = 1      # row-chunked solve: chunks of the depth split
 
 
-# The workloads the build is measured on (tanh MLPs / residual nets with
+# The measured workloads (tanh MLPs / residual nets with
 # random weights, a standalone block-bidiagonal solve, and the collapsed-skip
 # ResNet).
 WORKLOADS = {
