@@ -72,7 +72,11 @@ def denoising_steps(p: dict, eps):
     isa = (1.0 / torch.sqrt(alpha[t - 1])).float()[:, None]
     sb = torch.sqrt(beta[t - 1]).float()[:, None]
     te = temb[t - 1]                              # [L, h]
-    eye = torch.eye(w, dtype=torch.float32, device=dev)
+    # W2 diag(d) W1 = sum_k d_k W2[:, k] W1[k, :]: the h rank-one products,
+    # K[k] = W2[:, k] W1[k, :] flattened [h, w*w], so that the Jacobians of
+    # all steps are one GEMM of the activation slopes against K
+    K = (W2.t()[:, :, None] * W1[:, None, :]).reshape(W1.shape[0], w * w).contiguous()
+    neg_ci = -(c * isa)                           # [L, 1]
 
     def pre(Zprev):
         return torch.matmul(Zprev, W1.t().contiguous()) + b1 + te
@@ -84,7 +88,10 @@ def denoising_steps(p: dict, eps):
     def jac_fn(Zprev):
         th = torch.tanh(pre(Zprev))
         d = 1.0 - th * th                         # [B, L, h]
-        Jg = torch.matmul(W2 * d[..., None, :], W1)   # [B, L, w, w]
-        return (eye - c[..., None] * Jg) * isa[..., None]
+        # (I - c_t W2 diag(d) W1) / sqrt(alpha_t): the products' part in one
+        # GEMM, then 1 / sqrt(alpha_t) on the diagonal
+        J = torch.matmul(d * neg_ci, K).view(*d.shape[:-1], w, w)   # [B, L, w, w]
+        J.diagonal(dim1=-2, dim2=-1).add_(isa)
+        return J
 
     return step_fn, jac_fn
