@@ -158,3 +158,23 @@ def test_mfma_summary_weights_by_dispatch_and_splits_the_tail(tmp_path):
     assert out["pcr_tail_mfma_util_pct"] == pytest.approx(50.0)
     assert "other" not in out["by_kernel"]
     assert out["kernel_source_sha256"] == pmc_traffic.kernel_source_sha256()
+
+
+def test_denoising_step_jacobians_match_autograd():
+    """The sampler example's step Jacobians (one GEMM of the activation slopes
+    against the denoiser's rank-one products, the 1/sqrt(alpha) diagonal added
+    in place) equal autograd's Jacobian of its step function, on the CPU."""
+    torch = pytest.importorskip("torch")
+    from paper_2309_16318_amd import generic, synth
+    B, L, w, h = 2, 6, 4, 8
+    d = synth.diffusion_inputs(B, L, w, h, seed=3)
+    p = {k: torch.from_numpy(d[k]).double() for k in ("W1", "b1", "W2", "b2", "temb")}
+    eps = torch.from_numpy(d["eps"]).double()
+    step_fn, jac_fn = generic.denoising_steps(p, eps)
+    Zprev = torch.randn(B, L, w, dtype=torch.float64, generator=torch.Generator().manual_seed(4))
+    J = jac_fn(Zprev)
+    assert J.shape == (B, L, w, w)
+    full = torch.autograd.functional.jacobian(step_fn, Zprev)   # [B, L, w, B, L, w]
+    for b in range(B):
+        for l in range(L):
+            torch.testing.assert_close(J[b, l], full[b, l, :, b, l, :], rtol=1e-6, atol=1e-6)
