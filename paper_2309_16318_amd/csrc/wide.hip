@@ -11,7 +11,9 @@
 // At these widths the block product is a real matrix product (2 w^3 flops on
 // 12 w^2 bytes: 43 flop/B at w = 256, above the fp32 MFMA ridge), so each
 // product is tiled into 128 x 128 output tiles, one workgroup per tile, k in
-// chunks of 32 double-buffered through LDS, on v_mfma_f32_32x32x2_f32.
+// chunks of 16 double-buffered through LDS (the next chunk stored part by part
+// beside the current chunk's products), three workgroups per CU, on
+// v_mfma_f32_32x32x2_f32.
 // Workgroups are dispatched round-robin over the 8 XCDs; the tile index is
 // remapped so that the tiles of one product run on one XCD (its L2 then
 // serves the row and column panels the tiles share).
@@ -27,7 +29,9 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kWide = kMaxWideWidth;  // 1024
 constexpr int kTile = 128;            // output tile of the block product
-constexpr int kKC = 32;               // k chunk
+constexpr int kKC = 16;               // k chunk
+constexpr int kFpr = kKC / 4;         // float4 per row of a k chunk
+constexpr int kNp = kTile * kKC / (4 * 256);  // float4 per thread per tile chunk
 constexpr int kPitch = kKC + 4;       // LDS row pitch (conflict-free 16-byte reads)
 constexpr int kXcds = 8;
 
@@ -113,13 +117,13 @@ __device__ inline void stage_vec(float* z, const float* __restrict__ src, int w)
 // Zero outside the block.  256 threads, four float4 each.
 template <bool VEC, bool TR>
 __device__ inline void tile_load(const float* __restrict__ blk, int w, int r0, int c0,
-                                 v4f (&reg)[4]) {
+                                 v4f (&reg)[kNp]) {
     const int t = threadIdx.x;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < kNp; ++p) {
         const int f = t + kThreads * p;
         if constexpr (!TR) {
-            const int r = r0 + (f >> 3), c = c0 + 4 * (f & 7);
+            const int r = r0 + f / kFpr, c = c0 + 4 * (f % kFpr);
             if constexpr (VEC) {
                 reg[p] = (r < w && c < w) ? *reinterpret_cast<const v4f*>(blk + (long long)r * w + c)
                                           : v4f{0.f, 0.f, 0.f, 0.f};
@@ -142,15 +146,28 @@ __device__ inline void tile_load(const float* __restrict__ blk, int w, int r0, i
     }
 }
 
+// Part p of tile_store below.
+template <bool TR>
+__device__ inline void tile_store_part(float* T, const v4f (&reg)[kNp], int p) {
+    const int f = threadIdx.x + kThreads * p;
+    if constexpr (!TR) {
+        *reinterpret_cast<v4f*>(T + (f / kFpr) * kPitch + 4 * (f % kFpr)) = reg[p];
+    } else {
+        const int c = f >> 5, r = 4 * (f & 31);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) T[(r + e) * kPitch + c] = reg[p][e];
+    }
+}
+
 // The registers of tile_load into T[r][c] (pitch kPitch).
 template <bool TR>
-__device__ inline void tile_store(float* T, const v4f (&reg)[4]) {
+__device__ inline void tile_store(float* T, const v4f (&reg)[kNp]) {
     const int t = threadIdx.x;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < kNp; ++p) {
         const int f = t + kThreads * p;
         if constexpr (!TR) {
-            *reinterpret_cast<v4f*>(T + (f >> 3) * kPitch + 4 * (f & 7)) = reg[p];
+            *reinterpret_cast<v4f*>(T + (f / kFpr) * kPitch + 4 * (f % kFpr)) = reg[p];
         } else {
             const int c = f >> 5, r = 4 * (f & 31);
 #pragma unroll
@@ -166,7 +183,7 @@ __device__ inline void tile_store(float* T, const v4f (&reg)[4]) {
 // 32 x 32 tiles.  The k order inside a chunk: lane half h supplies
 // k = 8q + 4h + e to the MFMA of step (q, e), for both operands.
 template <bool VEC, bool TRANS>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void
 pcr_wide_prod(BlockSrc Ain, VecSrc rin, float* __restrict__ Aout, VecDst rout, int L, int w,
               int s, int nt, long long items, long long per_xcd) {
     __shared__ float TA[2][kTile * kPitch];  // A_l tile, [i][k]
@@ -200,7 +217,7 @@ pcr_wide_prod(BlockSrc Ain, VecSrc rin, float* __restrict__ Aout, VecDst rout, i
         for (int c = 0; c < 2; ++c) acc[a][c] = v16f{};
     float mva = 0.f;
     const int nk = (w + kKC - 1) / kKC;
-    v4f ra[4], rb[4];
+    v4f ra[kNp], rb[kNp];
     tile_load<VEC, TRANS>(Al, w, i0, 0, ra);
     tile_load<VEC, !TRANS>(Ap, w, j0, 0, rb);
     tile_store<TRANS>(TA[0], ra);
@@ -228,17 +245,19 @@ pcr_wide_prod(BlockSrc Ain, VecSrc rin, float* __restrict__ Aout, VecDst rout, i
                 acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[e], b0[e], acc[1][0], 0, 0, 0);
                 acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[e], b1[e], acc[1][1], 0, 0, 0);
             }
+            // the next chunk's part q into the other buffer, beside this
+            // step's products (that buffer is not read before the barrier)
+            if (more && q < kNp) {
+                tile_store_part<TRANS>(TA[buf ^ 1], ra, q);
+                tile_store_part<!TRANS>(TB[buf ^ 1], rb, q);
+            }
         }
         if (mv) {
             // thread t: row t / 2 of the tile, half t % 2 of the chunk's columns
-            const float* arow = TA[buf] + (t >> 1) * kPitch + 16 * (t & 1);
-            const float* rv = rp + kc * kKC + 16 * (t & 1);
+            const float* arow = TA[buf] + (t >> 1) * kPitch + (kKC / 2) * (t & 1);
+            const float* rv = rp + kc * kKC + (kKC / 2) * (t & 1);
 #pragma unroll
-            for (int c = 0; c < 16; ++c) mva = fmaf(arow[c], rv[c], mva);
-        }
-        if (more) {
-            tile_store<TRANS>(TA[buf ^ 1], ra);
-            tile_store<!TRANS>(TB[buf ^ 1], rb);
+            for (int c = 0; c < kKC / 2; ++c) mva = fmaf(arow[c], rv[c], mva);
         }
         __syncthreads();
     }
