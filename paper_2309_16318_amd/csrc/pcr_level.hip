@@ -503,13 +503,17 @@ __device__ inline void regs_to_lds(const v4f* pre, float* buf, bool trans) {
 // 16-byte chunks XOR-swizzled by row, and read back so that lane t holds row
 // 8p + t/8, columns 4(t%8) .. +3: each global store then covers 8 whole
 // 128-byte rows of the tile instead of 32-byte pieces of 32 rows.
-__device__ inline void stage_tile(float* stg, const v16f& acc, int i, int h, v4f (&cst)[4]) {
+// stage_tile in two parts (so that other work can run between them): the
+// tile into the staging area, then back out as whole rows.
+__device__ inline void stage_tile_in(float* stg, const v16f& acc, int i, int h) {
     wave_sync();
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         v4f x = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
         *reinterpret_cast<v4f*>(stg + i * 32 + 4 * ((2 * q + h) ^ (i & 7))) = x;
     }
+}
+__device__ inline void stage_tile_out(const float* stg, v4f (&cst)[4]) {
     wave_sync();
     const int t = threadIdx.x & 63;
 #pragma unroll
@@ -517,6 +521,10 @@ __device__ inline void stage_tile(float* stg, const v16f& acc, int i, int h, v4f
         const int r = 8 * p + t / 8;
         cst[p] = *reinterpret_cast<const v4f*>(stg + r * 32 + 4 * ((t % 8) ^ (r & 7)));
     }
+}
+__device__ inline void stage_tile(float* stg, const v16f& acc, int i, int h, v4f (&cst)[4]) {
+    stage_tile_in(stg, acc, i, h);
+    stage_tile_out(stg, cst);
 }
 
 template <int W>
@@ -1133,26 +1141,37 @@ __global__ __launch_bounds__(256) void pcr_level2_wave(BlockSrc Ain, VecSrc rin,
 // of 32-byte pieces of 32 rows).  Measured at w = 128 (one box): pair kernel
 // 1177 -> 1160 us on the B 16, L 1024 solve; at w = 32 (one wave per
 // workgroup) the extra 4 KiB and registers cost occupancy and it was slower.
+// Column tile tc of a product strip, read back from the staging area as in
+// tiles_store_staged, to global memory.
+template <int W>
+__device__ __forceinline__ void tile_rows_store(float* dst, const v4f (&cst)[4], int R, int tc) {
+    const int lane = threadIdx.x & 63;
+    float* d = dst + (R - (R & 31) + lane / 8) * W + 4 * (lane % 8);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) *reinterpret_cast<v4f*>(d + 8 * p * W + 32 * tc) = cst[p];
+}
+
 template <int W, int TC0, int NTC>
 __device__ __forceinline__ void tiles_store_staged(float* dst, const v16f (&acc)[NTC], int R,
                                                    int h, float* stg) {
-    const int i = R & 31, lane = threadIdx.x & 63;
-    float* d = dst + (R - i + lane / 8) * W + 4 * (lane % 8);
 #pragma unroll
     for (int tc = 0; tc < NTC; ++tc) {
         v4f cst[4];
-        stage_tile(stg, acc[tc], i, h, cst);
-#pragma unroll
-        for (int p = 0; p < 4; ++p)
-            *reinterpret_cast<v4f*>(d + 8 * p * W + 32 * (TC0 + tc)) = cst[p];
+        stage_tile(stg, acc[tc], R & 31, h, cst);
+        tile_rows_store<W>(dst, cst, R, TC0 + tc);
     }
 }
 
 // Level-2s product of an element, A''_m = A'_m A'_{m-2} (A'_{m-2} in YT),
-// two column tiles at a time, each pair stored as soon as it is done (so no
-// whole product strip is held; at w = 128 through stg); returns A'_m r'_{m-2}
-// (r'_{m-2} in LDS).  side(q) runs at k-step q of the first pair of column
-// tiles (see strip_product).
+// two column tiles at a time (so no whole product strip is held); returns
+// A'_m r'_{m-2} (r'_{m-2} in LDS).  side(q) runs at k-step q of the first
+// pair of column tiles (see strip_product).  At w = 128 the tiles go out
+// through stg, the first pair's beside the second pair's products (separate
+// accumulators; per tile, at three k-steps: into stg, back as whole rows,
+// to memory), the second pair's after them.  Measured on one box: pair
+// kernel 1123 -> 1112 us on the B 16, L 1024 solve against the first pair
+// stored between the two; the second pair's stores moved beside the next
+// element's level-s product in the same way gained nothing more.
 template <int W, class F = NoSide>
 __device__ __forceinline__ float second_product(const float* YT, const StripC<W>& pC,
                                                 const float* rpp, float* dst, int i, int h,
@@ -1163,9 +1182,15 @@ __device__ __forceinline__ float second_product(const float* YT, const StripC<W>
     const float part = strip_matvec<W>(pC, rpp, h);
     strip_product<W, 0, N0, false>(YT, pC, acc, i, h, nullptr, side);
     if constexpr (T == 4) {
-        tiles_store_staged<W, 0, N0>(dst, acc, R, h, stg);
-        strip_product<W, 2, 2, false>(YT, pC, acc, i, h);
-        tiles_store_staged<W, 2, 2>(dst, acc, R, h, stg);
+        v16f acc2[2];
+        v4f cst[4];
+        auto out = [&](int q) {
+            if (q == 1 || q == 5) stage_tile_in(stg, acc[q / 4], i, h);
+            if (q == 2 || q == 6) stage_tile_out(stg, cst);
+            if (q == 3 || q == 7) tile_rows_store<W>(dst, cst, R, q / 4);
+        };
+        strip_product<W, 2, 2, false>(YT, pC, acc2, i, h, nullptr, out);
+        tiles_store_staged<W, 2, 2>(dst, acc2, R, h, stg);
     } else {
         tiles_store<W, 0, N0>(dst, acc, R, h);
     }
@@ -1249,7 +1274,7 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
     float* Ob = Aout + (long long)b * L * W * W;
 
     StripA<W> a;             // A_m, then A_{m+1}
-    StripC<W> pE, pO;        // A'_m of even / odd elements
+    StripC<W> pE, pO;        // A'_m of even / odd elements (w >= 64: of m % 3 = 0, 1)
     auto load = [&](int row) {
         if constexpr (SRCB)
             strip_load_bwd<W>(bw, b, L, row, a, R, h);
@@ -1266,13 +1291,22 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
     if (t < W) rv[mw & 1][t] = rb[(long long)l * rin.rstride + t];
     if (mw >= 1) load(l);
     __syncthreads();
-    // element m: a = A_m on entry and A_{m+1} on exit, pC <- A'_m, pP =
-    // A'_{m-1}.  A_m replaces A_{m-1} in X as soon as the first product is
-    // done, and only then is A_{m+1} requested into the same registers.
-    // Two barriers per element: B0 after the reads of X and rv, B1 after
-    // those of Y and rp.  X and rv are rewritten between B0 and B1 (read
-    // again after B1), Y and rp after B1 (read again after the next B0).
-    auto element = [&](int m, StripC<W>& pC, StripC<W>& pP) {
+    // element m: a = A_m on entry and A_{m+1} on exit, pC <- A'_m.  A_m
+    // replaces A_{m-1} in X as soon as the first product is done, and only
+    // then is A_{m+1} requested into the same registers.  Two barriers per
+    // element: B0 after the reads of X and rv, B1 after those of Y and rp.
+    // X and rv are rewritten between B0 and B1 (read again after B1), Y and
+    // rp after B1 (read again after the next B0).
+    // YD (w = 64, 128): A'_{m-2} (pY) goes to Y beside the level-s product
+    // of element m, which reads neither Y nor pY, so three product strips
+    // are held (A'_{m-2}, A'_{m-1}, A'_m).  Otherwise (w = 32, whose three
+    // waves per SIMD leave no registers for a third strip) A'_{m-1} (pY)
+    // goes to Y after B1 of element m and two strips are held.  Measured on
+    // one box: w = 128 pair 1159 -> 1145 us on the B 16, L 1024 solve
+    // (B 16, L 1024 residual forward + backward 19.99 -> 19.67 ms); w = 64
+    // backward (B 64, L 1024) 1.66 -> 1.63 ms.
+    constexpr bool YD = W >= 64;
+    auto element = [&](int m, StripC<W>& pC, StripC<W>& pY) {
         const bool more = m < m1;
         const bool have_prev = m > mw;  // state of element m-1 is valid
         const bool out_row = m >= m0;
@@ -1282,9 +1316,14 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
         // old value of a register set stays live across elements)
         float r1 = rv[m & 1][R];
         const bool prod1 = m >= 2 && have_prev;
+        const bool puty = YD && m >= 4 && m - 2 > mw;
+        auto yside = [&](int q) {
+            if (puty) strip_put_T_quad<W>(Y, pY, R, h, q);
+        };
         if (prod1) {
-            r1 += strip_product<W, 0, S::T, true>(X, a, pC, i, h, rv[(m + 1) & 1]);
+            r1 += strip_product<W, 0, S::T, true>(X, a, pC, i, h, rv[(m + 1) & 1], yside);
         } else {
+            if (puty) strip_put_T<W>(Y, pY, R, h);
             if (m >= 1 && have_prev) r1 += strip_matvec<W>(a, rv[(m + 1) & 1], h);
             strip_zero<W>(pC);
         }
@@ -1327,15 +1366,28 @@ __attribute__((amdgpu_waves_per_eu(W == 32 ? 3 : W == 64 ? 2 : 1))) void pcr_lev
         if (out_row && h == 0) ob[(long long)l * rout.rstride + R] = r2;
         __syncthreads();  // B1: Y and rp are read
         if (h == 0) rp[m & 1][R] = r1;
-        if (more && m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pP, R, h);  // A'_{m-1}
+        if constexpr (!YD)
+            if (more && m >= 3 && m - 1 > mw) strip_put_T<W>(Y, pY, R, h);  // A'_{m-1}
         l += s;
     };
-    // an even and an odd element per loop step, so that every register set
-    // keeps its role through the loop (no parity branch to merge); an odd
-    // first element starts the loop with its even slot skipped
-    for (int m = mw & ~1; m <= m1; m += 2) {
-        if (m >= mw) element(m, pE, pO);
-        if (m + 1 <= m1) element(m + 1, pO, pE);
+    if constexpr (YD) {
+        // three elements per loop step, so that every register set keeps its
+        // role (set m % 3 receives A'_m, p3 for m % 3 = 2); elements before
+        // mw are skipped
+        StripC<W> p3;
+        for (int m = mw - mw % 3; m <= m1; m += 3) {
+            if (m >= mw) element(m, pE, pO);
+            if (m + 1 >= mw && m + 1 <= m1) element(m + 1, pO, p3);
+            if (m + 2 >= mw && m + 2 <= m1) element(m + 2, p3, pE);
+        }
+    } else {
+        // an even and an odd element per loop step, so that every register
+        // set keeps its role through the loop (no parity branch to merge);
+        // an odd first element starts the loop with its even slot skipped
+        for (int m = mw & ~1; m <= m1; m += 2) {
+            if (m >= mw) element(m, pE, pO);
+            if (m + 1 <= m1) element(m + 1, pO, pE);
+        }
     }
 }
 
